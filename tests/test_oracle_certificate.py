@@ -1,0 +1,178 @@
+"""Pins for the oracle's certificates and storage counts.
+
+The strongest pin: the paper's detailed synthetic TT tables (Sec. 7.2 Table
+tab:tt_three_way_detail and Sec. 7.3 Table tab:synthetic_tt_d6_detail) are
+reproduced at every printed digit -- TT-SVD, left-orthogonal gauge, rounding
+of the cores, FP64 reconstruction, eta, the verdict of Thm thm:tt_conditional
+and the exact storage ratio, for all 40 rows.  The tensors are defined by
+formula in the paper.  Metrics are divided by ||T||_F as in the tables; the
+synthetic tensors are NOT normalised before TT-SVD (rounding is not scale
+invariant, so normalising would move eta in the third digit).
+
+The matrix certificate (Thm thm:matrix_rank_compensation) is pinned by the
+printed storage ratios and by the inequalities the theorem proves."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_12969_amd import synth
+from conftest import read_golden
+
+_TENSORS = {
+    "decay_3d": synth.decay_3d,
+    "hilbert_3d": synth.hilbert_3d,
+    "hilbert_6d": synth.hilbert_6d,
+    "decay_6d": synth.decay_6d,
+}
+
+
+def _fmt_ratio(x: float, printed: str) -> str:
+    # the three-way table prints ratios above 1000 as ">1000"
+    if printed == ">1000":
+        return ">1000" if x > 1000 else f"{x:.2f}"
+    return f"{x:.2f}"
+
+
+def _check_rows(rows):
+    cache = {}
+    for row in rows:
+        name = row["dataset"]
+        if name not in cache:
+            cache[name] = (_TENSORS[name](), {})
+        T, bases = cache[name]
+        d = T.ndim
+        R, Rp, prec = int(row["R"]), int(row["Rplus"]), row["prec"]
+        if R not in bases:
+            bases[R] = O.tt_svd(T, ranks=[R] * (d - 1))
+        aug = O.left_orthogonalize(O.tt_svd(T, ranks=[Rp] * (d - 1)))
+        c = O.tt_certificate(T, bases[R], aug, prec)
+        nT = c["norm_ref"]
+        got = {
+            "E_R": f"{c['E_base'] / nT:.2e}",
+            "new_error": f"{c['err_new'] / nT:.2e}",
+            "eta": f"{c['eta'] / nT:.2e}",
+            "err_ratio": _fmt_ratio(c["err_new"] / c["E_base"], row["err_ratio"]),
+            "mem_ratio": f"{c['bytes_aug'] / c['bytes_base']:.2f}",
+            "cert": "Yes" if c["certified"] else "No",
+        }
+        want = {k: row[k] for k in got}
+        assert got == want, f"{name} {R}->{Rp} {prec}"
+        # invariants of the theorem on every row
+        assert abs(c["E_aug"] - c["eta"]) <= c["err_new"] * (1 + 1e-12) + 1e-300
+        assert c["err_new"] <= (c["E_aug"] + c["eta"]) * (1 + 1e-12)
+        if c["certified"]:
+            assert c["err_new"] <= c["E_base"] * (1 + 1e-12)
+            assert c["gain"] >= 0.0
+
+
+@pytest.mark.slow
+def test_three_way_table_reproduced():
+    rows = read_golden("tt_three_way_detail.csv")
+    assert len(rows) == 24
+    _check_rows(rows)
+
+
+@pytest.mark.slow
+def test_six_way_table_reproduced():
+    rows = read_golden("tt_six_way_detail.csv")
+    assert len(rows) == 16
+    _check_rows(rows)
+
+
+def test_matrix_storage_ratios_printed():
+    for row in read_golden("matrix_storage_ratios.csv"):
+        k = int(row["k"])
+        m, n = 494, 494            # any shape: the ratio is (b/64)(k+1)/k
+        prec = row["prec"]
+        same = prec.endswith("same")
+        p = prec.replace("same", "")
+        aug = O.storage_bytes(m, n, k if same else k + 1, p)
+        base = O.storage_bytes(m, n, k, "fp64")
+        ratio = aug / base
+        # equal to the printed value within half a unit of its last digit
+        # (the tables round ties differently: 0.25625 prints as 0.2563 in one
+        # and 26.25% as 26.2% in the other)
+        if row["format"] == "4f":
+            assert abs(ratio - float(row["printed"])) <= 0.5e-4 + 1e-12
+        else:
+            assert abs(100 * ratio - float(row["printed"])) <= 0.05 + 1e-12
+
+
+def test_hyperspectral_storage_printed():
+    for row in read_golden("hyperspectral_storage.csv"):
+        dims = [int(row["n1"]), int(row["n2"]), int(row["n3"])]
+        ranks = [1, int(row["R1"]), int(row["R2"]), 1]
+        b = O.tt_storage_bytes(dims, ranks, row["prec"])
+        assert f"{b / 2 ** 20:.2f}" == row["mib"]
+        assert str(round(8 * dims[0] * dims[1] * dims[2] / b)) == row["comp"]
+
+
+def test_storage_formula_cases():
+    # b k (m+n+1) bits (Sec. 4.2); the 494_bus crossover example of Sec. 4.3:
+    # factors exceed the 494^2 dense entries for k >= 247
+    assert O.storage_bytes(512, 256, 20, "fp64") == 8 * 20 * 769
+    assert O.storage_bytes(512, 256, 21, "fp16") == 2 * 21 * 769
+    assert min(k for k in range(1, 495) if k * (494 + 494 + 1) >= 494 * 494) == 247
+
+
+def _matrix_case(prec):
+    w = synth.matrix_small()
+    k = w["k"]
+    U, S, Vt = O.svd(w["A"])
+    return w, k, O.matrix_certificate(S, U[:, :k + 1], S[:k + 1], Vt[:k + 1].T, k, prec, A=w["A"])
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+def test_matrix_certificate_invariants(prec):
+    w, k, c = _matrix_case(prec)
+    # the tail norms come from the spectrum; eta from the rounded factors
+    assert c["E_base"] >= c["E_aug"]
+    assert abs(c["E_base"] ** 2 - c["E_aug"] ** 2 - c["gain"]) <= 1e-12 * c["E_base"] ** 2
+    # triangle inequality sandwich (proof of the theorem)
+    assert abs(c["E_aug"] - c["eta"]) <= c["err_new"] * (1 + 1e-12)
+    assert c["err_new"] <= (c["E_aug"] + c["eta"]) * (1 + 1e-12)
+    # direct and squared forms agree when eta <= E_k (eq. matrix_condition_squared)
+    sq = (c["eta"] <= c["E_base"]) and (c["gain"] >= 2 * c["eta"] * c["E_base"] - c["eta"] ** 2)
+    assert sq == c["certified"]
+    # on this truncation-dominated matrix both precisions certify and win
+    assert c["certified"] and c["acc_win"] and c["mem_win"] and c["outcome"] == 2
+    assert c["bytes_base"] == O.storage_bytes(512, 256, 20, "fp64")
+    # eta is the storage perturbation only: of order u ||A_{k+1}||_F
+    u = {"fp32": 2.0 ** -24, "fp16": 2.0 ** -11}[prec]
+    assert 0.01 * u * c["norm_ref"] < c["eta"] < 10 * u * c["norm_ref"]
+
+
+def test_matrix_certificate_fp64_is_exact():
+    # rounding FP64 factors to FP64 is the identity: eta = 0 exactly
+    w, k, c = _matrix_case("fp64")
+    assert c["eta"] == 0.0
+    assert c["certified"]            # E_{k+1} <= E_k always
+    assert not c["mem_win"] and c["outcome"] == 1
+
+
+def test_certificate_detects_a_failing_case():
+    """A spectrum whose (k+1)-th value is far below the FP16 perturbation
+    floor: the certificate must fail for FP16 and hold for FP32, as in the
+    paper's tail-rank stress rows (Sec. 4.3)."""
+    m, n, k = 300, 200, 30
+    rng = synth.rng_for(synth.W_RANDOM, 40)
+    U = synth.haar(rng, m, n)
+    V = synth.haar(rng, n, n)
+    sig = np.concatenate([np.ones(k), 1e-6 * 0.5 ** np.arange(n - k)])
+    A = O.lowrank_dense(U, sig, V)
+    c16 = O.matrix_certificate(sig, U[:, :k + 1], sig[:k + 1], V[:, :k + 1], k, "fp16", A=A)
+    c32 = O.matrix_certificate(sig, U[:, :k + 1], sig[:k + 1], V[:, :k + 1], k, "fp32", A=A)
+    assert not c16["certified"] and c16["outcome"] == 0 and not c16["acc_win"]
+    assert c32["certified"] or c32["eta"] > c32["E_base"] - c32["E_aug"]
+
+
+def test_tt_compensation_algorithm_outcomes():
+    # Algorithm alg:tt_compensation on decay_3d at R = 4 -> 5: FP16 gives a
+    # certified memory win, FP32 4 -> 8 a certified non-increase only
+    T = synth.decay_3d()
+    r16 = O.tt_compensation(T, R=[4, 4], R_plus=[5, 5], prec="fp16")
+    assert r16["outcome"] == 2
+    r32 = O.tt_compensation(T, R=[4, 4], delta=4, prec="fp32")
+    assert r32["ranks_aug"] == [1, 8, 8, 1] and r32["outcome"] == 1
