@@ -1,0 +1,242 @@
+/*
+ * lrc.h -- C ABI of the low-precision rank-compensation hot path on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Problem statements follow El Mountasser & Jbilou, "Low-Precision Rank
+ * Compensation for Matrices and Tensor Trains":
+ *   - factor apply, Sec. 4.4 eq. gpu_matrix_apply;
+ *   - Tensor-Train reconstruction, Sec. 5.1 and Sec. 7.5
+ *     eq. gpu_tt_reconstruction;
+ *   - certificates, Thm thm:matrix_rank_compensation (Sec. 4.1) and
+ *     Thm thm:tt_conditional (Sec. 6) with Algorithm alg:tt_compensation
+ *     (Sec. 7.1);
+ *   - storage counts, Sec. 4.2 and Sec. 5.1.
+ *
+ * Conventions shared by every entry point
+ *   Pointers.  Arrays named "device" live in device memory of the current
+ *     HIP device (hipSetDevice / torch.cuda.set_device).  Arrays named
+ *     "host" live in host memory.  The caller owns every array; the library
+ *     never frees, reallocates or writes a caller input.
+ *   Layout.  Dense, row-major (C order), no padding, every element in the
+ *     storage precision `prec` unless stated otherwise.
+ *   Precision codes.  LRC_FP64 = IEEE binary64 with binary64 accumulation;
+ *     LRC_FP32 = binary32 with binary32 accumulation; LRC_FP16 = binary16
+ *     storage with binary32 accumulation (the paper's protocol, Sec. 3.4).
+ *   Streams.  Work is enqueued on the calling thread's stream
+ *     (lrc_set_stream, default the null stream).  lrc_matrix_apply and
+ *     lrc_tt_reconstruct return without synchronizing; lrc_certify
+ *     synchronizes its stream before it returns.
+ *   Errors.  0 on success, a negative LRC_E* code otherwise; the message is
+ *     available from lrc_last_error() on the same thread.  All argument
+ *     checks run on the host before any HIP call; outputs are unspecified
+ *     after an error.  No C++ exception crosses this interface.
+ *   Workspace.  The library keeps one grow-only device workspace per
+ *     (device, stream), allocated on first use and released by
+ *     lrc_shutdown().  Calls on the same stream are ordered; calls issued
+ *     concurrently from several host threads on the SAME stream race on it.
+ */
+#ifndef LRC_H
+#define LRC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LRC_VERSION 1
+
+/* storage precisions */
+#define LRC_FP64 0
+#define LRC_FP32 1
+#define LRC_FP16 2
+
+/* return codes */
+#define LRC_OK 0
+#define LRC_EINVAL (-1)     /* null pointer, bad size, rank, precision or aliasing */
+#define LRC_EOVERFLOW (-2)  /* a size or byte count overflows int64 */
+#define LRC_EHIP (-3)       /* HIP runtime or launch error */
+#define LRC_ENOMEM (-4)     /* device workspace allocation failed */
+#define LRC_ENODEV (-5)     /* no gfx950 device is current */
+
+/* apply kernels (regime dispatch, Sec. 4.4: the speedup depends strongly on
+ * the batch size) */
+#define LRC_PATH_AUTO 0     /* choose by batch size */
+#define LRC_PATH_STREAM 1   /* streaming wavefront-reduction path (small batch) */
+#define LRC_PATH_MFMA 2     /* matrix-core path (large batch) */
+
+/* certificate kinds */
+#define LRC_CERT_MATRIX 0
+#define LRC_CERT_TT 1
+
+/* Outcomes of Algorithm alg:tt_compensation (Sec. 7.1), also used for the
+ * matrix certificate. */
+#define LRC_OUTCOME_FALLBACK 0       /* keep the FP64 baseline */
+#define LRC_OUTCOME_CERTIFIED 1      /* certified non-increase, no memory win */
+#define LRC_OUTCOME_CERTIFIED_MEM 2  /* certified non-increase and memory win */
+
+/*
+ * lrc_matrix_apply -- Y = U diag(s) (V^T X)   (Sec. 4.4 eq. gpu_matrix_apply)
+ *
+ * The paper writes the product for a b x n batch X_p as
+ * Y_p = [(X_p V_r) diag(s_r)] U_r^T; here X = X_p^T (n x batch) and
+ * Y = Y_p^T (m x batch), so the numbers are identical.
+ *   U  device, m x k      stored left factor U_k
+ *   s  device, k          stored singular values s_k
+ *   V  device, n x k      stored right factor V_k (V, not V^T)
+ *   X  device, n x batch  input batch
+ *   Y  device, m x batch  output, written in `prec`; must not overlap any input
+ * Phase 1 forms T' = diag(s) V^T X in the accumulation precision (for FP16
+ * it is rounded once to binary16 as the input of the second product);
+ * phase 2 forms Y = U T'.  Sums are split in a fixed order, so the result is
+ * bitwise reproducible run to run.
+ * Errors: LRC_EINVAL if a pointer is NULL, m, n, k or batch < 1, k >
+ * min(m, n), prec is unknown or Y overlaps an input; LRC_EOVERFLOW if an
+ * element count overflows; LRC_ENOMEM / LRC_EHIP / LRC_ENODEV from the
+ * runtime.
+ */
+int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X, void* Y,
+                     int64_t m, int64_t n, int64_t k, int64_t batch, int prec);
+
+/* The apply kernel pair LRC_PATH_AUTO selects for these sizes (pure host
+ * function, no device needed).  Returns LRC_PATH_STREAM or LRC_PATH_MFMA, or
+ * LRC_EINVAL for invalid sizes. */
+int lrc_matrix_apply_path(int64_t m, int64_t n, int64_t k, int64_t batch, int prec);
+
+/* Force the apply kernel pair used by later lrc_matrix_apply calls on the
+ * calling thread (LRC_PATH_AUTO restores the dispatch).  Returns LRC_EINVAL
+ * for an unknown path. */
+int lrc_set_apply_path(int path);
+
+/*
+ * lrc_tt_reconstruct -- dense tensor from Tensor-Train cores
+ *   T(i_1..i_d) = G_1(i_1) G_2(i_2) ... G_d(i_d)   (Sec. 5.1; Sec. 7.5)
+ *   cores  host array of d device pointers; core l (0-based) is
+ *          ranks[l] x dims[l] x ranks[l+1], row-major, in `prec`
+ *   dims   host, d mode sizes n_l >= 1
+ *   ranks  host, d+1 TT ranks with ranks[0] = ranks[d] = 1, all >= 1
+ *   d      number of cores, 1 <= d <= LRC_TT_MAX_D
+ *   out    device, prod(dims) entries in C order (i_d fastest), in `prec`;
+ *          must not overlap a core
+ * The cores are contracted left to right (the paper's reshape chain) with
+ * the partial interfaces kept on chip and the last contraction fused with
+ * the output stores; intermediate sums use the accumulation precision and,
+ * for FP16, the last interface is rounded once to binary16.
+ * Errors: LRC_EINVAL for NULL pointers, d out of range, a dimension or rank
+ * < 1, ranks[0] or ranks[d] != 1, a rank above LRC_TT_MAX_RANK, an unknown
+ * prec or overlapping output; LRC_EOVERFLOW if prod(dims) overflows.
+ */
+#define LRC_TT_MAX_D 16
+#define LRC_TT_MAX_RANK 512
+int lrc_tt_reconstruct(const void* const* cores, const int64_t* dims, const int64_t* ranks,
+                       int d, void* out, int prec);
+
+/*
+ * lrc_certify -- rank-compensation certificate
+ *
+ * Matrix (kind = LRC_CERT_MATRIX), Thm thm:matrix_rank_compensation:
+ *   base rank k in FP64, compensated rank k+1 stored in `prec`.
+ *   sigma       host, n_sigma >= k+1 singular values of A, non-increasing
+ *   U, s, V     device FP64 rank-(k+1) factors: U m x (k+1), s (k+1), V n x (k+1)
+ *   Uh, sh, Vh  device, the same factors as stored in `prec` (each rounded
+ *               individually, Remark after the theorem)
+ *   A           device FP64 m x n, or NULL (then err_new is NaN and the
+ *               accuracy-win flags are 0)
+ *   E_k and E_{k+1} come from sigma (Eckart-Young); eta = ||A_{k+1} -
+ *   A_hat_{k+1}||_F with both contracted in FP64; certified iff
+ *   E_{k+1} + eta <= E_k, compared exactly in FP64 (eq. matrix_condition).
+ *
+ * Tensor Train (kind = LRC_CERT_TT), Thm thm:tt_conditional, Algorithm
+ * alg:tt_compensation steps 5-9:
+ *   d, dims     host, as in lrc_tt_reconstruct
+ *   T           device FP64 dense tensor (C order), required
+ *   ranks_base, cores_base   host ranks / host array of device FP64 cores
+ *                            of the baseline T_R
+ *   ranks_aug, cores_aug     the same for the augmented FP64 T_{R+}, in the
+ *                            gauge that was rounded (left-orthogonal)
+ *   cores_aug_h              host array of device cores of T_{R+} as
+ *                            stored in `prec`
+ *   E_R = ||T - T_R||, E_{R+} = ||T - T_{R+}||, S_TT = E_R^2 - E_{R+}^2,
+ *   eta_TT = ||T_{R+} - T_hat_{R+}||, all contracted in FP64; certified iff
+ *   E_{R+} + eta_TT <= E_R (eq. tt_condition).
+ *
+ * Result fields: absolute Frobenius values (divide by norm_ref for the
+ * paper's relative units); bytes are exact stored bytes (Sec. 4.2 / 5.1);
+ * the flags follow the vocabulary of Sec. 4.1 with strict comparisons for
+ * wins.  Synchronizes the stream.
+ * Errors: LRC_EINVAL for missing arrays, inconsistent sizes or ranks, prec
+ * not FP32/FP16/FP64, or sigma not non-increasing.
+ */
+typedef struct lrc_cert_args {
+    int kind;                       /* LRC_CERT_MATRIX or LRC_CERT_TT */
+    int prec;                       /* storage precision of the compensated form */
+    /* matrix */
+    int64_t m, n, k;
+    const double* sigma;            /* host */
+    int64_t n_sigma;
+    const double* U;                /* device FP64 */
+    const double* s;
+    const double* V;
+    const void* Uh;                 /* device, prec */
+    const void* sh;
+    const void* Vh;
+    const double* A;                /* device FP64 or NULL */
+    /* tensor train */
+    int d;
+    const int64_t* dims;            /* host */
+    const double* T;                /* device FP64 */
+    const int64_t* ranks_base;      /* host, d+1 */
+    const double* const* cores_base;    /* host array of device pointers */
+    const int64_t* ranks_aug;       /* host, d+1 */
+    const double* const* cores_aug;     /* host array of device pointers */
+    const void* const* cores_aug_h;     /* host array of device pointers, prec */
+} lrc_cert_args;
+
+typedef struct lrc_cert_result {
+    double E_base;       /* E_k or E_R */
+    double E_aug;        /* E_{k+1} or E_{R+} */
+    double eta;          /* eta_{k+1} or eta_TT */
+    double err_new;      /* ||A - A_hat|| or ||T - T_hat|| (NaN if A is NULL) */
+    double gain;         /* sigma_{k+1}^2 or S_TT */
+    double margin;       /* E_base - E_aug - eta */
+    double norm_ref;     /* ||A||_F (from sigma) or ||T||_F */
+    int64_t bytes_base;  /* FP64 storage at the base rank */
+    int64_t bytes_aug;   /* `prec` storage at the compensated rank */
+    int certified;       /* E_aug + eta <= E_base */
+    int acc_nonincrease; /* err_new <= E_base */
+    int acc_win;         /* err_new <  E_base */
+    int mem_win;         /* bytes_aug < bytes_base */
+    int practical_win;   /* acc_win && mem_win */
+    int outcome;         /* LRC_OUTCOME_* */
+} lrc_cert_result;
+
+int lrc_certify(const lrc_cert_args* args, lrc_cert_result* res);
+
+/* Stored bytes of rank-k factors in `prec`: (b/8) k (m+n+1)  (Sec. 4.2).
+ * Returns LRC_EINVAL for bad arguments or LRC_EOVERFLOW on overflow. */
+int64_t lrc_storage_bytes(int64_t m, int64_t n, int64_t k, int prec);
+
+/* Stored bytes of TT cores: (b/8) sum_l R_{l-1} n_l R_l  (Sec. 5.1).
+ * dims and ranks are host arrays of length d and d+1. */
+int64_t lrc_tt_storage_bytes(const int64_t* dims, const int64_t* ranks, int d, int prec);
+
+/* Stream for later calls on the calling thread (a hipStream_t; NULL = the
+ * null stream).  Never fails. */
+int lrc_set_stream(void* hip_stream);
+
+/* Message for the last non-zero return on the calling thread ("" if none).
+ * The pointer stays valid until the next call on the same thread. */
+const char* lrc_last_error(void);
+
+/* Releases every library-owned device workspace.  Later calls allocate
+ * again.  No call may be in flight. */
+void lrc_shutdown(void);
+
+/* LRC_VERSION of the built library. */
+int lrc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LRC_H */

@@ -1,0 +1,559 @@
+// C ABI of the rank-compensation hot path (declared in include/lrc.h).
+//
+// Every entry point validates its arguments on the host first, then
+// enqueues kernels on the calling thread's stream.  Workspace is grow-only,
+// one per (device, stream), so repeated calls allocate nothing after the
+// first; lrc_shutdown releases it.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/lrc.h"
+#include "lrc_internal.h"
+
+using namespace lrc;
+
+namespace {
+
+thread_local std::string g_err;
+thread_local hipStream_t g_stream = nullptr;
+thread_local int g_force_path = LRC_PATH_AUTO;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int fail_hip(hipError_t e, const char* what) {
+    return fail(e == hipErrorOutOfMemory ? LRC_ENOMEM : LRC_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool valid_prec(int p) { return p == LRC_FP64 || p == LRC_FP32 || p == LRC_FP16; }
+
+// a * b without overflow (both >= 0)
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+    if (a != 0 && b > INT64_MAX / a) return false;
+    *out = a * b;
+    return true;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const char* pa = static_cast<const char*>(a);
+    const char* pb = static_cast<const char*>(b);
+    return pa < pb + nb && pb < pa + na;
+}
+
+std::mutex g_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+std::map<int, std::pair<bool, size_t>> g_dev;   // device -> (is gfx950, max LDS per block)
+
+int current_device(int* dev, size_t* max_lds) {
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return fail(LRC_ENODEV, "no HIP device: %s", hipGetErrorString(e));
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_dev.find(*dev);
+    if (it == g_dev.end()) {
+        hipDeviceProp_t prop;
+        e = hipGetDeviceProperties(&prop, *dev);
+        if (e != hipSuccess) return fail(LRC_ENODEV, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+        const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+        int lds = 0;
+        if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, *dev) != hipSuccess || lds <= 0)
+            lds = 65536;
+        it = g_dev.emplace(*dev, std::make_pair(ok, (size_t)lds)).first;
+    }
+    if (!it->second.first) return fail(LRC_ENODEV, "device %d is not a gfx950 (MI355X) GPU", *dev);
+    if (max_lds) *max_lds = it->second.second;
+    return LRC_OK;
+}
+
+Workspace& workspace_for(int dev, hipStream_t s) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    return g_ws[std::make_pair(dev, s)];
+}
+
+double half_bits_to_double(uint16_t b) {
+    const int sg = (b >> 15) & 1, ex = (b >> 10) & 0x1F, fr = b & 0x3FF;
+    double v;
+    if (ex == 0) v = std::ldexp((double)fr, -24);
+    else if (ex == 31) v = fr ? NAN : INFINITY;
+    else v = std::ldexp((double)(1024 + fr), ex - 25);
+    return sg ? -v : v;
+}
+
+// host copy of `count` stored values as binary64
+int fetch_widened(const void* dev_ptr, int prec, int64_t count, std::vector<double>& out, hipStream_t st) {
+    out.assign((size_t)count, 0.0);
+    const size_t nb = (size_t)count * elem_bytes(prec);
+    std::vector<unsigned char> raw(nb);
+    hipError_t e = hipMemcpyAsync(raw.data(), dev_ptr, nb, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail_hip(e, "copy to host");
+    for (int64_t i = 0; i < count; ++i) {
+        if (prec == LRC_FP64) {
+            double v;
+            std::memcpy(&v, raw.data() + 8 * i, 8);
+            out[i] = v;
+        } else if (prec == LRC_FP32) {
+            float v;
+            std::memcpy(&v, raw.data() + 4 * i, 4);
+            out[i] = v;
+        } else {
+            uint16_t v;
+            std::memcpy(&v, raw.data() + 2 * i, 2);
+            out[i] = half_bits_to_double(v);
+        }
+    }
+    return LRC_OK;
+}
+
+int64_t tt_count(const int64_t* dims, const int64_t* ranks, int d) {
+    int64_t tot = 0;
+    for (int l = 0; l < d; ++l) {
+        int64_t a, b;
+        if (!mul_ok(ranks[l], dims[l], &a) || !mul_ok(a, ranks[l + 1], &b) || tot > INT64_MAX - b) return -1;
+        tot += b;
+    }
+    return tot;
+}
+
+int check_tt_shape(const int64_t* dims, const int64_t* ranks, int d, int64_t* total) {
+    if (!dims || !ranks) return fail(LRC_EINVAL, "dims and ranks must not be NULL");
+    if (d < 1 || d > LRC_TT_MAX_D) return fail(LRC_EINVAL, "d = %d outside [1, %d]", d, LRC_TT_MAX_D);
+    if (ranks[0] != 1 || ranks[d] != 1) return fail(LRC_EINVAL, "boundary ranks must be 1 (got %lld, %lld)",
+                                                    (long long)ranks[0], (long long)ranks[d]);
+    int64_t n = 1;
+    for (int l = 0; l < d; ++l) {
+        if (dims[l] < 1) return fail(LRC_EINVAL, "dims[%d] = %lld < 1", l, (long long)dims[l]);
+        if (!mul_ok(n, dims[l], &n)) return fail(LRC_EOVERFLOW, "number of tensor entries overflows");
+    }
+    for (int l = 0; l <= d; ++l) {
+        if (ranks[l] < 1) return fail(LRC_EINVAL, "ranks[%d] = %lld < 1", l, (long long)ranks[l]);
+        if (ranks[l] > LRC_TT_MAX_RANK)
+            return fail(LRC_EINVAL, "ranks[%d] = %lld above %d", l, (long long)ranks[l], LRC_TT_MAX_RANK);
+    }
+    if (tt_count(dims, ranks, d) < 0) return fail(LRC_EOVERFLOW, "core sizes overflow");
+    int64_t bytes;
+    if (!mul_ok(n, 8, &bytes)) return fail(LRC_EOVERFLOW, "tensor byte count overflows");
+    *total = n;
+    return LRC_OK;
+}
+
+int tt_reconstruct_impl(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, void* out,
+                        int prec, Workspace* ws_override) {
+    int dev;
+    size_t max_lds;
+    int rc = current_device(&dev, &max_lds);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    const int64_t N = [&] {
+        int64_t n = 1;
+        for (int l = 0; l < d; ++l) n *= dims[l];
+        return n;
+    }();
+    if (d == 1) {
+        hipError_t e = hipMemcpyAsync(out, cores[0], (size_t)N * elem_bytes(prec), hipMemcpyDeviceToDevice, st);
+        return e == hipSuccess ? LRC_OK : fail_hip(e, "copy of the single core");
+    }
+    TTPlan plan;
+    if (plan_tt(plan, dims, ranks, d, prec, max_lds) != 0)
+        return fail(LRC_EINVAL, "TT ranks (%lld into the last core) exceed the on-chip buffers of the fused kernel",
+                    (long long)ranks[d - 1]);
+    Workspace& ws = ws_override ? *ws_override : workspace_for(dev, st);
+    if (!ws_override) {
+        ws.reset();
+        hipError_t e = ws.reserve(plan.stage_bytes, 0, st);
+        if (e != hipSuccess) return fail_hip(e, "workspace");
+    }
+    hipError_t e = launch_tt(plan, cores, out, ws, st);
+    return e == hipSuccess ? LRC_OK : fail_hip(e, "TT reconstruction launch");
+}
+
+}  // namespace
+
+// ------------------------------------------------------------- Workspace --
+namespace lrc {
+hipError_t Workspace::reserve(size_t bytes, size_t counters_needed, hipStream_t stream) {
+    bytes = (size_t)round_up((int64_t)bytes, 256) + 256;
+    if (bytes > cap) {
+        if (base) {
+            hipError_t e = hipStreamSynchronize(stream);
+            if (e != hipSuccess) return e;
+            (void)hipFree(base);
+            base = nullptr;
+            cap = 0;
+        }
+        size_t want = std::max(bytes, cap + cap / 2);
+        hipError_t e = hipMalloc(reinterpret_cast<void**>(&base), want);
+        if (e != hipSuccess) {
+            base = nullptr;
+            return e;
+        }
+        cap = want;
+    }
+    if (counters_needed > n_counters) {
+        if (counters) {
+            hipError_t e = hipStreamSynchronize(stream);
+            if (e != hipSuccess) return e;
+            (void)hipFree(counters);
+            counters = nullptr;
+            n_counters = 0;
+        }
+        size_t want = std::max<size_t>(counters_needed, 1024);
+        hipError_t e = hipMalloc(reinterpret_cast<void**>(&counters), want * sizeof(int));
+        if (e != hipSuccess) {
+            counters = nullptr;
+            return e;
+        }
+        e = hipMemset(counters, 0, want * sizeof(int));
+        if (e != hipSuccess) return e;
+        n_counters = want;
+    }
+    used = 0;
+    return hipSuccess;
+}
+
+void* Workspace::take(size_t bytes) {
+    size_t b = (size_t)round_up((int64_t)bytes, 256);
+    if (b == 0) return nullptr;
+    if (!base || used + b > cap) {
+        overrun = true;
+        return nullptr;
+    }
+    void* p = base + used;
+    used += b;
+    return p;
+}
+
+void Workspace::release() {
+    if (base) (void)hipFree(base);
+    if (counters) (void)hipFree(counters);
+    base = nullptr;
+    counters = nullptr;
+    cap = n_counters = used = 0;
+}
+}  // namespace lrc
+
+// ------------------------------------------------------------------ ABI ---
+extern "C" {
+
+int lrc_version(void) { return LRC_VERSION; }
+
+int lrc_set_stream(void* hip_stream) {
+    g_stream = static_cast<hipStream_t>(hip_stream);
+    return LRC_OK;
+}
+
+const char* lrc_last_error(void) { return g_err.c_str(); }
+
+int lrc_set_apply_path(int path) {
+    if (path != LRC_PATH_AUTO && path != LRC_PATH_STREAM && path != LRC_PATH_MFMA)
+        return fail(LRC_EINVAL, "unknown apply path %d", path);
+    g_force_path = path;
+    return LRC_OK;
+}
+
+static int check_apply(int64_t m, int64_t n, int64_t k, int64_t batch, int prec) {
+    if (!valid_prec(prec)) return fail(LRC_EINVAL, "unknown precision code %d", prec);
+    if (m < 1 || n < 1 || k < 1 || batch < 1)
+        return fail(LRC_EINVAL, "sizes must be >= 1 (m=%lld n=%lld k=%lld batch=%lld)", (long long)m,
+                    (long long)n, (long long)k, (long long)batch);
+    if (k > std::min(m, n)) return fail(LRC_EINVAL, "k = %lld exceeds min(m, n)", (long long)k);
+    int64_t t;
+    const int64_t e = elem_bytes(prec);
+    if (!mul_ok(m, k, &t) || !mul_ok(t, e, &t) || !mul_ok(n, k, &t) || !mul_ok(t, e, &t) || !mul_ok(n, batch, &t) ||
+        !mul_ok(t, e, &t) || !mul_ok(m, batch, &t) || !mul_ok(t, e, &t))
+        return fail(LRC_EOVERFLOW, "array sizes overflow int64");
+    return LRC_OK;
+}
+
+int lrc_matrix_apply_path(int64_t m, int64_t n, int64_t k, int64_t batch, int prec) {
+    int rc = check_apply(m, n, k, batch, prec);
+    if (rc) return rc;
+    return plan_apply(m, n, k, batch, prec, LRC_PATH_AUTO).path;
+}
+
+int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X, void* Y, int64_t m, int64_t n,
+                     int64_t k, int64_t batch, int prec) {
+    if (!U || !s || !V || !X || !Y) return fail(LRC_EINVAL, "NULL array argument");
+    int rc = check_apply(m, n, k, batch, prec);
+    if (rc) return rc;
+    const size_t e = elem_bytes(prec);
+    const size_t ny = (size_t)m * batch * e;
+    if (overlaps(Y, ny, U, (size_t)m * k * e) || overlaps(Y, ny, s, (size_t)k * e) ||
+        overlaps(Y, ny, V, (size_t)n * k * e) || overlaps(Y, ny, X, (size_t)n * batch * e))
+        return fail(LRC_EINVAL, "output Y overlaps an input");
+    int dev;
+    rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    ApplyPlan plan = plan_apply(m, n, k, batch, prec, g_force_path);
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t he = ws.reserve(apply_workspace_bytes(plan), plan.counters, st);
+    if (he != hipSuccess) return fail_hip(he, "workspace");
+    he = launch_apply(plan, U, s, V, X, Y, m, n, k, batch, prec, ws, st);
+    if (he != hipSuccess) return fail_hip(he, "apply launch");
+    return LRC_OK;
+}
+
+int lrc_tt_reconstruct(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, void* out,
+                       int prec) {
+    if (!cores || !out) return fail(LRC_EINVAL, "NULL array argument");
+    if (!valid_prec(prec)) return fail(LRC_EINVAL, "unknown precision code %d", prec);
+    int64_t N;
+    int rc = check_tt_shape(dims, ranks, d, &N);
+    if (rc) return rc;
+    const size_t e = elem_bytes(prec);
+    for (int l = 0; l < d; ++l) {
+        if (!cores[l]) return fail(LRC_EINVAL, "cores[%d] is NULL", l);
+        const size_t cb = (size_t)ranks[l] * dims[l] * ranks[l + 1] * e;
+        if (overlaps(out, (size_t)N * e, cores[l], cb)) return fail(LRC_EINVAL, "output overlaps cores[%d]", l);
+    }
+    return tt_reconstruct_impl(cores, dims, ranks, d, out, prec, nullptr);
+}
+
+int64_t lrc_storage_bytes(int64_t m, int64_t n, int64_t k, int prec) {
+    if (!valid_prec(prec) || m < 1 || n < 1 || k < 0) return fail(LRC_EINVAL, "bad storage arguments");
+    int64_t s, t;
+    if (m > INT64_MAX - n - 1) return fail(LRC_EOVERFLOW, "m + n + 1 overflows");
+    if (!mul_ok(k, m + n + 1, &s) || !mul_ok(s, elem_bytes(prec), &t)) return fail(LRC_EOVERFLOW, "overflow");
+    return t;
+}
+
+int64_t lrc_tt_storage_bytes(const int64_t* dims, const int64_t* ranks, int d, int prec) {
+    if (!valid_prec(prec)) return fail(LRC_EINVAL, "unknown precision code %d", prec);
+    int64_t N;
+    int rc = check_tt_shape(dims, ranks, d, &N);
+    if (rc) return rc;
+    int64_t c = tt_count(dims, ranks, d), t;
+    if (c < 0 || !mul_ok(c, elem_bytes(prec), &t)) return fail(LRC_EOVERFLOW, "overflow");
+    return t;
+}
+
+void lrc_shutdown(void) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    for (auto& kv : g_ws) kv.second.release();
+    g_ws.clear();
+}
+
+// --------------------------------------------------------- certificates ---
+static void finish_flags(lrc_cert_result* r, bool have_err) {
+    r->margin = r->E_base - r->E_aug - r->eta;
+    r->certified = (r->E_aug + r->eta <= r->E_base) ? 1 : 0;
+    r->acc_nonincrease = (have_err && r->err_new <= r->E_base) ? 1 : 0;
+    r->acc_win = (have_err && r->err_new < r->E_base) ? 1 : 0;
+    r->mem_win = (r->bytes_aug < r->bytes_base) ? 1 : 0;
+    r->practical_win = (r->acc_win && r->mem_win) ? 1 : 0;
+    r->outcome = r->certified ? (r->mem_win ? LRC_OUTCOME_CERTIFIED_MEM : LRC_OUTCOME_CERTIFIED) : LRC_OUTCOME_FALLBACK;
+}
+
+static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
+    const int64_t m = a->m, n = a->n, k = a->k, r = k + 1;
+    if (m < 1 || n < 1 || k < 1) return fail(LRC_EINVAL, "sizes must be >= 1");
+    if (r > std::min(m, n)) return fail(LRC_EINVAL, "k + 1 = %lld exceeds min(m, n)", (long long)r);
+    if (!a->sigma || a->n_sigma < r) return fail(LRC_EINVAL, "sigma must hold at least k + 1 values");
+    if (!a->U || !a->s || !a->V || !a->Uh || !a->sh || !a->Vh) return fail(LRC_EINVAL, "NULL factor argument");
+    for (int64_t j = 0; j < a->n_sigma; ++j) {
+        if (!(a->sigma[j] >= 0.0)) return fail(LRC_EINVAL, "sigma[%lld] is negative or NaN", (long long)j);
+        if (j > 0 && a->sigma[j] > a->sigma[j - 1]) return fail(LRC_EINVAL, "sigma is not non-increasing");
+    }
+    int64_t t;
+    if (!mul_ok(m, n, &t) || !mul_ok(t, 8, &t) || !mul_ok(std::max(m, n), 2 * r, &t) || !mul_ok(t, 8, &t))
+        return fail(LRC_EOVERFLOW, "sizes overflow");
+    int dev;
+    int rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+
+    // Eckart-Young tails from one reverse cumulative sum
+    std::vector<double> E((size_t)a->n_sigma + 1, 0.0);
+    double acc = 0.0;
+    for (int64_t j = a->n_sigma - 1; j >= 0; --j) {
+        const double sq = a->sigma[j] * a->sigma[j];   // separate statements: no fused multiply-add
+        acc += sq;
+        E[(size_t)j] = std::sqrt(acc);
+    }
+    res->E_base = E[(size_t)k];
+    res->E_aug = E[(size_t)k + 1];
+    res->norm_ref = E[0];
+    res->gain = a->sigma[k] * a->sigma[k];  // sigma_{k+1}^2 (1-based)
+    res->bytes_base = lrc_storage_bytes(m, n, k, LRC_FP64);
+    res->bytes_aug = lrc_storage_bytes(m, n, r, a->prec);
+
+    // workspace
+    const int64_t w2 = 2 * r;
+    size_t cnt1, cnt2;
+    const size_t gp1 = gram_workspace_bytes(m, w2, &cnt1);
+    const size_t gp2 = gram_workspace_bytes(n, w2, &cnt2);
+    size_t need = (size_t)(m + n) * w2 * 8 + 2 * (size_t)w2 * w2 * 8 + gp1 + gp2 + 16 * 256;
+    const bool have_A = a->A != nullptr;
+    if (have_A) need += (size_t)(m + n) * r * 8 + err_workspace_bytes(m, n) + 256;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t he = ws.reserve(need, std::max(cnt1, cnt2), st);
+    if (he != hipSuccess) return fail_hip(he, "workspace");
+    double* P = static_cast<double*>(ws.take((size_t)m * w2 * 8));
+    double* Q = static_cast<double*>(ws.take((size_t)n * w2 * 8));
+    double* Gu = static_cast<double*>(ws.take((size_t)w2 * w2 * 8));
+    double* Gq = static_cast<double*>(ws.take((size_t)w2 * w2 * 8));
+    if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
+    he = launch_diff_factors(a->U, a->Uh, a->prec, m, r, P, st);
+    if (he == hipSuccess) he = launch_diff_factors(a->V, a->Vh, a->prec, n, r, Q, st);
+    if (he == hipSuccess) he = launch_gram(P, m, w2, Gu, ws, st);
+    if (he == hipSuccess) he = launch_gram(Q, n, w2, Gq, ws, st);
+    if (he != hipSuccess) return fail_hip(he, "certificate launch");
+    double* errsum = nullptr;
+    if (have_A) {
+        double* W = static_cast<double*>(ws.take((size_t)m * r * 8));
+        double* Vw = static_cast<double*>(ws.take((size_t)n * r * 8));
+        double* part = static_cast<double*>(ws.take(err_workspace_bytes(m, n)));
+        errsum = static_cast<double*>(ws.take(8));
+        if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
+        int64_t nparts = 0;
+        he = launch_widen_scaled(a->Uh, a->sh, a->prec, m, r, W, st);
+        if (he == hipSuccess) he = launch_widen_scaled(a->Vh, nullptr, a->prec, n, r, Vw, st);
+        if (he == hipSuccess) he = launch_err_dense(a->A, W, Vw, m, n, r, part, &nparts, st);
+        if (he == hipSuccess) he = launch_reduce_rows(part, nparts, 1, errsum, st);
+        if (he != hipSuccess) return fail_hip(he, "error-norm launch");
+    }
+    std::vector<double> hGu((size_t)w2 * w2), hGq((size_t)w2 * w2), s64, sh64;
+    double err2 = NAN;
+    he = hipMemcpyAsync(hGu.data(), Gu, hGu.size() * 8, hipMemcpyDeviceToHost, st);
+    if (he == hipSuccess) he = hipMemcpyAsync(hGq.data(), Gq, hGq.size() * 8, hipMemcpyDeviceToHost, st);
+    if (he == hipSuccess && have_A) he = hipMemcpyAsync(&err2, errsum, 8, hipMemcpyDeviceToHost, st);
+    if (he == hipSuccess) he = hipStreamSynchronize(st);
+    if (he != hipSuccess) return fail_hip(he, "certificate readback");
+    rc = fetch_widened(a->s, LRC_FP64, r, s64, st);
+    if (rc) return rc;
+    rc = fetch_widened(a->sh, a->prec, r, sh64, st);
+    if (rc) return rc;
+
+    // eta^2 = ||P M Q^T||_F^2 = trace(M^T Gu M Gq) with P = [U dU], Q = [V dV]
+    // and M = [[dS, S^], [S^, S^]] (rows U | dU, columns V | dV), i.e.
+    //   A^_{k+1} - A_{k+1} = U dS V^T + U S^ dV^T + dU S^ V^T + dU S^ dV^T.
+    // Every term is of the size of the perturbation, so nothing of the size
+    // of ||A|| cancels.  Column a of M has two non-zeros:
+    //   a < r : M[a][a] = dS_a,  M[r+a][a] = S^_a
+    //   a >= r: M[a-r][a] = S^_{a-r}, M[a][a] = S^_{a-r}
+    auto nz = [&](int64_t col, int64_t* rows, double* vals) {
+        if (col < r) {
+            rows[0] = col;
+            vals[0] = sh64[(size_t)col] - s64[(size_t)col];
+            rows[1] = r + col;
+            vals[1] = sh64[(size_t)col];
+        } else {
+            rows[0] = col - r;
+            vals[0] = sh64[(size_t)(col - r)];
+            rows[1] = col;
+            vals[1] = sh64[(size_t)(col - r)];
+        }
+    };
+    double eta2 = 0.0;
+    for (int64_t ca = 0; ca < w2; ++ca) {
+        int64_t ra[2];
+        double va[2];
+        nz(ca, ra, va);
+        for (int64_t cb = 0; cb < w2; ++cb) {
+            int64_t rb[2];
+            double vb[2];
+            nz(cb, rb, vb);
+            double h = 0.0;
+            for (int x = 0; x < 2; ++x)
+                for (int y = 0; y < 2; ++y) h += va[x] * hGu[(size_t)(ra[x] * w2 + rb[y])] * vb[y];
+            eta2 += h * hGq[(size_t)(cb * w2 + ca)];
+        }
+    }
+    res->eta = std::sqrt(std::max(eta2, 0.0));
+    res->err_new = have_A ? std::sqrt(err2) : NAN;
+    finish_flags(res, have_A);
+    return LRC_OK;
+}
+
+static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
+    const int d = a->d;
+    int64_t N, Nb;
+    int rc = check_tt_shape(a->dims, a->ranks_base, d, &N);
+    if (rc) return rc;
+    rc = check_tt_shape(a->dims, a->ranks_aug, d, &Nb);
+    if (rc) return rc;
+    if (!a->T || !a->cores_base || !a->cores_aug || !a->cores_aug_h) return fail(LRC_EINVAL, "NULL TT argument");
+    for (int l = 0; l < d; ++l)
+        if (!a->cores_base[l] || !a->cores_aug[l] || !a->cores_aug_h[l])
+            return fail(LRC_EINVAL, "core %d is NULL", l);
+    int dev;
+    rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    const int64_t cnt_aug = tt_count(a->dims, a->ranks_aug, d);
+    const int64_t groups = sumsq5_groups(N);
+    size_t need = 3 * (size_t)N * 8 + (size_t)cnt_aug * 8 + 5 * (size_t)groups * 8 + 64 + (size_t)(8 + d) * 256;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t he = ws.reserve(need, 0, st);
+    if (he != hipSuccess) return fail_hip(he, "workspace");
+    double* TR = static_cast<double*>(ws.take((size_t)N * 8));
+    double* TRp = static_cast<double*>(ws.take((size_t)N * 8));
+    double* Th = static_cast<double*>(ws.take((size_t)N * 8));
+    std::vector<const void*> wide(d);
+    for (int l = 0; l < d; ++l) {
+        const int64_t c = a->ranks_aug[l] * a->dims[l] * a->ranks_aug[l + 1];
+        double* w = static_cast<double*>(ws.take((size_t)c * 8));
+        if (ws.overrun || !w) return fail(LRC_ENOMEM, "certificate workspace too small");
+        he = launch_widen(a->cores_aug_h[l], a->prec, c, w, st);
+        if (he != hipSuccess) return fail_hip(he, "widen launch");
+        wide[l] = w;
+    }
+    double* part = static_cast<double*>(ws.take(5 * (size_t)groups * 8));
+    double* sums = static_cast<double*>(ws.take(5 * 8));
+    if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
+    // FP64 reconstructions (the fused kernel needs no workspace in FP64)
+    std::vector<const void*> cb(a->cores_base, a->cores_base + d), ca(a->cores_aug, a->cores_aug + d);
+    rc = tt_reconstruct_impl(cb.data(), a->dims, a->ranks_base, d, TR, LRC_FP64, &ws);
+    if (rc) return rc;
+    rc = tt_reconstruct_impl(ca.data(), a->dims, a->ranks_aug, d, TRp, LRC_FP64, &ws);
+    if (rc) return rc;
+    rc = tt_reconstruct_impl(wide.data(), a->dims, a->ranks_aug, d, Th, LRC_FP64, &ws);
+    if (rc) return rc;
+    he = launch_sumsq5(a->T, TR, TRp, Th, N, part, groups, st);
+    if (he == hipSuccess) he = launch_reduce_rows(part, groups, 5, sums, st);
+    double h[5];
+    if (he == hipSuccess) he = hipMemcpyAsync(h, sums, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (he == hipSuccess) he = hipStreamSynchronize(st);
+    if (he != hipSuccess) return fail_hip(he, "TT certificate");
+    res->E_base = std::sqrt(h[0]);
+    res->E_aug = std::sqrt(h[1]);
+    res->eta = std::sqrt(h[2]);
+    res->err_new = std::sqrt(h[3]);
+    res->norm_ref = std::sqrt(h[4]);
+    res->gain = h[0] - h[1];
+    res->bytes_base = lrc_tt_storage_bytes(a->dims, a->ranks_base, d, LRC_FP64);
+    res->bytes_aug = lrc_tt_storage_bytes(a->dims, a->ranks_aug, d, a->prec);
+    finish_flags(res, true);
+    return LRC_OK;
+}
+
+int lrc_certify(const lrc_cert_args* args, lrc_cert_result* res) {
+    if (!args || !res) return fail(LRC_EINVAL, "NULL args or result");
+    if (!valid_prec(args->prec)) return fail(LRC_EINVAL, "unknown precision code %d", args->prec);
+    std::memset(res, 0, sizeof(*res));
+    if (args->kind == LRC_CERT_MATRIX) return certify_matrix(args, res);
+    if (args->kind == LRC_CERT_TT) return certify_tt(args, res);
+    return fail(LRC_EINVAL, "unknown certificate kind %d", args->kind);
+}
+
+}  // extern "C"

@@ -1,0 +1,119 @@
+// Device-side building blocks for the gfx950 kernels: storage/accumulation
+// types per precision, the 16x16 MFMA instructions used for each, fragment
+// loads, wave reductions and the deterministic split-reduction handshake.
+//
+// MFMA convention used everywhere (16 x 16 output block, K step KB):
+//   lane l supplies A-operand row (l & 15) and B-operand column (l & 15);
+//   the K slice it supplies is [(l >> 4) * KPL, (l >> 4) * KPL + KPL) of the
+//   step, the same slice for A and B, so the sum over K is exact whatever
+//   order the hardware uses inside the step;
+//   lane l receives D[4 * (l >> 4) + v][l & 15], v = 0..3.
+// Kernels orient the MFMA so that the four values a lane receives are
+// consecutive in the output's contiguous dimension.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lrc {
+
+typedef _Float16 half_t;
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+typedef double double4_t __attribute__((ext_vector_type(4)));
+
+template <typename T> struct PrecTraits;
+
+// binary64 storage, binary64 accumulation: v_mfma_f64_16x16x4_f64
+template <> struct PrecTraits<double> {
+    using acc = double;
+    using accv = double4_t;
+    using frag = double;
+    static constexpr int KPL = 1;   // K values per lane per MFMA
+    static constexpr int KB = 4;    // K per MFMA
+};
+
+// binary32 storage, binary32 accumulation: v_mfma_f32_16x16x4_f32
+template <> struct PrecTraits<float> {
+    using acc = float;
+    using accv = float4_t;
+    using frag = float;
+    static constexpr int KPL = 1;
+    static constexpr int KB = 4;
+};
+
+// binary16 storage, binary32 accumulation: v_mfma_f32_16x16x32_f16 (gfx950)
+template <> struct PrecTraits<half_t> {
+    using acc = float;
+    using accv = float4_t;
+    using frag = half8_t;
+    static constexpr int KPL = 8;
+    static constexpr int KB = 32;
+};
+
+__device__ __forceinline__ double4_t mfma(double a, double b, double4_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ float4_t mfma(float a, float b, float4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ float4_t mfma(half8_t a, half8_t b, float4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+template <typename T>
+__device__ __forceinline__ typename PrecTraits<T>::frag load_frag(const T* p);
+
+template <> __device__ __forceinline__ double load_frag<double>(const double* p) { return *p; }
+template <> __device__ __forceinline__ float load_frag<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ half8_t load_frag<half_t>(const half_t* p) {
+    return *reinterpret_cast<const half8_t*>(p);   // 16-byte aligned by construction
+}
+
+template <typename A>
+__device__ __forceinline__ A zero_accv() {
+    A z;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) z[v] = 0;
+    return z;
+}
+
+// Conversions from the accumulation type to the storage type use the
+// hardware's round-to-nearest-even conversion (subnormals preserved).
+template <typename T, typename Acc>
+__device__ __forceinline__ T to_storage(Acc x) { return static_cast<T>(x); }
+
+template <typename T>
+__device__ __forceinline__ typename PrecTraits<T>::acc to_acc(T x) {
+    return static_cast<typename PrecTraits<T>::acc>(x);
+}
+
+// Sum over the 64 lanes of a wavefront, fixed butterfly order.
+template <typename Acc>
+__device__ __forceinline__ Acc wave_sum(Acc x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// Split-reduction handshake.  Every workgroup that contributes a partial
+// result for `slot` calls this after writing its partial; exactly one (the
+// last to arrive) gets `true` and then reads all partials in a fixed order,
+// so the final sum does not depend on scheduling.  The counter is reset by
+// the winner, so it is zero again for the next launch.
+__device__ __forceinline__ bool arrive_last(int* counter, int expected, int* lds_flag) {
+    __threadfence();          // release this workgroup's partial (device scope)
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int old = atomicAdd(counter, 1);
+        int last = (old == expected - 1);
+        if (last) *counter = 0;
+        *lds_flag = last;
+    }
+    __syncthreads();
+    bool last = *lds_flag != 0;
+    if (last) __threadfence();   // acquire the other workgroups' partials
+    return last;
+}
+
+}  // namespace lrc

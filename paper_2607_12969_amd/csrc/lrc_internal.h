@@ -1,0 +1,117 @@
+// Host-side interface between the C ABI layer (lrc_api.cpp) and the kernel
+// translation units.  Launchers validate nothing: lrc_api.cpp checks every
+// argument before calling them.  Each launcher returns hipSuccess or the
+// first launch error.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lrc {
+
+enum Prec { P64 = 0, P32 = 1, P16 = 2 };
+
+inline int elem_bytes(int prec) { return prec == P64 ? 8 : (prec == P32 ? 4 : 2); }
+inline int mfma_kb(int prec) { return prec == P16 ? 32 : 4; }
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Grow-only device workspace; `take` hands out 256-byte aligned slices of
+// one allocation, in call order, and fails with hipErrorOutOfMemory if the
+// reservation made by `reserve` is exceeded.
+struct Workspace {
+    char* base = nullptr;
+    size_t cap = 0;
+    size_t used = 0;
+    int* counters = nullptr;      // zero-initialised split-reduction counters
+    size_t n_counters = 0;
+    bool overrun = false;         // a take() exceeded the reservation
+    hipError_t reserve(size_t bytes, size_t counters_needed, hipStream_t stream);
+    void* take(size_t bytes);     // nullptr (and overrun = true) past the reservation
+    void reset() { used = 0; overrun = false; }
+    void release();
+};
+
+// ---------------------------------------------------------------- apply ---
+struct ApplyPlan {
+    int path;            // LRC_PATH_STREAM or LRC_PATH_MFMA
+    int64_t Kp;          // k rounded up to the MFMA K step (rows of T'^T)
+    // phase 1 (split over n)
+    int splits;
+    int64_t chunk;       // rows of V / X per split
+    int tiles_m, tiles_n;
+    size_t part_bytes;   // partial-sum buffer
+    size_t mid_bytes;    // T'^T buffer
+    size_t counters;
+};
+
+ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int path);
+size_t apply_workspace_bytes(const ApplyPlan& p);
+
+hipError_t launch_apply(const ApplyPlan& p, const void* U, const void* s, const void* V,
+                        const void* X, void* Y, int64_t m, int64_t n, int64_t k, int64_t b,
+                        int prec, Workspace& ws, hipStream_t stream);
+
+// ------------------------------------------------------- certificate (matrix)
+// G = P^T P for P (rows x cols, row-major, FP64): a split-sum Gram product.
+size_t gram_workspace_bytes(int64_t rows, int64_t cols, size_t* counters);
+hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G,
+                       Workspace& ws, hipStream_t stream);
+
+// P[i][t] = ref[i][t]; P[i][r + t] = widen(h[i][t]) - ref[i][t]   (rows x 2r)
+hipError_t launch_diff_factors(const double* ref, const void* h, int prec, int64_t rows,
+                               int64_t r, double* P, hipStream_t stream);
+// W[i][t] = widen(h[i][t]) * widen(hs[t])  (hs may be NULL: factor 1)
+hipError_t launch_widen_scaled(const void* h, const void* hs, int prec, int64_t rows,
+                               int64_t r, double* W, hipStream_t stream);
+// out[i] = widen(src[i])
+hipError_t launch_widen(const void* src, int prec, int64_t count, double* out, hipStream_t stream);
+
+// Partial sums of (A - W Vw^T)^2 over m x n, one per workgroup; returns the
+// number of partials written to `part` via *nparts.
+size_t err_workspace_bytes(int64_t m, int64_t n);
+hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, int64_t m,
+                            int64_t n, int64_t r, double* part, int64_t* nparts,
+                            hipStream_t stream);
+
+// Five partial sums per workgroup over a dense tensor: (T - a)^2, (T - b)^2,
+// (b - c)^2, (T - c)^2, T^2; written as part[q * groups + g].
+int64_t sumsq5_groups(int64_t count);
+hipError_t launch_sumsq5(const double* T, const double* a, const double* b, const double* c,
+                         int64_t count, double* part, int64_t groups, hipStream_t stream);
+
+// Fixed-order sum of `count` partials for each of `nsums` rows (part is
+// nsums x count, row-major) into out[nsums] (device).
+hipError_t launch_reduce_rows(const double* part, int64_t count, int nsums, double* out,
+                              hipStream_t stream);
+
+// ------------------------------------------------------------------- TT ---
+constexpr int kMaxD = 16;
+
+struct TTPlan {
+    int d;
+    int prec;
+    int64_t dims[kMaxD];
+    int64_t ranks[kMaxD + 1];
+    int64_t NL;          // rows of the left interface Z_{d-2} (1 when d <= 2)
+    int64_t n_mid;       // n_{d-1}
+    int64_t n_last;      // n_d
+    int rL, rM;          // r_{d-2}, r_{d-1}
+    int Kp2, Kp3;        // rL, rM rounded to the MFMA K step
+    int Rt;              // rM rounded up to 16 (row blocks of the middle product)
+    int BL, BI, P;       // left rows and middle indices per block, P = BL * BI
+    int64_t num_i_blocks, num_L_blocks;
+    int grid_L;          // workgroups along the left index (each loops over L blocks)
+    int chain_rmax;      // largest rank among levels 1..d-2 (chain buffers)
+    size_t lds_bytes;
+    size_t stage_bytes;  // staged (transposed, padded) FP16 operands
+};
+
+// Returns 0, or -1 when the ranks do not fit the fused kernel's on-chip
+// buffers (max_lds = the device's per-workgroup LDS limit).
+int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* ranks, int d, int prec, size_t max_lds);
+
+hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Workspace& ws,
+                     hipStream_t stream);
+
+}  // namespace lrc

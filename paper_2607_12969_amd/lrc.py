@@ -1,0 +1,267 @@
+"""Python binding of the rank-compensation hot path (liblrc.so, gfx950).
+
+Argument marshalling only: torch tensors are checked for device, dtype and
+layout, their data pointers and torch's current stream are passed to the C
+ABI declared in include/lrc.h, and every computation runs in the library's
+HIP kernels.  There is no CPU fallback: if the library is missing this
+module raises on first use.
+
+Precision follows the tensors' dtype: float64 -> FP64, float32 -> FP32,
+float16 -> FP16 (FP32 accumulation).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblrc.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "lrc.h")
+
+FP64, FP32, FP16 = 0, 1, 2
+PATH_AUTO, PATH_STREAM, PATH_MFMA = 0, 1, 2
+CERT_MATRIX, CERT_TT = 0, 1
+ERRORS = {-1: "EINVAL", -2: "EOVERFLOW", -3: "EHIP", -4: "ENOMEM", -5: "ENODEV"}
+PREC_NAMES = {"fp64": FP64, "fp32": FP32, "fp16": FP16}
+
+
+class LrcError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+
+
+class CertArgs(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int), ("prec", ctypes.c_int),
+        ("m", _i64), ("n", _i64), ("k", _i64),
+        ("sigma", ctypes.POINTER(ctypes.c_double)), ("n_sigma", _i64),
+        ("U", _vp), ("s", _vp), ("V", _vp),
+        ("Uh", _vp), ("sh", _vp), ("Vh", _vp),
+        ("A", _vp),
+        ("d", ctypes.c_int),
+        ("dims", ctypes.POINTER(_i64)),
+        ("T", _vp),
+        ("ranks_base", ctypes.POINTER(_i64)), ("cores_base", ctypes.POINTER(_vp)),
+        ("ranks_aug", ctypes.POINTER(_i64)), ("cores_aug", ctypes.POINTER(_vp)),
+        ("cores_aug_h", ctypes.POINTER(_vp)),
+    ]
+
+
+class CertResult(ctypes.Structure):
+    _fields_ = [
+        ("E_base", ctypes.c_double), ("E_aug", ctypes.c_double), ("eta", ctypes.c_double),
+        ("err_new", ctypes.c_double), ("gain", ctypes.c_double), ("margin", ctypes.c_double),
+        ("norm_ref", ctypes.c_double),
+        ("bytes_base", _i64), ("bytes_aug", _i64),
+        ("certified", ctypes.c_int), ("acc_nonincrease", ctypes.c_int), ("acc_win", ctypes.c_int),
+        ("mem_win", ctypes.c_int), ("practical_win", ctypes.c_int), ("outcome", ctypes.c_int),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_12969_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    L.lrc_matrix_apply.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, ctypes.c_int]
+    L.lrc_matrix_apply.restype = ctypes.c_int
+    L.lrc_matrix_apply_path.argtypes = [_i64, _i64, _i64, _i64, ctypes.c_int]
+    L.lrc_matrix_apply_path.restype = ctypes.c_int
+    L.lrc_set_apply_path.argtypes = [ctypes.c_int]
+    L.lrc_set_apply_path.restype = ctypes.c_int
+    L.lrc_tt_reconstruct.argtypes = [ctypes.POINTER(_vp), ctypes.POINTER(_i64), ctypes.POINTER(_i64),
+                                     ctypes.c_int, _vp, ctypes.c_int]
+    L.lrc_tt_reconstruct.restype = ctypes.c_int
+    L.lrc_certify.argtypes = [ctypes.POINTER(CertArgs), ctypes.POINTER(CertResult)]
+    L.lrc_certify.restype = ctypes.c_int
+    L.lrc_storage_bytes.argtypes = [_i64, _i64, _i64, ctypes.c_int]
+    L.lrc_storage_bytes.restype = _i64
+    L.lrc_tt_storage_bytes.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.c_int, ctypes.c_int]
+    L.lrc_tt_storage_bytes.restype = _i64
+    L.lrc_set_stream.argtypes = [_vp]
+    L.lrc_set_stream.restype = ctypes.c_int
+    L.lrc_last_error.argtypes = []
+    L.lrc_last_error.restype = ctypes.c_char_p
+    L.lrc_shutdown.argtypes = []
+    L.lrc_shutdown.restype = None
+    L.lrc_version.argtypes = []
+    L.lrc_version.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def header_symbols():
+    """Function names declared in include/lrc.h."""
+    with open(HEADER) as fh:
+        text = fh.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]*?\b(lrc_\w+)\s*\(", text, flags=re.M)))
+
+
+def _check(rc: int):
+    if rc < 0:
+        raise LrcError(rc, lib().lrc_last_error().decode())
+    return rc
+
+
+def _prec_of(t) -> int:
+    import torch
+    m = {torch.float64: FP64, torch.float32: FP32, torch.float16: FP16}
+    if t.dtype not in m:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return m[t.dtype]
+
+
+def _dev(*ts):
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("tensors must be on the GPU")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous (row-major)")
+
+
+def _bind_stream(device=None):
+    import torch
+    st = torch.cuda.current_stream(device)
+    lib().lrc_set_stream(_vp(st.cuda_stream))
+
+
+# ------------------------------------------------------------------ API ---
+
+def storage_bytes(m: int, n: int, k: int, prec) -> int:
+    p = PREC_NAMES.get(prec, prec)
+    return _check(lib().lrc_storage_bytes(m, n, k, p))
+
+
+def tt_storage_bytes(dims, ranks, prec) -> int:
+    p = PREC_NAMES.get(prec, prec)
+    d = len(dims)
+    D = (_i64 * d)(*dims)
+    R = (_i64 * (d + 1))(*ranks)
+    return _check(lib().lrc_tt_storage_bytes(D, R, d, p))
+
+
+def apply_path(m: int, n: int, k: int, batch: int, prec) -> int:
+    p = PREC_NAMES.get(prec, prec)
+    return _check(lib().lrc_matrix_apply_path(m, n, k, batch, p))
+
+
+def set_apply_path(path: int):
+    _check(lib().lrc_set_apply_path(path))
+
+
+def matrix_apply(U, s, V, X, Y=None):
+    """Y = U diag(s) (V^T X): U (m x k), s (k), V (n x k), X (n x batch)."""
+    import torch
+    _dev(U, s, V, X)
+    prec = _prec_of(U)
+    for t in (s, V, X):
+        if t.dtype != U.dtype:
+            raise TypeError("all factors and the batch must share one dtype")
+    m, k = U.shape
+    n, b = X.shape
+    if V.shape != (n, k) or s.shape != (k,):
+        raise ValueError("shape mismatch")
+    if Y is None:
+        Y = torch.empty((m, b), dtype=U.dtype, device=U.device)
+    _dev(Y)
+    _bind_stream(U.device)
+    _check(lib().lrc_matrix_apply(U.data_ptr(), s.data_ptr(), V.data_ptr(), X.data_ptr(), Y.data_ptr(),
+                                  m, n, k, b, prec))
+    return Y
+
+
+def tt_shape(cores):
+    dims = [int(c.shape[1]) for c in cores]
+    ranks = [int(cores[0].shape[0])] + [int(c.shape[2]) for c in cores]
+    return dims, ranks
+
+
+def tt_reconstruct(cores, out=None):
+    """Dense tensor (C order) from TT cores G_l of shape (r_{l-1}, n_l, r_l)."""
+    import torch
+    _dev(*cores)
+    prec = _prec_of(cores[0])
+    dims, ranks = tt_shape(cores)
+    d = len(cores)
+    if out is None:
+        out = torch.empty(dims, dtype=cores[0].dtype, device=cores[0].device)
+    _dev(out)
+    ptrs = (_vp * d)(*[c.data_ptr() for c in cores])
+    D = (_i64 * d)(*dims)
+    R = (_i64 * (d + 1))(*ranks)
+    _bind_stream(cores[0].device)
+    _check(lib().lrc_tt_reconstruct(ptrs, D, R, d, out.data_ptr(), prec))
+    return out
+
+
+def _result(res: CertResult) -> dict:
+    out = {f: getattr(res, f) for f, _ in CertResult._fields_}
+    for f in ("certified", "acc_nonincrease", "acc_win", "mem_win", "practical_win"):
+        out[f] = bool(out[f])
+    return out
+
+
+def certify_matrix(sigma, U, s, V, Uh, sh, Vh, k: int, A=None) -> dict:
+    """Matrix certificate for base rank k (FP64) vs rank k+1 stored as
+    (Uh, sh, Vh).  sigma: host sequence of singular values."""
+    import numpy as np
+    _dev(U, s, V, Uh, sh, Vh)
+    if A is not None:
+        _dev(A)
+    sig = np.ascontiguousarray(np.asarray(sigma, dtype=np.float64))
+    a = CertArgs()
+    a.kind = CERT_MATRIX
+    a.prec = _prec_of(Uh)
+    a.m, a.n, a.k = int(U.shape[0]), int(V.shape[0]), int(k)
+    a.sigma = sig.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    a.n_sigma = len(sig)
+    a.U, a.s, a.V = U.data_ptr(), s.data_ptr(), V.data_ptr()
+    a.Uh, a.sh, a.Vh = Uh.data_ptr(), sh.data_ptr(), Vh.data_ptr()
+    a.A = A.data_ptr() if A is not None else None
+    res = CertResult()
+    _bind_stream(U.device)
+    _check(lib().lrc_certify(ctypes.byref(a), ctypes.byref(res)))
+    return _result(res)
+
+
+def certify_tt(T, base_cores, aug_cores, aug_cores_h) -> dict:
+    """TT certificate: T dense FP64; FP64 base and augmented cores; the
+    augmented cores as stored (FP32 or FP16)."""
+    _dev(T, *base_cores, *aug_cores, *aug_cores_h)
+    d = len(base_cores)
+    dims, rb = tt_shape(base_cores)
+    _, ra = tt_shape(aug_cores)
+    a = CertArgs()
+    a.kind = CERT_TT
+    a.prec = _prec_of(aug_cores_h[0])
+    a.d = d
+    D = (_i64 * d)(*dims)
+    RB = (_i64 * (d + 1))(*rb)
+    RA = (_i64 * (d + 1))(*ra)
+    PB = (_vp * d)(*[c.data_ptr() for c in base_cores])
+    PA = (_vp * d)(*[c.data_ptr() for c in aug_cores])
+    PH = (_vp * d)(*[c.data_ptr() for c in aug_cores_h])
+    a.dims, a.ranks_base, a.ranks_aug = D, RB, RA
+    a.cores_base, a.cores_aug, a.cores_aug_h = PB, PA, PH
+    a.T = T.data_ptr()
+    res = CertResult()
+    _bind_stream(T.device)
+    _check(lib().lrc_certify(ctypes.byref(a), ctypes.byref(res)))
+    return _result(res)
+
+
+def shutdown():
+    lib().lrc_shutdown()

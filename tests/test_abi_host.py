@@ -1,0 +1,131 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/lrc.h declares, computes storage counts exactly, and
+rejects bad arguments before touching the device."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_12969_amd import lrc
+
+L = None
+
+
+def setup_module():
+    global L
+    L = lrc.lib()
+
+
+def test_exports_every_declared_symbol():
+    declared = lrc.header_symbols()
+    assert len(declared) >= 11
+    for name in declared:
+        assert hasattr(L, name), name
+    assert L.lrc_version() == 1
+
+
+@pytest.mark.parametrize("m,n,k", [(512, 256, 20), (8192, 8192, 257), (65536, 4096, 513), (1, 1, 1)])
+def test_storage_bytes_match_oracle(m, n, k):
+    for prec in ("fp64", "fp32", "fp16"):
+        assert lrc.storage_bytes(m, n, k, prec) == O.storage_bytes(m, n, k, prec)
+
+
+def test_tt_storage_bytes_match_oracle():
+    cases = [((145, 145, 200), (1, 32, 32, 1)), ((16,) * 6, (1, 9, 17, 25, 17, 9, 1)), ((7,), (1, 1))]
+    for dims, ranks in cases:
+        for prec in ("fp64", "fp32", "fp16"):
+            assert lrc.tt_storage_bytes(dims, ranks, prec) == O.tt_storage_bytes(dims, ranks, prec)
+
+
+def test_storage_overflow_and_invalid():
+    assert L.lrc_storage_bytes(2 ** 62, 2 ** 62, 10, 0) == -2
+    assert L.lrc_storage_bytes(10, 10, 3, 7) == -1
+    with pytest.raises(lrc.LrcError):
+        lrc.tt_storage_bytes((4, 5), (2, 3, 1), "fp64")      # ranks[0] != 1
+
+
+def test_apply_path_dispatch():
+    assert lrc.apply_path(8192, 8192, 257, 1, "fp16") == lrc.PATH_STREAM
+    assert lrc.apply_path(8192, 8192, 257, 8, "fp64") == lrc.PATH_STREAM
+    assert lrc.apply_path(8192, 8192, 257, 9, "fp32") == lrc.PATH_MFMA
+    assert lrc.apply_path(8192, 8192, 257, 4096, "fp16") == lrc.PATH_MFMA
+    assert L.lrc_matrix_apply_path(10, 10, 11, 4, 0) == -1   # k > min(m, n)
+    assert L.lrc_set_apply_path(3) == -1
+    assert L.lrc_set_apply_path(0) == 0
+
+
+def _apply(ptrs, m, n, k, b, prec):
+    return L.lrc_matrix_apply(*ptrs, m, n, k, b, prec)
+
+
+def test_apply_argument_errors():
+    good = [0x10000, 0x20000, 0x30000, 0x40000, 0x90000000]
+    assert _apply([0] + good[1:], 10, 10, 3, 4, 0) == -1                 # NULL
+    assert _apply(good, 0, 10, 3, 4, 0) == -1                           # m < 1
+    assert _apply(good, 10, 10, 0, 4, 0) == -1                          # k < 1
+    assert _apply(good, 10, 10, 11, 4, 0) == -1                         # k > min(m, n)
+    assert _apply(good, 10, 10, 3, 0, 0) == -1                          # batch < 1
+    assert _apply(good, 10, 10, 3, 4, 5) == -1                          # bad precision
+    assert _apply(good, 2 ** 40, 2 ** 40, 3, 2 ** 40, 0) == -2          # overflow
+    overl = [0x10000, 0x20000, 0x30000, 0x40000, 0x10008]               # Y overlaps U
+    assert _apply(overl, 10, 10, 3, 4, 0) == -1
+    assert b"overlaps" in L.lrc_last_error()
+
+
+def _tt(dims, ranks, d, prec=0, cores=None, out=0x90000000):
+    D = (ctypes.c_int64 * max(1, len(dims)))(*dims)
+    R = (ctypes.c_int64 * max(1, len(ranks)))(*ranks)
+    if cores is None:
+        cores = [0x10000 * (i + 1) for i in range(max(1, d))]
+    P = (ctypes.c_void_p * len(cores))(*cores)
+    return L.lrc_tt_reconstruct(P, D, R, d, out, prec)
+
+
+def test_tt_argument_errors():
+    assert _tt((4, 5), (1, 3, 1), 0) == -1                  # d < 1
+    assert _tt((4, 5), (1, 3, 1), 17) == -1                 # d > max
+    assert _tt((4, 5), (2, 3, 1), 2) == -1                  # ranks[0] != 1
+    assert _tt((4, 5), (1, 3, 2), 2) == -1                  # ranks[d] != 1
+    assert _tt((4, 0), (1, 3, 1), 2) == -1                  # dim < 1
+    assert _tt((4, 5), (1, 0, 1), 2) == -1                  # rank < 1
+    assert _tt((4, 5), (1, 513, 1), 2) == -1                # rank above the limit
+    assert _tt((4, 5), (1, 3, 1), 2, prec=9) == -1          # bad precision
+    assert _tt((4, 5), (1, 3, 1), 2, cores=[0x10000, 0]) == -1
+    assert _tt((2 ** 40, 2 ** 40), (1, 3, 1), 2) == -2      # entry count overflow
+    assert _tt((4, 5), (1, 3, 1), 2, out=0x10008) == -1     # output overlaps a core
+
+
+def test_certify_argument_errors():
+    a = lrc.CertArgs()
+    r = lrc.CertResult()
+    a.kind = 5
+    a.prec = 1
+    assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
+    a.kind = lrc.CERT_MATRIX
+    a.m, a.n, a.k = 10, 8, 8                                 # k + 1 > min(m, n)
+    sig = np.linspace(1, 0.1, 8)
+    a.sigma = sig.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    a.n_sigma = 8
+    assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
+    a.k = 3
+    a.U = a.s = a.V = a.Uh = a.sh = a.Vh = 0x10000
+    bad = np.array([1.0, 2.0, 0.5, 0.1])                      # not non-increasing
+    a.sigma = bad.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    a.n_sigma = 4
+    assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
+    assert b"non-increasing" in L.lrc_last_error()
+    a.kind = lrc.CERT_TT
+    a.d = 0
+    assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
+
+
+def test_valid_call_without_gpu_reports_no_device():
+    try:
+        import torch
+        if torch.cuda.is_available():
+            pytest.skip("a GPU is present")
+    except ImportError:
+        pass
+    good = [0x10000, 0x20000, 0x30000, 0x40000, 0x90000000]
+    assert _apply(good, 10, 10, 3, 4, 0) == -5
