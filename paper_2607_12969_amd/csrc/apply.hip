@@ -48,7 +48,7 @@ template <> struct ApplyCfg<half_t> { using C = Cfg<half_t, 64, 64, 32, 2, 2>; }
 
 // One BK step of MFMAs on LDS tiles As[BM][LDK] (rows = m) and Bs[BN][LDK]
 // (rows = n).  acc[fn][fm][v] = C[m = wm*WTM + fm*16 + (lane&15)]
-//                                [n = wn*WTN + fn*16 + 4*(lane>>4) + v].
+//                                [n = wn*WTN + fn*16 + acc_row<T>(lane>>4, v)].
 template <class C, typename T>
 __device__ __forceinline__ void mma_tile(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM],
                                          int wm, int wn, int lane) {
@@ -197,7 +197,7 @@ __global__ __launch_bounds__(C::NT) void k_atb(
             const int64_t mm = m0 + wm * C::WTM + fm * 16 + r;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int64_t nn = n0 + wn * C::WTN + fn * 16 + 4 * g + v;
+                const int64_t nn = n0 + wn * C::WTN + fn * 16 + acc_row<T>(g, v);
                 if (MODE == ATB_APPLY) {
                     if (nn < N && mm < Mout) {
                         const Acc sm = (mm < M) ? to_acc(svals[mm]) : Acc(0);
@@ -259,19 +259,21 @@ __global__ __launch_bounds__(C::NT) void k_abt(
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm) {
                 const int64_t mm = m0 + wm * C::WTM + fm * 16 + r;
-                const int64_t nn = n0 + wn * C::WTN + fn * 16 + 4 * g;
+                const int64_t nb = n0 + wn * C::WTN + fn * 16;
                 if (mm >= M) continue;
-                T* dst = Y + mm * ldy + nn;
-                if (vec4 && nn + 3 < N) {
+                T* dst = Y + mm * ldy + nb;
+                if (AccRowsContiguous<T>::value && vec4 && nb + 4 * g + 3 < N) {
                     typedef T vec_t __attribute__((ext_vector_type(4)));
                     vec_t w;
 #pragma unroll
                     for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[fn][fm][v]);
-                    *reinterpret_cast<vec_t*>(dst) = w;
+                    *reinterpret_cast<vec_t*>(dst + 4 * g) = w;
                 } else {
 #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        if (nn + v < N) dst[v] = to_storage<T>(acc[fn][fm][v]);
+                    for (int v = 0; v < 4; ++v) {
+                        const int row = acc_row<T>(g, v);
+                        if (nb + row < N) dst[row] = to_storage<T>(acc[fn][fm][v]);
+                    }
                 }
             }
     } else {
@@ -283,7 +285,7 @@ __global__ __launch_bounds__(C::NT) void k_abt(
                 const int64_t mm = m0 + wm * C::WTM + fm * 16 + r;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int64_t nn = n0 + wn * C::WTN + fn * 16 + 4 * g + v;
+                    const int64_t nn = n0 + wn * C::WTN + fn * 16 + acc_row<T>(g, v);
                     if (mm < M && nn < N) {
                         const double dlt = Aref[mm * ldr + nn] - (double)acc[fn][fm][v];
                         sum += dlt * dlt;

@@ -7,9 +7,11 @@
 //   the K slice it supplies is [(l >> 4) * KPL, (l >> 4) * KPL + KPL) of the
 //   step, the same slice for A and B, so the sum over K is exact whatever
 //   order the hardware uses inside the step;
-//   lane l receives D[4 * (l >> 4) + v][l & 15], v = 0..3.
-// Kernels orient the MFMA so that the four values a lane receives are
-// consecutive in the output's contiguous dimension.
+//   lane l receives D[row][l & 15] for v = 0..3 with row = acc_row<T>(l >> 4, v):
+//   4 * (l >> 4) + v for the f32 and f16 instructions (four consecutive rows)
+//   but (l >> 4) + 4 * v for v_mfma_f64_16x16x4_f64 (rows strided by 4).
+// Kernels orient the MFMA so that the rows of D run along the output's
+// contiguous dimension, so f32/f16 lanes hold four consecutive outputs.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -60,6 +62,14 @@ __device__ __forceinline__ float4_t mfma(float a, float b, float4_t c) {
 __device__ __forceinline__ float4_t mfma(half8_t a, half8_t b, float4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
+
+// Row of the 16 x 16 MFMA result held in accumulator element v by lane
+// group g = lane >> 4 (see the convention above).
+template <typename T> __device__ __forceinline__ int acc_row(int g, int v) { return 4 * g + v; }
+template <> __device__ __forceinline__ int acc_row<double>(int g, int v) { return g + 4 * v; }
+// true when a lane's four accumulator rows are consecutive
+template <typename T> struct AccRowsContiguous { static constexpr bool value = true; };
+template <> struct AccRowsContiguous<double> { static constexpr bool value = false; };
 
 template <typename T>
 __device__ __forceinline__ typename PrecTraits<T>::frag load_frag(const T* p);

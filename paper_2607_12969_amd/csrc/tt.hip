@@ -11,8 +11,8 @@
 //   2. the middle contraction Z_{d-1}(L, i) = Z_{d-2}(L) G_{d-1}(i) for BI
 //      middle indices i, on the matrix cores, into LDS;
 //   3. the last contraction out(L, i, :) = Z_{d-1}(L, i) G_d, on the matrix
-//      cores, stored straight from the accumulators, four consecutive
-//      outputs per lane.
+//      cores, stored straight from the accumulators (four consecutive
+//      outputs per lane for FP32/FP16).
 // Only the cores are read and only the tensor is written: no interface
 // matrix goes to HBM.  For FP16 the accumulation is FP32 and the interface
 // Z_{d-1} is rounded once to FP16 as the input of the last product; the
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
                 T* dst = Zf + (Lr * a.BI + il) * a.Kp3;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int t = tb * 16 + 4 * g + v;
+                    const int t = tb * 16 + acc_row<T>(g, v);
                     if (t < tcap) dst[t] = to_storage<T>(acc[v]);
                 }
             }
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
                     }
                 }
             }
-            const int64_t cc = (int64_t)cbk * 16 + 4 * g;
+            const int64_t cb0 = (int64_t)cbk * 16;
 #pragma unroll
             for (int pb = 0; pb < 4; ++pb) {
                 if (pb >= n_pb) continue;
@@ -264,17 +264,19 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
                 const int Lr = p / a.BI, il = p % a.BI;
                 const int64_t L = L0 + Lr, i = i0 + il;
                 if (Lr >= a.BL || L >= a.NL || i >= a.n_mid) continue;
-                T* dst = static_cast<T*>(a.out) + (L * a.n_mid + i) * a.n_last + cc;
-                if (a.vec4 && cc + 3 < a.n_last) {
+                T* dst = static_cast<T*>(a.out) + (L * a.n_mid + i) * a.n_last + cb0;
+                if (AccRowsContiguous<T>::value && a.vec4 && cb0 + 4 * g + 3 < a.n_last) {
                     typedef T vec_t __attribute__((ext_vector_type(4)));
                     vec_t w;
 #pragma unroll
                     for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[pb][v]);
-                    *reinterpret_cast<vec_t*>(dst) = w;
+                    *reinterpret_cast<vec_t*>(dst + 4 * g) = w;
                 } else {
 #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        if (cc + v < a.n_last) dst[v] = to_storage<T>(acc[pb][v]);
+                    for (int v = 0; v < 4; ++v) {
+                        const int row = acc_row<T>(g, v);
+                        if (cb0 + row < a.n_last) dst[row] = to_storage<T>(acc[pb][v]);
+                    }
                 }
             }
         }
