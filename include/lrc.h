@@ -232,6 +232,21 @@ const char* lrc_last_error(void);
  * again.  No call may be in flight. */
 void lrc_shutdown(void);
 
+/*
+ * Kernel timing (measurement tools).  While enabled, the library records a
+ * pair of hipEvents on the launch stream around every kernel it launches,
+ * labelled by kernel ("apply_p2_mfma_f16", "tt_fused_f64", ...); the extra
+ * event records cost a few microseconds per launch.  lrc_profile_read
+ * waits for the recorded events and returns the number of launches and the
+ * summed elapsed milliseconds for one label (0 and 0.0 if unseen).
+ * lrc_profile_labels writes the comma-separated labels seen so far into buf
+ * (truncated to len-1 characters) and returns the full length.
+ */
+int lrc_profile_enable(int on);
+void lrc_profile_reset(void);
+int lrc_profile_read(const char* label, int64_t* launches, double* total_ms);
+int64_t lrc_profile_labels(char* buf, int64_t len);
+
 /* LRC_VERSION of the built library. */
 int lrc_version(void);
 

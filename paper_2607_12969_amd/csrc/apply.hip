@@ -455,6 +455,20 @@ size_t apply_workspace_bytes(const ApplyPlan& p) {
     return round_up(p.part_bytes, 256) + round_up(p.mid_bytes, 256);
 }
 
+template <typename T> static const char* p1_stream_label();
+template <typename T> static const char* p2_stream_label();
+template <typename T> static const char* p1_mfma_label();
+template <typename T> static const char* p2_mfma_label();
+#define LRC_LABELS(T, S)                                                          \
+    template <> const char* p1_stream_label<T>() { return "apply_p1_stream_" S; } \
+    template <> const char* p2_stream_label<T>() { return "apply_p2_stream_" S; } \
+    template <> const char* p1_mfma_label<T>() { return "apply_p1_mfma_" S; }     \
+    template <> const char* p2_mfma_label<T>() { return "apply_p2_mfma_" S; }
+LRC_LABELS(double, "f64")
+LRC_LABELS(float, "f32")
+LRC_LABELS(half_t, "f16")
+#undef LRC_LABELS
+
 template <typename T>
 static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const T* V, const T* X,
                               T* Y, int64_t m, int64_t n, int64_t k, int64_t b, Workspace& ws,
@@ -467,13 +481,17 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     const int64_t ldt = p.Kp;
     if (p.path == 1) {
         dim3 g1(p.tiles_m, p.splits);
+        {
+            KernelTimer t1(p1_stream_label<T>(), stream);
 #define LRC_P1S(NB) hipLaunchKernelGGL((k_p1_stream<T, NB>), g1, dim3(256), 0, stream, V, X, s, Tt, ldt, part, counters, n, k, b, p.chunk, p.splits)
-        if (b <= 1) LRC_P1S(1); else if (b <= 2) LRC_P1S(2); else if (b <= 4) LRC_P1S(4); else LRC_P1S(8);
+            if (b <= 1) LRC_P1S(1); else if (b <= 2) LRC_P1S(2); else if (b <= 4) LRC_P1S(4); else LRC_P1S(8);
 #undef LRC_P1S
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t rows_per_wg = 16;
         dim3 g2((unsigned)((m + rows_per_wg - 1) / rows_per_wg));
+        KernelTimer t2(p2_stream_label<T>(), stream);
 #define LRC_P2S(NB) hipLaunchKernelGGL((k_p2_stream<T, NB>), g2, dim3(256), (size_t)k * NB * sizeof(Acc), stream, U, Tt, ldt, Y, m, k, b)
         if (b <= 1) LRC_P2S(1); else if (b <= 2) LRC_P2S(2); else if (b <= 4) LRC_P2S(4); else LRC_P2S(8);
 #undef LRC_P2S
@@ -481,11 +499,15 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     }
     using C = typename ApplyCfg<T>::C;
     dim3 g1(p.tiles_n, p.tiles_m, p.splits);
+    {
+    KernelTimer t1(p1_mfma_label<T>(), stream);
     hipLaunchKernelGGL((k_atb<T, C, ATB_APPLY>), g1, dim3(C::NT), 0, stream, V, k, X, b, k, b, n,
                        p.chunk, p.splits, part, counters, s, (void*)Tt, ldt, ldt);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g2((unsigned)((b + C::BN - 1) / C::BN), (unsigned)((m + C::BM - 1) / C::BM));
+    KernelTimer t2(p2_mfma_label<T>(), stream);
     const int vec4 = (b % 4 == 0) && ((reinterpret_cast<uintptr_t>(Y) % (4 * sizeof(T))) == 0);
     hipLaunchKernelGGL((k_abt<T, C, ABT_STORE>), g2, dim3(C::NT), 0, stream, U, k, m, k, (const T*)Tt,
                        ldt, b, ldt, ldt, Y, b, vec4, (const double*)nullptr, (int64_t)0, (double*)nullptr);
@@ -540,6 +562,7 @@ hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G, W
     double* part = static_cast<double*>(ws.take((size_t)t * t * sp * 64 * 64 * sizeof(double)));
     if (ws.overrun || (sp > 1 && ws.n_counters < (size_t)t * t)) return hipErrorOutOfMemory;
     dim3 g(t, t, sp);
+    KernelTimer tm("cert_gram_f64", stream);
     hipLaunchKernelGGL((k_atb<double, GramC, ATB_GRAM>), g, dim3(GramC::NT), 0, stream, P, cols, P, cols,
                        cols, cols, rows, ch, sp, part, ws.counters, (const double*)nullptr, (void*)G, cols,
                        cols);
@@ -555,6 +578,7 @@ hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, 
     dim3 g((unsigned)((n + 63) / 64), (unsigned)((m + 63) / 64));
     *nparts = (int64_t)g.x * g.y;
     const int64_t K = round_up(r, GramC::BK);
+    KernelTimer tm("cert_err_dense_f64", stream);
     hipLaunchKernelGGL((k_abt<double, GramC, ABT_ERR>), g, dim3(GramC::NT), 0, stream, W, r, m, r, Vw, r, n, r,
                        K, (double*)nullptr, (int64_t)0, 0, A, n, part);
     return hipGetLastError();

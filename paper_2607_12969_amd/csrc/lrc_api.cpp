@@ -179,11 +179,68 @@ int tt_reconstruct_impl(const void* const* cores, const int64_t* dims, const int
         hipError_t e = ws.reserve(plan.stage_bytes, 0, st);
         if (e != hipSuccess) return fail_hip(e, "workspace");
     }
-    hipError_t e = launch_tt(plan, cores, out, ws, st);
+    hipError_t e = launch_tt(plan, cores, out, ws, st, ws_override ? "cert_tt_fused_f64" : nullptr);
     return e == hipSuccess ? LRC_OK : fail_hip(e, "TT reconstruction launch");
 }
 
 }  // namespace
+
+// ------------------------------------------------------- kernel timing ---
+namespace {
+std::mutex g_pmu;
+bool g_prof = false;
+struct PendingTime {
+    std::string label;
+    hipEvent_t a, b;
+};
+std::vector<PendingTime> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+std::map<std::string, std::pair<int64_t, double>> g_times;
+
+hipEvent_t pool_event() {
+    if (!g_event_pool.empty()) {
+        hipEvent_t e = g_event_pool.back();
+        g_event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+int drain_times() {
+    for (auto& p : g_pending) {
+        float ms = 0.0f;
+        hipError_t e = hipEventSynchronize(p.b);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.a, p.b);
+        if (e != hipSuccess) return fail_hip(e, "kernel timing");
+        auto& slot = g_times[p.label];
+        slot.first += 1;
+        slot.second += ms;
+        g_event_pool.push_back(p.a);
+        g_event_pool.push_back(p.b);
+    }
+    g_pending.clear();
+    return LRC_OK;
+}
+}  // namespace
+
+namespace lrc {
+KernelTimer::KernelTimer(const char* lbl, hipStream_t s) : label(lbl), stream(s), start(nullptr) {
+    std::lock_guard<std::mutex> lk(g_pmu);
+    if (!g_prof) return;
+    hipEvent_t e = pool_event();
+    if (e && hipEventRecord(e, s) == hipSuccess) start = e;
+}
+
+KernelTimer::~KernelTimer() {
+    if (!start) return;
+    std::lock_guard<std::mutex> lk(g_pmu);
+    hipEvent_t e = pool_event();
+    if (e && hipEventRecord(e, stream) == hipSuccess)
+        g_pending.push_back(PendingTime{label, static_cast<hipEvent_t>(start), e});
+}
+}  // namespace lrc
 
 // ------------------------------------------------------------- Workspace --
 namespace lrc {
@@ -343,6 +400,45 @@ int64_t lrc_tt_storage_bytes(const int64_t* dims, const int64_t* ranks, int d, i
     int64_t c = tt_count(dims, ranks, d), t;
     if (c < 0 || !mul_ok(c, elem_bytes(prec), &t)) return fail(LRC_EOVERFLOW, "overflow");
     return t;
+}
+
+int lrc_profile_enable(int on) {
+    std::lock_guard<std::mutex> lk(g_pmu);
+    g_prof = on != 0;
+    return LRC_OK;
+}
+
+void lrc_profile_reset(void) {
+    std::lock_guard<std::mutex> lk(g_pmu);
+    (void)drain_times();
+    g_times.clear();
+}
+
+int lrc_profile_read(const char* label, int64_t* launches, double* total_ms) {
+    if (!label || !launches || !total_ms) return fail(LRC_EINVAL, "NULL argument");
+    std::lock_guard<std::mutex> lk(g_pmu);
+    int rc = drain_times();
+    if (rc) return rc;
+    auto it = g_times.find(label);
+    *launches = it == g_times.end() ? 0 : it->second.first;
+    *total_ms = it == g_times.end() ? 0.0 : it->second.second;
+    return LRC_OK;
+}
+
+int64_t lrc_profile_labels(char* buf, int64_t len) {
+    std::lock_guard<std::mutex> lk(g_pmu);
+    int rc = drain_times();
+    if (rc) return rc;
+    std::string all;
+    for (auto& kv : g_times) {
+        if (!all.empty()) all += ",";
+        all += kv.first;
+    }
+    if (buf && len > 0) {
+        std::strncpy(buf, all.c_str(), (size_t)len - 1);
+        buf[len - 1] = 0;
+    }
+    return (int64_t)all.size();
 }
 
 void lrc_shutdown(void) {

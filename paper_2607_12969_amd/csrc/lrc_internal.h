@@ -32,6 +32,19 @@ struct Workspace {
     void release();
 };
 
+// Kernel timing: when enabled (lrc_profile_enable), a pair of hipEvents is
+// recorded on the launch stream around every kernel the library launches,
+// keyed by a kernel label; lrc_profile_read sums the elapsed times.
+struct KernelTimer {
+    KernelTimer(const char* label, hipStream_t stream);
+    ~KernelTimer();
+    KernelTimer(const KernelTimer&) = delete;
+    KernelTimer& operator=(const KernelTimer&) = delete;
+    const char* label;
+    hipStream_t stream;
+    void* start;   // hipEvent_t, or nullptr when profiling is off
+};
+
 // ---------------------------------------------------------------- apply ---
 struct ApplyPlan {
     int path;            // LRC_PATH_STREAM or LRC_PATH_MFMA
@@ -111,7 +124,8 @@ struct TTPlan {
 // buffers (max_lds = the device's per-workgroup LDS limit).
 int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* ranks, int d, int prec, size_t max_lds);
 
+// `label` names the launch for the kernel timers (nullptr: "tt_fused_<type>").
 hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Workspace& ws,
-                     hipStream_t stream);
+                     hipStream_t stream, const char* label = nullptr);
 
 }  // namespace lrc

@@ -59,6 +59,7 @@ static unsigned grid_for(int64_t total) {
 hipError_t launch_diff_factors(const double* ref, const void* h, int prec, int64_t rows, int64_t r, double* P,
                                hipStream_t stream) {
     const unsigned g = grid_for(rows * r);
+    KernelTimer tm("cert_diff_factors", stream);
     if (prec == P64)
         hipLaunchKernelGGL(k_diff_factors<double>, dim3(g), dim3(256), 0, stream, ref, (const double*)h, rows, r, P);
     else if (prec == P32)
@@ -71,6 +72,7 @@ hipError_t launch_diff_factors(const double* ref, const void* h, int prec, int64
 hipError_t launch_widen_scaled(const void* h, const void* hs, int prec, int64_t rows, int64_t r, double* W,
                                hipStream_t stream) {
     const unsigned g = grid_for(rows * r);
+    KernelTimer tm("cert_widen", stream);
     if (prec == P64)
         hipLaunchKernelGGL(k_widen_scaled<double>, dim3(g), dim3(256), 0, stream, (const double*)h, (const double*)hs, rows, r, W);
     else if (prec == P32)
@@ -82,6 +84,7 @@ hipError_t launch_widen_scaled(const void* h, const void* hs, int prec, int64_t 
 
 hipError_t launch_widen(const void* src, int prec, int64_t count, double* out, hipStream_t stream) {
     const unsigned g = grid_for(count);
+    KernelTimer tm("cert_widen", stream);
     if (prec == P64)
         hipLaunchKernelGGL(k_widen<double>, dim3(g), dim3(256), 0, stream, (const double*)src, count, out);
     else if (prec == P32)
@@ -131,6 +134,7 @@ int64_t sumsq5_groups(int64_t count) {
 
 hipError_t launch_sumsq5(const double* T, const double* a, const double* b, const double* c, int64_t count,
                          double* part, int64_t groups, hipStream_t stream) {
+    KernelTimer tm("cert_sumsq5_f64", stream);
     hipLaunchKernelGGL(k_sumsq5, dim3((unsigned)groups), dim3(256), 0, stream, T, a, b, c, count, part);
     return hipGetLastError();
 }
@@ -150,6 +154,7 @@ __global__ __launch_bounds__(256) void k_reduce_rows(const double* __restrict__ 
 }
 
 hipError_t launch_reduce_rows(const double* part, int64_t count, int nsums, double* out, hipStream_t stream) {
+    KernelTimer tm("cert_reduce_rows", stream);
     hipLaunchKernelGGL(k_reduce_rows, dim3(nsums), dim3(256), 0, stream, part, count, out);
     return hipGetLastError();
 }

@@ -345,7 +345,7 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* ranks, int d, int pre
 
 template <typename T>
 static hipError_t tt_typed(const TTPlan& p, const void* const* cores, void* out, Workspace& ws,
-                           hipStream_t stream) {
+                           hipStream_t stream, const char* label) {
     TTArgs a{};
     a.d = p.d;
     for (int c = 0; c < p.d; ++c) {
@@ -383,6 +383,7 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* cores, void* out,
         const int64_t tot = p.n_mid * p.Rt * p.Kp2 + p.n_last * p.Kp3;
         int64_t gs = (tot + 255) / 256;
         if (gs > 2048) gs = 2048;
+        KernelTimer ts("tt_stage_f16", stream);
         hipLaunchKernelGGL(k_stage_f16, dim3((unsigned)gs), dim3(256), 0, stream, (const half_t*)cores[p.d - 2],
                            (const half_t*)cores[p.d - 1], smid, slast, p.n_mid, p.n_last, p.rL, p.rM, p.Kp2, p.Kp3,
                            p.Rt);
@@ -392,14 +393,17 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* cores, void* out,
         a.st_last = slast;
     }
     dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
+    if (!label) label = p.prec == P64 ? "tt_fused_f64" : (p.prec == P32 ? "tt_fused_f32" : "tt_fused_f16");
+    KernelTimer tk(label, stream);
     hipLaunchKernelGGL(k_tt_fused<T>, grid, dim3(256), p.lds_bytes, stream, a);
     return hipGetLastError();
 }
 
-hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Workspace& ws, hipStream_t stream) {
-    if (p.prec == P64) return tt_typed<double>(p, cores, out, ws, stream);
-    if (p.prec == P32) return tt_typed<float>(p, cores, out, ws, stream);
-    return tt_typed<half_t>(p, cores, out, ws, stream);
+hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Workspace& ws, hipStream_t stream,
+                     const char* label) {
+    if (p.prec == P64) return tt_typed<double>(p, cores, out, ws, stream, label);
+    if (p.prec == P32) return tt_typed<float>(p, cores, out, ws, stream, label);
+    return tt_typed<half_t>(p, cores, out, ws, stream, label);
 }
 
 }  // namespace lrc

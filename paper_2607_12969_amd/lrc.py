@@ -99,6 +99,14 @@ def lib():
     L.lrc_shutdown.restype = None
     L.lrc_version.argtypes = []
     L.lrc_version.restype = ctypes.c_int
+    L.lrc_profile_enable.argtypes = [ctypes.c_int]
+    L.lrc_profile_enable.restype = ctypes.c_int
+    L.lrc_profile_reset.argtypes = []
+    L.lrc_profile_reset.restype = None
+    L.lrc_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(_i64), ctypes.POINTER(ctypes.c_double)]
+    L.lrc_profile_read.restype = ctypes.c_int
+    L.lrc_profile_labels.argtypes = [ctypes.c_char_p, _i64]
+    L.lrc_profile_labels.restype = _i64
     _lib = L
     return L
 
@@ -261,6 +269,28 @@ def certify_tt(T, base_cores, aug_cores, aug_cores_h) -> dict:
     _bind_stream(T.device)
     _check(lib().lrc_certify(ctypes.byref(a), ctypes.byref(res)))
     return _result(res)
+
+
+def profile_enable(on: bool = True):
+    _check(lib().lrc_profile_enable(1 if on else 0))
+
+
+def profile_reset():
+    lib().lrc_profile_reset()
+
+
+def profile_read() -> dict:
+    """{kernel label: (launches, total milliseconds)} for every label seen."""
+    L = lib()
+    n = _check(L.lrc_profile_labels(None, 0))
+    buf = ctypes.create_string_buffer(n + 1)
+    L.lrc_profile_labels(buf, n + 1)
+    out = {}
+    for lab in filter(None, buf.value.decode().split(",")):
+        cnt, ms = _i64(), ctypes.c_double()
+        _check(L.lrc_profile_read(lab.encode(), ctypes.byref(cnt), ctypes.byref(ms)))
+        out[lab] = (cnt.value, ms.value)
+    return out
 
 
 def shutdown():

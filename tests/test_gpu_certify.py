@@ -163,7 +163,8 @@ def test_tt_sixway_workload(lrc):
     """16^6 with exact TT ranks (8,16,24,16,8): E_R is at round-off, so the
     verdict is 'No' for both precisions; E_R itself is only compared to the
     size of the FP64 rounding noise."""
-    T = O.tt_full(synth.tt_sixway_cores())
+    from test_gpu_tt import sixway_tensor
+    T = sixway_tensor()
     base = O.tt_svd(T, ranks=[8, 16, 24, 16, 8])
     aug = O.left_orthogonalize(O.tt_svd(T, ranks=[9, 17, 25, 17, 9]))
     for prec in ("fp32", "fp16"):

@@ -96,10 +96,19 @@ def test_cube_workload(lrc, cube):
         _check(lrc, aug, prec, "256^3 compensated")
 
 
+def sixway_tensor():
+    """16^6 tensor of the rank-(8,16,24,16,8) generator cores, scaled to unit
+    root-mean-square entry: unscaled, its entries (median 6e-7) sit below the
+    FP16 normal range and rounding the exact result once to FP16 would
+    already cost 8e-3 in relative Frobenius norm."""
+    T = O.tt_full(synth.tt_sixway_cores())
+    return T * (np.sqrt(T.size) / O.fro(T))
+
+
 def test_sixway_workload(lrc):
     """16^6 from rank-(8,16,24,16,8) generator cores: FP64 at those ranks,
     FP32/FP16 at (9,17,25,17,9), both from TT-SVD."""
-    T = O.tt_full(synth.tt_sixway_cores())
+    T = sixway_tensor()
     base = O.tt_svd(T, ranks=[8, 16, 24, 16, 8])
     aug = O.left_orthogonalize(O.tt_svd(T, ranks=[9, 17, 25, 17, 9]))
     _check(lrc, base, "fp64", "16^6 base")
