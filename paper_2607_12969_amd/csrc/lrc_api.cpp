@@ -154,7 +154,7 @@ int check_tt_shape(const int64_t* dims, const int64_t* ranks, int d, int64_t* to
 }
 
 int tt_reconstruct_impl(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, void* out,
-                        int prec, Workspace* ws_override) {
+                        int prec) {
     int dev;
     size_t max_lds;
     int rc = current_device(&dev, &max_lds);
@@ -170,16 +170,15 @@ int tt_reconstruct_impl(const void* const* cores, const int64_t* dims, const int
         return e == hipSuccess ? LRC_OK : fail_hip(e, "copy of the single core");
     }
     TTPlan plan;
-    if (plan_tt(plan, dims, ranks, d, prec, max_lds) != 0)
+    const int64_t* rs[1] = {ranks};
+    if (plan_tt(plan, dims, rs, 1, d, prec, max_lds) != 0)
         return fail(LRC_EINVAL, "TT ranks (%lld into the last core) exceed the on-chip buffers of the fused kernel",
                     (long long)ranks[d - 1]);
-    Workspace& ws = ws_override ? *ws_override : workspace_for(dev, st);
-    if (!ws_override) {
-        ws.reset();
-        hipError_t e = ws.reserve(plan.stage_bytes, 0, st);
-        if (e != hipSuccess) return fail_hip(e, "workspace");
-    }
-    hipError_t e = launch_tt(plan, cores, out, ws, st, ws_override ? "cert_tt_fused_f64" : nullptr);
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t e0 = ws.reserve(plan.stage_bytes, 0, st);
+    if (e0 != hipSuccess) return fail_hip(e0, "workspace");
+    hipError_t e = launch_tt(plan, cores, out, ws, st);
     return e == hipSuccess ? LRC_OK : fail_hip(e, "TT reconstruction launch");
 }
 
@@ -381,7 +380,7 @@ int lrc_tt_reconstruct(const void* const* cores, const int64_t* dims, const int6
         const size_t cb = (size_t)ranks[l] * dims[l] * ranks[l + 1] * e;
         if (overlaps(out, (size_t)N * e, cores[l], cb)) return fail(LRC_EINVAL, "output overlaps cores[%d]", l);
     }
-    return tt_reconstruct_impl(cores, dims, ranks, d, out, prec, nullptr);
+    return tt_reconstruct_impl(cores, dims, ranks, d, out, prec);
 }
 
 int64_t lrc_storage_bytes(int64_t m, int64_t n, int64_t k, int prec) {
@@ -580,6 +579,27 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
     return LRC_OK;
 }
 
+// FP64 reconstruction into a caller-provided buffer on the calling thread's
+// stream (the FP64 kernel takes no workspace); used by the TT certificate.
+static int tt_into(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, double* out,
+                   Workspace& ws) {
+    hipStream_t st = g_stream;
+    if (d == 1) {
+        hipError_t e = hipMemcpyAsync(out, cores[0], (size_t)dims[0] * 8, hipMemcpyDeviceToDevice, st);
+        return e == hipSuccess ? LRC_OK : fail_hip(e, "copy of the single core");
+    }
+    int dev;
+    size_t max_lds;
+    int rc = current_device(&dev, &max_lds);
+    if (rc) return rc;
+    TTPlan plan;
+    const int64_t* rs[1] = {ranks};
+    if (plan_tt(plan, dims, rs, 1, d, LRC_FP64, max_lds) != 0)
+        return fail(LRC_EINVAL, "TT ranks exceed the on-chip buffers of the fused kernel");
+    hipError_t e = launch_tt(plan, cores, out, ws, st, "cert_tt_fused_f64");
+    return e == hipSuccess ? LRC_OK : fail_hip(e, "TT reconstruction launch");
+}
+
 static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
     const int d = a->d;
     int64_t N, Nb;
@@ -619,11 +639,11 @@ static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
     if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
     // FP64 reconstructions (the fused kernel needs no workspace in FP64)
     std::vector<const void*> cb(a->cores_base, a->cores_base + d), ca(a->cores_aug, a->cores_aug + d);
-    rc = tt_reconstruct_impl(cb.data(), a->dims, a->ranks_base, d, TR, LRC_FP64, &ws);
+    rc = tt_into(cb.data(), a->dims, a->ranks_base, d, TR, ws);
     if (rc) return rc;
-    rc = tt_reconstruct_impl(ca.data(), a->dims, a->ranks_aug, d, TRp, LRC_FP64, &ws);
+    rc = tt_into(ca.data(), a->dims, a->ranks_aug, d, TRp, ws);
     if (rc) return rc;
-    rc = tt_reconstruct_impl(wide.data(), a->dims, a->ranks_aug, d, Th, LRC_FP64, &ws);
+    rc = tt_into(wide.data(), a->dims, a->ranks_aug, d, Th, ws);
     if (rc) return rc;
     he = launch_sumsq5(a->T, TR, TRp, Th, N, part, groups, st);
     if (he == hipSuccess) he = launch_reduce_rows(part, groups, 5, sums, st);

@@ -100,19 +100,25 @@ hipError_t launch_reduce_rows(const double* part, int64_t count, int nsums, doub
 
 // ------------------------------------------------------------------- TT ---
 constexpr int kMaxD = 16;
+constexpr int kTTMaxSets = 1;
+
+struct TTPlanSet {
+    int64_t ranks[kMaxD + 1];
+    int rL, rM;          // r_{d-2}, r_{d-1}
+    int Kp2, Kp3;        // rL, rM rounded to the MFMA K step
+    int Rt;              // rM rounded up to 16 (row blocks of the middle product)
+};
 
 struct TTPlan {
     int d;
     int prec;
+    int nsets;           // core sets sharing one block layout (1)
     int64_t dims[kMaxD];
-    int64_t ranks[kMaxD + 1];
+    TTPlanSet set[kTTMaxSets];
     int64_t NL;          // rows of the left interface Z_{d-2} (1 when d <= 2)
     int64_t n_mid;       // n_{d-1}
     int64_t n_last;      // n_d
-    int rL, rM;          // r_{d-2}, r_{d-1}
-    int Kp2, Kp3;        // rL, rM rounded to the MFMA K step
-    int Rt;              // rM rounded up to 16 (row blocks of the middle product)
-    int BL, BI, P;       // left rows and middle indices per block, P = BL * BI
+    int BL, BI, P;       // left rows and middle indices per block, P = BL * BI rounded to 16
     int64_t num_i_blocks, num_L_blocks;
     int grid_L;          // workgroups along the left index (each loops over L blocks)
     int chain_rmax;      // largest rank among levels 1..d-2 (chain buffers)
@@ -120,9 +126,11 @@ struct TTPlan {
     size_t stage_bytes;  // staged (transposed, padded) FP16 operands
 };
 
-// Returns 0, or -1 when the ranks do not fit the fused kernel's on-chip
-// buffers (max_lds = the device's per-workgroup LDS limit).
-int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* ranks, int d, int prec, size_t max_lds);
+// rank_sets[q] is the rank vector (d+1 entries) of core set q.  Returns 0,
+// or -1 when the ranks do not fit the fused kernel's on-chip buffers
+// (max_lds = the device's per-workgroup LDS limit).
+int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int nsets, int d, int prec,
+            size_t max_lds);
 
 // `label` names the launch for the kernel timers (nullptr: "tt_fused_<type>").
 hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Workspace& ws,
