@@ -22,6 +22,10 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 def flags():
     return ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            # keep matrix-core accumulators in ordinary VGPRs: the default AGPR
+            # form copies every loop-carried accumulator out and back each
+            # iteration, which halves the FP64 matrix-core rate
+            "-mllvm", "-amdgpu-mfma-vgpr-form=1",
             "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 

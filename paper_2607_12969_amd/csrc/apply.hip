@@ -14,9 +14,14 @@
 //   streaming  batch <= 8: one lane per column of V (phase 1) and wavefront
 //              dot products with a butterfly reduction over rows of U
 //              (phase 2); the factors are read once, coalesced.
-//   MFMA       otherwise: 64 x 64 output tiles on the 16x16 matrix cores
-//              (f64 16x16x4, f32 16x16x4, f16 16x16x32 with FP32 accumulation),
-//              operands staged through LDS, register double-buffered.
+//   MFMA       otherwise: 128 x 128 (large shapes) or 64 x 64 output tiles
+//              on the 16x16 matrix cores (f64 16x16x4, f32 16x16x4, f16
+//              16x16x32 with FP32 accumulation); operands move in 16-byte
+//              chunks where the pitch allows, are staged through LDS and
+//              register double-buffered; workgroups are renumbered so that
+//              tiles sharing an operand run on the same XCD.
+#include <cstdlib>
+
 #include "lrc_device.h"
 #include "lrc_internal.h"
 
@@ -28,88 +33,270 @@ struct Cfg {
     static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_;
     static constexpr int NT = WM * WN * 64;
     static constexpr int KPL = PrecTraits<T>::KPL, KB = PrecTraits<T>::KB;
-    static constexpr int PAD = (KPL == 8) ? 8 : 1;   // keeps f16 rows 16-byte aligned
-    static constexpr int LDK = BK + PAD;
+    static constexpr int VEC = 16 / (int)sizeof(T);       // elements per 16-byte access
+    // tiles with K contiguous: [rows][BK + PADK]; f16 rows stay 16-byte aligned
+    static constexpr int PADK = (KPL == 8) ? 8 : 1;
+    static constexpr int LDK = BK + PADK;
+    // tiles with rows contiguous: [BK][rows + PADR]; the pad shifts successive
+    // K rows across the LDS banks read by one fragment load
+    static constexpr int PADR = (sizeof(T) == 8) ? 2 : 16;
+    static constexpr int LDA_R = BM + PADR, LDB_R = BN + PADR;
     static constexpr int WTM = BM / WM, WTN = BN / WN;
     static constexpr int FM = WTM / 16, FN = WTN / 16;
-    static constexpr int EA = BM * BK / NT, EB = BN * BK / NT;   // staged elements per thread
     using Acc = typename PrecTraits<T>::acc;
     using AccV = typename PrecTraits<T>::accv;
     using Frag = typename PrecTraits<T>::frag;
     static_assert(BK % KB == 0, "BK must be a multiple of the MFMA K step");
     static_assert(WTM % 16 == 0 && WTN % 16 == 0, "wave tile must be a multiple of 16");
-    static_assert((BM * BK) % NT == 0 && (BN * BK) % NT == 0, "tile must split evenly");
+    static_assert((BM * BK) % (NT * VEC) == 0 && (BN * BK) % (NT * VEC) == 0, "tile must split evenly");
 };
 
-template <typename T> struct ApplyCfg;
-template <> struct ApplyCfg<double> { using C = Cfg<double, 64, 64, 16, 2, 2>; };
-template <> struct ApplyCfg<float> { using C = Cfg<float, 64, 64, 16, 2, 2>; };
-template <> struct ApplyCfg<half_t> { using C = Cfg<half_t, 64, 64, 32, 2, 2>; };
+// large tiles for large problems, small tiles when a dimension is small
+template <typename T> struct BigCfg;
+// FP64 stays at 64 x 64: a 128 x 128 FP64 accumulator tile does not fit the
+// 256 VGPRs of a wave next to its operands
+template <> struct BigCfg<double> { using C = Cfg<double, 64, 64, 16, 2, 2>; };
+template <> struct BigCfg<float> { using C = Cfg<float, 128, 128, 16, 2, 2>; };
+template <> struct BigCfg<half_t> { using C = Cfg<half_t, 128, 128, 32, 2, 2>; };
+template <typename T> struct SmallCfg;
+template <> struct SmallCfg<double> { using C = Cfg<double, 64, 64, 16, 2, 2>; };
+template <> struct SmallCfg<float> { using C = Cfg<float, 64, 64, 16, 2, 2>; };
+template <> struct SmallCfg<half_t> { using C = Cfg<half_t, 64, 64, 32, 2, 2>; };
 
-// One BK step of MFMAs on LDS tiles As[BM][LDK] (rows = m) and Bs[BN][LDK]
-// (rows = n).  acc[fn][fm][v] = C[m = wm*WTM + fm*16 + (lane&15)]
-//                                [n = wn*WTN + fn*16 + acc_row<T>(lane>>4, v)].
+// ---- global -> registers -> LDS tile movers ---------------------------------
+// Each workgroup keeps NS K steps of global loads in flight in registers
+// (kStages = NS): the loads of step j + NS are issued right after step j has been
+// written to LDS, so their latency overlaps NS - 1 steps of matrix-core work.
+// fetch() only issues loads; stash() writes LDS.
+//
+// Rows past the matrix edge are read from a clamped, in-bounds address and
+// left unmasked: they only feed output rows / columns that are discarded (or
+// forced to zero) at the epilogue.  The K range is exact: only the last step
+// of a K range can be partial, and there the missing K values are zeroed.
+static constexpr int kStages = 3;
+
+// Every thread moves whole 16-byte chunks: sources have a 16-byte aligned
+// base and a pitch that is a multiple of the chunk (operands that are not
+// are first copied into a padded workspace), so a chunk that starts inside a
+// row stays inside that row's pitch.
+
+// A tile of BK x ROWS elements taken from a source laid out [K][ld] with the
+// ROWS index contiguous, into LDS [BK][ROWS + PADR].
+template <class C, int ROWS, typename T>
+struct RowsTile {
+    static constexpr int CH = C::VEC;                            // elements per move
+    static constexpr int E = C::BK * ROWS / (C::NT * CH);        // moves per thread
+    static constexpr int LD = ROWS + C::PADR;                    // LDS pitch
+    static constexpr int RC = ROWS / CH;                         // moves per K row
+    static constexpr int KS = C::NT / RC;                        // K rows between a thread's moves
+    static_assert(C::NT % RC == 0, "a thread keeps one column position");
+    typedef T vec_t __attribute__((ext_vector_type(CH)));
+    vec_t reg[E];
+    // per-thread geometry: K row of move 0 and element offset of its column
+    struct Geo {
+        const T* base;   // source + r0 (uniform)
+        int64_t ld;
+        int kk0;         // K row of move 0 within a step
+        int col;         // column offset within the tile, clamped into the matrix
+        int lcol;        // LDS column of this thread
+    };
+    __device__ __forceinline__ static Geo geo(const T* src, int64_t ld, int64_t r0, int64_t rlim, int tid) {
+        Geo g;
+        g.base = src + r0;
+        g.ld = ld;
+        g.kk0 = tid / RC;
+        g.lcol = (tid % RC) * CH;
+        g.col = (r0 + g.lcol < rlim) ? g.lcol : 0;
+        return g;
+    }
+    __device__ __forceinline__ void fetch(const Geo& g, int64_t k0, bool partial, int64_t klim) {
+        if (!partial) {
+            const T* p = g.base + (k0 + g.kk0) * g.ld + g.col;
+#pragma unroll
+            for (int e = 0; e < E; ++e) reg[e] = *reinterpret_cast<const vec_t*>(p + (int64_t)(e * KS) * g.ld);
+        } else {
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int64_t gk = k0 + g.kk0 + e * KS;
+                reg[e] = *reinterpret_cast<const vec_t*>(g.base + (gk < klim ? gk : klim - 1) * g.ld + g.col);
+            }
+        }
+    }
+    __device__ __forceinline__ void stash(T* S, const Geo& g, int64_t k0, bool partial, int64_t klim) const {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int kk = g.kk0 + e * KS;
+            vec_t w = reg[e];
+            if (partial && k0 + kk >= klim) {
+#pragma unroll
+                for (int v = 0; v < CH; ++v) w[v] = T(0);
+            }
+            *reinterpret_cast<vec_t*>(S + kk * LD + g.lcol) = w;
+        }
+    }
+};
+
+// A tile of ROWS x BK elements from a source laid out [rows][ld] with K
+// contiguous, into LDS [ROWS][LDK].
+template <class C, int ROWS, typename T>
+struct KTile {
+    static constexpr int CH = C::VEC;
+    static constexpr int E = C::BK * ROWS / (C::NT * CH);
+    static constexpr int KC = C::BK / CH;                        // moves per row
+    static constexpr int RS = C::NT / KC;                        // rows between a thread's moves
+    static_assert(C::NT % KC == 0, "a thread keeps one K position");
+    typedef T vec_t __attribute__((ext_vector_type(CH)));
+    vec_t reg[E];
+    struct Geo {
+        const T* base;   // source + r0 * ld (uniform)
+        int64_t ld;
+        int rr0;         // row of move 0 within the tile
+        int rmax;        // last row inside the matrix, relative to r0
+        int kq;          // K offset of this thread within a step
+    };
+    __device__ __forceinline__ static Geo geo(const T* src, int64_t ld, int64_t r0, int64_t rlim, int tid) {
+        Geo g;
+        g.base = src + r0 * ld;
+        g.ld = ld;
+        g.rr0 = tid / KC;
+        g.kq = (tid % KC) * CH;
+        const int64_t rm = rlim - 1 - r0;
+        g.rmax = rm < ROWS ? (int)rm : ROWS;
+        return g;
+    }
+    __device__ __forceinline__ void fetch(const Geo& g, int64_t k0, bool partial, int64_t klim) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            int rr = g.rr0 + e * RS;
+            rr = rr < g.rmax ? rr : g.rmax;
+            int64_t gk = k0 + g.kq;
+            if (partial && gk >= klim) gk = 0;
+            reg[e] = *reinterpret_cast<const vec_t*>(g.base + (int64_t)rr * g.ld + gk);
+        }
+    }
+    __device__ __forceinline__ void stash(T* S, const Geo& g, int64_t k0, bool partial, int64_t klim) const {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int rr = g.rr0 + e * RS;
+            vec_t w = reg[e];
+            if (partial) {
+                const int64_t gk = k0 + g.kq;
+#pragma unroll
+                for (int v = 0; v < CH; ++v)
+                    if (gk + v >= klim) w[v] = T(0);
+            }
+            T* dst = S + rr * C::LDK + g.kq;
+            if constexpr ((C::LDK * sizeof(T)) % 16 == 0) {
+                *reinterpret_cast<vec_t*>(dst) = w;
+            } else {
+#pragma unroll
+                for (int v = 0; v < CH; ++v) dst[v] = w[v];
+            }
+        }
+    }
+};
+
+// MFMA operand fragment from a [BK][LD] (rows contiguous) tile for the 16
+// rows starting at `rbase`; k0 is the first K value of this lane's slice.
+// FP64 / FP32 take one K value per lane: a single LDS read.  FP16 takes 8
+// consecutive K values of one row, which lie in 8 different LDS rows; two
+// transposing LDS reads (ds_read_b64_tr_b16) gather them.  Within each group
+// of 16 lanes, lane s points at the 4 consecutive rows 4(s&3).. of K row
+// k0 + (s>>2); the instruction then returns to lane i the value of row i
+// from the K rows addressed by lanes i/4, i/4+4, i/4+8, i/4+12, i.e. K
+// values k0..k0+3 of its own row (a second read covers k0+4..k0+7).
+template <typename T, int LD>
+__device__ __forceinline__ typename PrecTraits<T>::frag frag_rows(const T* S, int rbase, int k0, int lane) {
+    if constexpr (PrecTraits<T>::KPL == 1) {
+        return S[k0 * LD + rbase + (lane & 15)];
+    } else {
+        static_assert(PrecTraits<T>::KPL == 8 && LD % 4 == 0, "transposing read needs 8-byte aligned rows");
+        typedef short s4_t __attribute__((ext_vector_type(4)));
+        const int s = lane & 15;
+        const T* p = S + (k0 + (s >> 2)) * LD + rbase + 4 * (s & 3);
+        const s4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4_t*)(p));
+        const s4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4_t*)(p + 4 * LD));
+        typedef short s8_t __attribute__((ext_vector_type(8)));
+        const s8_t both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(typename PrecTraits<T>::frag, both);
+    }
+}
+
+// One BK step of MFMAs.  Rows-contiguous tiles (phase 1, Gram):
+// acc[fn][fm][v] = C[m = wm*WTM + fm*16 + (lane&15)][n = wn*WTN + fn*16 + acc_row<T>(lane>>4, v)]
+// Fragments whose 16 rows (columns) all lie past the matrix edge are
+// skipped: nfm / nfn count the live ones of this wave (wave-uniform).  Only
+// edge tiles take the guarded form; interior tiles run branch-free.
+template <class C, bool GUARD, typename T>
+__device__ __forceinline__ void mma_rows_g(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM],
+                                           int wm, int wn, int lane, int nfm, int nfn) {
+    const int g = lane >> 4;
+#pragma unroll
+    for (int kk = 0; kk < C::BK; kk += C::KB) {
+        typename C::Frag a[C::FN], b[C::FM];
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn)
+            if (!GUARD || fn < nfn) a[fn] = frag_rows<T, C::LDB_R>(Bs, wn * C::WTN + fn * 16, kk + g * C::KPL, lane);
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm)
+            if (!GUARD || fm < nfm) b[fm] = frag_rows<T, C::LDA_R>(As, wm * C::WTM + fm * 16, kk + g * C::KPL, lane);
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm)
+                if (!GUARD || (fn < nfn && fm < nfm)) acc[fn][fm] = mfma(a[fn], b[fm], acc[fn][fm]);
+    }
+}
 template <class C, typename T>
-__device__ __forceinline__ void mma_tile(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM],
-                                         int wm, int wn, int lane) {
+__device__ __forceinline__ void mma_rows(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM],
+                                         int wm, int wn, int lane, int nfm, int nfn) {
+    if (nfm == C::FM && nfn == C::FN) mma_rows_g<C, false>(As, Bs, acc, wm, wn, lane, nfm, nfn);
+    else if (nfm > 0 && nfn > 0) mma_rows_g<C, true>(As, Bs, acc, wm, wn, lane, nfm, nfn);
+}
+
+// Same for K-contiguous tiles As[BM][LDK], Bs[BN][LDK] (phase 2, error norm).
+template <class C, bool GUARD, typename T>
+__device__ __forceinline__ void mma_k_g(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM], int wm,
+                                        int wn, int lane, int nfm, int nfn) {
     const int r = lane & 15, g = lane >> 4;
 #pragma unroll
     for (int kk = 0; kk < C::BK; kk += C::KB) {
         typename C::Frag a[C::FN], b[C::FM];
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
-            a[fn] = load_frag<T>(Bs + (wn * C::WTN + fn * 16 + r) * C::LDK + kk + g * C::KPL);
+            if (!GUARD || fn < nfn) a[fn] = load_frag<T>(Bs + (wn * C::WTN + fn * 16 + r) * C::LDK + kk + g * C::KPL);
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm)
-            b[fm] = load_frag<T>(As + (wm * C::WTM + fm * 16 + r) * C::LDK + kk + g * C::KPL);
+            if (!GUARD || fm < nfm) b[fm] = load_frag<T>(As + (wm * C::WTM + fm * 16 + r) * C::LDK + kk + g * C::KPL);
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
-            for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = mfma(a[fn], b[fm], acc[fn][fm]);
+            for (int fm = 0; fm < C::FM; ++fm)
+                if (!GUARD || (fn < nfn && fm < nfm)) acc[fn][fm] = mfma(a[fn], b[fm], acc[fn][fm]);
     }
+}
+template <class C, typename T>
+__device__ __forceinline__ void mma_k(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM], int wm,
+                                      int wn, int lane, int nfm, int nfn) {
+    if (nfm == C::FM && nfn == C::FN) mma_k_g<C, false>(As, Bs, acc, wm, wn, lane, nfm, nfn);
+    else if (nfm > 0 && nfn > 0) mma_k_g<C, true>(As, Bs, acc, wm, wn, lane, nfm, nfn);
 }
 
-// Global -> registers for a ROWS x BK tile whose source is [K][ld] with the
-// row index contiguous (a transposed read): consecutive threads read
-// consecutive rows, i.e. consecutive addresses.
-template <class C, int ROWS, int E, typename T>
-__device__ __forceinline__ void fetch_rowm(T (&reg)[E], const T* __restrict__ src, int64_t ld,
-                                           int64_t r0, int64_t rlim, int64_t k0, int64_t klim, int tid) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int idx = tid + e * C::NT;
-        const int rr = idx % ROWS, kk = idx / ROWS;
-        const int64_t gr = r0 + rr, gk = k0 + kk;
-        reg[e] = (gr < rlim && gk < klim) ? src[gk * ld + gr] : T(0);
-    }
+// Workgroups are handed to the 8 XCDs in turn; renumber them so that each
+// XCD works through one contiguous range of tiles, whose shared operands
+// then meet in that XCD's L2.
+__device__ __forceinline__ int64_t xcd_tile(int64_t total) {
+    const int64_t L = blockIdx.x;
+    return (total % 8 == 0) ? (L % 8) * (total / 8) + L / 8 : L;
 }
-template <class C, int ROWS, int E, typename T>
-__device__ __forceinline__ void stash_rowm(T* S, const T (&reg)[E], int tid) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int idx = tid + e * C::NT;
-        S[(idx % ROWS) * C::LDK + idx / ROWS] = reg[e];
-    }
-}
-// Same for a source [rows][ld] with the K index contiguous.
-template <class C, int ROWS, int E, typename T>
-__device__ __forceinline__ void fetch_rowk(T (&reg)[E], const T* __restrict__ src, int64_t ld,
-                                           int64_t r0, int64_t rlim, int64_t k0, int64_t klim, int tid) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int idx = tid + e * C::NT;
-        const int kk = idx % C::BK, rr = idx / C::BK;
-        const int64_t gr = r0 + rr, gk = k0 + kk;
-        reg[e] = (gr < rlim && gk < klim) ? src[gr * ld + gk] : T(0);
-    }
-}
-template <class C, int ROWS, int E, typename T>
-__device__ __forceinline__ void stash_rowk(T* S, const T (&reg)[E], int tid) {
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int idx = tid + e * C::NT;
-        S[(idx / C::BK) * C::LDK + idx % C::BK] = reg[e];
-    }
+
+// live 16-wide fragments of a wave tile starting at `start` in a dimension of `lim`
+template <int F>
+__device__ __forceinline__ int live_frags(int64_t start, int64_t lim) {
+    const int64_t rem = lim - start;
+    if (rem <= 0) return 0;
+    const int64_t f = (rem + 15) / 16;
+    return f < F ? (int)f : F;
 }
 
 enum { ATB_APPLY = 0, ATB_GRAM = 1 };
@@ -122,19 +309,24 @@ enum { ATB_APPLY = 0, ATB_GRAM = 1 };
 template <typename T, class C, int MODE>
 __global__ __launch_bounds__(C::NT) void k_atb(
     const T* __restrict__ Asrc, int64_t lda, const T* __restrict__ Bsrc, int64_t ldb,
-    int64_t M, int64_t N, int64_t K, int64_t chunk, int splits,
+    int64_t M, int64_t N, int64_t K, int64_t chunk, int tiles_m, int tiles_n, int splits,
     typename C::Acc* __restrict__ part, int* __restrict__ counters,
     const T* __restrict__ svals, void* __restrict__ out, int64_t ldo, int64_t Mout) {
     using Acc = typename C::Acc;
     using AccV = typename C::AccV;
-    __shared__ alignas(16) T As[C::BM * C::LDK];
-    __shared__ alignas(16) T Bs[C::BN * C::LDK];
+    __shared__ alignas(16) T As[C::BK * C::LDA_R];
+    __shared__ alignas(16) T Bs[C::BK * C::LDB_R];
     __shared__ int last_flag;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / C::WN, wn = wave % C::WN;
-    const int64_t m0 = (int64_t)blockIdx.y * C::BM, n0 = (int64_t)blockIdx.x * C::BN;
-    const int sp = blockIdx.z;
+    // logical order: m tile fastest (tiles sharing a block of B columns are neighbours), then n, then split
+    const int64_t lt = xcd_tile((int64_t)tiles_m * tiles_n * splits);
+    const int64_t tile = lt % ((int64_t)tiles_m * tiles_n);
+    const int sp = (int)(lt / ((int64_t)tiles_m * tiles_n));
+    const int64_t m0 = (tile % tiles_m) * C::BM, n0 = (tile / tiles_m) * C::BN;
+    const int nfm = live_frags<C::FM>(m0 + wm * C::WTM, M), nfn = live_frags<C::FN>(n0 + wn * C::WTN, N);
     const int64_t kbeg = (int64_t)sp * chunk;
     const int64_t kend = (kbeg + chunk < K) ? kbeg + chunk : K;
 
@@ -144,34 +336,53 @@ __global__ __launch_bounds__(C::NT) void k_atb(
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = zero_accv<AccV>();
 
-    T ra[C::EA], rb[C::EB];
-    if (kbeg < kend) {
-        fetch_rowm<C, C::BM>(ra, Asrc, lda, m0, M, kbeg, kend, tid);
-        fetch_rowm<C, C::BN>(rb, Bsrc, ldb, n0, N, kbeg, kend, tid);
-    }
-    for (int64_t k0 = kbeg; k0 < kend; k0 += C::BK) {
-        stash_rowm<C, C::BM>(As, ra, tid);
-        stash_rowm<C, C::BN>(Bs, rb, tid);
-        __syncthreads();
-        if (k0 + C::BK < kend) {
-            fetch_rowm<C, C::BM>(ra, Asrc, lda, m0, M, k0 + C::BK, kend, tid);
-            fetch_rowm<C, C::BN>(rb, Bsrc, ldb, n0, N, k0 + C::BK, kend, tid);
+    using TA = RowsTile<C, C::BM, T>;
+    using TB = RowsTile<C, C::BN, T>;
+    const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid);
+    const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
+    constexpr int NS = kStages;
+    TA ta[NS];
+    TB tb[NS];
+    const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
+    const int last_partial = ((kend - kbeg) % C::BK) ? nsteps - 1 : -1;
+#pragma unroll
+    for (int st = 0; st < NS; ++st)
+        if (st < nsteps) {
+            ta[st].fetch(ga, kbeg + st * C::BK, st == last_partial, kend);
+            tb[st].fetch(gb, kbeg + st * C::BK, st == last_partial, kend);
         }
-        mma_tile<C>(As, Bs, acc, wm, wn, lane);
-        __syncthreads();
+    for (int j0 = 0; j0 < nsteps; j0 += NS) {
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            const int j = j0 + st;
+            if (j < nsteps) {
+                const int64_t k0 = kbeg + (int64_t)j * C::BK;
+                ta[st].stash(As, ga, k0, j == last_partial, kend);
+                tb[st].stash(Bs, gb, k0, j == last_partial, kend);
+                __syncthreads();
+                const int jn = j + NS;
+                if (jn < nsteps) {
+                    ta[st].fetch(ga, kbeg + (int64_t)jn * C::BK, jn == last_partial, kend);
+                    tb[st].fetch(gb, kbeg + (int64_t)jn * C::BK, jn == last_partial, kend);
+                }
+                mma_rows<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
+                __syncthreads();
+            }
+        }
     }
 
     const int r = lane & 15, g = lane >> 4;
     if (splits > 1) {
-        const int64_t tile = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+        // partials of dead fragments are neither written nor read
         constexpr int NV = C::FN * C::FM * 4;
         Acc* mine = part + ((tile * splits + sp) * NV) * C::NT;
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm)
+                if (fn < nfn && fm < nfm)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) mine[((fn * C::FM + fm) * 4 + v) * C::NT + tid] = acc[fn][fm][v];
+                    for (int v = 0; v < 4; ++v) mine[((fn * C::FM + fm) * 4 + v) * C::NT + tid] = acc[fn][fm][v];
         if (!arrive_last(counters + tile, splits, &last_flag)) return;
         // every partial, this workgroup's included, is read back in split order
 #pragma unroll
@@ -184,9 +395,10 @@ __global__ __launch_bounds__(C::NT) void k_atb(
             for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
                 for (int fm = 0; fm < C::FM; ++fm)
+                    if (fn < nfn && fm < nfm)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        acc[fn][fm][v] += __builtin_nontemporal_load(&src[((fn * C::FM + fm) * 4 + v) * C::NT + tid]);
+                        for (int v = 0; v < 4; ++v)
+                            acc[fn][fm][v] += __builtin_nontemporal_load(&src[((fn * C::FM + fm) * 4 + v) * C::NT + tid]);
         }
     }
 
@@ -200,8 +412,8 @@ __global__ __launch_bounds__(C::NT) void k_atb(
                 const int64_t nn = n0 + wn * C::WTN + fn * 16 + acc_row<T>(g, v);
                 if (MODE == ATB_APPLY) {
                     if (nn < N && mm < Mout) {
-                        const Acc sm = (mm < M) ? to_acc(svals[mm]) : Acc(0);
-                        static_cast<T*>(out)[nn * ldo + mm] = to_storage<T>(sm * acc[fn][fm][v]);
+                        const Acc val = (mm < M) ? to_acc(svals[mm]) * acc[fn][fm][v] : Acc(0);
+                        static_cast<T*>(out)[nn * ldo + mm] = to_storage<T>(val);
                     }
                 } else {
                     if (nn < N && mm < M) static_cast<double*>(out)[mm * ldo + nn] = (double)acc[fn][fm][v];
@@ -219,7 +431,7 @@ enum { ABT_STORE = 0, ABT_ERR = 1 };
 template <typename T, class C, int MODE>
 __global__ __launch_bounds__(C::NT) void k_abt(
     const T* __restrict__ Asrc, int64_t lda, int64_t M, int64_t Ka,
-    const T* __restrict__ Bsrc, int64_t ldb, int64_t N, int64_t Kb, int64_t K,
+    const T* __restrict__ Bsrc, int64_t ldb, int64_t N, int64_t Kb, int64_t K, int tiles_m, int tiles_n,
     T* __restrict__ Y, int64_t ldy, int vec4,
     const double* __restrict__ Aref, int64_t ldr, double* __restrict__ part) {
     using AccV = typename C::AccV;
@@ -227,9 +439,13 @@ __global__ __launch_bounds__(C::NT) void k_abt(
     __shared__ alignas(16) T Bs[C::BN * C::LDK];
     __shared__ double wsum[C::NT / 64];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / C::WN, wn = wave % C::WN;
-    const int64_t m0 = (int64_t)blockIdx.y * C::BM, n0 = (int64_t)blockIdx.x * C::BN;
+    // logical order: n tile fastest (tiles sharing rows of A are neighbours)
+    const int64_t tile = xcd_tile((int64_t)tiles_m * tiles_n);
+    const int64_t m0 = (tile / tiles_n) * C::BM, n0 = (tile % tiles_n) * C::BN;
+    const int nfm = live_frags<C::FM>(m0 + wm * C::WTM, M), nfn = live_frags<C::FN>(n0 + wn * C::WTN, N);
 
     AccV acc[C::FN][C::FM];
 #pragma unroll
@@ -237,19 +453,39 @@ __global__ __launch_bounds__(C::NT) void k_abt(
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = zero_accv<AccV>();
 
-    T ra[C::EA], rb[C::EB];
-    fetch_rowk<C, C::BM>(ra, Asrc, lda, m0, M, 0, Ka, tid);
-    fetch_rowk<C, C::BN>(rb, Bsrc, ldb, n0, N, 0, Kb, tid);
-    for (int64_t k0 = 0; k0 < K; k0 += C::BK) {
-        stash_rowk<C, C::BM>(As, ra, tid);
-        stash_rowk<C, C::BN>(Bs, rb, tid);
-        __syncthreads();
-        if (k0 + C::BK < K) {
-            fetch_rowk<C, C::BM>(ra, Asrc, lda, m0, M, k0 + C::BK, Ka, tid);
-            fetch_rowk<C, C::BN>(rb, Bsrc, ldb, n0, N, k0 + C::BK, Kb, tid);
+    using TA = KTile<C, C::BM, T>;
+    using TB = KTile<C, C::BN, T>;
+    const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid);
+    const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
+    constexpr int NS = kStages;
+    TA ta[NS];
+    TB tb[NS];
+    const int nsteps = (int)((K + C::BK - 1) / C::BK);
+#pragma unroll
+    for (int st = 0; st < NS; ++st)
+        if (st < nsteps) {
+            const int64_t k0 = (int64_t)st * C::BK;
+            ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
+            tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
         }
-        mma_tile<C>(As, Bs, acc, wm, wn, lane);
-        __syncthreads();
+    for (int j0 = 0; j0 < nsteps; j0 += NS) {
+#pragma unroll
+        for (int st = 0; st < NS; ++st) {
+            const int j = j0 + st;
+            if (j < nsteps) {
+                const int64_t k0 = (int64_t)j * C::BK;
+                ta[st].stash(As, ga, k0, k0 + C::BK > Ka, Ka);
+                tb[st].stash(Bs, gb, k0, k0 + C::BK > Kb, Kb);
+                __syncthreads();
+                const int64_t kn = k0 + (int64_t)NS * C::BK;
+                if (kn < K) {
+                    ta[st].fetch(ga, kn, kn + C::BK > Ka, Ka);
+                    tb[st].fetch(gb, kn, kn + C::BK > Kb, Kb);
+                }
+                mma_k<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
+                __syncthreads();
+            }
+        }
     }
 
     const int r = lane & 15, g = lane >> 4;
@@ -298,9 +534,46 @@ __global__ __launch_bounds__(C::NT) void k_abt(
         if (tid == 0) {
             double t = 0.0;
             for (int w = 0; w < C::NT / 64; ++w) t += wsum[w];
-            part[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = t;
+            part[tile] = t;
         }
     }
+}
+
+// 16-byte vector access is possible when the pitch and base are aligned.
+template <typename T>
+static bool vec_ok(const void* p, int64_t ld) {
+    constexpr int VEC = 16 / (int)sizeof(T);
+    return (ld % VEC == 0) && (reinterpret_cast<uintptr_t>(p) % 16 == 0);
+}
+
+template <typename T, class C, int MODE, class... Args>
+static void launch_atb(dim3 grid, hipStream_t st, Args... args) {
+    hipLaunchKernelGGL((k_atb<T, C, MODE>), grid, dim3(C::NT), 0, st, args...);
+}
+template <typename T, class C, int MODE, class... Args>
+static void launch_abt(dim3 grid, hipStream_t st, Args... args) {
+    hipLaunchKernelGGL((k_abt<T, C, MODE>), grid, dim3(C::NT), 0, st, args...);
+}
+
+// dst[i][j] = src[i][j] for j < cols, 0 for cols <= j < ldd: a copy of an
+// operand whose pitch or base rules out 16-byte moves.
+template <typename T>
+__global__ __launch_bounds__(256) void k_pitch_copy(const T* __restrict__ src, int64_t rows, int64_t cols,
+                                                    int64_t lds, T* __restrict__ dst, int64_t ldd) {
+    const int64_t total = rows * ldd;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
+        const int64_t i = idx / ldd, j = idx % ldd;
+        dst[idx] = (j < cols) ? src[i * lds + j] : T(0);
+    }
+}
+
+template <typename T>
+static void pitch_copy(const T* src, int64_t rows, int64_t cols, int64_t lds, T* dst, int64_t ldd,
+                       hipStream_t stream) {
+    int64_t g = (rows * ldd + 255) / 256;
+    if (g > 8192) g = 8192;
+    if (g < 1) g = 1;
+    hipLaunchKernelGGL(k_pitch_copy<T>, dim3((unsigned)g), dim3(256), 0, stream, src, rows, cols, lds, dst, ldd);
 }
 
 // --------------------------------------------------------- streaming path --
@@ -413,8 +686,26 @@ __global__ __launch_bounds__(256) void k_p2_stream(
 static constexpr int kStreamMaxBatch = 8;
 static constexpr int kStreamRowsTarget = 64;     // rows of V per workgroup chunk (phase 1)
 
-ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int path) {
-    (void)m;
+static constexpr int64_t kBigTarget = 512;       // phase-1 workgroups aimed for (128 x 128 tiles)
+static constexpr int64_t kSmallTarget = 1024;    // same for 64 x 64 tiles
+
+// LRC_APPLY_TILE=64 or 128 pins the MFMA tile edge of both phases (tuning aid).
+static int forced_tile() {
+    static const int t = [] {
+        const char* e = std::getenv("LRC_APPLY_TILE");
+        const int v = e ? std::atoi(e) : 0;
+        return (v == 64 || v == 128) ? v : 0;
+    }();
+    return t;
+}
+
+static bool needs_stage(const void* p, int64_t ld, int prec) {
+    const int64_t vec = 16 / (int64_t)elem_bytes(prec);
+    return (ld % vec != 0) || (reinterpret_cast<uintptr_t>(p) % 16 != 0);
+}
+
+ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int path, const void* U,
+                     const void* V, const void* X) {
     ApplyPlan p{};
     if (path != 1 && path != 2) path = (b <= kStreamMaxBatch) ? 1 : 2;
     if (path == 1 && b > kStreamMaxBatch) path = 2;
@@ -434,25 +725,46 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         p.counters = (size_t)p.tiles_m;
     } else {
         const int BK = (prec == P16) ? 32 : 16;
-        p.tiles_m = (int)((k + 63) / 64);
-        p.tiles_n = (int)((b + 63) / 64);
+        // phase 1: C = V^T X is k x b, summed over n
+        p.big1 = (k >= 128 && b >= 128) ? 1 : 0;
+        if (forced_tile()) p.big1 = forced_tile() == 128;
+        if (prec == P64) p.big1 = 0;
+        const int T1 = p.big1 ? 128 : 64;
+        p.tiles_m = (int)((k + T1 - 1) / T1);
+        p.tiles_n = (int)((b + T1 - 1) / T1);
         const int64_t base = (int64_t)p.tiles_m * p.tiles_n;
-        int64_t splits = (1024 + base - 1) / base;
+        const int64_t target = p.big1 ? kBigTarget : kSmallTarget;
+        int64_t splits = (target + base - 1) / base;
         int64_t max_splits = n / (4 * BK);
         if (max_splits < 1) max_splits = 1;
         if (splits > max_splits) splits = max_splits;
         if (splits < 1) splits = 1;
         p.chunk = round_up((n + splits - 1) / splits, BK);
         p.splits = (int)((n + p.chunk - 1) / p.chunk);
-        p.part_bytes = (p.splits > 1) ? (size_t)base * p.splits * 64 * 64 * acc_b : 0;
+        p.part_bytes = (p.splits > 1) ? (size_t)base * p.splits * T1 * T1 * acc_b : 0;
         p.counters = (p.splits > 1) ? (size_t)base : 0;
+        // phase 2: Y = U T' is m x b
+        const int64_t big_tiles = ((m + 127) / 128) * ((b + 127) / 128);
+        p.big2 = (m >= 128 && b >= 128 && big_tiles >= 256) ? 1 : 0;
+        if (forced_tile()) p.big2 = forced_tile() == 128;
+        if (prec == P64) p.big2 = 0;
     }
     p.mid_bytes = (size_t)b * p.Kp * elem_bytes(prec);
+    if (path == 2) {
+        p.ldx = round_up(b, 8);
+        p.stage_u = needs_stage(U, k, prec);
+        p.stage_v = needs_stage(V, k, prec);
+        p.stage_x = needs_stage(X, b, prec);
+        const size_t e = elem_bytes(prec);
+        p.stage_bytes = (p.stage_u ? round_up((size_t)m * p.Kp * e, 256) : 0) +
+                        (p.stage_v ? round_up((size_t)n * p.Kp * e, 256) : 0) +
+                        (p.stage_x ? round_up((size_t)n * p.ldx * e, 256) : 0);
+    }
     return p;
 }
 
 size_t apply_workspace_bytes(const ApplyPlan& p) {
-    return round_up(p.part_bytes, 256) + round_up(p.mid_bytes, 256);
+    return round_up(p.part_bytes, 256) + round_up(p.mid_bytes, 256) + p.stage_bytes;
 }
 
 template <typename T> static const char* p1_stream_label();
@@ -497,20 +809,62 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
 #undef LRC_P2S
         return hipGetLastError();
     }
-    using C = typename ApplyCfg<T>::C;
-    dim3 g1(p.tiles_n, p.tiles_m, p.splits);
+    // operands whose pitch or base rule out 16-byte moves go through a padded copy
+    const T *Ug = U, *Vg = V, *Xg = X;
+    int64_t ldu = k, ldv = k, ldx = b;
+    if (p.stage_u || p.stage_v || p.stage_x) {
+        KernelTimer ts("apply_stage", stream);
+        if (p.stage_u) {
+            T* d = static_cast<T*>(ws.take((size_t)m * p.Kp * sizeof(T)));
+            if (!d) return hipErrorOutOfMemory;
+            pitch_copy<T>(U, m, k, k, d, p.Kp, stream);
+            Ug = d;
+            ldu = p.Kp;
+        }
+        if (p.stage_v) {
+            T* d = static_cast<T*>(ws.take((size_t)n * p.Kp * sizeof(T)));
+            if (!d) return hipErrorOutOfMemory;
+            pitch_copy<T>(V, n, k, k, d, p.Kp, stream);
+            Vg = d;
+            ldv = p.Kp;
+        }
+        if (p.stage_x) {
+            T* d = static_cast<T*>(ws.take((size_t)n * p.ldx * sizeof(T)));
+            if (!d) return hipErrorOutOfMemory;
+            pitch_copy<T>(X, n, b, b, d, p.ldx, stream);
+            Xg = d;
+            ldx = p.ldx;
+        }
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     {
-    KernelTimer t1(p1_mfma_label<T>(), stream);
-    hipLaunchKernelGGL((k_atb<T, C, ATB_APPLY>), g1, dim3(C::NT), 0, stream, V, k, X, b, k, b, n,
-                       p.chunk, p.splits, part, counters, s, (void*)Tt, ldt, ldt);
+        KernelTimer t1(p1_mfma_label<T>(), stream);
+        const dim3 g1((unsigned)((int64_t)p.tiles_m * p.tiles_n * p.splits));
+        if (p.big1)
+            launch_atb<T, typename BigCfg<T>::C, ATB_APPLY>(g1, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk,
+                                                            p.tiles_m, p.tiles_n, p.splits, part, counters, s,
+                                                            (void*)Tt, ldt, ldt);
+        else
+            launch_atb<T, typename SmallCfg<T>::C, ATB_APPLY>(g1, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk,
+                                                              p.tiles_m, p.tiles_n, p.splits, part, counters, s,
+                                                              (void*)Tt, ldt, ldt);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    dim3 g2((unsigned)((b + C::BN - 1) / C::BN), (unsigned)((m + C::BM - 1) / C::BM));
     KernelTimer t2(p2_mfma_label<T>(), stream);
     const int vec4 = (b % 4 == 0) && ((reinterpret_cast<uintptr_t>(Y) % (4 * sizeof(T))) == 0);
-    hipLaunchKernelGGL((k_abt<T, C, ABT_STORE>), g2, dim3(C::NT), 0, stream, U, k, m, k, (const T*)Tt,
-                       ldt, b, ldt, ldt, Y, b, vec4, (const double*)nullptr, (int64_t)0, (double*)nullptr);
+    const int T2 = p.big2 ? 128 : 64;
+    const int tm = (int)((m + T2 - 1) / T2), tn = (int)((b + T2 - 1) / T2);
+    const dim3 g2((unsigned)((int64_t)tm * tn));
+    if (p.big2)
+        launch_abt<T, typename BigCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt, ldt,
+                                                        tm, tn, Y, b, vec4, (const double*)nullptr, (int64_t)0,
+                                                        (double*)nullptr);
+    else
+        launch_abt<T, typename SmallCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt,
+                                                          ldt, tm, tn, Y, b, vec4, (const double*)nullptr,
+                                                          (int64_t)0, (double*)nullptr);
     return hipGetLastError();
 }
 
@@ -561,11 +915,11 @@ hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G, W
     gram_plan(rows, cols, &t, &sp, &ch);
     double* part = static_cast<double*>(ws.take((size_t)t * t * sp * 64 * 64 * sizeof(double)));
     if (ws.overrun || (sp > 1 && ws.n_counters < (size_t)t * t)) return hipErrorOutOfMemory;
-    dim3 g(t, t, sp);
+    if (!vec_ok<double>(P, cols)) return hipErrorInvalidValue;   // the factor builders keep 2r columns
+    const dim3 g((unsigned)((int64_t)t * t * sp));
     KernelTimer tm("cert_gram_f64", stream);
-    hipLaunchKernelGGL((k_atb<double, GramC, ATB_GRAM>), g, dim3(GramC::NT), 0, stream, P, cols, P, cols,
-                       cols, cols, rows, ch, sp, part, ws.counters, (const double*)nullptr, (void*)G, cols,
-                       cols);
+    launch_atb<double, GramC, ATB_GRAM>(g, stream, P, cols, P, cols, cols, cols, rows, ch, t, t, sp, part,
+                                        ws.counters, (const double*)nullptr, (void*)G, cols, cols);
     return hipGetLastError();
 }
 
@@ -574,13 +928,14 @@ size_t err_workspace_bytes(int64_t m, int64_t n) {
 }
 
 hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, int64_t m, int64_t n,
-                            int64_t r, double* part, int64_t* nparts, hipStream_t stream) {
-    dim3 g((unsigned)((n + 63) / 64), (unsigned)((m + 63) / 64));
-    *nparts = (int64_t)g.x * g.y;
+                            int64_t r, int64_t ldw, double* part, int64_t* nparts, hipStream_t stream) {
+    const int tm = (int)((m + 63) / 64), tn = (int)((n + 63) / 64);
+    *nparts = (int64_t)tm * tn;
     const int64_t K = round_up(r, GramC::BK);
-    KernelTimer tm("cert_err_dense_f64", stream);
-    hipLaunchKernelGGL((k_abt<double, GramC, ABT_ERR>), g, dim3(GramC::NT), 0, stream, W, r, m, r, Vw, r, n, r,
-                       K, (double*)nullptr, (int64_t)0, 0, A, n, part);
+    if (!vec_ok<double>(W, ldw) || !vec_ok<double>(Vw, ldw)) return hipErrorInvalidValue;
+    KernelTimer tm_("cert_err_dense_f64", stream);
+    launch_abt<double, GramC, ABT_ERR>(dim3((unsigned)*nparts), stream, W, ldw, m, r, Vw, ldw, n, r, K, tm, tn,
+                                       (double*)nullptr, (int64_t)0, 0, A, n, part);
     return hipGetLastError();
 }
 

@@ -357,7 +357,7 @@ int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X,
     rc = current_device(&dev, nullptr);
     if (rc) return rc;
     hipStream_t st = g_stream;
-    ApplyPlan plan = plan_apply(m, n, k, batch, prec, g_force_path);
+    ApplyPlan plan = plan_apply(m, n, k, batch, prec, g_force_path, U, V, X);
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
     hipError_t he = ws.reserve(apply_workspace_bytes(plan), plan.counters, st);
@@ -497,7 +497,8 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
     const size_t gp2 = gram_workspace_bytes(n, w2, &cnt2);
     size_t need = (size_t)(m + n) * w2 * 8 + 2 * (size_t)w2 * w2 * 8 + gp1 + gp2 + 16 * 256;
     const bool have_A = a->A != nullptr;
-    if (have_A) need += (size_t)(m + n) * r * 8 + err_workspace_bytes(m, n) + 256;
+    const int64_t rp = round_up(r, 2);   // pitch of the widened factors: 16-byte rows
+    if (have_A) need += (size_t)(m + n) * rp * 8 + err_workspace_bytes(m, n) + 4 * 256;
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
     hipError_t he = ws.reserve(need, std::max(cnt1, cnt2), st);
@@ -514,15 +515,15 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
     if (he != hipSuccess) return fail_hip(he, "certificate launch");
     double* errsum = nullptr;
     if (have_A) {
-        double* W = static_cast<double*>(ws.take((size_t)m * r * 8));
-        double* Vw = static_cast<double*>(ws.take((size_t)n * r * 8));
+        double* W = static_cast<double*>(ws.take((size_t)m * rp * 8));
+        double* Vw = static_cast<double*>(ws.take((size_t)n * rp * 8));
         double* part = static_cast<double*>(ws.take(err_workspace_bytes(m, n)));
         errsum = static_cast<double*>(ws.take(8));
         if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
         int64_t nparts = 0;
-        he = launch_widen_scaled(a->Uh, a->sh, a->prec, m, r, W, st);
-        if (he == hipSuccess) he = launch_widen_scaled(a->Vh, nullptr, a->prec, n, r, Vw, st);
-        if (he == hipSuccess) he = launch_err_dense(a->A, W, Vw, m, n, r, part, &nparts, st);
+        he = launch_widen_scaled(a->Uh, a->sh, a->prec, m, r, rp, W, st);
+        if (he == hipSuccess) he = launch_widen_scaled(a->Vh, nullptr, a->prec, n, r, rp, Vw, st);
+        if (he == hipSuccess) he = launch_err_dense(a->A, W, Vw, m, n, r, rp, part, &nparts, st);
         if (he == hipSuccess) he = launch_reduce_rows(part, nparts, 1, errsum, st);
         if (he != hipSuccess) return fail_hip(he, "error-norm launch");
     }

@@ -53,12 +53,19 @@ struct ApplyPlan {
     int splits;
     int64_t chunk;       // rows of V / X per split
     int tiles_m, tiles_n;
+    int big1, big2;      // 128 x 128 tiles (else 64 x 64) for phase 1 / phase 2
+    // operands copied to a padded pitch first (MFMA path): U, V with pitch Kp, X with ldx
+    int stage_u, stage_v, stage_x;
+    int64_t ldx;
+    size_t stage_bytes;
     size_t part_bytes;   // partial-sum buffer
     size_t mid_bytes;    // T'^T buffer
     size_t counters;
 };
 
-ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int path);
+// U, V, X are only inspected for alignment (may be null).
+ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int path, const void* U = nullptr,
+                     const void* V = nullptr, const void* X = nullptr);
 size_t apply_workspace_bytes(const ApplyPlan& p);
 
 hipError_t launch_apply(const ApplyPlan& p, const void* U, const void* s, const void* V,
@@ -74,17 +81,19 @@ hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G,
 // P[i][t] = ref[i][t]; P[i][r + t] = widen(h[i][t]) - ref[i][t]   (rows x 2r)
 hipError_t launch_diff_factors(const double* ref, const void* h, int prec, int64_t rows,
                                int64_t r, double* P, hipStream_t stream);
-// W[i][t] = widen(h[i][t]) * widen(hs[t])  (hs may be NULL: factor 1)
+// W[i][t] = widen(h[i][t]) * widen(hs[t])  (hs may be NULL: factor 1), rows of
+// pitch ldw >= r with zero padding
 hipError_t launch_widen_scaled(const void* h, const void* hs, int prec, int64_t rows,
-                               int64_t r, double* W, hipStream_t stream);
+                               int64_t r, int64_t ldw, double* W, hipStream_t stream);
 // out[i] = widen(src[i])
 hipError_t launch_widen(const void* src, int prec, int64_t count, double* out, hipStream_t stream);
 
 // Partial sums of (A - W Vw^T)^2 over m x n, one per workgroup; returns the
 // number of partials written to `part` via *nparts.
 size_t err_workspace_bytes(int64_t m, int64_t n);
+// W and Vw have pitch ldw (even, 16-byte aligned bases).
 hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, int64_t m,
-                            int64_t n, int64_t r, double* part, int64_t* nparts,
+                            int64_t n, int64_t r, int64_t ldw, double* part, int64_t* nparts,
                             hipStream_t stream);
 
 // Five partial sums per workgroup over a dense tensor: (T - a)^2, (T - b)^2,

@@ -34,12 +34,14 @@ __global__ __launch_bounds__(256) void k_diff_factors(const double* __restrict__
 // is exact in binary64 (at most 2 x 24 significand bits).
 template <typename T>
 __global__ __launch_bounds__(256) void k_widen_scaled(const T* __restrict__ h, const T* __restrict__ hs,
-                                                      int64_t rows, int64_t r, double* __restrict__ W) {
-    const int64_t total = rows * r;
+                                                      int64_t rows, int64_t r, int64_t ldw,
+                                                      double* __restrict__ W) {
+    const int64_t total = rows * ldw;
     for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
-        const int64_t t = idx % r;
-        const double sc = hs ? widen1(hs[t]) : 1.0;
-        W[idx] = widen1(h[idx]) * sc;
+        const int64_t i = idx / ldw, t = idx % ldw;
+        double v = 0.0;
+        if (t < r) v = widen1(h[i * r + t]) * (hs ? widen1(hs[t]) : 1.0);
+        W[idx] = v;
     }
 }
 
@@ -69,16 +71,16 @@ hipError_t launch_diff_factors(const double* ref, const void* h, int prec, int64
     return hipGetLastError();
 }
 
-hipError_t launch_widen_scaled(const void* h, const void* hs, int prec, int64_t rows, int64_t r, double* W,
-                               hipStream_t stream) {
-    const unsigned g = grid_for(rows * r);
+hipError_t launch_widen_scaled(const void* h, const void* hs, int prec, int64_t rows, int64_t r, int64_t ldw,
+                               double* W, hipStream_t stream) {
+    const unsigned g = grid_for(rows * ldw);
     KernelTimer tm("cert_widen", stream);
     if (prec == P64)
-        hipLaunchKernelGGL(k_widen_scaled<double>, dim3(g), dim3(256), 0, stream, (const double*)h, (const double*)hs, rows, r, W);
+        hipLaunchKernelGGL(k_widen_scaled<double>, dim3(g), dim3(256), 0, stream, (const double*)h, (const double*)hs, rows, r, ldw, W);
     else if (prec == P32)
-        hipLaunchKernelGGL(k_widen_scaled<float>, dim3(g), dim3(256), 0, stream, (const float*)h, (const float*)hs, rows, r, W);
+        hipLaunchKernelGGL(k_widen_scaled<float>, dim3(g), dim3(256), 0, stream, (const float*)h, (const float*)hs, rows, r, ldw, W);
     else
-        hipLaunchKernelGGL(k_widen_scaled<half_t>, dim3(g), dim3(256), 0, stream, (const half_t*)h, (const half_t*)hs, rows, r, W);
+        hipLaunchKernelGGL(k_widen_scaled<half_t>, dim3(g), dim3(256), 0, stream, (const half_t*)h, (const half_t*)hs, rows, r, ldw, W);
     return hipGetLastError();
 }
 
