@@ -3,8 +3,8 @@
 //
 // Apply (Sec. 4.4 eq. gpu_matrix_apply), two phases:
 //   phase 1  T'^T[c][j] = s_j * sum_i V[i][j] X[i][c]   (sum split over i in a
-//            fixed number of chunks, combined in chunk order by the last
-//            workgroup to finish: deterministic, no floating-point atomics)
+//            fixed number of chunks whose partials a second kernel adds in
+//            chunk order: deterministic, no floating-point atomics)
 //   phase 2  Y[i][c]    = sum_j U[i][j] T'^T[c][j]
 // T'^T is kept in the storage type: FP64 / FP32 accumulate and store in
 // their own precision; FP16 accumulates in FP32 and rounds T' once to FP16
@@ -17,9 +17,10 @@
 //   MFMA       otherwise: 128 x 128 (large shapes) or 64 x 64 output tiles
 //              on the 16x16 matrix cores (f64 16x16x4, f32 16x16x4, f16
 //              16x16x32 with FP32 accumulation); operands move in 16-byte
-//              chunks where the pitch allows, are staged through LDS and
-//              register double-buffered; workgroups are renumbered so that
-//              tiles sharing an operand run on the same XCD.
+//              chunks (operands with an unaligned pitch are first copied
+//              into a padded workspace), are staged through LDS with three
+//              K steps of loads in flight; workgroups are renumbered so
+//              that tiles sharing an operand run on the same XCD.
 #include <cstdlib>
 
 #include "lrc_device.h"
@@ -301,8 +302,41 @@ __device__ __forceinline__ int live_frags(int64_t start, int64_t lim) {
 
 enum { ATB_APPLY = 0, ATB_GRAM = 1 };
 
+// Store one finished fragment of C = A^T B (thread tid of the tile's
+// workgroup, fragment (fn, fm), tile origin (m0, n0)).
+//   ATB_APPLY: T'^T[n][ldo] = s[m] * C rounded to T, for m < Mout; rows
+//              m >= M are written as zeros (their accumulators hold data of
+//              clamped rows).
+//   ATB_GRAM : G[m][ldo] = C in double (T = double), m < M.
+template <typename T, class C, int MODE>
+__device__ __forceinline__ void atb_store(const typename C::AccV& a, int tid, int fn, int fm, int64_t m0,
+                                          int64_t n0, int64_t M, int64_t N, const T* __restrict__ svals,
+                                          void* __restrict__ out, int64_t ldo, int64_t Mout) {
+    using Acc = typename C::Acc;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / C::WN, wn = wave % C::WN;
+    const int r = lane & 15, g = lane >> 4;
+    const int64_t mm = m0 + wm * C::WTM + fm * 16 + r;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        const int64_t nn = n0 + wn * C::WTN + fn * 16 + acc_row<T>(g, v);
+        if (MODE == ATB_APPLY) {
+            if (nn < N && mm < Mout) {
+                const Acc val = (mm < M) ? to_acc(svals[mm]) * a[v] : Acc(0);
+                static_cast<T*>(out)[nn * ldo + mm] = to_storage<T>(val);
+            }
+        } else {
+            if (nn < N && mm < M) static_cast<double*>(out)[mm * ldo + nn] = (double)a[v];
+        }
+    }
+}
+
 // C[m][n] = sum_{i in chunk} A[i][m] B[i][n]  (both sources [K][ld], row
-// index contiguous).  Grid (tiles_n, tiles_m, splits).
+// index contiguous).  One workgroup per (tile, split).  With one split the
+// workgroup stores its tile (atb_store); otherwise it writes a partial tile
+// and k_atb_finish, launched next on the same stream, sums them.  Kernel
+// boundaries order the partials: no device-scope fences, which on this
+// chip write back and invalidate the L2 of the XCD.
 //   ATB_APPLY: out is T'^T[n][ldo] in T, value s[m] * C (s[m] = 0 for m >= M),
 //              written for m < Mout (zero padding rows included).
 //   ATB_GRAM : out is G[m][ldo] in double (T = double).
@@ -310,13 +344,11 @@ template <typename T, class C, int MODE>
 __global__ __launch_bounds__(C::NT) void k_atb(
     const T* __restrict__ Asrc, int64_t lda, const T* __restrict__ Bsrc, int64_t ldb,
     int64_t M, int64_t N, int64_t K, int64_t chunk, int tiles_m, int tiles_n, int splits,
-    typename C::Acc* __restrict__ part, int* __restrict__ counters,
-    const T* __restrict__ svals, void* __restrict__ out, int64_t ldo, int64_t Mout) {
-    using Acc = typename C::Acc;
+    typename C::Acc* __restrict__ part, const T* __restrict__ svals, void* __restrict__ out, int64_t ldo,
+    int64_t Mout) {
     using AccV = typename C::AccV;
     __shared__ alignas(16) T As[C::BK * C::LDA_R];
     __shared__ alignas(16) T Bs[C::BK * C::LDB_R];
-    __shared__ int last_flag;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -343,83 +375,82 @@ __global__ __launch_bounds__(C::NT) void k_atb(
     constexpr int NS = kStages;
     TA ta[NS];
     TB tb[NS];
+    // Every stage slot issues its loads unconditionally (steps past the end
+    // read clamped addresses and are never used), so the order of loads is
+    // the same on every path and each wait covers exactly one stage.
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
-    const int last_partial = ((kend - kbeg) % C::BK) ? nsteps - 1 : -1;
 #pragma unroll
-    for (int st = 0; st < NS; ++st)
-        if (st < nsteps) {
-            ta[st].fetch(ga, kbeg + st * C::BK, st == last_partial, kend);
-            tb[st].fetch(gb, kbeg + st * C::BK, st == last_partial, kend);
-        }
+    for (int st = 0; st < NS; ++st) {
+        const int64_t k0 = kbeg + (int64_t)st * C::BK;
+        ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
+        tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
+    }
     for (int j0 = 0; j0 < nsteps; j0 += NS) {
 #pragma unroll
         for (int st = 0; st < NS; ++st) {
             const int j = j0 + st;
-            if (j < nsteps) {
-                const int64_t k0 = kbeg + (int64_t)j * C::BK;
-                ta[st].stash(As, ga, k0, j == last_partial, kend);
-                tb[st].stash(Bs, gb, k0, j == last_partial, kend);
-                __syncthreads();
-                const int jn = j + NS;
-                if (jn < nsteps) {
-                    ta[st].fetch(ga, kbeg + (int64_t)jn * C::BK, jn == last_partial, kend);
-                    tb[st].fetch(gb, kbeg + (int64_t)jn * C::BK, jn == last_partial, kend);
-                }
-                mma_rows<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
-                __syncthreads();
+            const int64_t k0 = kbeg + (int64_t)j * C::BK;
+            const bool live = j < nsteps;
+            if (live) {
+                ta[st].stash(As, ga, k0, k0 + C::BK > kend, kend);
+                tb[st].stash(Bs, gb, k0, k0 + C::BK > kend, kend);
             }
+            __syncthreads();
+            const int64_t kn = k0 + (int64_t)NS * C::BK;
+            ta[st].fetch(ga, kn, kn + C::BK > kend, kend);
+            tb[st].fetch(gb, kn, kn + C::BK > kend, kend);
+            if (live) mma_rows<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
+            __syncthreads();
         }
     }
 
-    const int r = lane & 15, g = lane >> 4;
     if (splits > 1) {
-        // partials of dead fragments are neither written nor read
-        constexpr int NV = C::FN * C::FM * 4;
-        Acc* mine = part + ((tile * splits + sp) * NV) * C::NT;
+        // partial tile: one accumulator vector per fragment, consecutive
+        // threads on consecutive vectors; k_atb_finish sums the splits
+        constexpr int NF = C::FN * C::FM;
+        AccV* mine = reinterpret_cast<AccV*>(part) + ((tile * splits + sp) * NF) * C::NT + tid;
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
-            for (int fm = 0; fm < C::FM; ++fm)
-                if (fn < nfn && fm < nfm)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) mine[((fn * C::FM + fm) * 4 + v) * C::NT + tid] = acc[fn][fm][v];
-        if (!arrive_last(counters + tile, splits, &last_flag)) return;
-        // every partial, this workgroup's included, is read back in split order
-#pragma unroll
-        for (int fn = 0; fn < C::FN; ++fn)
-#pragma unroll
-            for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = zero_accv<AccV>();
-        for (int q = 0; q < splits; ++q) {
-            const Acc* src = part + ((tile * splits + q) * NV) * C::NT;
-#pragma unroll
-            for (int fn = 0; fn < C::FN; ++fn)
-#pragma unroll
-                for (int fm = 0; fm < C::FM; ++fm)
-                    if (fn < nfn && fm < nfm)
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            acc[fn][fm][v] += __builtin_nontemporal_load(&src[((fn * C::FM + fm) * 4 + v) * C::NT + tid]);
-        }
+            for (int fm = 0; fm < C::FM; ++fm) mine[(fn * C::FM + fm) * C::NT] = acc[fn][fm];
+        return;
     }
-
 #pragma unroll
     for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm) {
-            const int64_t mm = m0 + wm * C::WTM + fm * 16 + r;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int64_t nn = n0 + wn * C::WTN + fn * 16 + acc_row<T>(g, v);
-                if (MODE == ATB_APPLY) {
-                    if (nn < N && mm < Mout) {
-                        const Acc val = (mm < M) ? to_acc(svals[mm]) * acc[fn][fm][v] : Acc(0);
-                        static_cast<T*>(out)[nn * ldo + mm] = to_storage<T>(val);
-                    }
-                } else {
-                    if (nn < N && mm < M) static_cast<double*>(out)[mm * ldo + nn] = (double)acc[fn][fm][v];
-                }
-            }
-        }
+        for (int fm = 0; fm < C::FM; ++fm)
+            atb_store<T, C, MODE>(acc[fn][fm], tid, fn, fm, m0, n0, M, N, svals, out, ldo, Mout);
+}
+
+// Sum of the split partials of k_atb, in split order, then the same store.
+// One workgroup per (tile, fragment); thread t holds the vector that thread
+// t of the tile's workgroups produced.
+template <typename T, class C, int MODE>
+__global__ __launch_bounds__(C::NT) void k_atb_finish(
+    const typename C::AccV* __restrict__ part, int64_t M, int64_t N, int tiles_m, int splits,
+    const T* __restrict__ svals, void* __restrict__ out, int64_t ldo, int64_t Mout) {
+    using AccV = typename C::AccV;
+    constexpr int NF = C::FN * C::FM;
+    const int tid = threadIdx.x;
+    const int64_t tile = blockIdx.x / NF;
+    const int f = blockIdx.x % NF;
+    const AccV* src = part + (tile * splits * NF + f) * C::NT + tid;
+    const int64_t qs = (int64_t)NF * C::NT;      // stride between splits
+    AccV acc = zero_accv<AccV>();
+    int q = 0;
+    for (; q + 4 <= splits; q += 4) {
+        const AccV p0 = __builtin_nontemporal_load(src + (q + 0) * qs);
+        const AccV p1 = __builtin_nontemporal_load(src + (q + 1) * qs);
+        const AccV p2 = __builtin_nontemporal_load(src + (q + 2) * qs);
+        const AccV p3 = __builtin_nontemporal_load(src + (q + 3) * qs);
+        acc += p0;
+        acc += p1;
+        acc += p2;
+        acc += p3;
+    }
+    for (; q < splits; ++q) acc += __builtin_nontemporal_load(src + q * qs);
+    const int64_t m0 = (tile % tiles_m) * C::BM, n0 = (tile / tiles_m) * C::BN;
+    atb_store<T, C, MODE>(acc, tid, f / C::FM, f % C::FM, m0, n0, M, N, svals, out, ldo, Mout);
 }
 
 enum { ABT_STORE = 0, ABT_ERR = 1 };
@@ -462,29 +493,27 @@ __global__ __launch_bounds__(C::NT) void k_abt(
     TB tb[NS];
     const int nsteps = (int)((K + C::BK - 1) / C::BK);
 #pragma unroll
-    for (int st = 0; st < NS; ++st)
-        if (st < nsteps) {
-            const int64_t k0 = (int64_t)st * C::BK;
-            ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
-            tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
-        }
+    for (int st = 0; st < NS; ++st) {
+        const int64_t k0 = (int64_t)st * C::BK;
+        ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
+        tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
+    }
     for (int j0 = 0; j0 < nsteps; j0 += NS) {
 #pragma unroll
         for (int st = 0; st < NS; ++st) {
             const int j = j0 + st;
-            if (j < nsteps) {
-                const int64_t k0 = (int64_t)j * C::BK;
+            const int64_t k0 = (int64_t)j * C::BK;
+            const bool live = j < nsteps;
+            if (live) {
                 ta[st].stash(As, ga, k0, k0 + C::BK > Ka, Ka);
                 tb[st].stash(Bs, gb, k0, k0 + C::BK > Kb, Kb);
-                __syncthreads();
-                const int64_t kn = k0 + (int64_t)NS * C::BK;
-                if (kn < K) {
-                    ta[st].fetch(ga, kn, kn + C::BK > Ka, Ka);
-                    tb[st].fetch(gb, kn, kn + C::BK > Kb, Kb);
-                }
-                mma_k<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
-                __syncthreads();
             }
+            __syncthreads();
+            const int64_t kn = k0 + (int64_t)NS * C::BK;
+            ta[st].fetch(ga, kn, kn + C::BK > Ka, Ka);
+            tb[st].fetch(gb, kn, kn + C::BK > Kb, Kb);
+            if (live) mma_k<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
+            __syncthreads();
         }
     }
 
@@ -546,9 +575,24 @@ static bool vec_ok(const void* p, int64_t ld) {
     return (ld % VEC == 0) && (reinterpret_cast<uintptr_t>(p) % 16 == 0);
 }
 
-template <typename T, class C, int MODE, class... Args>
-static void launch_atb(dim3 grid, hipStream_t st, Args... args) {
-    hipLaunchKernelGGL((k_atb<T, C, MODE>), grid, dim3(C::NT), 0, st, args...);
+// k_atb over all (tile, split) workgroups, then k_atb_finish when the sum is split.
+template <typename T, class C, int MODE>
+static void run_atb(const char* label, const char* finish_label, hipStream_t st, const T* A, int64_t lda,
+                    const T* B, int64_t ldb, int64_t M, int64_t N, int64_t K, int64_t chunk, int tiles_m, int tiles_n,
+                    int splits, typename C::Acc* part, const T* svals, void* out, int64_t ldo, int64_t Mout) {
+    {
+        KernelTimer t(label, st);
+        const dim3 grid((unsigned)((int64_t)tiles_m * tiles_n * splits));
+        hipLaunchKernelGGL((k_atb<T, C, MODE>), grid, dim3(C::NT), 0, st, A, lda, B, ldb, M, N, K, chunk, tiles_m,
+                           tiles_n, splits, part, svals, out, ldo, Mout);
+    }
+    if (splits > 1) {
+        KernelTimer t(finish_label, st);
+        const dim3 grid((unsigned)((int64_t)tiles_m * tiles_n * C::FN * C::FM));
+        hipLaunchKernelGGL((k_atb_finish<T, C, MODE>), grid, dim3(C::NT), 0, st,
+                           reinterpret_cast<const typename C::AccV*>(part), M, N, tiles_m, splits, svals, out, ldo,
+                           Mout);
+    }
 }
 template <typename T, class C, int MODE, class... Args>
 static void launch_abt(dim3 grid, hipStream_t st, Args... args) {
@@ -580,16 +624,14 @@ static void pitch_copy(const T* src, int64_t rows, int64_t cols, int64_t lds, T*
 // Phase 1, batch <= NB: workgroup (jg, sp) owns columns [64 jg, 64 jg + 64)
 // of V and rows [sp*chunk, (sp+1)*chunk) of V and X.  Lane j of every wave
 // accumulates column j; the four waves take interleaved rows and are summed
-// in wave order.  The last workgroup of each column group combines the
-// per-chunk partials in chunk order, scales by s and writes T'^T.
+// in wave order.  k_p1_stream_finish then combines the per-chunk partials
+// in chunk order, scales by s and writes T'^T.
 template <typename T, int NB>
 __global__ __launch_bounds__(256) void k_p1_stream(
-    const T* __restrict__ V, const T* __restrict__ X, const T* __restrict__ s, T* __restrict__ Tt,
-    int64_t ldt, typename PrecTraits<T>::acc* __restrict__ part, int* __restrict__ counters,
+    const T* __restrict__ V, const T* __restrict__ X, typename PrecTraits<T>::acc* __restrict__ part,
     int64_t n, int64_t k, int64_t b, int64_t chunk, int splits) {
     using Acc = typename PrecTraits<T>::acc;
     __shared__ Acc red[4][64][NB];
-    __shared__ int last_flag;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int jg = blockIdx.x, sp = blockIdx.y;
     const int64_t j = (int64_t)jg * 64 + lane;
@@ -617,8 +659,16 @@ __global__ __launch_bounds__(256) void k_p1_stream(
             part[(((int64_t)jg * splits + sp) * 64 + lane) * NB + c] = t;
         }
     }
-    if (!arrive_last(counters + jg, splits, &last_flag)) return;
-    // columns of this group, including the zero rows j in [k, ldt) of T'^T
+}
+
+// One workgroup per column group: the columns of the group, including the
+// zero rows j in [k, ldt) of T'^T.
+template <typename T, int NB>
+__global__ __launch_bounds__(256) void k_p1_stream_finish(
+    const typename PrecTraits<T>::acc* __restrict__ part, const T* __restrict__ s, T* __restrict__ Tt,
+    int64_t ldt, int64_t k, int64_t b, int splits) {
+    using Acc = typename PrecTraits<T>::acc;
+    const int tid = threadIdx.x, jg = blockIdx.x;
     for (int idx = tid; idx < 64 * NB; idx += 256) {
         const int jl = idx / NB, c = idx % NB;
         const int64_t jj = (int64_t)jg * 64 + jl;
@@ -722,7 +772,6 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         p.splits = (int)((n + p.chunk - 1) / p.chunk);
         const int nb = (b <= 1) ? 1 : (b <= 2) ? 2 : (b <= 4) ? 4 : 8;
         p.part_bytes = (size_t)p.tiles_m * p.splits * 64 * nb * acc_b;
-        p.counters = (size_t)p.tiles_m;
     } else {
         const int BK = (prec == P16) ? 32 : 16;
         // phase 1: C = V^T X is k x b, summed over n
@@ -742,7 +791,6 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         p.chunk = round_up((n + splits - 1) / splits, BK);
         p.splits = (int)((n + p.chunk - 1) / p.chunk);
         p.part_bytes = (p.splits > 1) ? (size_t)base * p.splits * T1 * T1 * acc_b : 0;
-        p.counters = (p.splits > 1) ? (size_t)base : 0;
         // phase 2: Y = U T' is m x b
         const int64_t big_tiles = ((m + 127) / 128) * ((b + 127) / 128);
         p.big2 = (m >= 128 && b >= 128 && big_tiles >= 256) ? 1 : 0;
@@ -771,11 +819,13 @@ template <typename T> static const char* p1_stream_label();
 template <typename T> static const char* p2_stream_label();
 template <typename T> static const char* p1_mfma_label();
 template <typename T> static const char* p2_mfma_label();
+template <typename T> static const char* p1_finish_label();
 #define LRC_LABELS(T, S)                                                          \
     template <> const char* p1_stream_label<T>() { return "apply_p1_stream_" S; } \
     template <> const char* p2_stream_label<T>() { return "apply_p2_stream_" S; } \
     template <> const char* p1_mfma_label<T>() { return "apply_p1_mfma_" S; }     \
-    template <> const char* p2_mfma_label<T>() { return "apply_p2_mfma_" S; }
+    template <> const char* p2_mfma_label<T>() { return "apply_p2_mfma_" S; }     \
+    template <> const char* p1_finish_label<T>() { return "apply_p1_finish_" S; }
 LRC_LABELS(double, "f64")
 LRC_LABELS(float, "f32")
 LRC_LABELS(half_t, "f16")
@@ -788,14 +838,19 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     using Acc = typename PrecTraits<T>::acc;
     Acc* part = static_cast<Acc*>(ws.take(p.part_bytes));
     T* Tt = static_cast<T*>(ws.take(p.mid_bytes));
-    int* counters = ws.counters;
-    if (ws.overrun || !Tt || (p.counters && ws.n_counters < p.counters)) return hipErrorOutOfMemory;
+    if (ws.overrun || !Tt) return hipErrorOutOfMemory;
     const int64_t ldt = p.Kp;
     if (p.path == 1) {
         dim3 g1(p.tiles_m, p.splits);
         {
             KernelTimer t1(p1_stream_label<T>(), stream);
-#define LRC_P1S(NB) hipLaunchKernelGGL((k_p1_stream<T, NB>), g1, dim3(256), 0, stream, V, X, s, Tt, ldt, part, counters, n, k, b, p.chunk, p.splits)
+#define LRC_P1S(NB)                                                                                       \
+    do {                                                                                                  \
+        hipLaunchKernelGGL((k_p1_stream<T, NB>), g1, dim3(256), 0, stream, V, X, part, n, k, b, p.chunk,  \
+                           p.splits);                                                                     \
+        hipLaunchKernelGGL((k_p1_stream_finish<T, NB>), dim3(p.tiles_m), dim3(256), 0, stream, part, s,  \
+                           Tt, ldt, k, b, p.splits);                                                      \
+    } while (0)
             if (b <= 1) LRC_P1S(1); else if (b <= 2) LRC_P1S(2); else if (b <= 4) LRC_P1S(4); else LRC_P1S(8);
 #undef LRC_P1S
         }
@@ -838,18 +893,14 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    {
-        KernelTimer t1(p1_mfma_label<T>(), stream);
-        const dim3 g1((unsigned)((int64_t)p.tiles_m * p.tiles_n * p.splits));
-        if (p.big1)
-            launch_atb<T, typename BigCfg<T>::C, ATB_APPLY>(g1, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk,
-                                                            p.tiles_m, p.tiles_n, p.splits, part, counters, s,
-                                                            (void*)Tt, ldt, ldt);
-        else
-            launch_atb<T, typename SmallCfg<T>::C, ATB_APPLY>(g1, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk,
-                                                              p.tiles_m, p.tiles_n, p.splits, part, counters, s,
-                                                              (void*)Tt, ldt, ldt);
-    }
+    if (p.big1)
+        run_atb<T, typename BigCfg<T>::C, ATB_APPLY>(p1_mfma_label<T>(), p1_finish_label<T>(), stream, Vg, ldv, Xg,
+                                                     ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n, p.splits, part, s,
+                                                     (void*)Tt, ldt, ldt);
+    else
+        run_atb<T, typename SmallCfg<T>::C, ATB_APPLY>(p1_mfma_label<T>(), p1_finish_label<T>(), stream, Vg, ldv,
+                                                       Xg, ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n, p.splits,
+                                                       part, s, (void*)Tt, ldt, ldt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     KernelTimer t2(p2_mfma_label<T>(), stream);
@@ -900,11 +951,10 @@ static void gram_plan(int64_t rows, int64_t cols, int* tiles, int* splits, int64
     *tiles = t;
 }
 
-size_t gram_workspace_bytes(int64_t rows, int64_t cols, size_t* counters) {
+size_t gram_workspace_bytes(int64_t rows, int64_t cols) {
     int t, sp;
     int64_t ch;
     gram_plan(rows, cols, &t, &sp, &ch);
-    *counters = (size_t)t * t;
     return (size_t)t * t * sp * 64 * 64 * sizeof(double);
 }
 
@@ -914,12 +964,10 @@ hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G, W
     int64_t ch;
     gram_plan(rows, cols, &t, &sp, &ch);
     double* part = static_cast<double*>(ws.take((size_t)t * t * sp * 64 * 64 * sizeof(double)));
-    if (ws.overrun || (sp > 1 && ws.n_counters < (size_t)t * t)) return hipErrorOutOfMemory;
+    if (ws.overrun) return hipErrorOutOfMemory;
     if (!vec_ok<double>(P, cols)) return hipErrorInvalidValue;   // the factor builders keep 2r columns
-    const dim3 g((unsigned)((int64_t)t * t * sp));
-    KernelTimer tm("cert_gram_f64", stream);
-    launch_atb<double, GramC, ATB_GRAM>(g, stream, P, cols, P, cols, cols, cols, rows, ch, t, t, sp, part,
-                                        ws.counters, (const double*)nullptr, (void*)G, cols, cols);
+    run_atb<double, GramC, ATB_GRAM>("cert_gram_f64", "cert_gram_finish_f64", stream, P, cols, P, cols, cols, cols,
+                                     rows, ch, t, t, sp, part, (const double*)nullptr, (void*)G, cols, cols);
     return hipGetLastError();
 }
 

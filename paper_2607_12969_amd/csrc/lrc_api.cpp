@@ -176,7 +176,7 @@ int tt_reconstruct_impl(const void* const* cores, const int64_t* dims, const int
                     (long long)ranks[d - 1]);
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
-    hipError_t e0 = ws.reserve(plan.stage_bytes, 0, st);
+    hipError_t e0 = ws.reserve(plan.stage_bytes, st);
     if (e0 != hipSuccess) return fail_hip(e0, "workspace");
     hipError_t e = launch_tt(plan, cores, out, ws, st);
     return e == hipSuccess ? LRC_OK : fail_hip(e, "TT reconstruction launch");
@@ -243,7 +243,7 @@ KernelTimer::~KernelTimer() {
 
 // ------------------------------------------------------------- Workspace --
 namespace lrc {
-hipError_t Workspace::reserve(size_t bytes, size_t counters_needed, hipStream_t stream) {
+hipError_t Workspace::reserve(size_t bytes, hipStream_t stream) {
     bytes = (size_t)round_up((int64_t)bytes, 256) + 256;
     if (bytes > cap) {
         if (base) {
@@ -260,24 +260,6 @@ hipError_t Workspace::reserve(size_t bytes, size_t counters_needed, hipStream_t 
             return e;
         }
         cap = want;
-    }
-    if (counters_needed > n_counters) {
-        if (counters) {
-            hipError_t e = hipStreamSynchronize(stream);
-            if (e != hipSuccess) return e;
-            (void)hipFree(counters);
-            counters = nullptr;
-            n_counters = 0;
-        }
-        size_t want = std::max<size_t>(counters_needed, 1024);
-        hipError_t e = hipMalloc(reinterpret_cast<void**>(&counters), want * sizeof(int));
-        if (e != hipSuccess) {
-            counters = nullptr;
-            return e;
-        }
-        e = hipMemset(counters, 0, want * sizeof(int));
-        if (e != hipSuccess) return e;
-        n_counters = want;
     }
     used = 0;
     return hipSuccess;
@@ -297,10 +279,8 @@ void* Workspace::take(size_t bytes) {
 
 void Workspace::release() {
     if (base) (void)hipFree(base);
-    if (counters) (void)hipFree(counters);
     base = nullptr;
-    counters = nullptr;
-    cap = n_counters = used = 0;
+    cap = used = 0;
 }
 }  // namespace lrc
 
@@ -360,7 +340,7 @@ int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X,
     ApplyPlan plan = plan_apply(m, n, k, batch, prec, g_force_path, U, V, X);
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
-    hipError_t he = ws.reserve(apply_workspace_bytes(plan), plan.counters, st);
+    hipError_t he = ws.reserve(apply_workspace_bytes(plan), st);
     if (he != hipSuccess) return fail_hip(he, "workspace");
     he = launch_apply(plan, U, s, V, X, Y, m, n, k, batch, prec, ws, st);
     if (he != hipSuccess) return fail_hip(he, "apply launch");
@@ -492,16 +472,15 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
 
     // workspace
     const int64_t w2 = 2 * r;
-    size_t cnt1, cnt2;
-    const size_t gp1 = gram_workspace_bytes(m, w2, &cnt1);
-    const size_t gp2 = gram_workspace_bytes(n, w2, &cnt2);
+    const size_t gp1 = gram_workspace_bytes(m, w2);
+    const size_t gp2 = gram_workspace_bytes(n, w2);
     size_t need = (size_t)(m + n) * w2 * 8 + 2 * (size_t)w2 * w2 * 8 + gp1 + gp2 + 16 * 256;
     const bool have_A = a->A != nullptr;
     const int64_t rp = round_up(r, 2);   // pitch of the widened factors: 16-byte rows
     if (have_A) need += (size_t)(m + n) * rp * 8 + err_workspace_bytes(m, n) + 4 * 256;
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
-    hipError_t he = ws.reserve(need, std::max(cnt1, cnt2), st);
+    hipError_t he = ws.reserve(need, st);
     if (he != hipSuccess) return fail_hip(he, "workspace");
     double* P = static_cast<double*>(ws.take((size_t)m * w2 * 8));
     double* Q = static_cast<double*>(ws.take((size_t)n * w2 * 8));
@@ -621,7 +600,7 @@ static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
     size_t need = 3 * (size_t)N * 8 + (size_t)cnt_aug * 8 + 5 * (size_t)groups * 8 + 64 + (size_t)(8 + d) * 256;
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
-    hipError_t he = ws.reserve(need, 0, st);
+    hipError_t he = ws.reserve(need, st);
     if (he != hipSuccess) return fail_hip(he, "workspace");
     double* TR = static_cast<double*>(ws.take((size_t)N * 8));
     double* TRp = static_cast<double*>(ws.take((size_t)N * 8));

@@ -106,24 +106,4 @@ __device__ __forceinline__ Acc wave_sum(Acc x) {
     return x;
 }
 
-// Split-reduction handshake.  Every workgroup that contributes a partial
-// result for `slot` calls this after writing its partial; exactly one (the
-// last to arrive) gets `true` and then reads all partials in a fixed order,
-// so the final sum does not depend on scheduling.  The counter is reset by
-// the winner, so it is zero again for the next launch.
-__device__ __forceinline__ bool arrive_last(int* counter, int expected, int* lds_flag) {
-    __threadfence();          // release this workgroup's partial (device scope)
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int old = atomicAdd(counter, 1);
-        int last = (old == expected - 1);
-        if (last) *counter = 0;
-        *lds_flag = last;
-    }
-    __syncthreads();
-    bool last = *lds_flag != 0;
-    if (last) __threadfence();   // acquire the other workgroups' partials
-    return last;
-}
-
 }  // namespace lrc

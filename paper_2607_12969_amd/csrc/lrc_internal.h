@@ -23,10 +23,8 @@ struct Workspace {
     char* base = nullptr;
     size_t cap = 0;
     size_t used = 0;
-    int* counters = nullptr;      // zero-initialised split-reduction counters
-    size_t n_counters = 0;
     bool overrun = false;         // a take() exceeded the reservation
-    hipError_t reserve(size_t bytes, size_t counters_needed, hipStream_t stream);
+    hipError_t reserve(size_t bytes, hipStream_t stream);
     void* take(size_t bytes);     // nullptr (and overrun = true) past the reservation
     void reset() { used = 0; overrun = false; }
     void release();
@@ -60,7 +58,6 @@ struct ApplyPlan {
     size_t stage_bytes;
     size_t part_bytes;   // partial-sum buffer
     size_t mid_bytes;    // T'^T buffer
-    size_t counters;
 };
 
 // U, V, X are only inspected for alignment (may be null).
@@ -74,7 +71,7 @@ hipError_t launch_apply(const ApplyPlan& p, const void* U, const void* s, const 
 
 // ------------------------------------------------------- certificate (matrix)
 // G = P^T P for P (rows x cols, row-major, FP64): a split-sum Gram product.
-size_t gram_workspace_bytes(int64_t rows, int64_t cols, size_t* counters);
+size_t gram_workspace_bytes(int64_t rows, int64_t cols);
 hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G,
                        Workspace& ws, hipStream_t stream);
 
