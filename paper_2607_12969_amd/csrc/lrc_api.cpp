@@ -86,41 +86,6 @@ Workspace& workspace_for(int dev, hipStream_t s) {
     return g_ws[std::make_pair(dev, s)];
 }
 
-double half_bits_to_double(uint16_t b) {
-    const int sg = (b >> 15) & 1, ex = (b >> 10) & 0x1F, fr = b & 0x3FF;
-    double v;
-    if (ex == 0) v = std::ldexp((double)fr, -24);
-    else if (ex == 31) v = fr ? NAN : INFINITY;
-    else v = std::ldexp((double)(1024 + fr), ex - 25);
-    return sg ? -v : v;
-}
-
-// host copy of `count` stored values as binary64
-int fetch_widened(const void* dev_ptr, int prec, int64_t count, std::vector<double>& out, hipStream_t st) {
-    out.assign((size_t)count, 0.0);
-    const size_t nb = (size_t)count * elem_bytes(prec);
-    std::vector<unsigned char> raw(nb);
-    hipError_t e = hipMemcpyAsync(raw.data(), dev_ptr, nb, hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipStreamSynchronize(st);
-    if (e != hipSuccess) return fail_hip(e, "copy to host");
-    for (int64_t i = 0; i < count; ++i) {
-        if (prec == LRC_FP64) {
-            double v;
-            std::memcpy(&v, raw.data() + 8 * i, 8);
-            out[i] = v;
-        } else if (prec == LRC_FP32) {
-            float v;
-            std::memcpy(&v, raw.data() + 4 * i, 4);
-            out[i] = v;
-        } else {
-            uint16_t v;
-            std::memcpy(&v, raw.data() + 2 * i, 2);
-            out[i] = half_bits_to_double(v);
-        }
-    }
-    return LRC_OK;
-}
-
 int64_t tt_count(const int64_t* dims, const int64_t* ranks, int d) {
     int64_t tot = 0;
     for (int l = 0; l < d; ++l) {
@@ -474,7 +439,7 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
     const int64_t w2 = 2 * r;
     const size_t gp1 = gram_workspace_bytes(m, w2);
     const size_t gp2 = gram_workspace_bytes(n, w2);
-    size_t need = (size_t)(m + n) * w2 * 8 + 2 * (size_t)w2 * w2 * 8 + gp1 + gp2 + 16 * 256;
+    size_t need = (size_t)(m + n) * w2 * 8 + 2 * (size_t)w2 * w2 * 8 + gp1 + gp2 + (size_t)w2 * 8 + 16 * 256;
     const bool have_A = a->A != nullptr;
     const int64_t rp = round_up(r, 2);   // pitch of the widened factors: 16-byte rows
     if (have_A) need += (size_t)(m + n) * rp * 8 + err_workspace_bytes(m, n) + 4 * 256;
@@ -506,53 +471,18 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
         if (he == hipSuccess) he = launch_reduce_rows(part, nparts, 1, errsum, st);
         if (he != hipSuccess) return fail_hip(he, "error-norm launch");
     }
-    std::vector<double> hGu((size_t)w2 * w2), hGq((size_t)w2 * w2), s64, sh64;
-    double err2 = NAN;
-    he = hipMemcpyAsync(hGu.data(), Gu, hGu.size() * 8, hipMemcpyDeviceToHost, st);
-    if (he == hipSuccess) he = hipMemcpyAsync(hGq.data(), Gq, hGq.size() * 8, hipMemcpyDeviceToHost, st);
-    if (he == hipSuccess && have_A) he = hipMemcpyAsync(&err2, errsum, 8, hipMemcpyDeviceToHost, st);
+    // eta^2 on the device; the host reads back two numbers
+    double* eta_part = static_cast<double*>(ws.take((size_t)w2 * 8));
+    double* sums = static_cast<double*>(ws.take(16));
+    if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
+    he = launch_eta2(Gu, Gq, a->s, a->sh, a->prec, r, eta_part, st);
+    if (he == hipSuccess) he = launch_reduce_rows(eta_part, w2, 1, sums, st);
+    if (he == hipSuccess && have_A) he = hipMemcpyAsync(sums + 1, errsum, 8, hipMemcpyDeviceToDevice, st);
+    double hs[2] = {NAN, NAN};
+    if (he == hipSuccess) he = hipMemcpyAsync(hs, sums, have_A ? 16 : 8, hipMemcpyDeviceToHost, st);
     if (he == hipSuccess) he = hipStreamSynchronize(st);
     if (he != hipSuccess) return fail_hip(he, "certificate readback");
-    rc = fetch_widened(a->s, LRC_FP64, r, s64, st);
-    if (rc) return rc;
-    rc = fetch_widened(a->sh, a->prec, r, sh64, st);
-    if (rc) return rc;
-
-    // eta^2 = ||P M Q^T||_F^2 = trace(M^T Gu M Gq) with P = [U dU], Q = [V dV]
-    // and M = [[dS, S^], [S^, S^]] (rows U | dU, columns V | dV), i.e.
-    //   A^_{k+1} - A_{k+1} = U dS V^T + U S^ dV^T + dU S^ V^T + dU S^ dV^T.
-    // Every term is of the size of the perturbation, so nothing of the size
-    // of ||A|| cancels.  Column a of M has two non-zeros:
-    //   a < r : M[a][a] = dS_a,  M[r+a][a] = S^_a
-    //   a >= r: M[a-r][a] = S^_{a-r}, M[a][a] = S^_{a-r}
-    auto nz = [&](int64_t col, int64_t* rows, double* vals) {
-        if (col < r) {
-            rows[0] = col;
-            vals[0] = sh64[(size_t)col] - s64[(size_t)col];
-            rows[1] = r + col;
-            vals[1] = sh64[(size_t)col];
-        } else {
-            rows[0] = col - r;
-            vals[0] = sh64[(size_t)(col - r)];
-            rows[1] = col;
-            vals[1] = sh64[(size_t)(col - r)];
-        }
-    };
-    double eta2 = 0.0;
-    for (int64_t ca = 0; ca < w2; ++ca) {
-        int64_t ra[2];
-        double va[2];
-        nz(ca, ra, va);
-        for (int64_t cb = 0; cb < w2; ++cb) {
-            int64_t rb[2];
-            double vb[2];
-            nz(cb, rb, vb);
-            double h = 0.0;
-            for (int x = 0; x < 2; ++x)
-                for (int y = 0; y < 2; ++y) h += va[x] * hGu[(size_t)(ra[x] * w2 + rb[y])] * vb[y];
-            eta2 += h * hGq[(size_t)(cb * w2 + ca)];
-        }
-    }
+    const double eta2 = hs[0], err2 = hs[1];
     res->eta = std::sqrt(std::max(eta2, 0.0));
     res->err_new = have_A ? std::sqrt(err2) : NAN;
     finish_flags(res, have_A);

@@ -88,6 +88,10 @@ hipError_t launch_widen(const void* src, int prec, int64_t count, double* out, h
 // Partial sums of (A - W Vw^T)^2 over m x n, one per workgroup; returns the
 // number of partials written to `part` via *nparts.
 size_t err_workspace_bytes(int64_t m, int64_t n);
+// part[a] for a < 2r: the per-column terms of eta^2 = trace(M^T Gu M Gq) of
+// the matrix certificate (Gu, Gq: 2r x 2r Gram matrices of [U dU], [V dV]).
+hipError_t launch_eta2(const double* Gu, const double* Gq, const double* s, const void* sh, int prec, int64_t r,
+                       double* part, hipStream_t stream);
 // W and Vw have pitch ldw (even, 16-byte aligned bases).
 hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, int64_t m,
                             int64_t n, int64_t r, int64_t ldw, double* part, int64_t* nparts,

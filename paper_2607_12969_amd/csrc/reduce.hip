@@ -141,6 +141,74 @@ hipError_t launch_sumsq5(const double* T, const double* a, const double* b, cons
     return hipGetLastError();
 }
 
+// eta^2 = ||P M Q^T||_F^2 = trace(M^T Gu M Gq) for the matrix certificate
+// (Thm. thm:matrix_rank_compensation), with P = [U dU], Q = [V dV] and
+//   M = [[dS, S^], [S^, S^]]  (rows U | dU, columns V | dV),
+// since A^_{k+1} - A_{k+1} = U dS V^T + U S^ dV^T + dU S^ V^T + dU S^ dV^T.
+// Every term has the size of the perturbation, so nothing of the size of
+// ||A|| cancels.  Column a of M has two non-zeros:
+//   a < r : M[a][a] = dS_a,      M[r+a][a] = S^_a
+//   a >= r: M[a-r][a] = S^_{a-r}, M[a][a]  = S^_{a-r}
+// Workgroup ca writes part[ca] = sum_cb (M^T Gu M)[ca][cb] * Gq[cb][ca],
+// each term summed in a fixed order.
+// shv = S^ of the column's index modulo r
+__device__ __forceinline__ void eta_nz(int64_t col, int64_t r, const double* s, double shv, int64_t* rows,
+                                       double* vals) {
+    if (col < r) {
+        rows[0] = col;
+        vals[0] = shv - s[col];
+        rows[1] = r + col;
+        vals[1] = shv;
+    } else {
+        rows[0] = col - r;
+        vals[0] = shv;
+        rows[1] = col;
+        vals[1] = shv;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_eta2(const double* __restrict__ Gu, const double* __restrict__ Gq,
+                                              const double* __restrict__ s, const T* __restrict__ sh, int64_t r,
+                                              double* __restrict__ part) {
+    __shared__ double red[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t w2 = 2 * r;
+    const int64_t ca = blockIdx.x;
+    int64_t ra[2];
+    double va[2];
+    eta_nz(ca, r, s, widen1(sh[ca < r ? ca : ca - r]), ra, va);
+    double acc = 0.0;
+    for (int64_t cb = tid; cb < w2; cb += 256) {
+        int64_t rb[2];
+        double vb[2];
+        eta_nz(cb, r, s, widen1(sh[cb < r ? cb : cb - r]), rb, vb);
+        double h = 0.0;
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y) h += va[x] * Gu[ra[x] * w2 + rb[y]] * vb[y];
+        acc += h * Gq[cb * w2 + ca];
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) red[wave] = acc;
+    __syncthreads();
+    if (tid == 0) part[ca] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+hipError_t launch_eta2(const double* Gu, const double* Gq, const double* s, const void* sh, int prec, int64_t r,
+                       double* part, hipStream_t stream) {
+    KernelTimer tm("cert_eta2_f64", stream);
+    const dim3 g((unsigned)(2 * r));
+    if (prec == P64)
+        hipLaunchKernelGGL(k_eta2<double>, g, dim3(256), 0, stream, Gu, Gq, s, (const double*)sh, r, part);
+    else if (prec == P32)
+        hipLaunchKernelGGL(k_eta2<float>, g, dim3(256), 0, stream, Gu, Gq, s, (const float*)sh, r, part);
+    else
+        hipLaunchKernelGGL(k_eta2<half_t>, g, dim3(256), 0, stream, Gu, Gq, s, (const half_t*)sh, r, part);
+    return hipGetLastError();
+}
+
 // One workgroup per row: out[row] = sum_j part[row][j], fixed order.
 __global__ __launch_bounds__(256) void k_reduce_rows(const double* __restrict__ part, int64_t count,
                                                      double* __restrict__ out) {
