@@ -71,59 +71,60 @@ __global__ __launch_bounds__(256) void k_stage_f16(const half_t* __restrict__ gm
     }
 }
 
+// Core fragments are loaded from a clamped, in-bounds address and masked
+// afterwards, so that no branch surrounds the load.
+
 // A-operand fragment of the middle product: rows t, K index s, middle index i.
 template <typename T>
 __device__ __forceinline__ typename PrecTraits<T>::frag mid_frag(const TTSet& S, int64_t n_mid, int64_t i, int t,
                                                                  int s0) {
     const T* g = static_cast<const T*>(S.core[0]);
-    return (t < S.rM && s0 < S.rL && i < n_mid) ? g[((int64_t)s0 * n_mid + i) * S.rM + t] : T(0);
+    const bool ok = t < S.rM && s0 < S.rL && i < n_mid;
+    const T v = g[ok ? ((int64_t)s0 * n_mid + i) * S.rM + t : 0];
+    return ok ? v : T(0);
 }
 template <>
 __device__ __forceinline__ half8_t mid_frag<half_t>(const TTSet& S, int64_t n_mid, int64_t i, int t, int s0) {
-    if (i >= n_mid) {
-        half8_t z;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) z[e] = 0;
-        return z;
-    }
     const half_t* st = static_cast<const half_t*>(S.st_mid);
-    return *reinterpret_cast<const half8_t*>(st + (i * S.Rt + t) * S.Kp2 + s0);
+    const bool ok = i < n_mid;
+    half8_t v = *reinterpret_cast<const half8_t*>(st + (ok ? (i * S.Rt + t) * S.Kp2 + s0 : 0));
+    if (!ok) v = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    return v;
 }
 
 // A-operand fragment of the last product: rows c, K index t.
 template <typename T>
 __device__ __forceinline__ typename PrecTraits<T>::frag last_frag(const TTSet& S, int64_t n_last, int64_t c, int t0) {
     const T* g = static_cast<const T*>(S.core[1]);
-    return (t0 < S.rM && c < n_last) ? g[(int64_t)t0 * n_last + c] : T(0);
+    const bool ok = t0 < S.rM && c < n_last;
+    const T v = g[ok ? (int64_t)t0 * n_last + c : 0];
+    return ok ? v : T(0);
 }
 template <>
 __device__ __forceinline__ half8_t last_frag<half_t>(const TTSet& S, int64_t n_last, int64_t c, int t0) {
-    if (c >= n_last) {
-        half8_t z;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) z[e] = 0;
-        return z;
-    }
     const half_t* st = static_cast<const half_t*>(S.st_last);
-    return *reinterpret_cast<const half8_t*>(st + c * S.Kp3 + t0);
+    const bool ok = c < n_last;
+    half8_t v = *reinterpret_cast<const half8_t*>(st + (ok ? c * S.Kp3 + t0 : 0));
+    if (!ok) v = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    return v;
 }
 
 // Left interface rows Z_{d-2}(L) for L in [L0, L0 + BL) into Zl[BLpad][Kp2]
 // (storage type; rows >= BL and columns >= rL are zero).  lcore[c] is core c
 // of the left chain.
-template <typename T>
+template <typename T, int NT>
 __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* lcore, int64_t L0, T* Zl,
                            typename PrecTraits<T>::acc* cb0, typename PrecTraits<T>::acc* cb1) {
     using Acc = typename PrecTraits<T>::acc;
     const int tid = threadIdx.x;
     const int total = a.BLpad * S.Kp2;
     if (a.d == 2) {
-        for (int idx = tid; idx < total; idx += 256) Zl[idx] = (idx == 0) ? T(1) : T(0);
+        for (int idx = tid; idx < total; idx += NT) Zl[idx] = (idx == 0) ? T(1) : T(0);
         return;
     }
     if (a.d == 3) {
         const T* g1 = static_cast<const T*>(lcore[0]);
-        for (int idx = tid; idx < total; idx += 256) {
+        for (int idx = tid; idx < total; idx += NT) {
             const int Lr = idx / S.Kp2, s = idx % S.Kp2;
             const int64_t L = L0 + Lr;
             Zl[idx] = (Lr < a.BL && L < a.NL && s < S.rL) ? g1[L * S.rL + s] : T(0);
@@ -142,13 +143,13 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
         const int64_t nc = a.dims[c];
         const T* g = static_cast<const T*>(lcore[c]);
         if (c == 0) {
-            for (int idx = tid; idx < cnt * r1; idx += 256) {
+            for (int idx = tid; idx < cnt * r1; idx += NT) {
                 const int ql = idx / r1, t = idx % r1;
                 nxt[ql * a.chain_rmax + t] = to_acc(g[(qlo + ql) * r1 + t]);
             }
         } else {
             const int r0 = (int)S.ranks[c];
-            for (int idx = tid; idx < cnt * r1; idx += 256) {
+            for (int idx = tid; idx < cnt * r1; idx += NT) {
                 const int ql = idx / r1, t = idx % r1;
                 const int64_t q = qlo + ql;
                 const int pl = (int)(q / nc - qlo_prev);
@@ -165,7 +166,7 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
         nxt = tmp;
         qlo_prev = qlo;
     }
-    for (int idx = tid; idx < total; idx += 256) {
+    for (int idx = tid; idx < total; idx += NT) {
         const int Lr = idx / S.Kp2, s = idx % S.Kp2;
         const bool ok = (Lr < a.BL) && (L0 + Lr < a.NL) && (s < S.rL);
         Zl[idx] = ok ? to_storage<T>(cur[Lr * a.chain_rmax + s]) : T(0);
@@ -173,29 +174,66 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
     __syncthreads();   // the chain buffers are reused by the next set
 }
 
-// acc[j] += sum_kb A(kb) B_j(kb) for j < nb (nb <= 4); A fragments come from
-// global memory two K steps ahead of their use, B fragments from LDS.
-template <typename T, class AF, class BF>
-__device__ __forceinline__ void mma_pipelined(AF afrag, BF bfrag, int nkb, int nb,
-                                              typename PrecTraits<T>::accv (&acc)[4]) {
+// acc[c][j] += sum_kb A_c(kb) B_j(kb) for c < NC, j < NJ, over nkb >= 1 K
+// steps.  The loop is unrolled by two so that every step's operands were
+// requested a step earlier (B from LDS) or two steps earlier (A, core
+// fragments from global memory); indices past the end are clamped, so the
+// load sequence has no branches and every step's NC * NJ matrix-core
+// products issue back to back.  An odd last step runs after the loop.
+template <typename T, int NC, int NJ, class AF, class BF>
+__device__ __forceinline__ void mma_chain(AF afrag, BF bfrag, int nkb,
+                                          typename PrecTraits<T>::accv (&acc)[NC][NJ]) {
     using Frag = typename PrecTraits<T>::frag;
-    Frag a0 = afrag(0);
-    Frag a1 = (nkb > 1) ? afrag(1) : a0;
-    for (int kb = 0; kb < nkb; ++kb) {
-        const Frag av = a0;
-        a0 = a1;
-        if (kb + 2 < nkb) a1 = afrag(kb + 2);
+    Frag a0[NC], a1[NC], b0[NJ], b1[NJ];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (j < nb) acc[j] = mfma(av, bfrag(j, kb), acc[j]);
+    for (int c = 0; c < NC; ++c) {
+        a0[c] = afrag(c, 0);
+        a1[c] = afrag(c, 1);
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) b0[j] = bfrag(j, 0);
+    int kb = 0;
+    for (; kb + 1 < nkb; kb += 2) {
+        const int k2 = (kb + 2 < nkb) ? kb + 2 : nkb - 1;
+        const int k3 = (kb + 3 < nkb) ? kb + 3 : nkb - 1;
+        Frag n0[NC], n1[NC];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) b1[j] = bfrag(j, kb + 1);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) n0[c] = afrag(c, k2);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) acc[c][j] = mfma(a0[c], b0[j], acc[c][j]);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) b0[j] = bfrag(j, k2);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) n1[c] = afrag(c, k3);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) acc[c][j] = mfma(a1[c], b1[j], acc[c][j]);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            a0[c] = n0[c];
+            a1[c] = n1[c];
+        }
+    }
+    if (kb < nkb) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) acc[c][j] = mfma(a0[c], b0[j], acc[c][j]);
     }
 }
 
-template <typename T>
+// NPB = P / 16 row blocks of the tile, NLB = BLpad / 16 row blocks of the
+// left interface (both fixed at compile time, so that the matrix-core loops
+// carry no per-product branches).
+template <typename T, int NPB, int NLB>
 __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
-    using Acc = typename PrecTraits<T>::acc;
     using AccV = typename PrecTraits<T>::accv;
-    using Frag = typename PrecTraits<T>::frag;
+    using Acc = typename PrecTraits<T>::acc;
     constexpr int KB = PrecTraits<T>::KB, KPL = PrecTraits<T>::KPL;
     extern __shared__ double4_t smem_v[];
     char* smem = reinterpret_cast<char*>(smem_v);
@@ -205,11 +243,10 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
     Acc* cb0 = reinterpret_cast<Acc*>(smem + a.cb_off);
     Acc* cb1 = cb0 + (size_t)a.BL * a.chain_rmax;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, g = lane >> 4;
     const int64_t i0 = (int64_t)blockIdx.x * a.BI;
-    const int n_Lb = a.BLpad / 16;
-    const int n_pb = a.P / 16;
     const int n_cb = (int)((a.n_last + 15) / 16);
     const int n_tb = S.Rt / 16;
     const int tcap = (S.Rt < S.Kp3) ? S.Rt : S.Kp3;
@@ -221,68 +258,97 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
     for (int64_t lb = blockIdx.y; lb < a.num_L_blocks; lb += gridDim.y) {
         const int64_t L0 = lb * a.BL;
         __syncthreads();   // readers of the previous block are done
-        build_left<T>(a, S, S.core + 2, L0, Zl, cb0, cb1);
+        build_left<T, 256>(a, S, S.core + 2, L0, Zl, cb0, cb1);
         __syncthreads();
 
-        // middle product: work units (il, tb), each feeding n_Lb accumulators
+        // middle product: work units (il, tb), each feeding NLB accumulators
         for (int u = wave; u < a.BI * n_tb; u += 4) {
             const int il = u / n_tb, tb = u % n_tb;
             const int64_t i = i0 + il;
-            AccV acc[4];
+            AccV acc[1][NLB];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[j] = zero_accv<AccV>();
-            mma_pipelined<T>([&](int kb) { return mid_frag<T>(S, a.n_mid, i, tb * 16 + r, kb * KB + g * KPL); },
-                             [&](int j, int kb) { return load_frag<T>(Zl + (j * 16 + r) * S.Kp2 + kb * KB + g * KPL); },
-                             S.Kp2 / KB, n_Lb, acc);
+            for (int j = 0; j < NLB; ++j) acc[0][j] = zero_accv<AccV>();
+            mma_chain<T, 1, NLB>(
+                [&](int, int kb) { return mid_frag<T>(S, a.n_mid, i, tb * 16 + r, kb * KB + g * KPL); },
+                [&](int j, int kb) { return load_frag<T>(Zl + (j * 16 + r) * S.Kp2 + kb * KB + g * KPL); },
+                S.Kp2 / KB, acc);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (j >= n_Lb) continue;
+            for (int j = 0; j < NLB; ++j) {
                 const int Lr = j * 16 + r;
                 if (Lr >= a.BL) continue;
                 T* dst = Zf + (Lr * a.BI + il) * S.Kp3;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int t = tb * 16 + acc_row<T>(g, v);
-                    if (t < tcap) dst[t] = to_storage<T>(acc[j][v]);
+                    if (t < tcap) dst[t] = to_storage<T>(acc[0][j][v]);
                 }
             }
         }
         __syncthreads();
 
-        // last product, one 16-column block per wave at a time; each core
-        // fragment feeds the n_pb row blocks of the tile
-        for (int cbk = wave; cbk < n_cb; cbk += 4) {
-            const int64_t cbase = (int64_t)cbk * 16;
-            AccV acc[4];
+        // last product, NCB 16-column blocks per wave at a time (two for the
+        // FP64 / FP32 matrix-core chains, one for FP16, whose short K keeps
+        // the work per block small); each core fragment feeds the NPB row
+        // blocks of the tile
+        constexpr int NCB = (KPL == 8) ? 1 : 2;
+        for (int cp = wave; cp < (n_cb + NCB - 1) / NCB; cp += 4) {
+            AccV acc[NCB][NPB];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[j] = zero_accv<AccV>();
-            mma_pipelined<T>([&](int kb) { return last_frag<T>(S, a.n_last, cbase + r, kb * KB + g * KPL); },
-                             [&](int j, int kb) { return load_frag<T>(Zf + (j * 16 + r) * S.Kp3 + kb * KB + g * KPL); },
-                             S.Kp3 / KB, n_pb, acc);
+            for (int c = 0; c < NCB; ++c)
 #pragma unroll
-            for (int pb = 0; pb < 4; ++pb) {
-                if (pb >= n_pb) continue;
-                const int p = pb * 16 + r;
-                const int Lr = p / a.BI, il = p % a.BI;
-                const int64_t L = L0 + Lr, i = i0 + il;
-                if (Lr >= a.BL || L >= a.NL || i >= a.n_mid) continue;
-                T* dst = static_cast<T*>(a.out) + (L * a.n_mid + i) * a.n_last + cbase;
-                if (AccRowsContiguous<T>::value && a.vec4 && cbase + 4 * g + 3 < a.n_last) {
-                    typedef T vec_t __attribute__((ext_vector_type(4)));
-                    vec_t w;
+                for (int j = 0; j < NPB; ++j) acc[c][j] = zero_accv<AccV>();
+            mma_chain<T, NCB, NPB>(
+                [&](int c, int kb) {
+                    return last_frag<T>(S, a.n_last, (int64_t)(NCB * cp + c) * 16 + r, kb * KB + g * KPL);
+                },
+                [&](int j, int kb) { return load_frag<T>(Zf + (j * 16 + r) * S.Kp3 + kb * KB + g * KPL); },
+                S.Kp3 / KB, acc);
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[pb][v]);
-                    *reinterpret_cast<vec_t*>(dst + 4 * g) = w;
-                } else {
+            for (int c = 0; c < NCB; ++c) {
+                const int64_t cbase = (int64_t)(NCB * cp + c) * 16;
+                if (cbase >= a.n_last) continue;
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int row = acc_row<T>(g, v);
-                        if (cbase + row < a.n_last) dst[row] = to_storage<T>(acc[pb][v]);
+                for (int pb = 0; pb < NPB; ++pb) {
+                    const int p = pb * 16 + r;
+                    const int Lr = p / a.BI, il = p % a.BI;
+                    const int64_t L = L0 + Lr, i = i0 + il;
+                    if (Lr >= a.BL || L >= a.NL || i >= a.n_mid) continue;
+                    T* dst = static_cast<T*>(a.out) + (L * a.n_mid + i) * a.n_last + cbase;
+                    if (AccRowsContiguous<T>::value && a.vec4 && cbase + 4 * g + 3 < a.n_last) {
+                        typedef T vec_t __attribute__((ext_vector_type(4)));
+                        vec_t w;
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[c][pb][v]);
+                        *reinterpret_cast<vec_t*>(dst + 4 * g) = w;
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            const int row = acc_row<T>(g, v);
+                            if (cbase + row < a.n_last) dst[row] = to_storage<T>(acc[c][pb][v]);
+                        }
                     }
                 }
             }
         }
     }
+}
+
+template <typename T>
+static void launch_fused(int npb, int nlb, dim3 grid, size_t lds, hipStream_t st, const TTArgs& a) {
+#define LRC_TT(P, L) hipLaunchKernelGGL((k_tt_fused<T, P, L>), grid, dim3(256), lds, st, a)
+    switch (npb * 8 + nlb) {
+    case 1 * 8 + 1: LRC_TT(1, 1); break;
+    case 2 * 8 + 1: LRC_TT(2, 1); break;
+    case 2 * 8 + 2: LRC_TT(2, 2); break;
+    case 3 * 8 + 1: LRC_TT(3, 1); break;
+    case 3 * 8 + 2: LRC_TT(3, 2); break;
+    case 3 * 8 + 3: LRC_TT(3, 3); break;
+    case 4 * 8 + 1: LRC_TT(4, 1); break;
+    case 4 * 8 + 2: LRC_TT(4, 2); break;
+    case 4 * 8 + 3: LRC_TT(4, 3); break;
+    default: LRC_TT(4, 4); break;
+    }
+#undef LRC_TT
 }
 
 // ------------------------------------------------------------------- host --
@@ -349,6 +415,7 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     if (p.P == 0) return -1;
     p.num_i_blocks = (p.n_mid + p.BI - 1) / p.BI;
     p.num_L_blocks = (p.NL + p.BL - 1) / p.BL;
+
     int64_t want = 4096 / std::max<int64_t>(1, p.num_i_blocks);
     if (want < 1) want = 1;
     if (want > p.num_L_blocks) want = p.num_L_blocks;
@@ -423,7 +490,7 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
     if (!label) label = p.prec == P64 ? "tt_fused_f64" : (p.prec == P32 ? "tt_fused_f32" : "tt_fused_f16");
     KernelTimer tk(label, stream);
-    hipLaunchKernelGGL(k_tt_fused<T>, grid, dim3(256), p.lds_bytes, stream, a);
+    launch_fused<T>(p.P / 16, (int)round_up(p.BL, 16) / 16, grid, p.lds_bytes, stream, a);
     return hipGetLastError();
 }
 
