@@ -65,16 +65,12 @@ template <> struct SmallCfg<float> { using C = Cfg<float, 64, 64, 16, 2, 2>; };
 template <> struct SmallCfg<half_t> { using C = Cfg<half_t, 64, 64, 32, 2, 2>; };
 
 // ---- global -> registers -> LDS tile movers ---------------------------------
-// Each workgroup keeps NS K steps of global loads in flight in registers
-// (kStages = NS): the loads of step j + NS are issued right after step j has been
-// written to LDS, so their latency overlaps NS - 1 steps of matrix-core work.
-// fetch() only issues loads; stash() writes LDS.
-//
-// Rows past the matrix edge are read from a clamped, in-bounds address and
-// left unmasked: they only feed output rows / columns that are discarded (or
-// forced to zero) at the epilogue.  The K range is exact: only the last step
-// of a K range can be partial, and there the missing K values are zeroed.
-static constexpr int kStages = 3;
+// fetch() only issues loads into registers; stash() writes LDS.  Rows past
+// the matrix edge are read from a clamped, in-bounds address and left
+// unmasked: they only feed output rows / columns that are discarded (or
+// forced to zero) at the epilogue.  The K range is exact: only the last
+// step of a K range can be partial, and there the missing K values are
+// zeroed.
 
 // Every thread moves whole 16-byte chunks: sources have a 16-byte aligned
 // base and a pitch that is a multiple of the chunk (operands that are not
@@ -283,13 +279,28 @@ __device__ __forceinline__ void mma_k(const T* As, const T* Bs, typename C::AccV
     else if (nfm > 0 && nfn > 0) mma_k_g<C, true>(As, Bs, acc, wm, wn, lane, nfm, nfn);
 }
 
-// Workgroups are handed to the 8 XCDs in turn; renumber them so that each
-// XCD works through one contiguous range of tiles, whose shared operands
-// then meet in that XCD's L2.
+// Workgroups are handed to the 8 XCDs in turn (workgroup L to XCD L mod 8).
+// Renumber them so that XCD x works through the contiguous range
+// [x R, (x + 1) R) of logical tiles, R = ceil(total / 8), whose shared
+// operands then meet in that XCD's L2.  The grid is padded to 8 R
+// workgroups (xcd_grid); the numbers past `total` belong to no tile.
 __device__ __forceinline__ int64_t xcd_tile(int64_t total) {
     const int64_t L = blockIdx.x;
-    return (total % 8 == 0) ? (L % 8) * (total / 8) + L / 8 : L;
+    return (L % 8) * ((total + 7) / 8) + L / 8;
 }
+static inline unsigned xcd_grid(int64_t total) { return (unsigned)(((total + 7) / 8) * 8); }
+
+// Logical tiles of k_abt: groups of G = ceil(tiles_n / 8) n tiles, one group
+// per XCD; inside a group n runs fastest, so consecutive workgroups share
+// the rows of A, while the group's G column tiles of B stay in the L2.
+struct AbtOrder {
+    int64_t G, per_group, total;
+    __host__ __device__ AbtOrder(int tiles_m, int tiles_n) {
+        G = (tiles_n + 7) / 8;
+        per_group = (int64_t)tiles_m * G;
+        total = per_group * ((tiles_n + G - 1) / G);
+    }
+};
 
 // live 16-wide fragments of a wave tile starting at `start` in a dimension of `lim`
 template <int F>
@@ -298,6 +309,36 @@ __device__ __forceinline__ int live_frags(int64_t start, int64_t lim) {
     if (rem <= 0) return 0;
     const int64_t f = (rem + 15) / 16;
     return f < F ? (int)f : F;
+}
+
+// Main loop shared by the tile kernels: K steps j = 0 .. nsteps-1 with two
+// register stages of global loads and two LDS buffers.  Step s lives in
+// register stage s % 2 and LDS buffer s % 2; iteration j multiplies buffer
+// j % 2 while step j + 1 is written to the other buffer and the loads of
+// step j + 3 are issued, so one barrier per step suffices and each load has
+// two steps of matrix-core work to arrive.  Steps past the end are fetched
+// from clamped addresses (never stashed), so every path issues the same
+// loads and the compiler's waits cover exactly one stage.
+template <class Fetch, class Stash, class Mma>
+__device__ __forceinline__ void pipeline2(int nsteps, Fetch&& fetch, Stash&& stash, Mma&& mma) {
+    fetch(0, 0);
+    fetch(1, 1);
+    stash(0, 0, 0);
+    fetch(0, 2);
+    __syncthreads();
+    for (int j = 0; j < nsteps; j += 2) {
+        // even step j: buffer 0; odd step j + 1: buffer 1
+        mma(0);
+        if (j + 1 < nsteps) stash(1, 1, j + 1);
+        fetch(1, j + 3);
+        __syncthreads();
+        if (j + 1 < nsteps) {
+            mma(1);
+            if (j + 2 < nsteps) stash(0, 0, j + 2);
+            fetch(0, j + 4);
+            __syncthreads();
+        }
+    }
 }
 
 enum { ATB_APPLY = 0, ATB_GRAM = 1 };
@@ -347,14 +388,15 @@ __global__ __launch_bounds__(C::NT) void k_atb(
     typename C::Acc* __restrict__ part, const T* __restrict__ svals, void* __restrict__ out, int64_t ldo,
     int64_t Mout) {
     using AccV = typename C::AccV;
-    __shared__ alignas(16) T As[C::BK * C::LDA_R];
-    __shared__ alignas(16) T Bs[C::BK * C::LDB_R];
+    __shared__ alignas(16) T As[2][C::BK * C::LDA_R];
+    __shared__ alignas(16) T Bs[2][C::BK * C::LDB_R];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / C::WN, wn = wave % C::WN;
     // logical order: m tile fastest (tiles sharing a block of B columns are neighbours), then n, then split
     const int64_t lt = xcd_tile((int64_t)tiles_m * tiles_n * splits);
+    if (lt >= (int64_t)tiles_m * tiles_n * splits) return;
     const int64_t tile = lt % ((int64_t)tiles_m * tiles_n);
     const int sp = (int)(lt / ((int64_t)tiles_m * tiles_n));
     const int64_t m0 = (tile % tiles_m) * C::BM, n0 = (tile / tiles_m) * C::BN;
@@ -372,37 +414,22 @@ __global__ __launch_bounds__(C::NT) void k_atb(
     using TB = RowsTile<C, C::BN, T>;
     const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid);
     const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
-    constexpr int NS = kStages;
-    TA ta[NS];
-    TB tb[NS];
-    // Every stage slot issues its loads unconditionally (steps past the end
-    // read clamped addresses and are never used), so the order of loads is
-    // the same on every path and each wait covers exactly one stage.
+    TA ta[2];
+    TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
-#pragma unroll
-    for (int st = 0; st < NS; ++st) {
-        const int64_t k0 = kbeg + (int64_t)st * C::BK;
-        ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
-        tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
-    }
-    for (int j0 = 0; j0 < nsteps; j0 += NS) {
-#pragma unroll
-        for (int st = 0; st < NS; ++st) {
-            const int j = j0 + st;
+    pipeline2(
+        nsteps,
+        [&](int st, int j) {
             const int64_t k0 = kbeg + (int64_t)j * C::BK;
-            const bool live = j < nsteps;
-            if (live) {
-                ta[st].stash(As, ga, k0, k0 + C::BK > kend, kend);
-                tb[st].stash(Bs, gb, k0, k0 + C::BK > kend, kend);
-            }
-            __syncthreads();
-            const int64_t kn = k0 + (int64_t)NS * C::BK;
-            ta[st].fetch(ga, kn, kn + C::BK > kend, kend);
-            tb[st].fetch(gb, kn, kn + C::BK > kend, kend);
-            if (live) mma_rows<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
-            __syncthreads();
-        }
-    }
+            ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
+            tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
+        },
+        [&](int st, int buf, int j) {
+            const int64_t k0 = kbeg + (int64_t)j * C::BK;
+            ta[st].stash(As[buf], ga, k0, k0 + C::BK > kend, kend);
+            tb[st].stash(Bs[buf], gb, k0, k0 + C::BK > kend, kend);
+        },
+        [&](int buf) { mma_rows<C>(As[buf], Bs[buf], acc, wm, wn, lane, nfm, nfn); });
 
     if (splits > 1) {
         // partial tile: one accumulator vector per fragment, consecutive
@@ -456,7 +483,7 @@ __global__ __launch_bounds__(C::NT) void k_atb_finish(
 enum { ABT_STORE = 0, ABT_ERR = 1 };
 
 // C[m][n] = sum_k A[m][k] B[n][k]  (both sources with K contiguous).
-// Grid (tiles_n, tiles_m).
+// One workgroup per tile, in the order of AbtOrder.
 //   ABT_STORE: Y[m][ldy] = C rounded to T.
 //   ABT_ERR  : (T = double) partial sum of (Aref[m][n] - C)^2 per workgroup.
 template <typename T, class C, int MODE>
@@ -466,16 +493,21 @@ __global__ __launch_bounds__(C::NT) void k_abt(
     T* __restrict__ Y, int64_t ldy, int vec4,
     const double* __restrict__ Aref, int64_t ldr, double* __restrict__ part) {
     using AccV = typename C::AccV;
-    __shared__ alignas(16) T As[C::BM * C::LDK];
-    __shared__ alignas(16) T Bs[C::BN * C::LDK];
+    __shared__ alignas(16) T As[2][C::BM * C::LDK];
+    __shared__ alignas(16) T Bs[2][C::BN * C::LDK];
     __shared__ double wsum[C::NT / 64];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / C::WN, wn = wave % C::WN;
-    // logical order: n tile fastest (tiles sharing rows of A are neighbours)
-    const int64_t tile = xcd_tile((int64_t)tiles_m * tiles_n);
-    const int64_t m0 = (tile / tiles_n) * C::BM, n0 = (tile % tiles_n) * C::BN;
+    const AbtOrder ord(tiles_m, tiles_n);
+    const int64_t lt = xcd_tile(ord.total);
+    if (lt >= ord.total) return;
+    const int64_t mt = (lt % ord.per_group) / ord.G;
+    const int64_t nt = (lt / ord.per_group) * ord.G + (lt % ord.per_group) % ord.G;
+    if (nt >= tiles_n) return;
+    const int64_t tile = mt * tiles_n + nt;
+    const int64_t m0 = mt * C::BM, n0 = nt * C::BN;
     const int nfm = live_frags<C::FM>(m0 + wm * C::WTM, M), nfn = live_frags<C::FN>(n0 + wn * C::WTN, N);
 
     AccV acc[C::FN][C::FM];
@@ -488,34 +520,22 @@ __global__ __launch_bounds__(C::NT) void k_abt(
     using TB = KTile<C, C::BN, T>;
     const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid);
     const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
-    constexpr int NS = kStages;
-    TA ta[NS];
-    TB tb[NS];
+    TA ta[2];
+    TB tb[2];
     const int nsteps = (int)((K + C::BK - 1) / C::BK);
-#pragma unroll
-    for (int st = 0; st < NS; ++st) {
-        const int64_t k0 = (int64_t)st * C::BK;
-        ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
-        tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
-    }
-    for (int j0 = 0; j0 < nsteps; j0 += NS) {
-#pragma unroll
-        for (int st = 0; st < NS; ++st) {
-            const int j = j0 + st;
+    pipeline2(
+        nsteps,
+        [&](int st, int j) {
             const int64_t k0 = (int64_t)j * C::BK;
-            const bool live = j < nsteps;
-            if (live) {
-                ta[st].stash(As, ga, k0, k0 + C::BK > Ka, Ka);
-                tb[st].stash(Bs, gb, k0, k0 + C::BK > Kb, Kb);
-            }
-            __syncthreads();
-            const int64_t kn = k0 + (int64_t)NS * C::BK;
-            ta[st].fetch(ga, kn, kn + C::BK > Ka, Ka);
-            tb[st].fetch(gb, kn, kn + C::BK > Kb, Kb);
-            if (live) mma_k<C>(As, Bs, acc, wm, wn, lane, nfm, nfn);
-            __syncthreads();
-        }
-    }
+            ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
+            tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
+        },
+        [&](int st, int buf, int j) {
+            const int64_t k0 = (int64_t)j * C::BK;
+            ta[st].stash(As[buf], ga, k0, k0 + C::BK > Ka, Ka);
+            tb[st].stash(Bs[buf], gb, k0, k0 + C::BK > Kb, Kb);
+        },
+        [&](int buf) { mma_k<C>(As[buf], Bs[buf], acc, wm, wn, lane, nfm, nfn); });
 
     const int r = lane & 15, g = lane >> 4;
     if (MODE == ABT_STORE) {
@@ -582,7 +602,7 @@ static void run_atb(const char* label, const char* finish_label, hipStream_t st,
                     int splits, typename C::Acc* part, const T* svals, void* out, int64_t ldo, int64_t Mout) {
     {
         KernelTimer t(label, st);
-        const dim3 grid((unsigned)((int64_t)tiles_m * tiles_n * splits));
+        const dim3 grid(xcd_grid((int64_t)tiles_m * tiles_n * splits));
         hipLaunchKernelGGL((k_atb<T, C, MODE>), grid, dim3(C::NT), 0, st, A, lda, B, ldb, M, N, K, chunk, tiles_m,
                            tiles_n, splits, part, svals, out, ldo, Mout);
     }
@@ -907,7 +927,7 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     const int vec4 = (b % 4 == 0) && ((reinterpret_cast<uintptr_t>(Y) % (4 * sizeof(T))) == 0);
     const int T2 = p.big2 ? 128 : 64;
     const int tm = (int)((m + T2 - 1) / T2), tn = (int)((b + T2 - 1) / T2);
-    const dim3 g2((unsigned)((int64_t)tm * tn));
+    const dim3 g2(xcd_grid(AbtOrder(tm, tn).total));
     if (p.big2)
         launch_abt<T, typename BigCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt, ldt,
                                                         tm, tn, Y, b, vec4, (const double*)nullptr, (int64_t)0,
@@ -982,7 +1002,7 @@ hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, 
     const int64_t K = round_up(r, GramC::BK);
     if (!vec_ok<double>(W, ldw) || !vec_ok<double>(Vw, ldw)) return hipErrorInvalidValue;
     KernelTimer tm_("cert_err_dense_f64", stream);
-    launch_abt<double, GramC, ABT_ERR>(dim3((unsigned)*nparts), stream, W, ldw, m, r, Vw, ldw, n, r, K, tm, tn,
+    launch_abt<double, GramC, ABT_ERR>(dim3(xcd_grid(AbtOrder(tm, tn).total)), stream, W, ldw, m, r, Vw, ldw, n, r, K, tm, tn,
                                        (double*)nullptr, (int64_t)0, 0, A, n, part);
     return hipGetLastError();
 }
