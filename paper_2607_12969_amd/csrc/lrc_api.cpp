@@ -506,8 +506,24 @@ static int tt_into(const void* const* cores, const int64_t* dims, const int64_t*
     const int64_t* rs[1] = {ranks};
     if (plan_tt(plan, dims, rs, 1, d, LRC_FP64, max_lds) != 0)
         return fail(LRC_EINVAL, "TT ranks exceed the on-chip buffers of the fused kernel");
+    // the staged cores live only until this launch has run: the next
+    // reconstruction on the stream reuses their workspace
+    const size_t mark = ws.used;
     hipError_t e = launch_tt(plan, cores, out, ws, st, "cert_tt_fused_f64");
+    ws.used = mark;
     return e == hipSuccess ? LRC_OK : fail_hip(e, "TT reconstruction launch");
+}
+
+// workspace of the staged cores of one FP64 reconstruction (0 if it cannot be planned)
+static size_t tt_stage_need(const int64_t* dims, const int64_t* ranks, int d) {
+    if (d == 1) return 0;
+    int dev;
+    size_t max_lds;
+    if (current_device(&dev, &max_lds)) return 0;
+    TTPlan plan;
+    const int64_t* rs[1] = {ranks};
+    if (plan_tt(plan, dims, rs, 1, d, LRC_FP64, max_lds) != 0) return 0;
+    return plan.stage_bytes;
 }
 
 static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
@@ -528,6 +544,7 @@ static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
     const int64_t cnt_aug = tt_count(a->dims, a->ranks_aug, d);
     const int64_t groups = sumsq5_groups(N);
     size_t need = 3 * (size_t)N * 8 + (size_t)cnt_aug * 8 + 5 * (size_t)groups * 8 + 64 + (size_t)(8 + d) * 256;
+    need += std::max(tt_stage_need(a->dims, a->ranks_base, d), tt_stage_need(a->dims, a->ranks_aug, d)) + 512;
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
     hipError_t he = ws.reserve(need, st);
@@ -547,7 +564,7 @@ static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
     double* part = static_cast<double*>(ws.take(5 * (size_t)groups * 8));
     double* sums = static_cast<double*>(ws.take(5 * 8));
     if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
-    // FP64 reconstructions (the fused kernel needs no workspace in FP64)
+    // FP64 reconstructions, one after the other on the stream
     std::vector<const void*> cb(a->cores_base, a->cores_base + d), ca(a->cores_aug, a->cores_aug + d);
     rc = tt_into(cb.data(), a->dims, a->ranks_base, d, TR, ws);
     if (rc) return rc;

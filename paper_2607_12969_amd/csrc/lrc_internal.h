@@ -117,6 +117,7 @@ struct TTPlanSet {
     int rL, rM;          // r_{d-2}, r_{d-1}
     int Kp2, Kp3;        // rL, rM rounded to the MFMA K step
     int Rt;              // rM rounded up to 16 (row blocks of the middle product)
+    int ldl, ldf;        // LDS row pitches of Z_{d-2} and Z_{d-1} (padded against bank conflicts)
 };
 
 struct TTPlan {

@@ -21,6 +21,8 @@
 // are first copied to K-contiguous, zero-padded layouts (KBs to MBs) so a
 // lane loads its 8 K values at once.
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 
 #include "lrc_device.h"
 #include "lrc_internal.h"
@@ -31,8 +33,14 @@ struct TTSet {
     const void* core[kMaxD];  // [0] middle core, [1] last core, [2..] left chain
     int64_t ranks[kMaxD + 1];
     int rL, rM, Kp2, Kp3, Rt;
-    const void* st_mid;      // FP16 only: [n_mid][Rt][Kp2]
-    const void* st_last;     // FP16 only: [n_last][Kp3]
+    int ldl, ldf;            // LDS row pitches of Z_{d-2} and Z_{d-1} (elements)
+    // staged, zero-padded copies of the middle and last cores, laid out so
+    // that a lane's fragment for K step kb sits at a fixed offset plus kb
+    // times a uniform stride (see k_stage):
+    //   one K value per lane (FP64, FP32): mid [n_mid][Kp2][Rt], last [Kp3][ncp]
+    //   eight K values per lane (FP16):     mid [n_mid][Rt][Kp2], last [ncp][Kp3]
+    const void* st_mid;
+    const void* st_last;
     int zl_off, zf_off;      // byte offsets in LDS
 };
 
@@ -42,6 +50,7 @@ struct TTArgs {
     int64_t dims[kMaxD];
     int64_t divs[kMaxD];     // divs[c] = prod of dims[c+1 .. d-3] (left chain)
     int64_t NL, n_mid, n_last;
+    int ncp;                 // n_last rounded up to 16 (columns of the staged last core)
     int BL, BI, P, BLpad;
     int chain_rmax, cb_off;  // chain buffers: 2 x BL x chain_rmax (accumulation type)
     int64_t num_L_blocks;
@@ -50,63 +59,73 @@ struct TTArgs {
     int vec4;
 };
 
-// Copies of the FP16 middle and last cores with the contraction index
-// contiguous and zero padding.
-__global__ __launch_bounds__(256) void k_stage_f16(const half_t* __restrict__ gmid, const half_t* __restrict__ glast,
-                                                   half_t* __restrict__ smid, half_t* __restrict__ slast,
-                                                   int64_t n_mid, int64_t n_last, int rL, int rM, int Kp2, int Kp3,
-                                                   int Rt) {
+// Staged copies of the middle core G_{d-1} [rL][n_mid][rM] and the last core
+// G_d [rM][n_last], zero padded to Kp2 x Rt and Kp3 x ncp (layouts at TTSet).
+template <typename T>
+__global__ __launch_bounds__(256) void k_stage(const T* __restrict__ gmid, const T* __restrict__ glast,
+                                               T* __restrict__ smid, T* __restrict__ slast, int64_t n_mid,
+                                               int64_t n_last, int rL, int rM, int Kp2, int Kp3, int Rt, int ncp) {
+    constexpr bool kcontig = PrecTraits<T>::KPL > 1;
     const int64_t tot_mid = n_mid * Rt * Kp2;
-    const int64_t tot_last = n_last * Kp3;
+    const int64_t tot_last = (int64_t)ncp * Kp3;
     const int64_t stride = (int64_t)gridDim.x * 256;
     for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < tot_mid + tot_last; idx += stride) {
         if (idx < tot_mid) {
-            const int64_t s = idx % Kp2, t = (idx / Kp2) % Rt, i = idx / ((int64_t)Kp2 * Rt);
-            smid[idx] = (t < rM && s < rL) ? gmid[(s * n_mid + i) * rM + t] : half_t(0);
+            int64_t s, t, i;
+            if (kcontig) {
+                s = idx % Kp2;
+                t = (idx / Kp2) % Rt;
+                i = idx / ((int64_t)Kp2 * Rt);
+            } else {
+                t = idx % Rt;
+                s = (idx / Rt) % Kp2;
+                i = idx / ((int64_t)Kp2 * Rt);
+            }
+            smid[idx] = (t < rM && s < rL) ? gmid[(s * n_mid + i) * rM + t] : T(0);
         } else {
             const int64_t j = idx - tot_mid;
-            const int64_t t = j % Kp3, c = j / Kp3;
-            slast[j] = (t < rM) ? glast[t * n_last + c] : half_t(0);
+            int64_t t, c;
+            if (kcontig) {
+                t = j % Kp3;
+                c = j / Kp3;
+            } else {
+                c = j % ncp;
+                t = j / ncp;
+            }
+            slast[j] = (t < rM && c < n_last) ? glast[t * n_last + c] : T(0);
         }
     }
 }
 
-// Core fragments are loaded from a clamped, in-bounds address and masked
-// afterwards, so that no branch surrounds the load.
-
-// A-operand fragment of the middle product: rows t, K index s, middle index i.
+// Fragment address of the staged middle core for middle index i (clamped
+// into range: rows past the tensor are discarded at the store), output
+// column t, this lane's K group g; step kb adds kb * mid_step<T>(S).
 template <typename T>
-__device__ __forceinline__ typename PrecTraits<T>::frag mid_frag(const TTSet& S, int64_t n_mid, int64_t i, int t,
-                                                                 int s0) {
-    const T* g = static_cast<const T*>(S.core[0]);
-    const bool ok = t < S.rM && s0 < S.rL && i < n_mid;
-    const T v = g[ok ? ((int64_t)s0 * n_mid + i) * S.rM + t : 0];
-    return ok ? v : T(0);
+__device__ __forceinline__ const T* mid_base(const TTSet& S, int64_t n_mid, int64_t i, int t, int g) {
+    const T* st = static_cast<const T*>(S.st_mid);
+    const int64_t ic = i < n_mid ? i : n_mid - 1;
+    if constexpr (PrecTraits<T>::KPL > 1) return st + (ic * S.Rt + t) * S.Kp2 + g * PrecTraits<T>::KPL;
+    else return st + (ic * S.Kp2 + g) * S.Rt + t;
 }
-template <>
-__device__ __forceinline__ half8_t mid_frag<half_t>(const TTSet& S, int64_t n_mid, int64_t i, int t, int s0) {
-    const half_t* st = static_cast<const half_t*>(S.st_mid);
-    const bool ok = i < n_mid;
-    half8_t v = *reinterpret_cast<const half8_t*>(st + (ok ? (i * S.Rt + t) * S.Kp2 + s0 : 0));
-    if (!ok) v = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    return v;
-}
-
-// A-operand fragment of the last product: rows c, K index t.
 template <typename T>
-__device__ __forceinline__ typename PrecTraits<T>::frag last_frag(const TTSet& S, int64_t n_last, int64_t c, int t0) {
-    const T* g = static_cast<const T*>(S.core[1]);
-    const bool ok = t0 < S.rM && c < n_last;
-    const T v = g[ok ? (int64_t)t0 * n_last + c : 0];
-    return ok ? v : T(0);
+__device__ __forceinline__ int64_t mid_step(const TTSet& S) {
+    return PrecTraits<T>::KPL > 1 ? (int64_t)PrecTraits<T>::KB : (int64_t)PrecTraits<T>::KB * S.Rt;
 }
-template <>
-__device__ __forceinline__ half8_t last_frag<half_t>(const TTSet& S, int64_t n_last, int64_t c, int t0) {
-    const half_t* st = static_cast<const half_t*>(S.st_last);
-    const bool ok = c < n_last;
-    half8_t v = *reinterpret_cast<const half8_t*>(st + (ok ? c * S.Kp3 + t0 : 0));
-    if (!ok) v = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    return v;
+// Same for the staged last core, output column c (< ncp).
+template <typename T>
+__device__ __forceinline__ const T* last_base(const TTSet& S, int ncp, int64_t c, int g) {
+    const T* st = static_cast<const T*>(S.st_last);
+    if constexpr (PrecTraits<T>::KPL > 1) return st + c * S.Kp3 + g * PrecTraits<T>::KPL;
+    else return st + (int64_t)g * ncp + c;
+}
+template <typename T>
+__device__ __forceinline__ int64_t last_step(int ncp) {
+    return PrecTraits<T>::KPL > 1 ? (int64_t)PrecTraits<T>::KB : (int64_t)PrecTraits<T>::KB * ncp;
+}
+template <typename T>
+__device__ __forceinline__ typename PrecTraits<T>::frag core_frag(const T* p) {
+    if constexpr (PrecTraits<T>::KPL > 1) return *reinterpret_cast<const typename PrecTraits<T>::frag*>(p);
+    else return *p;
 }
 
 // Left interface rows Z_{d-2}(L) for L in [L0, L0 + BL) into Zl[BLpad][Kp2]
@@ -117,9 +136,12 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
                            typename PrecTraits<T>::acc* cb0, typename PrecTraits<T>::acc* cb1) {
     using Acc = typename PrecTraits<T>::acc;
     const int tid = threadIdx.x;
-    const int total = a.BLpad * S.Kp2;
+    const int total = a.BLpad * S.Kp2;   // rows of Zl have pitch S.ldl
     if (a.d == 2) {
-        for (int idx = tid; idx < total; idx += NT) Zl[idx] = (idx == 0) ? T(1) : T(0);
+        for (int idx = tid; idx < total; idx += NT) {
+            const int Lr = idx / S.Kp2, s = idx % S.Kp2;
+            Zl[Lr * S.ldl + s] = (idx == 0) ? T(1) : T(0);
+        }
         return;
     }
     if (a.d == 3) {
@@ -127,7 +149,7 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
         for (int idx = tid; idx < total; idx += NT) {
             const int Lr = idx / S.Kp2, s = idx % S.Kp2;
             const int64_t L = L0 + Lr;
-            Zl[idx] = (Lr < a.BL && L < a.NL && s < S.rL) ? g1[L * S.rL + s] : T(0);
+            Zl[Lr * S.ldl + s] = (Lr < a.BL && L < a.NL && s < S.rL) ? g1[L * S.rL + s] : T(0);
         }
         return;
     }
@@ -169,7 +191,7 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
     for (int idx = tid; idx < total; idx += NT) {
         const int Lr = idx / S.Kp2, s = idx % S.Kp2;
         const bool ok = (Lr < a.BL) && (L0 + Lr < a.NL) && (s < S.rL);
-        Zl[idx] = ok ? to_storage<T>(cur[Lr * a.chain_rmax + s]) : T(0);
+        Zl[Lr * S.ldl + s] = ok ? to_storage<T>(cur[Lr * a.chain_rmax + s]) : T(0);
     }
     __syncthreads();   // the chain buffers are reused by the next set
 }
@@ -180,9 +202,12 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
 // fragments from global memory); indices past the end are clamped, so the
 // load sequence has no branches and every step's NC * NJ matrix-core
 // products issue back to back.  An odd last step runs after the loop.
-template <typename T, int NC, int NJ, class AF, class BF>
+// With SWAP the products are B_j A_c instead (the accumulator then holds the
+// transposed block).
+template <typename T, int NC, int NJ, bool SWAP = false, class AF, class BF>
 __device__ __forceinline__ void mma_chain(AF afrag, BF bfrag, int nkb,
                                           typename PrecTraits<T>::accv (&acc)[NC][NJ]) {
+    auto mm = [](const auto& x, const auto& y, const auto& c) { return SWAP ? mfma(y, x, c) : mfma(x, y, c); };
     using Frag = typename PrecTraits<T>::frag;
     Frag a0[NC], a1[NC], b0[NJ], b1[NJ];
 #pragma unroll
@@ -204,7 +229,7 @@ __device__ __forceinline__ void mma_chain(AF afrag, BF bfrag, int nkb,
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) acc[c][j] = mfma(a0[c], b0[j], acc[c][j]);
+            for (int j = 0; j < NJ; ++j) acc[c][j] = mm(a0[c], b0[j], acc[c][j]);
 #pragma unroll
         for (int j = 0; j < NJ; ++j) b0[j] = bfrag(j, k2);
 #pragma unroll
@@ -212,7 +237,7 @@ __device__ __forceinline__ void mma_chain(AF afrag, BF bfrag, int nkb,
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) acc[c][j] = mfma(a1[c], b1[j], acc[c][j]);
+            for (int j = 0; j < NJ; ++j) acc[c][j] = mm(a1[c], b1[j], acc[c][j]);
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             a0[c] = n0[c];
@@ -223,7 +248,7 @@ __device__ __forceinline__ void mma_chain(AF afrag, BF bfrag, int nkb,
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) acc[c][j] = mfma(a0[c], b0[j], acc[c][j]);
+            for (int j = 0; j < NJ; ++j) acc[c][j] = mm(a0[c], b0[j], acc[c][j]);
     }
 }
 
@@ -253,7 +278,7 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
 
     // Z_{d-1} columns at and beyond min(Rt, Kp3) are never written by the
     // middle product; clear the buffer once.
-    for (int idx = tid; idx < a.P * S.Kp3; idx += 256) Zf[idx] = T(0);
+    for (int idx = tid; idx < a.P * S.ldf; idx += 256) Zf[idx] = T(0);
 
     for (int64_t lb = blockIdx.y; lb < a.num_L_blocks; lb += gridDim.y) {
         const int64_t L0 = lb * a.BL;
@@ -268,15 +293,17 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
             AccV acc[1][NLB];
 #pragma unroll
             for (int j = 0; j < NLB; ++j) acc[0][j] = zero_accv<AccV>();
+            const T* mb = mid_base<T>(S, a.n_mid, i, tb * 16 + r, g);
+            const int64_t ms = mid_step<T>(S);
             mma_chain<T, 1, NLB>(
-                [&](int, int kb) { return mid_frag<T>(S, a.n_mid, i, tb * 16 + r, kb * KB + g * KPL); },
-                [&](int j, int kb) { return load_frag<T>(Zl + (j * 16 + r) * S.Kp2 + kb * KB + g * KPL); },
+                [&](int, int kb) { return core_frag<T>(mb + kb * ms); },
+                [&](int j, int kb) { return load_frag<T>(Zl + (j * 16 + r) * S.ldl + kb * KB + g * KPL); },
                 S.Kp2 / KB, acc);
 #pragma unroll
             for (int j = 0; j < NLB; ++j) {
                 const int Lr = j * 16 + r;
                 if (Lr >= a.BL) continue;
-                T* dst = Zf + (Lr * a.BI + il) * S.Kp3;
+                T* dst = Zf + (Lr * a.BI + il) * S.ldf;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int t = tb * 16 + acc_row<T>(g, v);
@@ -291,18 +318,43 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
         // the work per block small); each core fragment feeds the NPB row
         // blocks of the tile
         constexpr int NCB = (KPL == 8) ? 1 : 2;
+        // FP64 accumulators hold rows g + 4v of a block: computing the
+        // transposed block makes each lane's values one tensor column of
+        // four rows, and lanes 0..15 sixteen consecutive columns
+        constexpr bool kRowsOut = !AccRowsContiguous<T>::value;
         for (int cp = wave; cp < (n_cb + NCB - 1) / NCB; cp += 4) {
             AccV acc[NCB][NPB];
 #pragma unroll
             for (int c = 0; c < NCB; ++c)
 #pragma unroll
                 for (int j = 0; j < NPB; ++j) acc[c][j] = zero_accv<AccV>();
-            mma_chain<T, NCB, NPB>(
-                [&](int c, int kb) {
-                    return last_frag<T>(S, a.n_last, (int64_t)(NCB * cp + c) * 16 + r, kb * KB + g * KPL);
-                },
-                [&](int j, int kb) { return load_frag<T>(Zf + (j * 16 + r) * S.Kp3 + kb * KB + g * KPL); },
+            const T* lb0 = last_base<T>(S, a.ncp, (int64_t)(NCB * cp) * 16 + r, g);
+            const int64_t lstep = last_step<T>(a.ncp);
+            const int64_t cstep = (KPL > 1) ? (int64_t)16 * S.Kp3 : 16;   // next column block
+            mma_chain<T, NCB, NPB, kRowsOut>(
+                [&](int c, int kb) { return core_frag<T>(lb0 + c * cstep + kb * lstep); },
+                [&](int j, int kb) { return load_frag<T>(Zf + (j * 16 + r) * S.ldf + kb * KB + g * KPL); },
                 S.Kp3 / KB, acc);
+            if constexpr (kRowsOut) {
+                // lane holds tensor rows p = pb*16 + acc_row(g, v) of column cbase + r:
+                // each store instruction writes whole 128-byte row segments
+#pragma unroll
+                for (int c = 0; c < NCB; ++c) {
+                    const int64_t col = (int64_t)(NCB * cp + c) * 16 + r;
+                    if (col >= a.n_last) continue;
+#pragma unroll
+                    for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            const int p = pb * 16 + acc_row<T>(g, v);
+                            const int Lr = (a.BI == 1) ? p : p / a.BI, il = (a.BI == 1) ? 0 : p % a.BI;
+                            const int64_t L = L0 + Lr, i = i0 + il;
+                            if (Lr >= a.BL || L >= a.NL || i >= a.n_mid) continue;
+                            static_cast<T*>(a.out)[(L * a.n_mid + i) * a.n_last + col] = to_storage<T>(acc[c][pb][v]);
+                        }
+                }
+                continue;
+            }
 #pragma unroll
             for (int c = 0; c < NCB; ++c) {
                 const int64_t cbase = (int64_t)(NCB * cp + c) * 16;
@@ -352,6 +404,14 @@ static void launch_fused(int npb, int nlb, dim3 grid, size_t lds, hipStream_t st
 }
 
 // ------------------------------------------------------------------- host --
+// Tuning aids: LRC_TT_P (rows per tile: 16, 32 or 64) and LRC_TT_WGS (target
+// workgroup count) override the defaults when set.
+static int tune_env(const char* name, int dflt) {
+    const char* e = std::getenv(name);
+    if (!e) return dflt;
+    const int v = std::atoi(e);
+    return v > 0 ? v : dflt;
+}
 int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int nsets, int d, int prec,
             size_t max_lds) {
     p = TTPlan{};
@@ -374,6 +434,12 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         s.rL = (int)rank_sets[q][d - 2];
         s.Kp2 = (int)round_up(s.rL, KB);
         s.Kp3 = (int)round_up(s.rM, KB);
+        // LDS pitches: consecutive rows of a fragment read land on
+        // different banks (one element of pad; 16 bytes for FP16 rows,
+        // which are read 16 bytes at a time)
+        const int pad = (prec == P16) ? 8 : 1;
+        s.ldl = s.Kp2 + pad;
+        s.ldf = s.Kp3 + pad;
         s.Rt = (int)round_up(s.rM, 16);
         if (d >= 4)
             for (int c = 1; c <= d - 2; ++c) p.chain_rmax = (int)std::max<int64_t>(p.chain_rmax, rank_sets[q][c]);
@@ -381,7 +447,7 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     // at most 64 KB of LDS per workgroup, so that at least two workgroups
     // share a compute unit
     if (max_lds > 65536) max_lds = 65536;
-    const int P0 = (prec == P64) ? 32 : 64;
+    const int P0 = tune_env("LRC_TT_P", (prec == P64) ? 32 : 64);
     for (int P = P0; P >= 16; P /= 2) {
         int BI, BL;
         if (d == 2) {
@@ -400,8 +466,8 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         if (Peff > 64 || BLpad > 64) continue;
         size_t lds = 0;
         for (int q = 0; q < nsets; ++q) {
-            lds += (size_t)round_up((int64_t)BLpad * p.set[q].Kp2 * e, 32);
-            lds += (size_t)round_up((int64_t)Peff * p.set[q].Kp3 * e, 32);
+            lds += (size_t)round_up((int64_t)BLpad * p.set[q].ldl * e, 32);
+            lds += (size_t)round_up((int64_t)Peff * p.set[q].ldf * e, 32);
         }
         if (d >= 4) lds += (size_t)2 * BL * p.chain_rmax * acc_b;
         if (lds <= max_lds) {
@@ -416,16 +482,17 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     p.num_i_blocks = (p.n_mid + p.BI - 1) / p.BI;
     p.num_L_blocks = (p.NL + p.BL - 1) / p.BL;
 
-    int64_t want = 4096 / std::max<int64_t>(1, p.num_i_blocks);
+    int64_t want = tune_env("LRC_TT_WGS", 4096) / std::max<int64_t>(1, p.num_i_blocks);
     if (want < 1) want = 1;
     if (want > p.num_L_blocks) want = p.num_L_blocks;
     if (want > 65535) want = 65535;
     p.grid_L = (int)want;
+    // staged cores (layouts at TTSet); ncp covers whole pairs of column blocks
     p.stage_bytes = 0;
-    if (prec == P16)
-        for (int q = 0; q < nsets; ++q)
-            p.stage_bytes += (size_t)(round_up(p.n_mid * p.set[q].Rt * p.set[q].Kp2 * 2, 256) +
-                                      round_up(p.n_last * p.set[q].Kp3 * 2, 256));
+    const int64_t ncp = round_up(p.n_last, 32);
+    for (int q = 0; q < nsets; ++q)
+        p.stage_bytes += (size_t)(round_up(p.n_mid * p.set[q].Rt * p.set[q].Kp2 * e, 256) +
+                                  round_up(ncp * p.set[q].Kp3 * e, 256));
     return 0;
 }
 
@@ -450,8 +517,13 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     a.BLpad = (int)round_up(p.BL, 16);
     a.chain_rmax = p.chain_rmax;
     a.num_L_blocks = p.num_L_blocks;
+    a.ncp = (int)round_up(p.n_last, 32);
     a.out = out;
     a.vec4 = out && (p.n_last % 4 == 0) && (reinterpret_cast<uintptr_t>(out) % (4 * sizeof(T)) == 0);
+    if (!label) label = p.prec == P64 ? "tt_fused_f64" : (p.prec == P32 ? "tt_fused_f32" : "tt_fused_f16");
+    // the staging copy is timed under the kernel's label with a "_stage" suffix
+    char stage_label[64];
+    std::snprintf(stage_label, sizeof(stage_label), "%s_stage", label);
     int off = 0;
     for (int q = 0; q < p.nsets; ++q) {
         TTSet& S = a.set[q];
@@ -464,22 +536,24 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
         S.rM = ps.rM;
         S.Kp2 = ps.Kp2;
         S.Kp3 = ps.Kp3;
+        S.ldl = ps.ldl;
+        S.ldf = ps.ldf;
         S.Rt = ps.Rt;
         S.zl_off = off;
-        off += (int)round_up((int64_t)a.BLpad * ps.Kp2 * (int64_t)sizeof(T), 32);
+        off += (int)round_up((int64_t)a.BLpad * ps.ldl * (int64_t)sizeof(T), 32);
         S.zf_off = off;
-        off += (int)round_up((int64_t)p.P * ps.Kp3 * (int64_t)sizeof(T), 32);
-        if (p.prec == P16) {
-            half_t* smid = static_cast<half_t*>(ws.take((size_t)p.n_mid * ps.Rt * ps.Kp2 * 2));
-            half_t* slast = static_cast<half_t*>(ws.take((size_t)p.n_last * ps.Kp3 * 2));
+        off += (int)round_up((int64_t)p.P * ps.ldf * (int64_t)sizeof(T), 32);
+        {
+            T* smid = static_cast<T*>(ws.take((size_t)p.n_mid * ps.Rt * ps.Kp2 * sizeof(T)));
+            T* slast = static_cast<T*>(ws.take((size_t)a.ncp * ps.Kp3 * sizeof(T)));
             if (ws.overrun || !smid || !slast) return hipErrorOutOfMemory;
-            const int64_t tot = p.n_mid * ps.Rt * ps.Kp2 + p.n_last * ps.Kp3;
+            const int64_t tot = p.n_mid * ps.Rt * ps.Kp2 + (int64_t)a.ncp * ps.Kp3;
             int64_t gs = (tot + 255) / 256;
-            if (gs > 2048) gs = 2048;
-            KernelTimer ts("tt_stage_f16", stream);
-            hipLaunchKernelGGL(k_stage_f16, dim3((unsigned)gs), dim3(256), 0, stream,
-                               (const half_t*)cores[q][p.d - 2], (const half_t*)cores[q][p.d - 1], smid, slast,
-                               p.n_mid, p.n_last, ps.rL, ps.rM, ps.Kp2, ps.Kp3, ps.Rt);
+            if (gs > 4096) gs = 4096;
+            KernelTimer ts(stage_label, stream);
+            hipLaunchKernelGGL(k_stage<T>, dim3((unsigned)gs), dim3(256), 0, stream, (const T*)cores[q][p.d - 2],
+                               (const T*)cores[q][p.d - 1], smid, slast, p.n_mid, p.n_last, ps.rL, ps.rM, ps.Kp2,
+                               ps.Kp3, ps.Rt, a.ncp);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
             S.st_mid = smid;
@@ -488,7 +562,6 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     }
     a.cb_off = off;
     dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
-    if (!label) label = p.prec == P64 ? "tt_fused_f64" : (p.prec == P32 ? "tt_fused_f32" : "tt_fused_f16");
     KernelTimer tk(label, stream);
     launch_fused<T>(p.P / 16, (int)round_up(p.BL, 16) / 16, grid, p.lds_bytes, stream, a);
     return hipGetLastError();
