@@ -526,6 +526,21 @@ static size_t tt_stage_need(const int64_t* dims, const int64_t* ranks, int d) {
     return plan.stage_bytes;
 }
 
+// Result fields from the five sums ||T-T_R||^2, ||T-T_R+||^2, ||T_R+-T^||^2,
+// ||T-T^||^2, ||T||^2.
+static void tt_cert_result(const double* h, const lrc_cert_args* a, lrc_cert_result* res) {
+    const int d = a->d;
+    res->E_base = std::sqrt(h[0]);
+    res->E_aug = std::sqrt(h[1]);
+    res->eta = std::sqrt(h[2]);
+    res->err_new = std::sqrt(h[3]);
+    res->norm_ref = std::sqrt(h[4]);
+    res->gain = h[0] - h[1];
+    res->bytes_base = lrc_tt_storage_bytes(a->dims, a->ranks_base, d, LRC_FP64);
+    res->bytes_aug = lrc_tt_storage_bytes(a->dims, a->ranks_aug, d, a->prec);
+    finish_flags(res, true);
+}
+
 static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
     const int d = a->d;
     int64_t N, Nb;
@@ -538,10 +553,48 @@ static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
         if (!a->cores_base[l] || !a->cores_aug[l] || !a->cores_aug_h[l])
             return fail(LRC_EINVAL, "core %d is NULL", l);
     int dev;
-    rc = current_device(&dev, nullptr);
+    size_t max_lds;
+    rc = current_device(&dev, &max_lds);
     if (rc) return rc;
     hipStream_t st = g_stream;
     const int64_t cnt_aug = tt_count(a->dims, a->ranks_aug, d);
+
+    // Fused path: the three FP64 reconstructions are formed tile by tile on
+    // chip and compared with T there (no dense intermediate tensors).
+    TTPlan cplan;
+    const int64_t* rsets[3] = {a->ranks_base, a->ranks_aug, a->ranks_aug};
+    if (d >= 2 && plan_tt(cplan, a->dims, rsets, 3, d, LRC_FP64, max_lds) == 0 && cplan.P <= 32) {
+        const int64_t nparts = tt_cert_parts(cplan);
+        const size_t need = (size_t)cnt_aug * 8 + cplan.stage_bytes + 5 * (size_t)nparts * 8 + 64 + (size_t)(8 + d) * 256;
+        Workspace& ws = workspace_for(dev, st);
+        ws.reset();
+        hipError_t he = ws.reserve(need, st);
+        if (he != hipSuccess) return fail_hip(he, "workspace");
+        std::vector<const void*> wide(d);
+        for (int l = 0; l < d; ++l) {
+            const int64_t c = a->ranks_aug[l] * a->dims[l] * a->ranks_aug[l + 1];
+            double* w = static_cast<double*>(ws.take((size_t)c * 8));
+            if (ws.overrun || !w) return fail(LRC_ENOMEM, "certificate workspace too small");
+            he = launch_widen(a->cores_aug_h[l], a->prec, c, w, st);
+            if (he != hipSuccess) return fail_hip(he, "widen launch");
+            wide[l] = w;
+        }
+        double* part = static_cast<double*>(ws.take(5 * (size_t)nparts * 8));
+        double* sums = static_cast<double*>(ws.take(5 * 8));
+        if (ws.overrun) return fail(LRC_ENOMEM, "certificate workspace too small");
+        std::vector<const void*> cb(a->cores_base, a->cores_base + d), ca(a->cores_aug, a->cores_aug + d);
+        const void* const* sets[3] = {cb.data(), ca.data(), wide.data()};
+        he = launch_tt_cert(cplan, sets, static_cast<const double*>(a->T), part, ws, st);
+        if (he == hipSuccess) he = launch_reduce_rows(part, nparts, 5, sums, st);
+        double h[5];
+        if (he == hipSuccess) he = hipMemcpyAsync(h, sums, sizeof(h), hipMemcpyDeviceToHost, st);
+        if (he == hipSuccess) he = hipStreamSynchronize(st);
+        if (he != hipSuccess) return fail_hip(he, "TT certificate");
+        tt_cert_result(h, a, res);
+        return LRC_OK;
+    }
+
+    // Otherwise: dense FP64 reconstructions, then one pass over the tensors.
     const int64_t groups = sumsq5_groups(N);
     size_t need = 3 * (size_t)N * 8 + (size_t)cnt_aug * 8 + 5 * (size_t)groups * 8 + 64 + (size_t)(8 + d) * 256;
     need += std::max(tt_stage_need(a->dims, a->ranks_base, d), tt_stage_need(a->dims, a->ranks_aug, d)) + 512;
@@ -578,15 +631,7 @@ static int certify_tt(const lrc_cert_args* a, lrc_cert_result* res) {
     if (he == hipSuccess) he = hipMemcpyAsync(h, sums, sizeof(h), hipMemcpyDeviceToHost, st);
     if (he == hipSuccess) he = hipStreamSynchronize(st);
     if (he != hipSuccess) return fail_hip(he, "TT certificate");
-    res->E_base = std::sqrt(h[0]);
-    res->E_aug = std::sqrt(h[1]);
-    res->eta = std::sqrt(h[2]);
-    res->err_new = std::sqrt(h[3]);
-    res->norm_ref = std::sqrt(h[4]);
-    res->gain = h[0] - h[1];
-    res->bytes_base = lrc_tt_storage_bytes(a->dims, a->ranks_base, d, LRC_FP64);
-    res->bytes_aug = lrc_tt_storage_bytes(a->dims, a->ranks_aug, d, a->prec);
-    finish_flags(res, true);
+    tt_cert_result(h, a, res);
     return LRC_OK;
 }
 

@@ -110,7 +110,7 @@ hipError_t launch_reduce_rows(const double* part, int64_t count, int nsums, doub
 
 // ------------------------------------------------------------------- TT ---
 constexpr int kMaxD = 16;
-constexpr int kTTMaxSets = 1;
+constexpr int kTTMaxSets = 3;
 
 struct TTPlanSet {
     int64_t ranks[kMaxD + 1];
@@ -123,7 +123,7 @@ struct TTPlanSet {
 struct TTPlan {
     int d;
     int prec;
-    int nsets;           // core sets sharing one block layout (1)
+    int nsets;           // core sets sharing one block layout (1; 3 for the certificate)
     int64_t dims[kMaxD];
     TTPlanSet set[kTTMaxSets];
     int64_t NL;          // rows of the left interface Z_{d-2} (1 when d <= 2)
@@ -146,5 +146,12 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
 // `label` names the launch for the kernel timers (nullptr: "tt_fused_<type>").
 hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Workspace& ws,
                      hipStream_t stream, const char* label = nullptr);
+
+// Fused TT certificate (FP64 plan with three core sets: base, augmented,
+// widened rounded augmented): part[s * tt_cert_parts(p) + w] receives the
+// five partial sums of workgroup w (order at k_tt_cert).
+int64_t tt_cert_parts(const TTPlan& p);
+hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, const double* Tref, double* part,
+                          Workspace& ws, hipStream_t stream);
 
 }  // namespace lrc

@@ -252,6 +252,63 @@ __device__ __forceinline__ void mma_chain(AF afrag, BF bfrag, int nkb,
     }
 }
 
+// Middle product of one tile, Z_{d-1}(L, i) = Z_{d-2}(L) G_{d-1}(i), from Zl
+// into Zf (rounded to T): work units (il, tb) over the four waves, each
+// feeding NLB accumulators.  Zf columns at and beyond min(Rt, Kp3) are never
+// written (the caller clears them once).
+template <typename T, int NLB>
+__device__ __forceinline__ void middle_product(const TTArgs& a, const TTSet& S, const T* Zl, T* Zf, int64_t i0,
+                                               int wave, int r, int g) {
+    using AccV = typename PrecTraits<T>::accv;
+    constexpr int KB = PrecTraits<T>::KB, KPL = PrecTraits<T>::KPL;
+    const int n_tb = S.Rt / 16;
+    const int tcap = (S.Rt < S.Kp3) ? S.Rt : S.Kp3;
+    for (int u = wave; u < a.BI * n_tb; u += 4) {
+        const int il = u / n_tb, tb = u % n_tb;
+        const int64_t i = i0 + il;
+        AccV acc[1][NLB];
+#pragma unroll
+        for (int j = 0; j < NLB; ++j) acc[0][j] = zero_accv<AccV>();
+        const T* mb = mid_base<T>(S, a.n_mid, i, tb * 16 + r, g);
+        const int64_t ms = mid_step<T>(S);
+        mma_chain<T, 1, NLB>(
+            [&](int, int kb) { return core_frag<T>(mb + kb * ms); },
+            [&](int j, int kb) { return load_frag<T>(Zl + (j * 16 + r) * S.ldl + kb * KB + g * KPL); },
+            S.Kp2 / KB, acc);
+#pragma unroll
+        for (int j = 0; j < NLB; ++j) {
+            const int Lr = j * 16 + r;
+            if (Lr >= a.BL) continue;
+            T* dst = Zf + (Lr * a.BI + il) * S.ldf;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int t = tb * 16 + acc_row<T>(g, v);
+                if (t < tcap) dst[t] = to_storage<T>(acc[0][j][v]);
+            }
+        }
+    }
+}
+
+// Last product of column blocks NCB*cp .. NCB*cp + NCB - 1 against Zf; with
+// SWAP the accumulators hold the transposed blocks (tensor rows in the
+// accumulator rows).
+template <typename T, int NCB, int NPB, bool SWAP>
+__device__ __forceinline__ void last_product(const TTArgs& a, const TTSet& S, const T* Zf, int cp, int r, int g,
+                                             typename PrecTraits<T>::accv (&acc)[NCB][NPB]) {
+    constexpr int KB = PrecTraits<T>::KB, KPL = PrecTraits<T>::KPL;
+#pragma unroll
+    for (int c = 0; c < NCB; ++c)
+#pragma unroll
+        for (int j = 0; j < NPB; ++j) acc[c][j] = zero_accv<typename PrecTraits<T>::accv>();
+    const T* lb0 = last_base<T>(S, a.ncp, (int64_t)(NCB * cp) * 16 + r, g);
+    const int64_t lstep = last_step<T>(a.ncp);
+    const int64_t cstep = (KPL > 1) ? (int64_t)16 * S.Kp3 : 16;   // next column block
+    mma_chain<T, NCB, NPB, SWAP>(
+        [&](int c, int kb) { return core_frag<T>(lb0 + c * cstep + kb * lstep); },
+        [&](int j, int kb) { return load_frag<T>(Zf + (j * 16 + r) * S.ldf + kb * KB + g * KPL); },
+        S.Kp3 / KB, acc);
+}
+
 // NPB = P / 16 row blocks of the tile, NLB = BLpad / 16 row blocks of the
 // left interface (both fixed at compile time, so that the matrix-core loops
 // carry no per-product branches).
@@ -259,7 +316,7 @@ template <typename T, int NPB, int NLB>
 __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
     using AccV = typename PrecTraits<T>::accv;
     using Acc = typename PrecTraits<T>::acc;
-    constexpr int KB = PrecTraits<T>::KB, KPL = PrecTraits<T>::KPL;
+    constexpr int KPL = PrecTraits<T>::KPL;
     extern __shared__ double4_t smem_v[];
     char* smem = reinterpret_cast<char*>(smem_v);
     const TTSet& S = a.set[0];
@@ -273,71 +330,33 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
     const int r = lane & 15, g = lane >> 4;
     const int64_t i0 = (int64_t)blockIdx.x * a.BI;
     const int n_cb = (int)((a.n_last + 15) / 16);
-    const int n_tb = S.Rt / 16;
-    const int tcap = (S.Rt < S.Kp3) ? S.Rt : S.Kp3;
 
-    // Z_{d-1} columns at and beyond min(Rt, Kp3) are never written by the
-    // middle product; clear the buffer once.
     for (int idx = tid; idx < a.P * S.ldf; idx += 256) Zf[idx] = T(0);
+
+    // last product: NCB 16-column blocks per wave at a time (two for the
+    // FP64 / FP32 matrix-core chains, one for FP16, whose short K keeps the
+    // work per block small); each core fragment feeds the NPB row blocks.
+    // FP64 accumulators hold rows g + 4v of a block: computing the
+    // transposed block makes each lane's values one tensor column of four
+    // rows, and lanes 0..15 sixteen consecutive columns.
+    constexpr int NCB = (KPL == 8) ? 1 : 2;
+    constexpr bool kRowsOut = !AccRowsContiguous<T>::value;
 
     for (int64_t lb = blockIdx.y; lb < a.num_L_blocks; lb += gridDim.y) {
         const int64_t L0 = lb * a.BL;
         __syncthreads();   // readers of the previous block are done
         build_left<T, 256>(a, S, S.core + 2, L0, Zl, cb0, cb1);
         __syncthreads();
-
-        // middle product: work units (il, tb), each feeding NLB accumulators
-        for (int u = wave; u < a.BI * n_tb; u += 4) {
-            const int il = u / n_tb, tb = u % n_tb;
-            const int64_t i = i0 + il;
-            AccV acc[1][NLB];
-#pragma unroll
-            for (int j = 0; j < NLB; ++j) acc[0][j] = zero_accv<AccV>();
-            const T* mb = mid_base<T>(S, a.n_mid, i, tb * 16 + r, g);
-            const int64_t ms = mid_step<T>(S);
-            mma_chain<T, 1, NLB>(
-                [&](int, int kb) { return core_frag<T>(mb + kb * ms); },
-                [&](int j, int kb) { return load_frag<T>(Zl + (j * 16 + r) * S.ldl + kb * KB + g * KPL); },
-                S.Kp2 / KB, acc);
-#pragma unroll
-            for (int j = 0; j < NLB; ++j) {
-                const int Lr = j * 16 + r;
-                if (Lr >= a.BL) continue;
-                T* dst = Zf + (Lr * a.BI + il) * S.ldf;
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int t = tb * 16 + acc_row<T>(g, v);
-                    if (t < tcap) dst[t] = to_storage<T>(acc[0][j][v]);
-                }
-            }
-        }
+        middle_product<T, NLB>(a, S, Zl, Zf, i0, wave, r, g);
         __syncthreads();
 
-        // last product, NCB 16-column blocks per wave at a time (two for the
-        // FP64 / FP32 matrix-core chains, one for FP16, whose short K keeps
-        // the work per block small); each core fragment feeds the NPB row
-        // blocks of the tile
-        constexpr int NCB = (KPL == 8) ? 1 : 2;
-        // FP64 accumulators hold rows g + 4v of a block: computing the
-        // transposed block makes each lane's values one tensor column of
-        // four rows, and lanes 0..15 sixteen consecutive columns
-        constexpr bool kRowsOut = !AccRowsContiguous<T>::value;
         for (int cp = wave; cp < (n_cb + NCB - 1) / NCB; cp += 4) {
             AccV acc[NCB][NPB];
-#pragma unroll
-            for (int c = 0; c < NCB; ++c)
-#pragma unroll
-                for (int j = 0; j < NPB; ++j) acc[c][j] = zero_accv<AccV>();
-            const T* lb0 = last_base<T>(S, a.ncp, (int64_t)(NCB * cp) * 16 + r, g);
-            const int64_t lstep = last_step<T>(a.ncp);
-            const int64_t cstep = (KPL > 1) ? (int64_t)16 * S.Kp3 : 16;   // next column block
-            mma_chain<T, NCB, NPB, kRowsOut>(
-                [&](int c, int kb) { return core_frag<T>(lb0 + c * cstep + kb * lstep); },
-                [&](int j, int kb) { return load_frag<T>(Zf + (j * 16 + r) * S.ldf + kb * KB + g * KPL); },
-                S.Kp3 / KB, acc);
+            last_product<T, NCB, NPB, kRowsOut>(a, S, Zf, cp, r, g, acc);
             if constexpr (kRowsOut) {
-                // lane holds tensor rows p = pb*16 + acc_row(g, v) of column cbase + r:
-                // each store instruction writes whole 128-byte row segments
+                // lane holds tensor rows p = pb*16 + acc_row(g, v) of column
+                // NCB*cp*16 + 16c + r: each store instruction writes whole
+                // 128-byte row segments
 #pragma unroll
                 for (int c = 0; c < NCB; ++c) {
                     const int64_t col = (int64_t)(NCB * cp + c) * 16 + r;
@@ -353,35 +372,142 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
                             static_cast<T*>(a.out)[(L * a.n_mid + i) * a.n_last + col] = to_storage<T>(acc[c][pb][v]);
                         }
                 }
-                continue;
-            }
+            } else {
 #pragma unroll
-            for (int c = 0; c < NCB; ++c) {
-                const int64_t cbase = (int64_t)(NCB * cp + c) * 16;
-                if (cbase >= a.n_last) continue;
+                for (int c = 0; c < NCB; ++c) {
+                    const int64_t cbase = (int64_t)(NCB * cp + c) * 16;
+                    if (cbase >= a.n_last) continue;
 #pragma unroll
-                for (int pb = 0; pb < NPB; ++pb) {
-                    const int p = pb * 16 + r;
-                    const int Lr = p / a.BI, il = p % a.BI;
-                    const int64_t L = L0 + Lr, i = i0 + il;
-                    if (Lr >= a.BL || L >= a.NL || i >= a.n_mid) continue;
-                    T* dst = static_cast<T*>(a.out) + (L * a.n_mid + i) * a.n_last + cbase;
-                    if (AccRowsContiguous<T>::value && a.vec4 && cbase + 4 * g + 3 < a.n_last) {
-                        typedef T vec_t __attribute__((ext_vector_type(4)));
-                        vec_t w;
+                    for (int pb = 0; pb < NPB; ++pb) {
+                        const int p = pb * 16 + r;
+                        const int Lr = p / a.BI, il = p % a.BI;
+                        const int64_t L = L0 + Lr, i = i0 + il;
+                        if (Lr >= a.BL || L >= a.NL || i >= a.n_mid) continue;
+                        T* dst = static_cast<T*>(a.out) + (L * a.n_mid + i) * a.n_last + cbase;
+                        if (a.vec4 && cbase + 4 * g + 3 < a.n_last) {
+                            typedef T vec_t __attribute__((ext_vector_type(4)));
+                            vec_t w;
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[c][pb][v]);
-                        *reinterpret_cast<vec_t*>(dst + 4 * g) = w;
-                    } else {
+                            for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[c][pb][v]);
+                            *reinterpret_cast<vec_t*>(dst + 4 * g) = w;
+                        } else {
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            const int row = acc_row<T>(g, v);
-                            if (cbase + row < a.n_last) dst[row] = to_storage<T>(acc[c][pb][v]);
+                            for (int v = 0; v < 4; ++v) {
+                                const int row = acc_row<T>(g, v);
+                                if (cbase + row < a.n_last) dst[row] = to_storage<T>(acc[c][pb][v]);
+                            }
                         }
                     }
                 }
             }
         }
+    }
+}
+
+// TT certificate (Thm. thm:tt_conditional) without dense reconstructions:
+// for each tile the FP64 reconstructions from the base cores (set 0), the
+// augmented cores (set 1) and the widened rounded augmented cores (set 2)
+// are formed on chip, one after the other, and compared with T.  Workgroup
+// w writes part[s * nparts + w] for the five sums
+//   s = 0 ||T - T_R||^2, 1 ||T - T_R+||^2, 2 ||T_R+ - T^_R+||^2,
+//       3 ||T - T^_R+||^2, 4 ||T||^2,
+// each accumulated per lane in a fixed order and combined in wave order.
+template <int NPB, int NLB>
+__global__ __launch_bounds__(256) void k_tt_cert(TTArgs a, const double* __restrict__ Tref,
+                                                 double* __restrict__ part, int64_t nparts) {
+    using T = double;
+    using AccV = double4_t;
+    extern __shared__ double4_t smem_v[];
+    char* smem = reinterpret_cast<char*>(smem_v);
+    T* Zl = reinterpret_cast<T*>(smem);
+    double* cb0 = reinterpret_cast<double*>(smem + a.cb_off);
+    double* cb1 = cb0 + (size_t)a.BL * a.chain_rmax;
+    __shared__ double red[4][5];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 15, g = lane >> 4;
+    const int64_t i0 = (int64_t)blockIdx.x * a.BI;
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    constexpr int NCB = 2;
+
+    for (int q = 0; q < 3; ++q) {
+        T* Zf = reinterpret_cast<T*>(smem + a.set[q].zf_off);
+        for (int idx = tid; idx < a.P * a.set[q].ldf; idx += 256) Zf[idx] = T(0);
+    }
+    double sum[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
+
+    for (int64_t lb = blockIdx.y; lb < a.num_L_blocks; lb += gridDim.y) {
+        const int64_t L0 = lb * a.BL;
+        for (int q = 0; q < 3; ++q) {
+            const TTSet& S = a.set[q];
+            __syncthreads();   // Zl (and, for q = 0, every Zf) is free again
+            build_left<T, 256>(a, S, S.core + 2, L0, Zl, cb0, cb1);
+            __syncthreads();
+            middle_product<T, NLB>(a, S, Zl, reinterpret_cast<T*>(smem + S.zf_off), i0, wave, r, g);
+        }
+        __syncthreads();
+
+        for (int cp = wave; cp < (n_cb + NCB - 1) / NCB; cp += 4) {
+            // transposed blocks: lane holds rows p = pb*16 + g + 4v of column col
+            AccV tv[NCB][NPB], rp[NCB][NPB], acc[NCB][NPB];
+            last_product<T, NCB, NPB, true>(a, a.set[0], reinterpret_cast<const T*>(smem + a.set[0].zf_off), cp, r,
+                                            g, acc);
+#pragma unroll
+            for (int c = 0; c < NCB; ++c) {
+                const int64_t col = (int64_t)(NCB * cp + c) * 16 + r;
+#pragma unroll
+                for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int p = pb * 16 + acc_row<T>(g, v);
+                        const int Lr = (a.BI == 1) ? p : p / a.BI, il = (a.BI == 1) ? 0 : p % a.BI;
+                        const int64_t L = L0 + Lr, i = i0 + il;
+                        const bool ok = col < a.n_last && Lr < a.BL && L < a.NL && i < a.n_mid;
+                        const double t = Tref[ok ? (L * a.n_mid + i) * a.n_last + col : 0];
+                        tv[c][pb][v] = ok ? t : 0.0;
+                        // rows outside the tensor compare zero with zero
+                        const double dr = ok ? tv[c][pb][v] - acc[c][pb][v] : 0.0;
+                        sum[0] += dr * dr;
+                        sum[4] += tv[c][pb][v] * tv[c][pb][v];
+                    }
+            }
+            last_product<T, NCB, NPB, true>(a, a.set[1], reinterpret_cast<const T*>(smem + a.set[1].zf_off), cp, r,
+                                            g, rp);
+            last_product<T, NCB, NPB, true>(a, a.set[2], reinterpret_cast<const T*>(smem + a.set[2].zf_off), cp, r,
+                                            g, acc);
+#pragma unroll
+            for (int c = 0; c < NCB; ++c) {
+                const int64_t col = (int64_t)(NCB * cp + c) * 16 + r;
+#pragma unroll
+                for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int p = pb * 16 + acc_row<T>(g, v);
+                        const int Lr = (a.BI == 1) ? p : p / a.BI, il = (a.BI == 1) ? 0 : p % a.BI;
+                        const int64_t L = L0 + Lr, i = i0 + il;
+                        const bool ok = col < a.n_last && Lr < a.BL && L < a.NL && i < a.n_mid;
+                        const double d1 = ok ? tv[c][pb][v] - rp[c][pb][v] : 0.0;
+                        const double d2 = ok ? rp[c][pb][v] - acc[c][pb][v] : 0.0;
+                        const double d3 = ok ? tv[c][pb][v] - acc[c][pb][v] : 0.0;
+                        sum[1] += d1 * d1;
+                        sum[2] += d2 * d2;
+                        sum[3] += d3 * d3;
+                    }
+            }
+        }
+        __syncthreads();   // the Zf buffers are rewritten for the next block
+    }
+
+#pragma unroll
+    for (int s = 0; s < 5; ++s) {
+        const double w = wave_sum(sum[s]);
+        if (lane == 0) red[wave][s] = w;
+    }
+    __syncthreads();
+    if (tid < 5) {
+        const int64_t wg = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+        part[tid * nparts + wg] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
     }
 }
 
@@ -444,9 +570,11 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         if (d >= 4)
             for (int c = 1; c <= d - 2; ++c) p.chain_rmax = (int)std::max<int64_t>(p.chain_rmax, rank_sets[q][c]);
     }
-    // at most 64 KB of LDS per workgroup, so that at least two workgroups
-    // share a compute unit
-    if (max_lds > 65536) max_lds = 65536;
+    // at most 64 KB of LDS per workgroup (80 KB for the three-set
+    // certificate kernel), so that at least two workgroups share a compute
+    // unit
+    const size_t lds_cap = nsets > 1 ? 81920 : 65536;
+    if (max_lds > lds_cap) max_lds = lds_cap;
     const int P0 = tune_env("LRC_TT_P", (prec == P64) ? 32 : 64);
     for (int P = P0; P >= 16; P /= 2) {
         int BI, BL;
@@ -464,11 +592,13 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         const int Peff = (int)round_up((int64_t)BL * BI, 16);
         const int BLpad = (int)round_up(BL, 16);
         if (Peff > 64 || BLpad > 64) continue;
-        size_t lds = 0;
+        // one Z_{d-2} buffer, shared by the sets in turn; one Z_{d-1} per set
+        size_t lds = 0, zl = 0;
         for (int q = 0; q < nsets; ++q) {
-            lds += (size_t)round_up((int64_t)BLpad * p.set[q].ldl * e, 32);
+            zl = std::max<size_t>(zl, (size_t)round_up((int64_t)BLpad * p.set[q].ldl * e, 32));
             lds += (size_t)round_up((int64_t)Peff * p.set[q].ldf * e, 32);
         }
+        lds += zl;
         if (d >= 4) lds += (size_t)2 * BL * p.chain_rmax * acc_b;
         if (lds <= max_lds) {
             p.BL = BL;
@@ -496,10 +626,11 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     return 0;
 }
 
+// Kernel arguments for the plan, with the cores of every set staged.
 template <typename T>
-static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, void* out, Workspace& ws,
-                           hipStream_t stream, const char* label) {
-    TTArgs a{};
+static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, void* out, Workspace& ws,
+                             hipStream_t stream, const char* label, TTArgs& a) {
+    a = TTArgs{};
     a.d = p.d;
     a.nsets = p.nsets;
     for (int c = 0; c < p.d; ++c) a.dims[c] = p.dims[c];
@@ -520,11 +651,13 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     a.ncp = (int)round_up(p.n_last, 32);
     a.out = out;
     a.vec4 = out && (p.n_last % 4 == 0) && (reinterpret_cast<uintptr_t>(out) % (4 * sizeof(T)) == 0);
-    if (!label) label = p.prec == P64 ? "tt_fused_f64" : (p.prec == P32 ? "tt_fused_f32" : "tt_fused_f16");
     // the staging copy is timed under the kernel's label with a "_stage" suffix
     char stage_label[64];
     std::snprintf(stage_label, sizeof(stage_label), "%s_stage", label);
+    // LDS: the shared Z_{d-2} buffer first, then one Z_{d-1} per set
     int off = 0;
+    for (int q = 0; q < p.nsets; ++q)
+        off = std::max(off, (int)round_up((int64_t)a.BLpad * p.set[q].ldl * (int64_t)sizeof(T), 32));
     for (int q = 0; q < p.nsets; ++q) {
         TTSet& S = a.set[q];
         const TTPlanSet& ps = p.set[q];
@@ -539,8 +672,7 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
         S.ldl = ps.ldl;
         S.ldf = ps.ldf;
         S.Rt = ps.Rt;
-        S.zl_off = off;
-        off += (int)round_up((int64_t)a.BLpad * ps.ldl * (int64_t)sizeof(T), 32);
+        S.zl_off = 0;
         S.zf_off = off;
         off += (int)round_up((int64_t)p.P * ps.ldf * (int64_t)sizeof(T), 32);
         {
@@ -561,9 +693,43 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
         }
     }
     a.cb_off = off;
+    return hipSuccess;
+}
+
+template <typename T>
+static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, void* out, Workspace& ws,
+                           hipStream_t stream, const char* label) {
+    if (!label) label = p.prec == P64 ? "tt_fused_f64" : (p.prec == P32 ? "tt_fused_f32" : "tt_fused_f16");
+    TTArgs a;
+    hipError_t e = prepare_tt<T>(p, cores, out, ws, stream, label, a);
+    if (e != hipSuccess) return e;
     dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
     KernelTimer tk(label, stream);
     launch_fused<T>(p.P / 16, (int)round_up(p.BL, 16) / 16, grid, p.lds_bytes, stream, a);
+    return hipGetLastError();
+}
+
+int64_t tt_cert_parts(const TTPlan& p) { return p.num_i_blocks * (int64_t)p.grid_L; }
+
+hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, const double* Tref, double* part,
+                          Workspace& ws, hipStream_t stream) {
+    if (p.prec != P64 || p.nsets != 3 || p.P > 32) return hipErrorInvalidValue;
+    TTArgs a;
+    hipError_t e = prepare_tt<double>(p, cores, nullptr, ws, stream, "cert_tt_fused_f64", a);
+    if (e != hipSuccess) return e;
+    const dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
+    const int64_t nparts = tt_cert_parts(p);
+    const int npb = p.P / 16, nlb = (int)round_up(p.BL, 16) / 16;
+    KernelTimer tk("cert_tt_fused_f64", stream);
+#define LRC_TTC(P, L) hipLaunchKernelGGL((k_tt_cert<P, L>), grid, dim3(256), p.lds_bytes, stream, a, Tref, part, nparts)
+    // the three sets' accumulators fit the registers for tiles of up to 32 rows
+    switch (npb * 8 + nlb) {
+    case 1 * 8 + 1: LRC_TTC(1, 1); break;
+    case 2 * 8 + 1: LRC_TTC(2, 1); break;
+    case 2 * 8 + 2: LRC_TTC(2, 2); break;
+    default: return hipErrorInvalidValue;
+    }
+#undef LRC_TTC
     return hipGetLastError();
 }
 
