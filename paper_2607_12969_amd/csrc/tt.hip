@@ -197,58 +197,74 @@ __device__ void build_left(const TTArgs& a, const TTSet& S, const void* const* l
 }
 
 // acc[c][j] += sum_kb A_c(kb) B_j(kb) for c < NC, j < NJ, over nkb >= 1 K
-// steps.  The loop is unrolled by two so that every step's operands were
-// requested a step earlier (B from LDS) or two steps earlier (A, core
-// fragments from global memory); indices past the end are clamped, so the
-// load sequence has no branches and every step's NC * NJ matrix-core
-// products issue back to back.  An odd last step runs after the loop.
-// With SWAP the products are B_j A_c instead (the accumulator then holds the
-// transposed block).
+// steps (with SWAP the products are B_j A_c: the accumulators then hold the
+// transposed blocks).  Four register sets hold the A fragments (core
+// fragments from global memory) of steps kb .. kb+3 and two sets the B
+// fragments (LDS) of steps kb, kb+1; each set is refilled right after the
+// step that used it, for the step four (A) or two (B) later, so no register
+// is copied and every load has several steps of matrix-core work to arrive.
+// Indices past the end are clamped, so the load sequence has no branches.
 template <typename T, int NC, int NJ, bool SWAP = false, class AF, class BF>
 __device__ __forceinline__ void mma_chain(AF afrag, BF bfrag, int nkb,
                                           typename PrecTraits<T>::accv (&acc)[NC][NJ]) {
-    auto mm = [](const auto& x, const auto& y, const auto& c) { return SWAP ? mfma(y, x, c) : mfma(x, y, c); };
     using Frag = typename PrecTraits<T>::frag;
-    Frag a0[NC], a1[NC], b0[NJ], b1[NJ];
+    auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
+    Frag x0[NC], x1[NC], y0[NC], y1[NC], be[NJ], bo[NJ];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-        a0[c] = afrag(c, 0);
-        a1[c] = afrag(c, 1);
+        x0[c] = afrag(c, 0);
+        x1[c] = afrag(c, cl(1));
+        y0[c] = afrag(c, cl(2));
+        y1[c] = afrag(c, cl(3));
     }
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) b0[j] = bfrag(j, 0);
+    for (int j = 0; j < NJ; ++j) {
+        be[j] = bfrag(j, 0);
+        bo[j] = bfrag(j, cl(1));
+    }
+    auto step = [&](Frag (&a)[NC], Frag (&b)[NJ]) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) acc[c][j] = SWAP ? mfma(b[j], a[c], acc[c][j]) : mfma(a[c], b[j], acc[c][j]);
+    };
+    auto refill_a = [&](Frag (&a)[NC], int k) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) a[c] = afrag(c, cl(k));
+    };
+    auto refill_b = [&](Frag (&b)[NJ], int k) {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) b[j] = bfrag(j, cl(k));
+    };
+    // the scheduling barriers keep each refill right behind its step (the
+    // scheduler would otherwise bunch the loads late and shorten their lead)
     int kb = 0;
-    for (; kb + 1 < nkb; kb += 2) {
-        const int k2 = (kb + 2 < nkb) ? kb + 2 : nkb - 1;
-        const int k3 = (kb + 3 < nkb) ? kb + 3 : nkb - 1;
-        Frag n0[NC], n1[NC];
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) b1[j] = bfrag(j, kb + 1);
-#pragma unroll
-        for (int c = 0; c < NC; ++c) n0[c] = afrag(c, k2);
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) acc[c][j] = mm(a0[c], b0[j], acc[c][j]);
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) b0[j] = bfrag(j, k2);
-#pragma unroll
-        for (int c = 0; c < NC; ++c) n1[c] = afrag(c, k3);
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) acc[c][j] = mm(a1[c], b1[j], acc[c][j]);
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            a0[c] = n0[c];
-            a1[c] = n1[c];
-        }
+    for (; kb + 3 < nkb; kb += 4) {
+        step(x0, be);
+        refill_a(x0, kb + 4);
+        refill_b(be, kb + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        step(x1, bo);
+        refill_a(x1, kb + 5);
+        refill_b(bo, kb + 3);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y0, be);
+        refill_a(y0, kb + 6);
+        refill_b(be, kb + 4);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y1, bo);
+        refill_a(y1, kb + 7);
+        refill_b(bo, kb + 5);
+        __builtin_amdgcn_sched_barrier(0);
     }
+    // remaining 1 to 3 steps: x0, x1, y0 hold A of steps kb .. kb+2
     if (kb < nkb) {
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-            for (int j = 0; j < NJ; ++j) acc[c][j] = mm(a0[c], b0[j], acc[c][j]);
+        step(x0, be);
+        if (kb + 1 < nkb) {
+            refill_b(be, kb + 2);
+            step(x1, bo);
+            if (kb + 2 < nkb) step(y0, be);
+        }
     }
 }
 
@@ -429,7 +445,7 @@ __global__ __launch_bounds__(256) void k_tt_cert(TTArgs a, const double* __restr
     const int r = lane & 15, g = lane >> 4;
     const int64_t i0 = (int64_t)blockIdx.x * a.BI;
     const int n_cb = (int)((a.n_last + 15) / 16);
-    constexpr int NCB = 2;
+    constexpr int NCB = 1;   // three sets of accumulators live at once
 
     for (int q = 0; q < 3; ++q) {
         T* Zf = reinterpret_cast<T*>(smem + a.set[q].zf_off);
