@@ -177,15 +177,16 @@ class Workload:
             out[f"apply_p2_mfma_{p}"] = (*p2, p)
             f, by = tt_counts(self.dims, self.tt_in[p][2] + [1], EBYTES[p])
             out[f"tt_fused_{p}"] = (f, by, p)
-        # certificate kernels (FP64): the dense reconstructions of T_R, T_R+
-        # and of the rounded cores alternate with ranks (64,64) / (65,65)
+        # TT certificate (FP64, one fused launch): the reconstructions of T_R
+        # (ranks 64, 64), T_R+ and of the rounded cores (65, 65) formed on
+        # chip and compared with T; bytes = T read once plus the three core sets
+        N = float(np.prod(self.dims))
         fb, bb = tt_counts(self.dims, [1, 64, 64, 1], 8)
         fa, ba = tt_counts(self.dims, [1, 65, 65, 1], 8)
-        out["cert_tt_fused_f64"] = ((fb + 2 * fa) / 3, (bb + 2 * ba) / 3, "f64")
+        out["cert_tt_fused_f64"] = (fb + 2 * fa + 9.0 * N, 8.0 * N + (bb - 8.0 * N) + 2 * (ba - 8.0 * N), "f64")
         r2 = 2 * (self.k + 1)
         gm, gn = gram_counts(m, r2), gram_counts(n, r2)
         out["cert_gram_f64"] = ((gm[0] + gn[0]) / 2, (gm[1] + gn[1]) / 2, "f64")
-        N = float(np.prod(self.dims))
         out["cert_sumsq5_f64"] = (11.0 * N, 32.0 * N, "f64")
         return out
 

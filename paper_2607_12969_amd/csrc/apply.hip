@@ -348,7 +348,9 @@ enum { ATB_APPLY = 0, ATB_GRAM = 1 };
 //   ATB_APPLY: T'^T[n][ldo] = s[m] * C rounded to T, for m < Mout; rows
 //              m >= M are written as zeros (their accumulators hold data of
 //              clamped rows).
-//   ATB_GRAM : G[m][ldo] = C in double (T = double), m < M.
+//   ATB_GRAM : G = P^T P is symmetric: only tiles on or above the diagonal
+//              are computed, and the value of (m, n), m <= n, is written to
+//              both G[m][n] and G[n][m] (T = double).
 template <typename T, class C, int MODE>
 __device__ __forceinline__ void atb_store(const typename C::AccV& a, int tid, int fn, int fm, int64_t m0,
                                           int64_t n0, int64_t M, int64_t N, const T* __restrict__ svals,
@@ -367,7 +369,10 @@ __device__ __forceinline__ void atb_store(const typename C::AccV& a, int tid, in
                 static_cast<T*>(out)[nn * ldo + mm] = to_storage<T>(val);
             }
         } else {
-            if (nn < N && mm < M) static_cast<double*>(out)[mm * ldo + nn] = (double)a[v];
+            if (nn < N && mm < M && mm <= nn) {
+                static_cast<double*>(out)[mm * ldo + nn] = (double)a[v];
+                static_cast<double*>(out)[nn * ldo + mm] = (double)a[v];
+            }
         }
     }
 }
@@ -399,6 +404,7 @@ __global__ __launch_bounds__(C::NT) void k_atb(
     if (lt >= (int64_t)tiles_m * tiles_n * splits) return;
     const int64_t tile = lt % ((int64_t)tiles_m * tiles_n);
     const int sp = (int)(lt / ((int64_t)tiles_m * tiles_n));
+    if (MODE == ATB_GRAM && tile % tiles_m > tile / tiles_m) return;   // below the diagonal
     const int64_t m0 = (tile % tiles_m) * C::BM, n0 = (tile / tiles_m) * C::BN;
     const int nfm = live_frags<C::FM>(m0 + wm * C::WTM, M), nfn = live_frags<C::FN>(n0 + wn * C::WTN, N);
     const int64_t kbeg = (int64_t)sp * chunk;
@@ -461,6 +467,7 @@ __global__ __launch_bounds__(C::NT) void k_atb_finish(
     const int tid = threadIdx.x;
     const int64_t tile = blockIdx.x / NF;
     const int f = blockIdx.x % NF;
+    if (MODE == ATB_GRAM && tile % tiles_m > tile / tiles_m) return;   // below the diagonal
     const AccV* src = part + (tile * splits * NF + f) * C::NT + tid;
     const int64_t qs = (int64_t)NF * C::NT;      // stride between splits
     AccV acc = zero_accv<AccV>();
