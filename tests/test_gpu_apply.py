@@ -134,3 +134,32 @@ def test_tail_workload_sampled(lrc, tail, k):
         print(f"apply 65536x4096 k={r} prec={prec}", flush=True)
         err = _sampled(lrc, w["U"][:, :r], w["sigma"][:r], w["V"][:, :r], w["X"], prec, rows, cols)
         assert err <= TOL[prec], (prec, err)
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_unaligned_operands_are_staged(lrc, prec):
+    """Operands whose base address is not 16-byte aligned (views one element
+    into a buffer) go through the padded copies of the MFMA path."""
+    import torch
+    m, n, k, b = 300, 500, 64, 128
+    d = synth.random_factors(m, n, k, b, tag=9)
+    hs = [stored_pair(a, prec) for a in (d["U"], d["s"], d["V"], d["X"])]
+    views = []
+    for h, _ in hs:
+        buf = torch.zeros(h.size + 1, dtype=torch.from_numpy(h).dtype, device="cuda")
+        v = buf[1:].view(h.shape)
+        v.copy_(torch.from_numpy(np.ascontiguousarray(h)))
+        views.append(v)
+    lrc.set_apply_path(2)
+    try:
+        lrc.profile_reset()
+        lrc.profile_enable(True)
+        Y = lrc.matrix_apply(*views)
+        torch.cuda.synchronize()
+        labels = lrc.profile_read()
+    finally:
+        lrc.profile_enable(False)
+        lrc.set_apply_path(0)
+    assert "apply_stage" in labels
+    u, s, v, x = [o for _, o in hs]
+    assert rel_fro(Y.cpu().numpy().astype(np.float64), O.apply(u, s, v, x)) <= TOL[prec]

@@ -174,3 +174,46 @@ def test_tt_sixway_workload(lrc):
         assert abs(got["eta"] - want["eta"]) <= 1e-6 * want["eta"]
         assert got["certified"] == want["certified"] == False   # noqa: E712
         assert got["outcome"] == want["outcome"] == 0
+
+
+def _tt_labels(lrc, T, base, aug, prec):
+    """Certificate plus the kernel labels its launches recorded."""
+    lrc.profile_reset()
+    lrc.profile_enable(True)
+    try:
+        got, want = _tt(lrc, T, base, aug, prec)
+        labels = {k: v[0] for k, v in lrc.profile_read().items()}
+    finally:
+        lrc.profile_enable(False)
+    return got, want, labels
+
+
+@pytest.mark.parametrize("dims,rb,ra", [
+    ((300, 200), (40,), (41,)),                 # d = 2: one middle and one last core
+    ((12, 40, 30, 50), (10, 24, 20), (11, 25, 21)),
+])
+def test_tt_fused_certificate_shapes(lrc, dims, rb, ra):
+    """The fused certificate kernel (one launch, no dense reconstructions)
+    on two-core and four-core trains."""
+    base = synth.random_tt_cores(dims, [1, *rb, 1], tag=21)
+    aug = O.left_orthogonalize(synth.random_tt_cores(dims, [1, *ra, 1], tag=22))
+    rng = np.random.default_rng(5)
+    T = O.tt_full(base) + 1e-3 * rng.standard_normal(dims)
+    for prec in ("fp32", "fp16"):
+        got, want, labels = _tt_labels(lrc, T, base, aug, prec)
+        assert labels.get("cert_tt_fused_f64") == 1 and "cert_sumsq5_f64" not in labels, labels
+        _compare(got, want, eta_rtol=1e-6, err_rtol=1e-6, e_atol=1e-12 * want["norm_ref"])
+
+
+def test_tt_certificate_unfused_fallback(lrc):
+    """Ranks whose three on-chip interface sets exceed the fused kernel's LDS
+    budget take the dense path: three FP64 reconstructions and one pass of
+    sums over the tensors."""
+    dims = (256, 4, 256)
+    base = synth.random_tt_cores(dims, [1, 200, 200, 1], tag=23)
+    aug = O.left_orthogonalize(synth.random_tt_cores(dims, [1, 201, 201, 1], tag=24))
+    rng = np.random.default_rng(6)
+    T = O.tt_full(base) + 1e-3 * rng.standard_normal(dims)
+    got, want, labels = _tt_labels(lrc, T, base, aug, "fp16")
+    assert labels.get("cert_tt_fused_f64") == 3 and labels.get("cert_sumsq5_f64") == 1, labels
+    _compare(got, want, eta_rtol=1e-6, err_rtol=1e-6, e_atol=1e-12 * want["norm_ref"])
