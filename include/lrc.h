@@ -243,6 +243,10 @@ void lrc_shutdown(void);
  * (truncated to len-1 characters) and returns the full length.
  */
 int lrc_profile_enable(int on);
+/* Restricts the event pairs to launches whose label equals `label` (NULL or
+ * "" removes the restriction), so that one kernel can be timed inside a
+ * longer run at the cost of its own two event records only. */
+int lrc_profile_filter(const char* label);
 void lrc_profile_reset(void);
 int lrc_profile_read(const char* label, int64_t* launches, double* total_ms);
 int64_t lrc_profile_labels(char* buf, int64_t len);

@@ -153,6 +153,7 @@ int tt_reconstruct_impl(const void* const* cores, const int64_t* dims, const int
 namespace {
 std::mutex g_pmu;
 bool g_prof = false;
+std::string g_prof_filter;   // empty: every label
 struct PendingTime {
     std::string label;
     hipEvent_t a, b;
@@ -193,6 +194,7 @@ namespace lrc {
 KernelTimer::KernelTimer(const char* lbl, hipStream_t s) : label(lbl), stream(s), start(nullptr) {
     std::lock_guard<std::mutex> lk(g_pmu);
     if (!g_prof) return;
+    if (!g_prof_filter.empty() && g_prof_filter != lbl) return;
     hipEvent_t e = pool_event();
     if (e && hipEventRecord(e, s) == hipSuccess) start = e;
 }
@@ -349,6 +351,12 @@ int64_t lrc_tt_storage_bytes(const int64_t* dims, const int64_t* ranks, int d, i
 int lrc_profile_enable(int on) {
     std::lock_guard<std::mutex> lk(g_pmu);
     g_prof = on != 0;
+    return LRC_OK;
+}
+
+int lrc_profile_filter(const char* label) {
+    std::lock_guard<std::mutex> lk(g_pmu);
+    g_prof_filter = label ? label : "";
     return LRC_OK;
 }
 

@@ -101,6 +101,8 @@ def lib():
     L.lrc_version.restype = ctypes.c_int
     L.lrc_profile_enable.argtypes = [ctypes.c_int]
     L.lrc_profile_enable.restype = ctypes.c_int
+    L.lrc_profile_filter.argtypes = [ctypes.c_char_p]
+    L.lrc_profile_filter.restype = ctypes.c_int
     L.lrc_profile_reset.argtypes = []
     L.lrc_profile_reset.restype = None
     L.lrc_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(_i64), ctypes.POINTER(ctypes.c_double)]
@@ -273,6 +275,11 @@ def certify_tt(T, base_cores, aug_cores, aug_cores_h) -> dict:
 
 def profile_enable(on: bool = True):
     _check(lib().lrc_profile_enable(1 if on else 0))
+
+
+def profile_filter(label=None):
+    """Time only launches labelled `label` (None: every launch)."""
+    _check(lib().lrc_profile_filter(label.encode() if label else None))
 
 
 def profile_reset():
