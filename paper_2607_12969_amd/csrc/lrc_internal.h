@@ -115,7 +115,7 @@ constexpr int kTTMaxSets = 3;
 struct TTPlanSet {
     int64_t ranks[kMaxD + 1];
     int rL, rM;          // r_{d-2}, r_{d-1}
-    int Kp2, Kp3;        // rL, rM rounded to the MFMA K step
+    int Kp2, Kp3;        // rL, rM rounded to the MFMA K step (Kp3: the largest over the plan's sets)
     int Rt;              // rM rounded up to 16 (row blocks of the middle product)
     int ldl, ldf;        // LDS row pitches of Z_{d-2} and Z_{d-1} (padded against bank conflicts)
 };

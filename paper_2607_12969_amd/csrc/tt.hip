@@ -420,11 +420,119 @@ __global__ __launch_bounds__(256) void k_tt_fused(TTArgs a) {
     }
 }
 
+// Left interface rows of a tile for d = 3 (rows of G_1), fetched into
+// registers ahead of their use.  The BLpad = 16 NLB rows are spread over
+// the 256 threads, TPR = 256 / BLpad threads per row; entry e of a thread is
+// column tid % TPR + TPR e of row tid / TPR (e < NE covers Kp2 <= TPR NE).
+// The loads are unconditional (clamped addresses) and masked only when
+// stored, so that they stay in flight across the work that runs meanwhile.
+template <int NLB, int NE>
+__device__ __forceinline__ void fetch_left3(const TTArgs& a, const TTSet& S, int64_t L0, int tid, double (&v)[NE]) {
+    constexpr int TPR = 256 / (16 * NLB);
+    const double* g1 = static_cast<const double*>(S.core[2]);
+    const int Lr = tid / TPR, c0 = tid % TPR;
+    const int64_t L = L0 + Lr;
+    const double* row = g1 + ((Lr < a.BL && L < a.NL) ? L : 0) * S.rL;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+        if (TPR * e >= S.Kp2) break;
+        const int c = c0 + TPR * e;
+        v[e] = row[c < S.rL ? c : 0];
+    }
+}
+template <int NLB, int NE>
+__device__ __forceinline__ void store_left3(const TTArgs& a, const TTSet& S, int64_t L0, int tid,
+                                            const double (&v)[NE], double* Zl) {
+    constexpr int TPR = 256 / (16 * NLB);
+    const int Lr = tid / TPR, c0 = tid % TPR;
+    const bool rok = Lr < a.BL && L0 + Lr < a.NL;
+    double* dst = Zl + Lr * S.ldl + c0;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+        if (TPR * e >= S.Kp2) break;
+        const int c = c0 + TPR * e;
+        if (c < S.Kp2) dst[TPR * e] = (rok && c < S.rL) ? v[e] : 0.0;
+    }
+}
+
+// acc[q][j] += sum_kb B_q(kb, j) A_q(kb) for the NS core sets at once
+// (transposed blocks, FP64): one chain whose steps issue the products of
+// every set, with the register rings of mma_chain (four A sets from global
+// memory, two B sets from LDS, each refilled right behind its step).
+template <int NS, int NJ, class AF, class BF>
+__device__ __forceinline__ void mma_chain_sets(AF afrag, BF bfrag, int nkb, double4_t (&acc)[NS][NJ]) {
+    auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
+    double x0[NS], x1[NS], y0[NS], y1[NS], be[NS][NJ], bo[NS][NJ];
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+        x0[q] = afrag(q, 0);
+        x1[q] = afrag(q, cl(1));
+        y0[q] = afrag(q, cl(2));
+        y1[q] = afrag(q, cl(3));
+    }
+#pragma unroll
+    for (int q = 0; q < NS; ++q)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            be[q][j] = bfrag(q, j, 0);
+            bo[q][j] = bfrag(q, j, cl(1));
+        }
+    auto step = [&](double (&x)[NS], double (&b)[NS][NJ]) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) acc[q][j] = mfma(b[q][j], x[q], acc[q][j]);
+    };
+    auto refill_a = [&](double (&x)[NS], int k) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q) x[q] = afrag(q, cl(k));
+    };
+    auto refill_b = [&](double (&b)[NS][NJ], int k) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) b[q][j] = bfrag(q, j, cl(k));
+    };
+    int kb = 0;
+    for (; kb + 3 < nkb; kb += 4) {
+        step(x0, be);
+        refill_a(x0, kb + 4);
+        refill_b(be, kb + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        step(x1, bo);
+        refill_a(x1, kb + 5);
+        refill_b(bo, kb + 3);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y0, be);
+        refill_a(y0, kb + 6);
+        refill_b(be, kb + 4);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y1, bo);
+        refill_a(y1, kb + 7);
+        refill_b(bo, kb + 5);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kb < nkb) {
+        step(x0, be);
+        if (kb + 1 < nkb) {
+            refill_b(be, kb + 2);
+            step(x1, bo);
+            if (kb + 2 < nkb) step(y0, be);
+        }
+    }
+}
+
 // TT certificate (Thm. thm:tt_conditional) without dense reconstructions:
 // for each tile the FP64 reconstructions from the base cores (set 0), the
 // augmented cores (set 1) and the widened rounded augmented cores (set 2)
-// are formed on chip, one after the other, and compared with T.  Workgroup
-// w writes part[s * nparts + w] for the five sums
+// are formed on chip and compared with T.  The three middle products run
+// one after the other through the shared Z_{d-2} buffer (for d = 3 the next
+// set's rows of G_1 are fetched while the current product runs); the last
+// products of the three sets share one matrix-core chain per column block,
+// with the block's values of T fetched before the chain.  All sets use one
+// K extent for the last product (the largest; the staged cores and the Z_{d-1}
+// columns beyond a set's rank are zero).  Workgroup w writes
+// part[s * nparts + w] for the five sums
 //   s = 0 ||T - T_R||^2, 1 ||T - T_R+||^2, 2 ||T_R+ - T^_R+||^2,
 //       3 ||T - T^_R+||^2, 4 ||T||^2,
 // each accumulated per lane in a fixed order and combined in wave order.
@@ -433,6 +541,7 @@ __global__ __launch_bounds__(256) void k_tt_cert(TTArgs a, const double* __restr
                                                  double* __restrict__ part, int64_t nparts) {
     using T = double;
     using AccV = double4_t;
+    constexpr int NE = 16;   // prefetched G_1 entries per thread (d = 3)
     extern __shared__ double4_t smem_v[];
     char* smem = reinterpret_cast<char*>(smem_v);
     T* Zl = reinterpret_cast<T*>(smem);
@@ -442,75 +551,101 @@ __global__ __launch_bounds__(256) void k_tt_cert(TTArgs a, const double* __restr
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int r = lane & 15, g = lane >> 4;
     const int64_t i0 = (int64_t)blockIdx.x * a.BI;
     const int n_cb = (int)((a.n_last + 15) / 16);
-    constexpr int NCB = 1;   // three sets of accumulators live at once
+    const T* Zf0 = reinterpret_cast<const T*>(smem + a.set[0].zf_off);
+    const T* Zf1 = reinterpret_cast<const T*>(smem + a.set[1].zf_off);
+    const T* Zf2 = reinterpret_cast<const T*>(smem + a.set[2].zf_off);
+    // d = 3 with every set's rows within the prefetch registers
+    bool pre = a.d == 3 && a.BLpad == 16 * NLB;
+    for (int q = 0; q < 3; ++q) pre = pre && a.set[q].Kp2 <= (256 / (16 * NLB)) * NE;
 
     for (int q = 0; q < 3; ++q) {
         T* Zf = reinterpret_cast<T*>(smem + a.set[q].zf_off);
         for (int idx = tid; idx < a.P * a.set[q].ldf; idx += 256) Zf[idx] = T(0);
     }
     double sum[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    const int Kp3 = a.set[0].Kp3;   // common to the three sets
+    const int nkb = Kp3 / 4;
 
     for (int64_t lb = blockIdx.y; lb < a.num_L_blocks; lb += gridDim.y) {
         const int64_t L0 = lb * a.BL;
+        // per-block copies of the thread index: addresses derived from them
+        // are formed in the phase that uses them instead of being kept live
+        // across the whole loop
+        int tm = tid;
+        asm volatile("" : "+v"(tm));
+        const int rm = tm & 15, gm = (tm & 63) >> 4;
+        double v[NE];
+        if (pre) fetch_left3<NLB, NE>(a, a.set[0], L0, tm, v);
         for (int q = 0; q < 3; ++q) {
             const TTSet& S = a.set[q];
             __syncthreads();   // Zl (and, for q = 0, every Zf) is free again
-            build_left<T, 256>(a, S, S.core + 2, L0, Zl, cb0, cb1);
-            __syncthreads();
-            middle_product<T, NLB>(a, S, Zl, reinterpret_cast<T*>(smem + S.zf_off), i0, wave, r, g);
+            if (pre) {
+                store_left3<NLB, NE>(a, S, L0, tm, v, Zl);
+                __syncthreads();
+                if (q < 2) fetch_left3<NLB, NE>(a, a.set[q + 1], L0, tm, v);
+            } else {
+                build_left<T, 256>(a, S, S.core + 2, L0, Zl, cb0, cb1);
+                __syncthreads();
+            }
+            middle_product<T, NLB>(a, S, Zl, reinterpret_cast<T*>(smem + S.zf_off), i0, wave, rm, gm);
         }
         __syncthreads();
 
-        for (int cp = wave; cp < (n_cb + NCB - 1) / NCB; cp += 4) {
+        int tl = tid;
+        asm volatile("" : "+v"(tl));
+        const int r = tl & 15, g = (tl & 63) >> 4;
+        for (int cp = wave; cp < n_cb; cp += 4) {
             // transposed blocks: lane holds rows p = pb*16 + g + 4v of column col
-            AccV tv[NCB][NPB], rp[NCB][NPB], acc[NCB][NPB];
-            last_product<T, NCB, NPB, true>(a, a.set[0], reinterpret_cast<const T*>(smem + a.set[0].zf_off), cp, r,
-                                            g, acc);
+            const int64_t col = (int64_t)cp * 16 + r;
+            double tv[NPB][4];
 #pragma unroll
-            for (int c = 0; c < NCB; ++c) {
-                const int64_t col = (int64_t)(NCB * cp + c) * 16 + r;
+            for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
-                for (int pb = 0; pb < NPB; ++pb)
+                for (int v4 = 0; v4 < 4; ++v4) {
+                    const int p = pb * 16 + acc_row<T>(g, v4);
+                    const int Lr = (a.BI == 1) ? p : p / a.BI, il = (a.BI == 1) ? 0 : p % a.BI;
+                    const int64_t L = L0 + Lr, i = i0 + il;
+                    const bool ok = col < a.n_last && Lr < a.BL && L < a.NL && i < a.n_mid;
+                    tv[pb][v4] = Tref[ok ? (L * a.n_mid + i) * a.n_last + col : 0];
+                }
+            AccV acc[3][NPB];
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int p = pb * 16 + acc_row<T>(g, v);
-                        const int Lr = (a.BI == 1) ? p : p / a.BI, il = (a.BI == 1) ? 0 : p % a.BI;
-                        const int64_t L = L0 + Lr, i = i0 + il;
-                        const bool ok = col < a.n_last && Lr < a.BL && L < a.NL && i < a.n_mid;
-                        const double t = Tref[ok ? (L * a.n_mid + i) * a.n_last + col : 0];
-                        tv[c][pb][v] = ok ? t : 0.0;
-                        // rows outside the tensor compare zero with zero
-                        const double dr = ok ? tv[c][pb][v] - acc[c][pb][v] : 0.0;
-                        sum[0] += dr * dr;
-                        sum[4] += tv[c][pb][v] * tv[c][pb][v];
-                    }
-            }
-            last_product<T, NCB, NPB, true>(a, a.set[1], reinterpret_cast<const T*>(smem + a.set[1].zf_off), cp, r,
-                                            g, rp);
-            last_product<T, NCB, NPB, true>(a, a.set[2], reinterpret_cast<const T*>(smem + a.set[2].zf_off), cp, r,
-                                            g, acc);
+            for (int q = 0; q < 3; ++q)
 #pragma unroll
-            for (int c = 0; c < NCB; ++c) {
-                const int64_t col = (int64_t)(NCB * cp + c) * 16 + r;
+                for (int j = 0; j < NPB; ++j) acc[q][j] = zero_accv<AccV>();
+            const T* lb0 = last_base<T>(a.set[0], a.ncp, col, g);
+            const T* lb1 = last_base<T>(a.set[1], a.ncp, col, g);
+            const T* lb2 = last_base<T>(a.set[2], a.ncp, col, g);
+            const int64_t lstep = last_step<T>(a.ncp);
+            mma_chain_sets<3, NPB>(
+                [&](int q, int kb) { return (q == 0 ? lb0 : (q == 1 ? lb1 : lb2))[kb * lstep]; },
+                [&](int q, int j, int kb) {
+                    const T* Zf = q == 0 ? Zf0 : (q == 1 ? Zf1 : Zf2);
+                    return Zf[(j * 16 + r) * a.set[q].ldf + kb * 4 + g];
+                },
+                nkb, acc);
 #pragma unroll
-                for (int pb = 0; pb < NPB; ++pb)
+            for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int p = pb * 16 + acc_row<T>(g, v);
-                        const int Lr = (a.BI == 1) ? p : p / a.BI, il = (a.BI == 1) ? 0 : p % a.BI;
-                        const int64_t L = L0 + Lr, i = i0 + il;
-                        const bool ok = col < a.n_last && Lr < a.BL && L < a.NL && i < a.n_mid;
-                        const double d1 = ok ? tv[c][pb][v] - rp[c][pb][v] : 0.0;
-                        const double d2 = ok ? rp[c][pb][v] - acc[c][pb][v] : 0.0;
-                        const double d3 = ok ? tv[c][pb][v] - acc[c][pb][v] : 0.0;
-                        sum[1] += d1 * d1;
-                        sum[2] += d2 * d2;
-                        sum[3] += d3 * d3;
-                    }
-            }
+                for (int v4 = 0; v4 < 4; ++v4) {
+                    const int p = pb * 16 + acc_row<T>(g, v4);
+                    const int Lr = (a.BI == 1) ? p : p / a.BI, il = (a.BI == 1) ? 0 : p % a.BI;
+                    const int64_t L = L0 + Lr, i = i0 + il;
+                    const bool ok = col < a.n_last && Lr < a.BL && L < a.NL && i < a.n_mid;
+                    // rows outside the tensor compare zero with zero
+                    const double t = ok ? tv[pb][v4] : 0.0;
+                    const double r0 = ok ? acc[0][pb][v4] : 0.0;
+                    const double r1 = ok ? acc[1][pb][v4] : 0.0;
+                    const double r2 = ok ? acc[2][pb][v4] : 0.0;
+                    const double d0 = t - r0, d1 = t - r1, d2 = r1 - r2, d3 = t - r2;
+                    sum[0] += d0 * d0;
+                    sum[1] += d1 * d1;
+                    sum[2] += d2 * d2;
+                    sum[3] += d3 * d3;
+                    sum[4] += t * t;
+                }
         }
         __syncthreads();   // the Zf buffers are rewritten for the next block
     }
@@ -585,6 +720,14 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         s.Rt = (int)round_up(s.rM, 16);
         if (d >= 4)
             for (int c = 1; c <= d - 2; ++c) p.chain_rmax = (int)std::max<int64_t>(p.chain_rmax, rank_sets[q][c]);
+    }
+    // the sets of one kernel share the K extent of the last product (their
+    // chains run in step); the staged cores are zero beyond each rank
+    int kp3 = 0;
+    for (int q = 0; q < nsets; ++q) kp3 = std::max(kp3, p.set[q].Kp3);
+    for (int q = 0; q < nsets; ++q) {
+        p.set[q].ldf += kp3 - p.set[q].Kp3;
+        p.set[q].Kp3 = kp3;
     }
     // at most 64 KB of LDS per workgroup (80 KB for the three-set
     // certificate kernel), so that at least two workgroups share a compute
