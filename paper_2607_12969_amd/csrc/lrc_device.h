@@ -106,4 +106,15 @@ __device__ __forceinline__ Acc wave_sum(Acc x) {
     return x;
 }
 
+// Workgroups are handed to the 8 XCDs in turn (workgroup L to XCD L mod 8).
+// Renumber them so that XCD x works through the contiguous range
+// [x R, (x + 1) R) of logical tiles, R = ceil(total / 8), whose shared
+// operands then meet in that XCD's L2.  The grid is padded to 8 R
+// workgroups (xcd_grid); the numbers past `total` belong to no tile.
+__device__ __forceinline__ int64_t xcd_tile(int64_t total) {
+    const int64_t L = blockIdx.x;
+    return (L % 8) * ((total + 7) / 8) + L / 8;
+}
+static inline unsigned xcd_grid(int64_t total) { return (unsigned)(((total + 7) / 8) * 8); }
+
 }  // namespace lrc

@@ -662,6 +662,199 @@ __global__ __launch_bounds__(256) void k_tt_cert(TTArgs a, const double* __restr
     }
 }
 
+// ---------------------------------------------------------------------------
+// Wave-tile TT certificate for d = 3 whose last-product K extent fits the
+// registers (Kp3 = 4 NKB <= 68).  Each wave owns 16 rows L0 .. L0+15 of G_1
+// for one middle index i and all n_3 columns, and works alone: no LDS and no
+// barriers.  For each set it forms Z_2(L, i, :) = G_1(L, :) G_2(:, i, :) as
+// the transposed product G_2(:, i, :)^T G_1(L, :)^T on the matrix cores: the
+// accumulator of column block tb holds, in lane (r, g), value v,
+// Z_2(L0 + r, i, 16 tb + g + 4 v), which is exactly the A fragment of the
+// last product for K step kb = 4 tb + v (lane (r, g) supplies
+// Z_2(L0 + r, i, 4 kb + g)).  So the three Z_2 tiles stay in registers, and
+// the last products of the three sets run as one fully unrolled chain per
+// 16-column block of the output; the staged last-core fragments are fetched
+// four steps ahead, the last four steps of a block fetching the first four
+// of the next.
+
+// Load at a uniform base plus a per-lane byte offset (one 32-bit register
+// per lane; the step offsets stay in scalar registers).
+__device__ __forceinline__ double ld_off(const double* base, uint32_t byte_off) {
+    return *reinterpret_cast<const double*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+
+// Middle product of one set for the wave's tile: acc[tb] for the NT column
+// blocks of Z_2, over Kp2 / 4 K steps.  A fragments come from the staged
+// middle core (zero beyond the ranks), B fragments straight from the rows of
+// G_1 (row and K index clamped into the core: clamped rows are discarded
+// with the tile's rows past NL, clamped K entries meet zero A entries).
+template <int NT>
+__device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
+                                         double4_t (&acc)[NT]) {
+    const double* mid = static_cast<const double*>(S.st_mid) + i * S.Kp2 * S.Rt;   // uniform
+    const uint32_t moff = (uint32_t)(g * S.Rt + r) * 8u;
+    const int64_t ms = 4 * (int64_t)S.Rt;
+    const int64_t row = (L0 + r < a.NL) ? L0 + r : a.NL - 1;
+    const double* zr = static_cast<const double*>(S.core[2]) + row * S.rL;
+    const int klast = S.rL - 1;
+    const int nkb = S.Kp2 / 4;
+    auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
+    auto bf = [&](int kb) {
+        const int k = 4 * cl(kb) + g;
+        return zr[k < klast ? k : klast];
+    };
+    auto af = [&](double (&x)[NT], int kb) {
+        const double* mk = mid + cl(kb) * ms;
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) x[tb] = ld_off(mk + 16 * tb, moff);
+    };
+#pragma unroll
+    for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<double4_t>();
+    double x0[NT], x1[NT], y0[NT], y1[NT];
+    af(x0, 0);
+    af(x1, 1);
+    af(y0, 2);
+    af(y1, 3);
+    double bx0 = bf(0), bx1 = bf(1), by0 = bf(2), by1 = bf(3);
+    auto step = [&](const double (&x)[NT], double b) {
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) acc[tb] = mfma(x[tb], b, acc[tb]);
+    };
+    int kb = 0;
+    for (; kb + 3 < nkb; kb += 4) {
+        step(x0, bx0);
+        af(x0, kb + 4);
+        bx0 = bf(kb + 4);
+        __builtin_amdgcn_sched_barrier(0);
+        step(x1, bx1);
+        af(x1, kb + 5);
+        bx1 = bf(kb + 5);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y0, by0);
+        af(y0, kb + 6);
+        by0 = bf(kb + 6);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y1, by1);
+        af(y1, kb + 7);
+        by1 = bf(kb + 7);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kb < nkb) step(x0, bx0);
+    if (kb + 1 < nkb) step(x1, bx1);
+    if (kb + 2 < nkb) step(y0, by0);
+}
+
+// Last products of the three sets for the wave's tile and the five sums.
+template <int NKB>
+__device__ __forceinline__ void last_w(const TTArgs& a, const double* __restrict__ Tref, int64_t i, int64_t L0,
+                                       int r, int g, const double (&zf)[3][NKB], double (&sum)[5]) {
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    const double* b0 = static_cast<const double*>(a.set[0].st_last);
+    const double* b1 = static_cast<const double*>(a.set[1].st_last);
+    const double* b2 = static_cast<const double*>(a.set[2].st_last);
+    // lane byte offset of block cp: (g ncp + 16 cp + r) * 8
+    uint32_t off = (uint32_t)(g * a.ncp + r) * 8u;
+    const int64_t ks0 = 4 * (int64_t)a.ncp;
+    auto ld = [&](double (&f)[3], int64_t ks, int kb, uint32_t o) {
+        f[0] = ld_off(b0 + kb * ks, o);
+        f[1] = ld_off(b1 + kb * ks, o);
+        f[2] = ld_off(b2 + kb * ks, o);
+    };
+    // N: fragments of steps 0..3 of a block, R: steps 4 .. NKB-1 in turn
+    double N[4][3], R[4][3];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) ld(N[s], ks0, s, off);
+    for (int cp = 0; cp < n_cb; ++cp) {
+        // per-block copy of the K stride: the step offsets are formed here
+        // rather than all kept live across the loop
+        int64_t ks = ks0;
+        asm volatile("" : "+s"(ks));
+        const uint32_t offn = cp + 1 < n_cb ? off + 16u * 8u : off;
+        const int64_t col = (int64_t)cp * 16 + r;
+        double tv[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t L = L0 + g + 4 * v;
+            const bool ok = L < a.NL && col < a.n_last;
+            tv[v] = Tref[ok ? (L * a.n_mid + i) * a.n_last + col : 0];
+        }
+        double4_t acc[3];
+#pragma unroll
+        for (int q = 0; q < 3; ++q) acc[q] = zero_accv<double4_t>();
+#pragma unroll
+        for (int s = 0; s < NKB; ++s) {
+#pragma unroll
+            for (int q = 0; q < 3; ++q) acc[q] = mfma(zf[q][s], s < 4 ? N[s][q] : R[s % 4][q], acc[q]);
+            const int k = s + 4;
+            if (k < NKB) ld(R[k % 4], ks, k, off);
+            else ld(N[k - NKB], ks, k - NKB, offn);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // lane holds rows L0 + g + 4v of column col
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const bool ok = L0 + g + 4 * v < a.NL && col < a.n_last;
+            const double t = ok ? tv[v] : 0.0;
+            const double r0 = ok ? acc[0][v] : 0.0;
+            const double r1 = ok ? acc[1][v] : 0.0;
+            const double r2 = ok ? acc[2][v] : 0.0;
+            const double d0 = t - r0, d1 = t - r1, d2 = r1 - r2, d3 = t - r2;
+            sum[0] += d0 * d0;
+            sum[1] += d1 * d1;
+            sum[2] += d2 * d2;
+            sum[3] += d3 * d3;
+            sum[4] += t * t;
+        }
+        off = offn;
+    }
+}
+
+// ntiles = n_2 * ceil(n_1 / 16) wave tiles, tile = i * ceil(n_1 / 16) + L
+// block (the four waves of a workgroup, and consecutive workgroups of one
+// XCD, share i and so the middle core slice in L2).  The grid is a multiple
+// of 8; workgroup w writes part[s * gridDim.x + w] (sums as in k_tt_cert).
+template <int NKB>
+__global__ __launch_bounds__(256) void k_tt_cert_w(TTArgs a, const double* __restrict__ Tref,
+                                                   double* __restrict__ part, int64_t ntiles) {
+    constexpr int NT = (NKB + 3) / 4;
+    __shared__ double red[4][5];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nLb = (a.NL + 15) / 16;
+    double sum[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    const int64_t wl = xcd_tile(gridDim.x);
+    for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
+        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16;
+        double zf[3][NKB];
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            // per-set copy of the lane index: the set's addresses are formed
+            // here instead of being kept live across the tile loop
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            double4_t acc[NT];
+            middle_w<NT>(a, a.set[q], i, L0, ln & 15, ln >> 4, acc);
+#pragma unroll
+            for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (4 * tb + v < NKB) zf[q][4 * tb + v] = acc[tb][v];
+        }
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        last_w<NKB>(a, Tref, i, L0, ln & 15, ln >> 4, zf, sum);
+    }
+#pragma unroll
+    for (int s = 0; s < 5; ++s) {
+        const double w = wave_sum(sum[s]);
+        if (lane == 0) red[wave][s] = w;
+    }
+    __syncthreads();
+    if (threadIdx.x < 5)
+        part[threadIdx.x * (int64_t)gridDim.x + blockIdx.x] =
+            ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
+}
+
 template <typename T>
 static void launch_fused(int npb, int nlb, dim3 grid, size_t lds, hipStream_t st, const TTArgs& a) {
 #define LRC_TT(P, L) hipLaunchKernelGGL((k_tt_fused<T, P, L>), grid, dim3(256), lds, st, a)
@@ -729,6 +922,47 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         p.set[q].ldf += kp3 - p.set[q].Kp3;
         p.set[q].Kp3 = kp3;
     }
+    // staged cores (layouts at TTSet); ncp covers whole pairs of column blocks
+    auto stage_bytes = [&]() {
+        size_t b = 0;
+        const int64_t ncp = round_up(p.n_last, 32);
+        for (int q = 0; q < nsets; ++q)
+            b += (size_t)(round_up(p.n_mid * p.set[q].Rt * p.set[q].Kp2 * e, 256) +
+                          round_up(ncp * p.set[q].Kp3 * e, 256));
+        return b;
+    };
+    // The FP64 certificate for d = 3 runs by wave tiles (k_tt_cert_w) when
+    // the last product's K extent fits one of its register layouts: every
+    // set then takes that extent (NKB K steps) and the matching column blocks
+    // of the middle product.  LRC_TT_CERT_WAVE=0 selects the LDS tiles.
+    const char* wv = std::getenv("LRC_TT_CERT_WAVE");
+    if (nsets == 3 && d == 3 && prec == P64 && !(wv && wv[0] == '0')) {
+        static const int kNkb[] = {4, 8, 12, 16, 17};
+        int nkb = 0;
+        for (int c : kNkb)
+            if (4 * c >= kp3) {
+                nkb = c;
+                break;
+            }
+        if (nkb > 0) {
+            for (int q = 0; q < nsets; ++q) {
+                p.set[q].Kp3 = 4 * nkb;
+                p.set[q].ldf = p.set[q].Kp3 + 1;
+                p.set[q].Rt = 16 * ((nkb + 3) / 4);
+            }
+            p.cert_nkb = nkb;
+            p.BL = 16;
+            p.BI = 1;
+            p.P = 16;
+            p.lds_bytes = 0;
+            p.num_i_blocks = p.n_mid;
+            p.num_L_blocks = (p.NL + 15) / 16;
+            p.grid_L = 1;
+            p.cert_tiles = p.num_i_blocks * p.num_L_blocks;
+            p.stage_bytes = stage_bytes();
+            return 0;
+        }
+    }
     // at most 64 KB of LDS per workgroup (80 KB for the three-set
     // certificate kernel), so that at least two workgroups share a compute
     // unit
@@ -776,12 +1010,7 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     if (want > p.num_L_blocks) want = p.num_L_blocks;
     if (want > 65535) want = 65535;
     p.grid_L = (int)want;
-    // staged cores (layouts at TTSet); ncp covers whole pairs of column blocks
-    p.stage_bytes = 0;
-    const int64_t ncp = round_up(p.n_last, 32);
-    for (int q = 0; q < nsets; ++q)
-        p.stage_bytes += (size_t)(round_up(p.n_mid * p.set[q].Rt * p.set[q].Kp2 * e, 256) +
-                                  round_up(ncp * p.set[q].Kp3 * e, 256));
+    p.stage_bytes = stage_bytes();
     return 0;
 }
 
@@ -868,7 +1097,14 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     return hipGetLastError();
 }
 
-int64_t tt_cert_parts(const TTPlan& p) { return p.num_i_blocks * (int64_t)p.grid_L; }
+// Workgroups of the wave-tile certificate: four tiles each, at most 4096.
+static int64_t cert_w_grid(const TTPlan& p) {
+    return xcd_grid(std::min<int64_t>((p.cert_tiles + 3) / 4, 4096));
+}
+
+int64_t tt_cert_parts(const TTPlan& p) {
+    return p.cert_nkb ? cert_w_grid(p) : p.num_i_blocks * (int64_t)p.grid_L;
+}
 
 hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, const double* Tref, double* part,
                           Workspace& ws, hipStream_t stream) {
@@ -876,6 +1112,21 @@ hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, cons
     TTArgs a;
     hipError_t e = prepare_tt<double>(p, cores, nullptr, ws, stream, "cert_tt_fused_f64", a);
     if (e != hipSuccess) return e;
+    if (p.cert_nkb) {
+        const dim3 gw((unsigned)cert_w_grid(p));
+        KernelTimer tk("cert_tt_fused_f64", stream);
+#define LRC_TTW(K) hipLaunchKernelGGL((k_tt_cert_w<K>), gw, dim3(256), 0, stream, a, Tref, part, p.cert_tiles)
+        switch (p.cert_nkb) {
+        case 4: LRC_TTW(4); break;
+        case 8: LRC_TTW(8); break;
+        case 12: LRC_TTW(12); break;
+        case 16: LRC_TTW(16); break;
+        case 17: LRC_TTW(17); break;
+        default: return hipErrorInvalidValue;
+        }
+#undef LRC_TTW
+        return hipGetLastError();
+    }
     const dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
     const int64_t nparts = tt_cert_parts(p);
     const int npb = p.P / 16, nlb = (int)round_up(p.BL, 16) / 16;

@@ -191,10 +191,19 @@ def _tt_labels(lrc, T, base, aug, prec):
 @pytest.mark.parametrize("dims,rb,ra", [
     ((300, 200), (40,), (41,)),                 # d = 2: one middle and one last core
     ((12, 40, 30, 50), (10, 24, 20), (11, 25, 21)),
+    # d = 3 by wave tiles, one case per register layout of the last product
+    # (K extent 16, 32, 48, 64, 68), ragged n_1 and n_3
+    ((37, 23, 45), (12, 13), (13, 14)),
+    ((64, 7, 40), (20, 30), (21, 31)),
+    ((48, 5, 100), (40, 44), (41, 45)),
+    ((70, 3, 90), (62, 62), (63, 63)),
+    ((80, 6, 70), (64, 64), (65, 65)),
+    ((40, 8200, 5), (3, 4), (4, 5)),             # more tiles than resident waves
+    ((100, 5, 90), (80, 80), (81, 81)),          # d = 3 beyond the wave layouts: LDS tiles
 ])
 def test_tt_fused_certificate_shapes(lrc, dims, rb, ra):
     """The fused certificate kernel (one launch, no dense reconstructions)
-    on two-core and four-core trains."""
+    on two-, three- and four-core trains."""
     base = synth.random_tt_cores(dims, [1, *rb, 1], tag=21)
     aug = O.left_orthogonalize(synth.random_tt_cores(dims, [1, *ra, 1], tag=22))
     rng = np.random.default_rng(5)
