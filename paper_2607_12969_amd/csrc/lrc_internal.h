@@ -135,8 +135,9 @@ struct TTPlan {
     int chain_rmax;      // largest rank among levels 1..d-2 (chain buffers)
     size_t lds_bytes;
     size_t stage_bytes;  // staged (transposed, padded) FP16 operands
-    int cert_nkb;        // certificate by wave tiles: K steps of the last product (0: by LDS tiles)
-    int64_t cert_tiles;  // wave tiles of the certificate
+    int wave_nkb;        // FP64, d = 3 by wave tiles: K steps of the last product (0: by LDS tiles)
+    int wave_npb;        // 16-row blocks per wave tile
+    int64_t wave_tiles;  // wave tiles
 };
 
 // rank_sets[q] is the rank vector (d+1 entries) of core set q.  Returns 0,

@@ -809,6 +809,112 @@ __device__ __forceinline__ void last_w(const TTArgs& a, const double* __restrict
     }
 }
 
+// Last product of a reconstruction wave tile: NPB row blocks of 16 rows,
+// stored straight from the accumulators (lane (r, g), value v: row
+// L0 + 16 pb + g + 4 v of column 16 cp + r, so that each store instruction
+// writes 128-byte row segments).  The core fragments run D steps ahead in
+// the ring of last_w (N: steps 0 .. D-1 of a block, R: the later steps;
+// the last D steps of a block fetch the first D of the next).
+template <int NKB, int NPB, int D>
+__device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t L0, int r, int g,
+                                             const double (&zf)[NPB][NKB]) {
+    static_assert(D <= NKB, "ring deeper than a block");
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    const double* b0 = static_cast<const double*>(a.set[0].st_last);
+    double* out = static_cast<double*>(a.out);
+    uint32_t off = (uint32_t)(g * a.ncp + r) * 8u;
+    const int64_t ks0 = 4 * (int64_t)a.ncp;
+    double N[D], R[D];
+#pragma unroll
+    for (int s = 0; s < D; ++s) N[s] = ld_off(b0 + s * ks0, off);
+    for (int cp = 0; cp < n_cb; ++cp) {
+        int64_t ks = ks0;
+        asm volatile("" : "+s"(ks));
+        const uint32_t offn = cp + 1 < n_cb ? off + 16u * 8u : off;
+        double4_t acc[NPB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<double4_t>();
+#pragma unroll
+        for (int s = 0; s < NKB; ++s) {
+            const double f = s < D ? N[s] : R[s % D];
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(zf[pb][s], f, acc[pb]);
+            const int k = s + D;
+            if (k < NKB) R[k % D] = ld_off(b0 + k * ks, off);
+            else N[k - NKB] = ld_off(b0 + (k - NKB) * ks, offn);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const int64_t col = (int64_t)cp * 16 + r;
+        if (col < a.n_last) {
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int64_t L = L0 + 16 * pb + g + 4 * v;
+                    if (L < a.NL) out[(L * a.n_mid + i) * a.n_last + col] = acc[pb][v];
+                }
+        }
+        off = offn;
+    }
+}
+
+// FP64 reconstruction for d = 3 by wave tiles: a tile is 16 NPB rows of G_1
+// for one middle index i (tile = i * ceil(n_1 / (16 NPB)) + row block), the
+// interfaces Z_2 of its row blocks held in registers as the A fragments of
+// the last product (see the wave-tile certificate below).  The core ring is
+// 8 steps deep (4 for four row blocks, whose steps are twice as long).
+template <int NKB, int NPB>
+__global__ __launch_bounds__(256) void k_tt_wave(TTArgs a, int64_t ntiles) {
+    constexpr int NT = (NKB + 3) / 4;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
+    const int64_t wl = xcd_tile(gridDim.x);
+    for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
+        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16 * NPB;
+        double zf[NPB][NKB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            double4_t acc[NT];
+            middle_w<NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+#pragma unroll
+            for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (4 * tb + v < NKB) zf[pb][4 * tb + v] = acc[tb][v];
+        }
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        last_store_w<NKB, NPB, (NKB < (NPB == 4 ? 4 : 8) ? NKB : (NPB == 4 ? 4 : 8))>(a, i, L0, ln & 15, ln >> 4, zf);
+    }
+}
+
+static void launch_wave(int nkb, int npb, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
+#define LRC_TW(K, P) hipLaunchKernelGGL((k_tt_wave<K, P>), grid, dim3(256), 0, st, a, ntiles)
+#define LRC_TWK(K) \
+    do {                                 \
+        if (npb == 1) LRC_TW(K, 1);      \
+        else if (npb == 4) LRC_TW(K, 4); \
+        else LRC_TW(K, 2);               \
+    } while (0)
+    switch (nkb) {
+    case 4: LRC_TWK(4); break;
+    case 8: LRC_TWK(8); break;
+    case 12: LRC_TWK(12); break;
+    case 16: LRC_TWK(16); break;
+    default: LRC_TWK(17); break;
+    }
+#undef LRC_TWK
+#undef LRC_TW
+}
+
+// Workgroups of the wave-tile kernels: four tiles each, at most 4096.
+static int64_t wave_grid(const TTPlan& p) {
+    return xcd_grid(std::min<int64_t>((p.wave_tiles + 3) / 4, 4096));
+}
+
 // ntiles = n_2 * ceil(n_1 / 16) wave tiles, tile = i * ceil(n_1 / 16) + L
 // block (the four waves of a workgroup, and consecutive workgroups of one
 // XCD, share i and so the middle core slice in L2).  The grid is a multiple
@@ -931,12 +1037,14 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
                           round_up(ncp * p.set[q].Kp3 * e, 256));
         return b;
     };
-    // The FP64 certificate for d = 3 runs by wave tiles (k_tt_cert_w) when
-    // the last product's K extent fits one of its register layouts: every
-    // set then takes that extent (NKB K steps) and the matching column blocks
-    // of the middle product.  LRC_TT_CERT_WAVE=0 selects the LDS tiles.
-    const char* wv = std::getenv("LRC_TT_CERT_WAVE");
-    if (nsets == 3 && d == 3 && prec == P64 && !(wv && wv[0] == '0')) {
+    // FP64 with d = 3 runs by wave tiles (k_tt_cert_w for the certificate,
+    // k_tt_wave for the reconstruction) when the last product's K extent
+    // fits one of their register layouts: every set then takes that extent
+    // (NKB K steps) and the matching column blocks of the middle product.
+    // LRC_TT_WAVE=0 selects the LDS tiles; LRC_TT_WAVE_NPB (1, 2 or 4) sets
+    // the row blocks per reconstruction tile.
+    const char* wv = std::getenv("LRC_TT_WAVE");
+    if (d == 3 && prec == P64 && (nsets == 1 || nsets == 3) && !(wv && wv[0] == '0')) {
         static const int kNkb[] = {4, 8, 12, 16, 17};
         int nkb = 0;
         for (int c : kNkb)
@@ -950,15 +1058,21 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
                 p.set[q].ldf = p.set[q].Kp3 + 1;
                 p.set[q].Rt = 16 * ((nkb + 3) / 4);
             }
-            p.cert_nkb = nkb;
-            p.BL = 16;
+            int npb = 1;
+            if (nsets == 1) {
+                npb = tune_env("LRC_TT_WAVE_NPB", 2);
+                if (npb != 1 && npb != 2 && npb != 4) npb = 2;
+            }
+            p.wave_nkb = nkb;
+            p.wave_npb = npb;
+            p.BL = 16 * npb;
             p.BI = 1;
-            p.P = 16;
+            p.P = 16 * npb;
             p.lds_bytes = 0;
             p.num_i_blocks = p.n_mid;
-            p.num_L_blocks = (p.NL + 15) / 16;
+            p.num_L_blocks = (p.NL + p.BL - 1) / p.BL;
             p.grid_L = 1;
-            p.cert_tiles = p.num_i_blocks * p.num_L_blocks;
+            p.wave_tiles = p.num_i_blocks * p.num_L_blocks;
             p.stage_bytes = stage_bytes();
             return 0;
         }
@@ -1091,19 +1205,21 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     TTArgs a;
     hipError_t e = prepare_tt<T>(p, cores, out, ws, stream, label, a);
     if (e != hipSuccess) return e;
+    if constexpr (sizeof(T) == 8) {
+        if (p.wave_nkb) {
+            KernelTimer tk(label, stream);
+            launch_wave(p.wave_nkb, p.wave_npb, dim3((unsigned)wave_grid(p)), stream, a, p.wave_tiles);
+            return hipGetLastError();
+        }
+    }
     dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
     KernelTimer tk(label, stream);
     launch_fused<T>(p.P / 16, (int)round_up(p.BL, 16) / 16, grid, p.lds_bytes, stream, a);
     return hipGetLastError();
 }
 
-// Workgroups of the wave-tile certificate: four tiles each, at most 4096.
-static int64_t cert_w_grid(const TTPlan& p) {
-    return xcd_grid(std::min<int64_t>((p.cert_tiles + 3) / 4, 4096));
-}
-
 int64_t tt_cert_parts(const TTPlan& p) {
-    return p.cert_nkb ? cert_w_grid(p) : p.num_i_blocks * (int64_t)p.grid_L;
+    return p.wave_nkb ? wave_grid(p) : p.num_i_blocks * (int64_t)p.grid_L;
 }
 
 hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, const double* Tref, double* part,
@@ -1112,11 +1228,11 @@ hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, cons
     TTArgs a;
     hipError_t e = prepare_tt<double>(p, cores, nullptr, ws, stream, "cert_tt_fused_f64", a);
     if (e != hipSuccess) return e;
-    if (p.cert_nkb) {
-        const dim3 gw((unsigned)cert_w_grid(p));
+    if (p.wave_nkb) {
+        const dim3 gw((unsigned)wave_grid(p));
         KernelTimer tk("cert_tt_fused_f64", stream);
-#define LRC_TTW(K) hipLaunchKernelGGL((k_tt_cert_w<K>), gw, dim3(256), 0, stream, a, Tref, part, p.cert_tiles)
-        switch (p.cert_nkb) {
+#define LRC_TTW(K) hipLaunchKernelGGL((k_tt_cert_w<K>), gw, dim3(256), 0, stream, a, Tref, part, p.wave_tiles)
+        switch (p.wave_nkb) {
         case 4: LRC_TTW(4); break;
         case 8: LRC_TTW(8); break;
         case 12: LRC_TTW(12); break;
