@@ -679,8 +679,9 @@ __global__ __launch_bounds__(256) void k_tt_cert(TTArgs a, const double* __restr
 
 // Load at a uniform base plus a per-lane byte offset (one 32-bit register
 // per lane; the step offsets stay in scalar registers).
-__device__ __forceinline__ double ld_off(const double* base, uint32_t byte_off) {
-    return *reinterpret_cast<const double*>(reinterpret_cast<const char*>(base) + byte_off);
+template <typename T>
+__device__ __forceinline__ T ld_off(const T* base, uint32_t byte_off) {
+    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
 // Middle product of one set for the wave's tile: acc[tb] for the NT column
@@ -688,14 +689,15 @@ __device__ __forceinline__ double ld_off(const double* base, uint32_t byte_off) 
 // middle core (zero beyond the ranks), B fragments straight from the rows of
 // G_1 (row and K index clamped into the core: clamped rows are discarded
 // with the tile's rows past NL, clamped K entries meet zero A entries).
-template <int NT>
+template <typename T, int NT>
 __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
-                                         double4_t (&acc)[NT]) {
-    const double* mid = static_cast<const double*>(S.st_mid) + i * S.Kp2 * S.Rt;   // uniform
-    const uint32_t moff = (uint32_t)(g * S.Rt + r) * 8u;
+                                         typename PrecTraits<T>::accv (&acc)[NT]) {
+    using AccV = typename PrecTraits<T>::accv;
+    const T* mid = static_cast<const T*>(S.st_mid) + i * S.Kp2 * S.Rt;   // uniform
+    const uint32_t moff = (uint32_t)(g * S.Rt + r) * (uint32_t)sizeof(T);
     const int64_t ms = 4 * (int64_t)S.Rt;
     const int64_t row = (L0 + r < a.NL) ? L0 + r : a.NL - 1;
-    const double* zr = static_cast<const double*>(S.core[2]) + row * S.rL;
+    const T* zr = static_cast<const T*>(S.core[2]) + row * S.rL;
     const int klast = S.rL - 1;
     const int nkb = S.Kp2 / 4;
     auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
@@ -703,20 +705,20 @@ __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_
         const int k = 4 * cl(kb) + g;
         return zr[k < klast ? k : klast];
     };
-    auto af = [&](double (&x)[NT], int kb) {
-        const double* mk = mid + cl(kb) * ms;
+    auto af = [&](T (&x)[NT], int kb) {
+        const T* mk = mid + cl(kb) * ms;
 #pragma unroll
         for (int tb = 0; tb < NT; ++tb) x[tb] = ld_off(mk + 16 * tb, moff);
     };
 #pragma unroll
-    for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<double4_t>();
-    double x0[NT], x1[NT], y0[NT], y1[NT];
+    for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<AccV>();
+    T x0[NT], x1[NT], y0[NT], y1[NT];
     af(x0, 0);
     af(x1, 1);
     af(y0, 2);
     af(y1, 3);
-    double bx0 = bf(0), bx1 = bf(1), by0 = bf(2), by1 = bf(3);
-    auto step = [&](const double (&x)[NT], double b) {
+    T bx0 = bf(0), bx1 = bf(1), by0 = bf(2), by1 = bf(3);
+    auto step = [&](const T (&x)[NT], T b) {
 #pragma unroll
         for (int tb = 0; tb < NT; ++tb) acc[tb] = mfma(x[tb], b, acc[tb]);
     };
@@ -878,7 +880,7 @@ __global__ __launch_bounds__(256) void k_tt_wave(TTArgs a, int64_t ntiles) {
             int ln = lane;
             asm volatile("" : "+v"(ln));
             double4_t acc[NT];
-            middle_w<NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+            middle_w<double, NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
 #pragma unroll
             for (int tb = 0; tb < NT; ++tb)
 #pragma unroll
@@ -898,6 +900,138 @@ static void launch_wave(int nkb, int npb, dim3 grid, hipStream_t st, const TTArg
         if (npb == 1) LRC_TW(K, 1);      \
         else if (npb == 4) LRC_TW(K, 4); \
         else LRC_TW(K, 2);               \
+    } while (0)
+    switch (nkb) {
+    case 4: LRC_TWK(4); break;
+    case 8: LRC_TWK(8); break;
+    case 12: LRC_TWK(12); break;
+    case 16: LRC_TWK(16); break;
+    default: LRC_TWK(17); break;
+    }
+#undef LRC_TWK
+#undef LRC_TW
+}
+
+// FP32 accumulators of the transposed middle product hold, in lane (r, g),
+// value v, Z_2(L0 + r, 16 tb + 4 g + v): lane group g has the four K values
+// of step kb = 4 tb + g.  The A fragment of the FP32 last product wants
+// lane group g to hold K value g of each step 4 tb + v: a 4 x 4 transpose
+// between the four 16-lane groups and the four values, done as a swap of
+// the off-diagonal 2 x 2 blocks across the 32-lane halves followed by a
+// transpose inside each block across neighbouring 16-lane rows (the gfx950
+// lane swaps permlane32_swap and permlane16_swap).
+__device__ __forceinline__ void swap32(float& x, float& y) {
+    const auto p = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, y),
+                                                    false, false);
+    x = __builtin_bit_cast(float, (unsigned)p[0]);
+    y = __builtin_bit_cast(float, (unsigned)p[1]);
+}
+__device__ __forceinline__ void swap16(float& x, float& y) {
+    const auto p = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, y),
+                                                    false, false);
+    x = __builtin_bit_cast(float, (unsigned)p[0]);
+    y = __builtin_bit_cast(float, (unsigned)p[1]);
+}
+__device__ __forceinline__ void transpose_groups(float4_t& a) {
+    float v0 = a[0], v1 = a[1], v2 = a[2], v3 = a[3];
+    swap32(v0, v2);
+    swap32(v1, v3);
+    swap16(v0, v1);
+    swap16(v2, v3);
+    a = float4_t{v0, v1, v2, v3};
+}
+
+// FP32 last product of a reconstruction wave tile, computed transposed
+// (core fragment as A, so that lane (r, g), value v holds row L0 + 16 pb + r,
+// column 16 cp + 4 g + v: four consecutive columns, stored as one 16-byte
+// vector where the row allows it).  Core ring as in last_store_w.
+template <int NKB, int NPB, int D>
+__device__ __forceinline__ void last_store_w32(const TTArgs& a, int64_t i, int64_t L0, int r, int g,
+                                               const float (&zf)[NPB][NKB]) {
+    static_assert(D <= NKB, "ring deeper than a block");
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    const float* b0 = static_cast<const float*>(a.set[0].st_last);
+    float* out = static_cast<float*>(a.out);
+    uint32_t off = (uint32_t)(g * a.ncp + r) * 4u;
+    const int64_t ks0 = 4 * (int64_t)a.ncp;
+    float N[D], R[D];
+#pragma unroll
+    for (int s = 0; s < D; ++s) N[s] = ld_off(b0 + s * ks0, off);
+    for (int cp = 0; cp < n_cb; ++cp) {
+        int64_t ks = ks0;
+        asm volatile("" : "+s"(ks));
+        const uint32_t offn = cp + 1 < n_cb ? off + 16u * 4u : off;
+        float4_t acc[NPB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<float4_t>();
+#pragma unroll
+        for (int s = 0; s < NKB; ++s) {
+            const float f = s < D ? N[s] : R[s % D];
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f, zf[pb][s], acc[pb]);
+            const int k = s + D;
+            if (k < NKB) R[k % D] = ld_off(b0 + k * ks, off);
+            else N[k - NKB] = ld_off(b0 + (k - NKB) * ks, offn);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const int64_t c0 = (int64_t)cp * 16 + 4 * g;
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            const int64_t L = L0 + 16 * pb + r;
+            if (L >= a.NL) continue;
+            float* dst = out + (L * a.n_mid + i) * a.n_last + c0;
+            if (a.vec4 && c0 + 3 < a.n_last) {
+                *reinterpret_cast<float4_t*>(dst) = acc[pb];
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (c0 + v < a.n_last) dst[v] = acc[pb][v];
+            }
+        }
+        off = offn;
+    }
+}
+
+// FP32 reconstruction for d = 3 by wave tiles (as k_tt_wave, with the
+// accumulators of the middle product transposed into A-fragment order).
+template <int NKB, int NPB>
+__global__ __launch_bounds__(256) void k_tt_wave32(TTArgs a, int64_t ntiles) {
+    constexpr int NT = (NKB + 3) / 4;
+    constexpr int D = NKB < 8 ? NKB : 8;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
+    const int64_t wl = xcd_tile(gridDim.x);
+    for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
+        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16 * NPB;
+        float zf[NPB][NKB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            float4_t acc[NT];
+            middle_w<float, NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+#pragma unroll
+            for (int tb = 0; tb < NT; ++tb) {
+                transpose_groups(acc[tb]);
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (4 * tb + v < NKB) zf[pb][4 * tb + v] = acc[tb][v];
+            }
+        }
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        last_store_w32<NKB, NPB, D>(a, i, L0, ln & 15, ln >> 4, zf);
+    }
+}
+
+static void launch_wave32(int nkb, int npb, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
+#define LRC_TW(K, P) hipLaunchKernelGGL((k_tt_wave32<K, P>), grid, dim3(256), 0, st, a, ntiles)
+#define LRC_TWK(K) \
+    do {                                 \
+        if (npb == 1) LRC_TW(K, 1);      \
+        else if (npb == 2) LRC_TW(K, 2); \
+        else LRC_TW(K, 4);               \
     } while (0)
     switch (nkb) {
     case 4: LRC_TWK(4); break;
@@ -939,7 +1073,7 @@ __global__ __launch_bounds__(256) void k_tt_cert_w(TTArgs a, const double* __res
             int ln = lane;
             asm volatile("" : "+v"(ln));
             double4_t acc[NT];
-            middle_w<NT>(a, a.set[q], i, L0, ln & 15, ln >> 4, acc);
+            middle_w<double, NT>(a, a.set[q], i, L0, ln & 15, ln >> 4, acc);
 #pragma unroll
             for (int tb = 0; tb < NT; ++tb)
 #pragma unroll
@@ -1037,14 +1171,15 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
                           round_up(ncp * p.set[q].Kp3 * e, 256));
         return b;
     };
-    // FP64 with d = 3 runs by wave tiles (k_tt_cert_w for the certificate,
-    // k_tt_wave for the reconstruction) when the last product's K extent
-    // fits one of their register layouts: every set then takes that extent
-    // (NKB K steps) and the matching column blocks of the middle product.
-    // LRC_TT_WAVE=0 selects the LDS tiles; LRC_TT_WAVE_NPB (1, 2 or 4) sets
-    // the row blocks per reconstruction tile.
+    // FP64 and FP32 with d = 3 run by wave tiles (k_tt_cert_w for the
+    // certificate, k_tt_wave / k_tt_wave32 for the reconstruction) when the
+    // last product's K extent fits one of their register layouts: every set
+    // then takes that extent (NKB K steps) and the matching column blocks of
+    // the middle product.  LRC_TT_WAVE=0 selects the LDS tiles;
+    // LRC_TT_WAVE_NPB (1, 2 or 4) sets the row blocks per reconstruction tile.
     const char* wv = std::getenv("LRC_TT_WAVE");
-    if (d == 3 && prec == P64 && (nsets == 1 || nsets == 3) && !(wv && wv[0] == '0')) {
+    if (d == 3 && ((prec == P64 && (nsets == 1 || nsets == 3)) || (prec == P32 && nsets == 1)) &&
+        !(wv && wv[0] == '0')) {
         static const int kNkb[] = {4, 8, 12, 16, 17};
         int nkb = 0;
         for (int c : kNkb)
@@ -1060,8 +1195,9 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
             }
             int npb = 1;
             if (nsets == 1) {
-                npb = tune_env("LRC_TT_WAVE_NPB", 2);
-                if (npb != 1 && npb != 2 && npb != 4) npb = 2;
+                const int dflt = prec == P64 ? 2 : 4;
+                npb = tune_env("LRC_TT_WAVE_NPB", dflt);
+                if (npb != 1 && npb != 2 && npb != 4) npb = dflt;
             }
             p.wave_nkb = nkb;
             p.wave_npb = npb;
@@ -1205,10 +1341,13 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     TTArgs a;
     hipError_t e = prepare_tt<T>(p, cores, out, ws, stream, label, a);
     if (e != hipSuccess) return e;
-    if constexpr (sizeof(T) == 8) {
+    if constexpr (sizeof(T) >= 4) {
         if (p.wave_nkb) {
             KernelTimer tk(label, stream);
-            launch_wave(p.wave_nkb, p.wave_npb, dim3((unsigned)wave_grid(p)), stream, a, p.wave_tiles);
+            if constexpr (sizeof(T) == 8)
+                launch_wave(p.wave_nkb, p.wave_npb, dim3((unsigned)wave_grid(p)), stream, a, p.wave_tiles);
+            else
+                launch_wave32(p.wave_nkb, p.wave_npb, dim3((unsigned)wave_grid(p)), stream, a, p.wave_tiles);
             return hipGetLastError();
         }
     }
