@@ -41,6 +41,7 @@ struct TTSet {
     //   eight K values per lane (FP16):     mid [n_mid][Rt][Kp2], last [ncp][Kp3]
     const void* st_mid;
     const void* st_last;
+    const void* st_left;     // FP16 wave tiles (d = 3): G_1 rows at pitch Kp2, zero padded
     int zl_off, zf_off;      // byte offsets in LDS
 };
 
@@ -94,6 +95,19 @@ __global__ __launch_bounds__(256) void k_stage(const T* __restrict__ gmid, const
             }
             slast[j] = (t < rM && c < n_last) ? glast[t * n_last + c] : T(0);
         }
+    }
+}
+
+// Rows of G_1 [n_1][r_1] at pitch Kp2, zero padded (FP16 wave tiles load a
+// lane's eight K values of a row with one aligned 16-byte load).
+template <typename T>
+__global__ __launch_bounds__(256) void k_stage_rows(const T* __restrict__ g1, T* __restrict__ dst, int64_t n1,
+                                                    int r1, int Kp2) {
+    const int64_t tot = n1 * Kp2;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < tot; idx += (int64_t)gridDim.x * 256) {
+        const int64_t L = idx / Kp2;
+        const int s = (int)(idx % Kp2);
+        dst[idx] = s < r1 ? g1[L * r1 + s] : T(0);
     }
 }
 
@@ -684,31 +698,43 @@ __device__ __forceinline__ T ld_off(const T* base, uint32_t byte_off) {
     return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
-// Middle product of one set for the wave's tile: acc[tb] for the NT column
-// blocks of Z_2, over Kp2 / 4 K steps.  A fragments come from the staged
-// middle core (zero beyond the ranks), B fragments straight from the rows of
-// G_1 (row and K index clamped into the core: clamped rows are discarded
-// with the tile's rows past NL, clamped K entries meet zero A entries).
+// Middle product of one set for the wave's tile (FP64 or FP32, one K value
+// per lane): acc[tb] for the NT column blocks of Z_2, over ceil(r_1 / 4) K
+// steps.  A fragments come straight from G_2 [r_1][n_2][r_2] (lane (r, g) of
+// step kb reads G_2(4 kb + g, i, 16 tb + r): sixteen consecutive entries per
+// lane group), B fragments from the rows of G_1.  Indices past the ranks
+// are clamped into the cores, so the loads are unconditional; the A values
+// there are replaced by zero right before their product (the Z_2 columns
+// past r_2 are then exactly zero), the clamped rows of G_1 belong to
+// discarded rows of the tile.
 template <typename T, int NT>
 __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
                                          typename PrecTraits<T>::accv (&acc)[NT]) {
     using AccV = typename PrecTraits<T>::accv;
-    const T* mid = static_cast<const T*>(S.st_mid) + i * S.Kp2 * S.Rt;   // uniform
-    const uint32_t moff = (uint32_t)(g * S.Rt + r) * (uint32_t)sizeof(T);
-    const int64_t ms = 4 * (int64_t)S.Rt;
+    const T* g2 = static_cast<const T*>(S.core[0]) + i * S.rM;   // uniform
+    const uint32_t ld2 = (uint32_t)(a.n_mid * S.rM);            // stride of the first index of G_2
     const int64_t row = (L0 + r < a.NL) ? L0 + r : a.NL - 1;
     const T* zr = static_cast<const T*>(S.core[2]) + row * S.rL;
-    const int klast = S.rL - 1;
-    const int nkb = S.Kp2 / 4;
+    const int klast = S.rL - 1, tlast = S.rM - 1;
+    const int nkb = (S.rL + 3) / 4;
+    uint32_t tcol[NT];   // clamped column offsets of the blocks
+    unsigned tok = 0;    // bit tb: column 16 tb + r lies inside the rank
+#pragma unroll
+    for (int tb = 0; tb < NT; ++tb) {
+        const int t = 16 * tb + r;
+        tcol[tb] = (uint32_t)(t < tlast ? t : tlast);
+        tok |= (t <= tlast ? 1u : 0u) << tb;
+    }
     auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
     auto bf = [&](int kb) {
         const int k = 4 * cl(kb) + g;
         return zr[k < klast ? k : klast];
     };
     auto af = [&](T (&x)[NT], int kb) {
-        const T* mk = mid + cl(kb) * ms;
+        const int sk = 4 * cl(kb) + g;
+        const uint32_t ro = (uint32_t)(sk < klast ? sk : klast) * ld2;
 #pragma unroll
-        for (int tb = 0; tb < NT; ++tb) x[tb] = ld_off(mk + 16 * tb, moff);
+        for (int tb = 0; tb < NT; ++tb) x[tb] = ld_off(g2, (ro + tcol[tb]) * (uint32_t)sizeof(T));
     };
 #pragma unroll
     for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<AccV>();
@@ -718,60 +744,80 @@ __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_
     af(y0, 2);
     af(y1, 3);
     T bx0 = bf(0), bx1 = bf(1), by0 = bf(2), by1 = bf(3);
-    auto step = [&](const T (&x)[NT], T b) {
+    auto step = [&](const T (&x)[NT], T b, int kb) {
+        const bool sok = 4 * kb + g <= klast;
 #pragma unroll
-        for (int tb = 0; tb < NT; ++tb) acc[tb] = mfma(x[tb], b, acc[tb]);
+        for (int tb = 0; tb < NT; ++tb) {
+            const T xa = (sok && ((tok >> tb) & 1u)) ? x[tb] : T(0);
+            acc[tb] = mfma(xa, b, acc[tb]);
+        }
     };
     int kb = 0;
     for (; kb + 3 < nkb; kb += 4) {
-        step(x0, bx0);
+        step(x0, bx0, kb);
         af(x0, kb + 4);
         bx0 = bf(kb + 4);
         __builtin_amdgcn_sched_barrier(0);
-        step(x1, bx1);
+        step(x1, bx1, kb + 1);
         af(x1, kb + 5);
         bx1 = bf(kb + 5);
         __builtin_amdgcn_sched_barrier(0);
-        step(y0, by0);
+        step(y0, by0, kb + 2);
         af(y0, kb + 6);
         by0 = bf(kb + 6);
         __builtin_amdgcn_sched_barrier(0);
-        step(y1, by1);
+        step(y1, by1, kb + 3);
         af(y1, kb + 7);
         by1 = bf(kb + 7);
         __builtin_amdgcn_sched_barrier(0);
     }
-    if (kb < nkb) step(x0, bx0);
-    if (kb + 1 < nkb) step(x1, bx1);
-    if (kb + 2 < nkb) step(y0, by0);
+    if (kb < nkb) step(x0, bx0, kb);
+    if (kb + 1 < nkb) step(x1, bx1, kb + 1);
+    if (kb + 2 < nkb) step(y0, by0, kb + 2);
+}
+
+// Byte offset of the last core's entry G_3(t, c) (row t clamped to the
+// rank: the matching A values, the Z_2 columns past the rank, are zero; c is
+// clamped by the caller, its outputs are discarded).
+template <typename T>
+__device__ __forceinline__ uint32_t last_off(int t, int tlast, uint32_t nl, uint32_t c) {
+    return ((uint32_t)(t < tlast ? t : tlast) * nl + c) * (uint32_t)sizeof(T);
 }
 
 // Last products of the three sets for the wave's tile and the five sums.
+// The fragments of G_3 [r_2][n_3] (lane (r, g) of step kb, block cp:
+// G_3(4 kb + g, 16 cp + r)) run four steps ahead: N holds steps 0..3 of a
+// block, R the later steps in turn, and the last four steps of a block
+// fetch the first four of the next.
 template <int NKB>
 __device__ __forceinline__ void last_w(const TTArgs& a, const double* __restrict__ Tref, int64_t i, int64_t L0,
                                        int r, int g, const double (&zf)[3][NKB], double (&sum)[5]) {
     const int n_cb = (int)((a.n_last + 15) / 16);
-    const double* b0 = static_cast<const double*>(a.set[0].st_last);
-    const double* b1 = static_cast<const double*>(a.set[1].st_last);
-    const double* b2 = static_cast<const double*>(a.set[2].st_last);
-    // lane byte offset of block cp: (g ncp + 16 cp + r) * 8
-    uint32_t off = (uint32_t)(g * a.ncp + r) * 8u;
-    const int64_t ks0 = 4 * (int64_t)a.ncp;
-    auto ld = [&](double (&f)[3], int64_t ks, int kb, uint32_t o) {
-        f[0] = ld_off(b0 + kb * ks, o);
-        f[1] = ld_off(b1 + kb * ks, o);
-        f[2] = ld_off(b2 + kb * ks, o);
+    const double* b0 = static_cast<const double*>(a.set[0].core[1]);
+    const double* b1 = static_cast<const double*>(a.set[1].core[1]);
+    const double* b2 = static_cast<const double*>(a.set[2].core[1]);
+    const int tl0 = a.set[0].rM - 1, tl1 = a.set[1].rM - 1, tl2 = a.set[2].rM - 1;
+    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
+    auto colc = [&](int cp) {
+        const uint32_t c = (uint32_t)(16 * cp + r);
+        return c < clast ? c : clast;
     };
-    // N: fragments of steps 0..3 of a block, R: steps 4 .. NKB-1 in turn
+    auto ld = [&](double (&f)[3], int gg, int kb, uint32_t c) {
+        const int t = 4 * kb + gg;
+        f[0] = ld_off(b0, last_off<double>(t, tl0, nl, c));
+        f[1] = ld_off(b1, last_off<double>(t, tl1, nl, c));
+        f[2] = ld_off(b2, last_off<double>(t, tl2, nl, c));
+    };
     double N[4][3], R[4][3];
+    uint32_t c = colc(0);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) ld(N[s], ks0, s, off);
+    for (int s = 0; s < 4; ++s) ld(N[s], g, s, c);
     for (int cp = 0; cp < n_cb; ++cp) {
-        // per-block copy of the K stride: the step offsets are formed here
+        // per-block copy of the lane group: the step offsets are formed here
         // rather than all kept live across the loop
-        int64_t ks = ks0;
-        asm volatile("" : "+s"(ks));
-        const uint32_t offn = cp + 1 < n_cb ? off + 16u * 8u : off;
+        int gg = g;
+        asm volatile("" : "+v"(gg));
+        const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
         const int64_t col = (int64_t)cp * 16 + r;
         double tv[4];
 #pragma unroll
@@ -788,8 +834,8 @@ __device__ __forceinline__ void last_w(const TTArgs& a, const double* __restrict
 #pragma unroll
             for (int q = 0; q < 3; ++q) acc[q] = mfma(zf[q][s], s < 4 ? N[s][q] : R[s % 4][q], acc[q]);
             const int k = s + 4;
-            if (k < NKB) ld(R[k % 4], ks, k, off);
-            else ld(N[k - NKB], ks, k - NKB, offn);
+            if (k < NKB) ld(R[k % 4], gg, k, c);
+            else ld(N[k - NKB], gg, k - NKB, cn);
             __builtin_amdgcn_sched_barrier(0);
         }
         // lane holds rows L0 + g + 4v of column col
@@ -807,7 +853,7 @@ __device__ __forceinline__ void last_w(const TTArgs& a, const double* __restrict
             sum[3] += d3 * d3;
             sum[4] += t * t;
         }
-        off = offn;
+        c = cn;
     }
 }
 
@@ -822,17 +868,22 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
                                              const double (&zf)[NPB][NKB]) {
     static_assert(D <= NKB, "ring deeper than a block");
     const int n_cb = (int)((a.n_last + 15) / 16);
-    const double* b0 = static_cast<const double*>(a.set[0].st_last);
+    const double* b0 = static_cast<const double*>(a.set[0].core[1]);
+    const int tl = a.set[0].rM - 1;
     double* out = static_cast<double*>(a.out);
-    uint32_t off = (uint32_t)(g * a.ncp + r) * 8u;
-    const int64_t ks0 = 4 * (int64_t)a.ncp;
+    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
+    auto colc = [&](int cp) {
+        const uint32_t c = (uint32_t)(16 * cp + r);
+        return c < clast ? c : clast;
+    };
     double N[D], R[D];
+    uint32_t c = colc(0);
 #pragma unroll
-    for (int s = 0; s < D; ++s) N[s] = ld_off(b0 + s * ks0, off);
+    for (int s = 0; s < D; ++s) N[s] = ld_off(b0, last_off<double>(4 * s + g, tl, nl, c));
     for (int cp = 0; cp < n_cb; ++cp) {
-        int64_t ks = ks0;
-        asm volatile("" : "+s"(ks));
-        const uint32_t offn = cp + 1 < n_cb ? off + 16u * 8u : off;
+        int gg = g;
+        asm volatile("" : "+v"(gg));
+        const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
         double4_t acc[NPB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<double4_t>();
@@ -842,8 +893,8 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
 #pragma unroll
             for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(zf[pb][s], f, acc[pb]);
             const int k = s + D;
-            if (k < NKB) R[k % D] = ld_off(b0 + k * ks, off);
-            else N[k - NKB] = ld_off(b0 + (k - NKB) * ks, offn);
+            if (k < NKB) R[k % D] = ld_off(b0, last_off<double>(4 * k + gg, tl, nl, c));
+            else N[k - NKB] = ld_off(b0, last_off<double>(4 * (k - NKB) + gg, tl, nl, cn));
             __builtin_amdgcn_sched_barrier(0);
         }
         const int64_t col = (int64_t)cp * 16 + r;
@@ -856,7 +907,7 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
                     if (L < a.NL) out[(L * a.n_mid + i) * a.n_last + col] = acc[pb][v];
                 }
         }
-        off = offn;
+        c = cn;
     }
 }
 
@@ -950,17 +1001,22 @@ __device__ __forceinline__ void last_store_w32(const TTArgs& a, int64_t i, int64
                                                const float (&zf)[NPB][NKB]) {
     static_assert(D <= NKB, "ring deeper than a block");
     const int n_cb = (int)((a.n_last + 15) / 16);
-    const float* b0 = static_cast<const float*>(a.set[0].st_last);
+    const float* b0 = static_cast<const float*>(a.set[0].core[1]);
+    const int tl = a.set[0].rM - 1;
     float* out = static_cast<float*>(a.out);
-    uint32_t off = (uint32_t)(g * a.ncp + r) * 4u;
-    const int64_t ks0 = 4 * (int64_t)a.ncp;
+    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
+    auto colc = [&](int cp) {
+        const uint32_t c = (uint32_t)(16 * cp + r);
+        return c < clast ? c : clast;
+    };
     float N[D], R[D];
+    uint32_t c = colc(0);
 #pragma unroll
-    for (int s = 0; s < D; ++s) N[s] = ld_off(b0 + s * ks0, off);
+    for (int s = 0; s < D; ++s) N[s] = ld_off(b0, last_off<float>(4 * s + g, tl, nl, c));
     for (int cp = 0; cp < n_cb; ++cp) {
-        int64_t ks = ks0;
-        asm volatile("" : "+s"(ks));
-        const uint32_t offn = cp + 1 < n_cb ? off + 16u * 4u : off;
+        int gg = g;
+        asm volatile("" : "+v"(gg));
+        const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
         float4_t acc[NPB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<float4_t>();
@@ -970,8 +1026,8 @@ __device__ __forceinline__ void last_store_w32(const TTArgs& a, int64_t i, int64
 #pragma unroll
             for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f, zf[pb][s], acc[pb]);
             const int k = s + D;
-            if (k < NKB) R[k % D] = ld_off(b0 + k * ks, off);
-            else N[k - NKB] = ld_off(b0 + (k - NKB) * ks, offn);
+            if (k < NKB) R[k % D] = ld_off(b0, last_off<float>(4 * k + gg, tl, nl, c));
+            else N[k - NKB] = ld_off(b0, last_off<float>(4 * (k - NKB) + gg, tl, nl, cn));
             __builtin_amdgcn_sched_barrier(0);
         }
         const int64_t c0 = (int64_t)cp * 16 + 4 * g;
@@ -988,7 +1044,7 @@ __device__ __forceinline__ void last_store_w32(const TTArgs& a, int64_t i, int64
                     if (c0 + v < a.n_last) dst[v] = acc[pb][v];
             }
         }
-        off = offn;
+        c = cn;
     }
 }
 
@@ -1039,6 +1095,174 @@ static void launch_wave32(int nkb, int npb, dim3 grid, hipStream_t st, const TTA
     case 12: LRC_TWK(12); break;
     case 16: LRC_TWK(16); break;
     default: LRC_TWK(17); break;
+    }
+#undef LRC_TWK
+#undef LRC_TW
+}
+
+// FP16 wave tiles: K steps of 32, lane (r, g) supplying K values
+// 8 g .. 8 g + 7 of row r (A) or column r (B) in one 16-byte fragment.
+// Middle product (transposed, FP32 accumulation): A from the staged middle
+// core [n_2][Rt][Kp2], B from the staged rows of G_1 [n_1][Kp2]; the
+// accumulator of column block tb holds, in lane (r, g), value v,
+// Z_2(L0 + r, 16 tb + 4 g + v).  Chains are two or three steps long, so the
+// fragments of two steps are fetched at once.
+template <int NT>
+__device__ __forceinline__ void middle_w16(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
+                                           float4_t (&acc)[NT]) {
+    const half_t* mid = static_cast<const half_t*>(S.st_mid) + i * S.Rt * S.Kp2;   // uniform
+    const uint32_t moff = (uint32_t)(r * S.Kp2 + 8 * g) * 2u;
+    const int64_t tstep = 16 * (int64_t)S.Kp2;   // next column block
+    const int64_t row = (L0 + r < a.NL) ? L0 + r : a.NL - 1;
+    const half_t* zr = static_cast<const half_t*>(S.st_left) + row * S.Kp2 + 8 * g;
+    const int nkb = S.Kp2 / 32;
+    auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
+    auto af = [&](half8_t (&x)[NT], int kb) {
+        const half_t* mk = mid + cl(kb) * 32;
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) x[tb] = ld_off(reinterpret_cast<const half8_t*>(mk + tb * tstep), moff);
+    };
+    auto bf = [&](int kb) { return *reinterpret_cast<const half8_t*>(zr + cl(kb) * 32); };
+#pragma unroll
+    for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<float4_t>();
+    half8_t x0[NT], x1[NT];
+    af(x0, 0);
+    af(x1, 1);
+    half8_t b0 = bf(0), b1 = bf(1);
+    auto step = [&](const half8_t (&x)[NT], half8_t b) {
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) acc[tb] = mfma(x[tb], b, acc[tb]);
+    };
+    int kb = 0;
+    for (; kb + 1 < nkb; kb += 2) {
+        step(x0, b0);
+        af(x0, kb + 2);
+        b0 = bf(kb + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        step(x1, b1);
+        af(x1, kb + 3);
+        b1 = bf(kb + 3);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kb < nkb) step(x0, b0);
+}
+
+// Round the FP32 accumulators of column blocks 2 kb and 2 kb + 1 to FP16 and
+// regroup them into the A fragment of K step kb of the last product: lane
+// group g needs Z_2(L0 + r, 32 kb + 8 g .. 8 g + 7), held as four values by
+// each of lane groups 2 (g mod 2) and 2 (g mod 2) + 1 of block 2 kb + g / 2.
+// With the values packed in pairs, a swap across the 32-lane halves and one
+// across neighbouring 16-lane rows bring them into place.
+__device__ __forceinline__ unsigned pack_h2(float lo, float hi) {
+    typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(unsigned, h2_t{(half_t)lo, (half_t)hi});
+}
+__device__ __forceinline__ void swap32u(unsigned& x, unsigned& y) {
+    const auto p = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+    x = p[0];
+    y = p[1];
+}
+__device__ __forceinline__ void swap16u(unsigned& x, unsigned& y) {
+    const auto p = __builtin_amdgcn_permlane16_swap(x, y, false, false);
+    x = p[0];
+    y = p[1];
+}
+__device__ __forceinline__ half8_t regroup16(const float4_t& X, const float4_t& Y) {
+    unsigned xa = pack_h2(X[0], X[1]), xb = pack_h2(X[2], X[3]);
+    unsigned ya = pack_h2(Y[0], Y[1]), yb = pack_h2(Y[2], Y[3]);
+    swap32u(xa, ya);
+    swap32u(xb, yb);
+    swap16u(xa, ya);
+    swap16u(xb, yb);
+    typedef unsigned u4_t __attribute__((ext_vector_type(4)));
+    return __builtin_bit_cast(half8_t, u4_t{xa, xb, ya, yb});
+}
+
+// FP16 last product of a reconstruction wave tile, computed transposed
+// (core fragment as A): lane (r, g), value v holds row L0 + 16 pb + r,
+// column 16 cp + 4 g + v (four consecutive columns, one 8-byte store where
+// the row allows it).  Each core fragment is refetched for the next column
+// block right after its use.
+template <int NKB, int NPB>
+__device__ __forceinline__ void last_store_w16(const TTArgs& a, int64_t i, int64_t L0, int r, int g,
+                                               const half8_t (&zf)[NPB][NKB]) {
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    const int Kp3 = a.set[0].Kp3;
+    const half8_t* b0 = static_cast<const half8_t*>(a.set[0].st_last);   // [ncp][Kp3], 16-byte units
+    half_t* out = static_cast<half_t*>(a.out);
+    uint32_t off = (uint32_t)(r * Kp3 + 8 * g) * 2u;
+    const uint32_t cstep = 16u * (uint32_t)Kp3 * 2u;
+    half8_t N[NKB];
+#pragma unroll
+    for (int s = 0; s < NKB; ++s) N[s] = ld_off(b0 + 4 * s, off);
+    for (int cp = 0; cp < n_cb; ++cp) {
+        const uint32_t offn = cp + 1 < n_cb ? off + cstep : off;
+        float4_t acc[NPB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<float4_t>();
+#pragma unroll
+        for (int s = 0; s < NKB; ++s) {
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(N[s], zf[pb][s], acc[pb]);
+            N[s] = ld_off(b0 + 4 * s, offn);
+        }
+        const int64_t c0 = (int64_t)cp * 16 + 4 * g;
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            const int64_t L = L0 + 16 * pb + r;
+            if (L >= a.NL) continue;
+            half_t* dst = out + (L * a.n_mid + i) * a.n_last + c0;
+            if (a.vec4 && c0 + 3 < a.n_last) {
+                typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+                *reinterpret_cast<h4_t*>(dst) = h4_t{(half_t)acc[pb][0], (half_t)acc[pb][1], (half_t)acc[pb][2],
+                                                     (half_t)acc[pb][3]};
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (c0 + v < a.n_last) dst[v] = (half_t)acc[pb][v];
+            }
+        }
+        off = offn;
+    }
+}
+
+template <int NKB, int NPB>
+__global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
+    constexpr int NT = 2 * NKB;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
+    const int64_t wl = xcd_tile(gridDim.x);
+    for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
+        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16 * NPB;
+        half8_t zf[NPB][NKB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            float4_t acc[NT];
+            middle_w16<NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) zf[pb][kb] = regroup16(acc[2 * kb], acc[2 * kb + 1]);
+        }
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        last_store_w16<NKB, NPB>(a, i, L0, ln & 15, ln >> 4, zf);
+    }
+}
+
+static void launch_wave16(int nkb, int npb, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
+#define LRC_TW(K, P) hipLaunchKernelGGL((k_tt_wave16<K, P>), grid, dim3(256), 0, st, a, ntiles)
+#define LRC_TWK(K) \
+    do {                                 \
+        if (npb == 1) LRC_TW(K, 1);      \
+        else if (npb == 2) LRC_TW(K, 2); \
+        else LRC_TW(K, 4);               \
+    } while (0)
+    switch (nkb) {
+    case 1: LRC_TWK(1); break;
+    case 2: LRC_TWK(2); break;
+    default: LRC_TWK(3); break;
     }
 #undef LRC_TWK
 #undef LRC_TW
@@ -1171,27 +1395,46 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
                           round_up(ncp * p.set[q].Kp3 * e, 256));
         return b;
     };
-    // FP64 and FP32 with d = 3 run by wave tiles (k_tt_cert_w for the
-    // certificate, k_tt_wave / k_tt_wave32 for the reconstruction) when the
-    // last product's K extent fits one of their register layouts: every set
-    // then takes that extent (NKB K steps) and the matching column blocks of
-    // the middle product.  LRC_TT_WAVE=0 selects the LDS tiles;
-    // LRC_TT_WAVE_NPB (1, 2 or 4) sets the row blocks per reconstruction tile.
+    // With d = 3 the kernels run by wave tiles (k_tt_cert_w for the FP64
+    // certificate, k_tt_wave / k_tt_wave32 / k_tt_wave16 for the
+    // reconstruction) when the last product's K extent fits one of their
+    // register layouts: NKB K steps of 4 (FP64, FP32: Kp3 = 4 NKB <= 68) or of
+    // 32 (FP16: Kp3 = 32 NKB <= 96).  Every set then takes that extent and
+    // the matching column blocks of the middle product.  LRC_TT_WAVE=0
+    // selects the LDS tiles; LRC_TT_WAVE_NPB (1, 2 or 4) sets the row blocks
+    // per reconstruction tile.
     const char* wv = std::getenv("LRC_TT_WAVE");
-    if (d == 3 && ((prec == P64 && (nsets == 1 || nsets == 3)) || (prec == P32 && nsets == 1)) &&
-        !(wv && wv[0] == '0')) {
-        static const int kNkb[] = {4, 8, 12, 16, 17};
+    bool wave_ok = d == 3 && !(wv && wv[0] == '0') &&
+                   ((prec == P64 && (nsets == 1 || nsets == 3)) || (prec != P64 && nsets == 1));
+    // FP64 / FP32 wave tiles read G_2 and G_3 in place with 32-bit byte offsets
+    for (int q = 0; q < nsets && wave_ok; ++q) {
+        const TTPlanSet& ps = p.set[q];
+        wave_ok = (double)ps.rL * p.n_mid * ps.rM * e < 4294967296.0 && (double)ps.rM * p.n_last * e < 4294967296.0;
+    }
+    if (wave_ok) {
         int nkb = 0;
-        for (int c : kNkb)
-            if (4 * c >= kp3) {
-                nkb = c;
-                break;
-            }
+        if (prec == P16) {
+            if (kp3 <= 96) nkb = kp3 / 32;
+        } else {
+            static const int kNkb[] = {4, 8, 12, 16, 17};
+            for (int c : kNkb)
+                if (4 * c >= kp3) {
+                    nkb = c;
+                    break;
+                }
+        }
         if (nkb > 0) {
             for (int q = 0; q < nsets; ++q) {
-                p.set[q].Kp3 = 4 * nkb;
-                p.set[q].ldf = p.set[q].Kp3 + 1;
-                p.set[q].Rt = 16 * ((nkb + 3) / 4);
+                TTPlanSet& ps = p.set[q];
+                if (prec == P16) {
+                    ps.Kp3 = 32 * nkb;
+                    ps.ldf = ps.Kp3 + 8;
+                    ps.Rt = 32 * nkb;
+                } else {
+                    ps.Kp3 = 4 * nkb;
+                    ps.ldf = ps.Kp3 + 1;
+                    ps.Rt = 16 * ((nkb + 3) / 4);
+                }
             }
             int npb = 1;
             if (nsets == 1) {
@@ -1209,7 +1452,8 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
             p.num_L_blocks = (p.NL + p.BL - 1) / p.BL;
             p.grid_L = 1;
             p.wave_tiles = p.num_i_blocks * p.num_L_blocks;
-            p.stage_bytes = stage_bytes();
+            // FP16 stages its cores (K-contiguous fragments); FP64 / FP32 read them in place
+            p.stage_bytes = prec == P16 ? stage_bytes() + (size_t)round_up(p.NL * p.set[0].Kp2 * e, 256) : 0;
             return 0;
         }
     }
@@ -1313,6 +1557,8 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
         S.zl_off = 0;
         S.zf_off = off;
         off += (int)round_up((int64_t)p.P * ps.ldf * (int64_t)sizeof(T), 32);
+        S.st_mid = S.st_last = S.st_left = nullptr;
+        if (p.wave_nkb && sizeof(T) >= 4) continue;   // the wave tiles read the cores in place
         {
             T* smid = static_cast<T*>(ws.take((size_t)p.n_mid * ps.Rt * ps.Kp2 * sizeof(T)));
             T* slast = static_cast<T*>(ws.take((size_t)a.ncp * ps.Kp3 * sizeof(T)));
@@ -1329,6 +1575,18 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
             S.st_mid = smid;
             S.st_last = slast;
         }
+        if (sizeof(T) == 2 && p.wave_nkb) {
+            T* sl = static_cast<T*>(ws.take((size_t)p.NL * ps.Kp2 * sizeof(T)));
+            if (ws.overrun || !sl) return hipErrorOutOfMemory;
+            int64_t gs = (p.NL * ps.Kp2 + 255) / 256;
+            if (gs > 4096) gs = 4096;
+            KernelTimer ts(stage_label, stream);
+            hipLaunchKernelGGL(k_stage_rows<T>, dim3((unsigned)gs), dim3(256), 0, stream, (const T*)cores[q][0], sl,
+                               p.NL, ps.rL, ps.Kp2);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            S.st_left = sl;
+        }
     }
     a.cb_off = off;
     return hipSuccess;
@@ -1341,15 +1599,13 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
     TTArgs a;
     hipError_t e = prepare_tt<T>(p, cores, out, ws, stream, label, a);
     if (e != hipSuccess) return e;
-    if constexpr (sizeof(T) >= 4) {
-        if (p.wave_nkb) {
-            KernelTimer tk(label, stream);
-            if constexpr (sizeof(T) == 8)
-                launch_wave(p.wave_nkb, p.wave_npb, dim3((unsigned)wave_grid(p)), stream, a, p.wave_tiles);
-            else
-                launch_wave32(p.wave_nkb, p.wave_npb, dim3((unsigned)wave_grid(p)), stream, a, p.wave_tiles);
-            return hipGetLastError();
-        }
+    if (p.wave_nkb) {
+        KernelTimer tk(label, stream);
+        const dim3 gw((unsigned)wave_grid(p));
+        if constexpr (sizeof(T) == 8) launch_wave(p.wave_nkb, p.wave_npb, gw, stream, a, p.wave_tiles);
+        else if constexpr (sizeof(T) == 4) launch_wave32(p.wave_nkb, p.wave_npb, gw, stream, a, p.wave_tiles);
+        else launch_wave16(p.wave_nkb, p.wave_npb, gw, stream, a, p.wave_tiles);
+        return hipGetLastError();
     }
     dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
     KernelTimer tk(label, stream);
