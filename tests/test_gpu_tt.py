@@ -127,7 +127,7 @@ def test_hyperspectral_shape(lrc, ranks_fp64, ranks_low):
         _check(lrc, aug, prec, "512x512x224 compensated")
 
 
-@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+@pytest.mark.parametrize("prec", ["fp64", "fp32", "fp16"])
 @pytest.mark.parametrize("layout", ["npb1", "npb2", "npb4", "lds"])
 @pytest.mark.parametrize("dims,ranks", [
     ((37, 23, 45), (1, 12, 13, 1)),     # last-product K extent 16
@@ -139,10 +139,11 @@ def test_hyperspectral_shape(lrc, ranks_fp64, ranks_low):
     ((9, 9000, 3), (1, 3, 3, 1)),       # more tiles than resident waves
 ])
 def test_three_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
-    """FP64 and FP32 three-core trains through every tile layout: wave
-    tiles of 16, 32 and 64 rows (each register layout of the last product)
-    and the LDS tiles, with ragged n_1 and n_3 (n_3 = 45: the FP32 rows are
-    not 16-byte aligned, so the vector stores fall back to scalar ones)."""
+    """Three-core trains in every precision through every tile layout:
+    wave tiles of 16, 32 and 64 rows (each register layout of the last
+    product; FP16 takes K steps of 32, so ranks up to 96 fit) and the LDS
+    tiles, with ragged n_1 and n_3 (odd n_3: the rows are not aligned for
+    the vector stores, which fall back to scalar ones)."""
     if layout == "lds":
         monkeypatch.setenv("LRC_TT_WAVE", "0")
     else:
