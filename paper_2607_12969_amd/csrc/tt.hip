@@ -58,7 +58,6 @@ struct TTArgs {
     TTSet set[kTTMaxSets];
     void* out;
     int vec4;
-    int pair16;              // wave-tile certificate: n_3 even, last cores and T 16-byte aligned
 };
 
 // Staged copies of the middle core G_{d-1} [rL][n_mid][rM] and the last core
@@ -1274,88 +1273,6 @@ static int64_t wave_grid(const TTPlan& p) {
     return xcd_grid(std::min<int64_t>((p.wave_tiles + 3) / 4, 4096));
 }
 
-// As last_w for even n_3 (with the last cores and T 16-byte aligned), each
-// lane owning two adjacent output columns: the block of 32 columns 32 cp + 2 r + e is computed as two
-// products (e = 0, 1), so that every core fragment and every value of T
-// comes in as one 16-byte load of a column pair (half the load
-// instructions).  With twice the products per step, a two-step ring (N: steps
-// 0, 1 of a block, R: the later steps) leads by as many cycles as the
-// four-step ring of last_w.
-typedef double double2_t __attribute__((ext_vector_type(2)));
-template <int NKB>
-__device__ __forceinline__ void last_w2(const TTArgs& a, const double* __restrict__ Tref, int64_t i, int64_t L0,
-                                        int r, int g, const double (&zf)[3][NKB], double (&sum)[5]) {
-    const int n_cp = (int)((a.n_last + 31) / 32);
-    const double2_t* b0 = static_cast<const double2_t*>(a.set[0].core[1]);
-    const double2_t* b1 = static_cast<const double2_t*>(a.set[1].core[1]);
-    const double2_t* b2 = static_cast<const double2_t*>(a.set[2].core[1]);
-    const int tl0 = a.set[0].rM - 1, tl1 = a.set[1].rM - 1, tl2 = a.set[2].rM - 1;
-    const uint32_t nl = (uint32_t)a.n_last, cmax = nl - 2;
-    auto colc = [&](int cp) {
-        const uint32_t c = (uint32_t)(32 * cp + 2 * r);
-        return c < cmax ? c : cmax;
-    };
-    auto ld = [&](double2_t (&f)[3], int gg, int kb, uint32_t c) {
-        const int t = 4 * kb + gg;
-        f[0] = ld_off(b0, last_off<double>(t, tl0, nl, c));
-        f[1] = ld_off(b1, last_off<double>(t, tl1, nl, c));
-        f[2] = ld_off(b2, last_off<double>(t, tl2, nl, c));
-    };
-    double2_t N[2][3], R[2][3];
-    uint32_t c = colc(0);
-    ld(N[0], g, 0, c);
-    ld(N[1], g, 1, c);
-    for (int cp = 0; cp < n_cp; ++cp) {
-        int gg = g;
-        asm volatile("" : "+v"(gg));
-        const uint32_t cn = colc(cp + 1 < n_cp ? cp + 1 : cp);
-        const int64_t col = (int64_t)cp * 32 + 2 * r;   // and col + 1 (n_3 is even)
-        double4_t acc[3][2];
-#pragma unroll
-        for (int q = 0; q < 3; ++q) acc[q][0] = acc[q][1] = zero_accv<double4_t>();
-#pragma unroll
-        for (int s = 0; s < NKB; ++s) {
-#pragma unroll
-            for (int q = 0; q < 3; ++q) {
-                const double2_t f = s < 2 ? N[s][q] : R[s % 2][q];
-                acc[q][0] = mfma(zf[q][s], f[0], acc[q][0]);
-                acc[q][1] = mfma(zf[q][s], f[1], acc[q][1]);
-            }
-            const int k = s + 2;
-            if (k < NKB) ld(R[k % 2], gg, k, c);
-            else ld(N[k - NKB], gg, k - NKB, cn);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        // the values of T, fetched after the block's last fragment loads (loads
-        // complete in order: fetched earlier, they would hold up the ring)
-        double2_t tv[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t L = L0 + g + 4 * v;
-            const bool ok = L < a.NL && col < a.n_last;
-            tv[v] = *reinterpret_cast<const double2_t*>(Tref + (ok ? (L * a.n_mid + i) * a.n_last + col : 0));
-        }
-        // lane holds rows L0 + g + 4v of columns col + e
-#pragma unroll
-        for (int e = 0; e < 2; ++e)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const bool ok = L0 + g + 4 * v < a.NL && col < a.n_last;
-                const double t = ok ? tv[v][e] : 0.0;
-                const double r0 = ok ? acc[0][e][v] : 0.0;
-                const double r1 = ok ? acc[1][e][v] : 0.0;
-                const double r2 = ok ? acc[2][e][v] : 0.0;
-                const double d0 = t - r0, d1 = t - r1, d2 = r1 - r2, d3 = t - r2;
-                sum[0] += d0 * d0;
-                sum[1] += d1 * d1;
-                sum[2] += d2 * d2;
-                sum[3] += d3 * d3;
-                sum[4] += t * t;
-            }
-        c = cn;
-    }
-}
-
 // ntiles = n_2 * ceil(n_1 / 16) wave tiles, tile = i * ceil(n_1 / 16) + L
 // block (the four waves of a workgroup, and consecutive workgroups of one
 // XCD, share i and so the middle core slice in L2).  The grid is a multiple
@@ -1389,8 +1306,7 @@ __global__ __launch_bounds__(256) void k_tt_cert_w(TTArgs a, const double* __res
         }
         int ln = lane;
         asm volatile("" : "+v"(ln));
-        if (a.pair16) last_w2<NKB>(a, Tref, i, L0, ln & 15, ln >> 4, zf, sum);
-        else last_w<NKB>(a, Tref, i, L0, ln & 15, ln >> 4, zf, sum);
+        last_w<NKB>(a, Tref, i, L0, ln & 15, ln >> 4, zf, sum);
     }
 #pragma unroll
     for (int s = 0; s < 5; ++s) {
@@ -1709,9 +1625,6 @@ hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, cons
     if (e != hipSuccess) return e;
     if (p.wave_nkb) {
         const dim3 gw((unsigned)wave_grid(p));
-        auto al16 = [](const void* q) { return reinterpret_cast<uintptr_t>(q) % 16 == 0; };
-        a.pair16 = p.n_last % 2 == 0 && al16(Tref) && al16(a.set[0].core[1]) && al16(a.set[1].core[1]) &&
-                   al16(a.set[2].core[1]);
         KernelTimer tk("cert_tt_fused_f64", stream);
 #define LRC_TTW(K) hipLaunchKernelGGL((k_tt_cert_w<K>), gw, dim3(256), 0, stream, a, Tref, part, p.wave_tiles)
         switch (p.wave_nkb) {
