@@ -771,6 +771,26 @@ static bool needs_stage(const void* p, int64_t ld, int prec) {
     return (ld % vec != 0) || (reinterpret_cast<uintptr_t>(p) % 16 != 0);
 }
 
+// Tile edges and K step of the matrix-core configurations, for the plan (the
+// grids and the split-K partial buffers are sized from the same constants
+// the kernels are compiled with).
+struct TileDims {
+    int bm, bn, bk;
+};
+template <class C>
+static TileDims dims_of() {
+    return TileDims{C::BM, C::BN, C::BK};
+}
+template <typename T> struct PrecCode;
+template <> struct PrecCode<double> { static constexpr int value = P64; };
+template <> struct PrecCode<float> { static constexpr int value = P32; };
+template <> struct PrecCode<half_t> { static constexpr int value = P16; };
+static TileDims cfg_dims(int prec, bool big) {
+    if (prec == P64) return big ? dims_of<BigCfg<double>::C>() : dims_of<SmallCfg<double>::C>();
+    if (prec == P32) return big ? dims_of<BigCfg<float>::C>() : dims_of<SmallCfg<float>::C>();
+    return big ? dims_of<BigCfg<half_t>::C>() : dims_of<SmallCfg<half_t>::C>();
+}
+
 ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int path, const void* U,
                      const void* V, const void* X) {
     ApplyPlan p{};
@@ -790,14 +810,14 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         const int nb = (b <= 1) ? 1 : (b <= 2) ? 2 : (b <= 4) ? 4 : 8;
         p.part_bytes = (size_t)p.tiles_m * p.splits * 64 * nb * acc_b;
     } else {
-        const int BK = (prec == P16) ? 32 : 16;
         // phase 1: C = V^T X is k x b, summed over n
         p.big1 = (k >= 128 && b >= 128) ? 1 : 0;
         if (forced_tile()) p.big1 = forced_tile() == 128;
         if (prec == P64) p.big1 = 0;
-        const int T1 = p.big1 ? 128 : 64;
-        p.tiles_m = (int)((k + T1 - 1) / T1);
-        p.tiles_n = (int)((b + T1 - 1) / T1);
+        const TileDims d1 = cfg_dims(prec, p.big1);
+        const int BK = d1.bk;
+        p.tiles_m = (int)((k + d1.bm - 1) / d1.bm);
+        p.tiles_n = (int)((b + d1.bn - 1) / d1.bn);
         const int64_t base = (int64_t)p.tiles_m * p.tiles_n;
         const int64_t target = p.big1 ? kBigTarget : kSmallTarget;
         int64_t splits = (target + base - 1) / base;
@@ -807,7 +827,7 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         if (splits < 1) splits = 1;
         p.chunk = round_up((n + splits - 1) / splits, BK);
         p.splits = (int)((n + p.chunk - 1) / p.chunk);
-        p.part_bytes = (p.splits > 1) ? (size_t)base * p.splits * T1 * T1 * acc_b : 0;
+        p.part_bytes = (p.splits > 1) ? (size_t)base * p.splits * d1.bm * d1.bn * acc_b : 0;
         // phase 2: Y = U T' is m x b
         const int64_t big_tiles = ((m + 127) / 128) * ((b + 127) / 128);
         p.big2 = (m >= 128 && b >= 128 && big_tiles >= 256) ? 1 : 0;
@@ -922,8 +942,8 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     if (e != hipSuccess) return e;
     KernelTimer t2(p2_mfma_label<T>(), stream);
     const int vec4 = (b % 4 == 0) && ((reinterpret_cast<uintptr_t>(Y) % (4 * sizeof(T))) == 0);
-    const int T2 = p.big2 ? 128 : 64;
-    const int tm = (int)((m + T2 - 1) / T2), tn = (int)((b + T2 - 1) / T2);
+    const TileDims d2 = cfg_dims(PrecCode<T>::value, p.big2);
+    const int tm = (int)((m + d2.bm - 1) / d2.bm), tn = (int)((b + d2.bn - 1) / d2.bn);
     const dim3 g2(xcd_grid(AbtOrder(tm, tn).total));
     if (p.big2)
         launch_abt<T, typename BigCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt, ldt,
@@ -959,14 +979,15 @@ using GramC = Cfg<double, 64, 64, 16, 2, 2>;
 // (measured on the 8192 x 514 factor blocks: 1024 leaves the compute units
 // unevenly loaded, beyond 2048 the partial tiles cost more than they save).
 static void gram_plan(int64_t rows, int64_t cols, int* tiles, int* splits, int64_t* chunk) {
-    const int t = (int)((cols + 63) / 64);
+    static_assert(GramC::BM == GramC::BN, "square Gram tiles");
+    const int t = (int)((cols + GramC::BM - 1) / GramC::BM);
     const int64_t base = (int64_t)t * t;
     int64_t sp = (1536 + base - 1) / base;
     int64_t mx = rows / 64;
     if (mx < 1) mx = 1;
     if (sp > mx) sp = mx;
     if (sp < 1) sp = 1;
-    *chunk = round_up((rows + sp - 1) / sp, 16);
+    *chunk = round_up((rows + sp - 1) / sp, GramC::BK);
     *splits = (int)((rows + *chunk - 1) / *chunk);
     *tiles = t;
 }
@@ -975,7 +996,7 @@ size_t gram_workspace_bytes(int64_t rows, int64_t cols) {
     int t, sp;
     int64_t ch;
     gram_plan(rows, cols, &t, &sp, &ch);
-    return (size_t)t * t * sp * 64 * 64 * sizeof(double);
+    return (size_t)t * t * sp * GramC::BM * GramC::BN * sizeof(double);
 }
 
 hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G, Workspace& ws,
@@ -983,7 +1004,7 @@ hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G, W
     int t, sp;
     int64_t ch;
     gram_plan(rows, cols, &t, &sp, &ch);
-    double* part = static_cast<double*>(ws.take((size_t)t * t * sp * 64 * 64 * sizeof(double)));
+    double* part = static_cast<double*>(ws.take(gram_workspace_bytes(rows, cols)));
     if (ws.overrun) return hipErrorOutOfMemory;
     if (!vec_ok<double>(P, cols)) return hipErrorInvalidValue;   // the factor builders keep 2r columns
     run_atb<double, GramC, ATB_GRAM>("cert_gram_f64", "cert_gram_finish_f64", stream, P, cols, P, cols, cols, cols,
@@ -992,12 +1013,12 @@ hipError_t launch_gram(const double* P, int64_t rows, int64_t cols, double* G, W
 }
 
 size_t err_workspace_bytes(int64_t m, int64_t n) {
-    return (size_t)((m + 63) / 64) * ((n + 63) / 64) * sizeof(double);
+    return (size_t)((m + GramC::BM - 1) / GramC::BM) * ((n + GramC::BN - 1) / GramC::BN) * sizeof(double);
 }
 
 hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, int64_t m, int64_t n,
                             int64_t r, int64_t ldw, double* part, int64_t* nparts, hipStream_t stream) {
-    const int tm = (int)((m + 63) / 64), tn = (int)((n + 63) / 64);
+    const int tm = (int)((m + GramC::BM - 1) / GramC::BM), tn = (int)((n + GramC::BN - 1) / GramC::BN);
     *nparts = (int64_t)tm * tn;
     const int64_t K = round_up(r, GramC::BK);
     if (!vec_ok<double>(W, ldw) || !vec_ok<double>(Vw, ldw)) return hipErrorInvalidValue;
