@@ -111,6 +111,28 @@ __global__ __launch_bounds__(256) void k_stage_rows(const T* __restrict__ g1, T*
     }
 }
 
+// Left interface of a train with d >= 4 for the wave tiles, one level per
+// launch: Z_c(p n_c + i, t) = sum_s Z_{c-1}(p, s) G_c(s, i, t) with Z_0 = G_1,
+// summed over s in order in the accumulation precision (the arithmetic of the
+// LDS tiles' chain); the last level is rounded once to the storage type.  Its
+// rows are the left indices (i_1 .. i_{d-2}) in C order, so it takes the place
+// of G_1 of a three-core train.
+template <typename In, typename G, typename Out>
+__global__ __launch_bounds__(256) void k_tt_left(const In* __restrict__ z, const G* __restrict__ g,
+                                                 Out* __restrict__ zo, int64_t P, int rin, int64_t n, int rout) {
+    using Acc = typename PrecTraits<G>::acc;
+    const int64_t tot = P * n * rout;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < tot; idx += (int64_t)gridDim.x * 256) {
+        const int t = (int)(idx % rout);
+        const int64_t q = idx / rout;
+        const int64_t i = q % n, pr = q / n;
+        const In* zr = z + pr * rin;
+        Acc sum = 0;
+        for (int s2 = 0; s2 < rin; ++s2) sum += static_cast<Acc>(zr[s2]) * static_cast<Acc>(g[((int64_t)s2 * n + i) * rout + t]);
+        zo[idx] = static_cast<Out>(sum);
+    }
+}
+
 // Fragment address of the staged middle core for middle index i (clamped
 // into range: rows past the tensor are discarded at the store), output
 // column t, this lane's K group g; step kb adds kb * mid_step<T>(S).
@@ -1404,7 +1426,7 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     // selects the LDS tiles; LRC_TT_WAVE_NPB (1, 2 or 4) sets the row blocks
     // per reconstruction tile.
     const char* wv = std::getenv("LRC_TT_WAVE");
-    bool wave_ok = d == 3 && !(wv && wv[0] == '0') &&
+    bool wave_ok = d >= 3 && !(wv && wv[0] == '0') &&
                    ((prec == P64 && (nsets == 1 || nsets == 3)) || (prec != P64 && nsets == 1));
     // FP64 / FP32 wave tiles read G_2 and G_3 in place with 32-bit byte offsets
     for (int q = 0; q < nsets && wave_ok; ++q) {
@@ -1454,6 +1476,20 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
             p.wave_tiles = p.num_i_blocks * p.num_L_blocks;
             // FP16 stages its cores (K-contiguous fragments); FP64 / FP32 read them in place
             p.stage_bytes = prec == P16 ? stage_bytes() + (size_t)round_up(p.NL * p.set[0].Kp2 * e, 256) : 0;
+            // d >= 4: the left interface of every set (storage type) and two
+            // chain buffers (accumulation type) for its levels
+            if (d >= 4) {
+                int64_t lev = 0;
+                for (int q = 0; q < nsets; ++q) {
+                    int64_t P = dims[0];
+                    for (int c = 1; c <= d - 4; ++c) {
+                        P *= dims[c];
+                        lev = std::max<int64_t>(lev, P * rank_sets[q][c + 1]);
+                    }
+                    p.stage_bytes += (size_t)round_up(p.NL * p.set[q].rL * e, 256);
+                }
+                p.stage_bytes += 2 * (size_t)round_up(lev * acc_b, 256);
+            }
             return 0;
         }
     }
@@ -1536,6 +1572,54 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
     // the staging copy is timed under the kernel's label with a "_stage" suffix
     char stage_label[64];
     std::snprintf(stage_label, sizeof(stage_label), "%s_stage", label);
+    // wave tiles of a train with d >= 4: its left interface takes the place of
+    // G_1 (formed here level by level, timed with the staging)
+    using Acc = typename PrecTraits<T>::acc;
+    const void* left[kTTMaxSets] = {};
+    if (p.wave_nkb && p.d >= 4) {
+        int64_t lev = 0;
+        for (int q = 0; q < p.nsets; ++q) {
+            int64_t P = p.dims[0];
+            for (int c = 1; c <= p.d - 4; ++c) {
+                P *= p.dims[c];
+                lev = std::max<int64_t>(lev, P * p.set[q].ranks[c + 1]);
+            }
+        }
+        Acc* buf[2] = {nullptr, nullptr};
+        if (lev > 0) {
+            buf[0] = static_cast<Acc*>(ws.take((size_t)lev * sizeof(Acc)));
+            buf[1] = static_cast<Acc*>(ws.take((size_t)lev * sizeof(Acc)));
+        }
+        KernelTimer ts(stage_label, stream);
+        for (int q = 0; q < p.nsets; ++q) {
+            T* fin = static_cast<T*>(ws.take((size_t)p.NL * p.set[q].rL * sizeof(T)));
+            if (ws.overrun || !fin || (lev > 0 && (!buf[0] || !buf[1]))) return hipErrorOutOfMemory;
+            const int64_t* rk = p.set[q].ranks;
+            int64_t P = p.dims[0];   // rows of the level's input
+            for (int c = 1; c <= p.d - 3; ++c) {
+                const int64_t tot = P * p.dims[c] * rk[c + 1];
+                const unsigned gs = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
+                const T* g = static_cast<const T*>(cores[q][c]);
+                const bool last = c == p.d - 3;
+                if (c == 1 && last)
+                    hipLaunchKernelGGL((k_tt_left<T, T, T>), dim3(gs), dim3(256), 0, stream,
+                                       static_cast<const T*>(cores[q][0]), g, fin, P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
+                else if (c == 1)   // writes buf[0]
+                    hipLaunchKernelGGL((k_tt_left<T, T, Acc>), dim3(gs), dim3(256), 0, stream,
+                                       static_cast<const T*>(cores[q][0]), g, buf[0], P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
+                else if (last)   // level c reads buf[c % 2] (written by level c - 1)
+                    hipLaunchKernelGGL((k_tt_left<Acc, T, T>), dim3(gs), dim3(256), 0, stream,
+                                       (const Acc*)buf[c % 2], g, fin, P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
+                else             // and writes buf[(c + 1) % 2]
+                    hipLaunchKernelGGL((k_tt_left<Acc, T, Acc>), dim3(gs), dim3(256), 0, stream,
+                                       (const Acc*)buf[c % 2], g, buf[(c + 1) % 2], P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
+                hipError_t e = hipGetLastError();
+                if (e != hipSuccess) return e;
+                P *= p.dims[c];
+            }
+            left[q] = fin;
+        }
+    }
     // LDS: the shared Z_{d-2} buffer first, then one Z_{d-1} per set
     int off = 0;
     for (int q = 0; q < p.nsets; ++q)
@@ -1546,6 +1630,7 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
         S.core[0] = cores[q][p.d - 2];
         S.core[1] = cores[q][p.d - 1];
         for (int c = 0; c <= p.d - 3; ++c) S.core[2 + c] = cores[q][c];
+        if (left[q]) S.core[2] = left[q];   // wave tiles: G_1 of the equivalent three-core train
         for (int c = 0; c <= p.d; ++c) S.ranks[c] = ps.ranks[c];
         S.rL = ps.rL;
         S.rM = ps.rM;
@@ -1581,7 +1666,7 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
             int64_t gs = (p.NL * ps.Kp2 + 255) / 256;
             if (gs > 4096) gs = 4096;
             KernelTimer ts(stage_label, stream);
-            hipLaunchKernelGGL(k_stage_rows<T>, dim3((unsigned)gs), dim3(256), 0, stream, (const T*)cores[q][0], sl,
+            hipLaunchKernelGGL(k_stage_rows<T>, dim3((unsigned)gs), dim3(256), 0, stream, (const T*)S.core[2], sl,
                                p.NL, ps.rL, ps.Kp2);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;

@@ -150,3 +150,20 @@ def test_three_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
         monkeypatch.setenv("LRC_TT_WAVE_NPB", layout[3])
     cores = synth.random_tt_cores(dims, ranks, tag=sum(dims) + sum(ranks))
     _check(lrc, cores, prec, f"{layout}{dims}")
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("layout", ["wave", "lds"])
+@pytest.mark.parametrize("dims,ranks", [
+    ((3, 4, 5, 6), (1, 3, 7, 5, 1)),
+    ((6, 5, 4, 3, 2), (1, 4, 9, 8, 2, 1)),
+    ((7, 9, 5, 33, 19), (1, 6, 20, 30, 17, 1)),
+])
+def test_many_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
+    """Trains of four and more cores: by wave tiles (the left interface
+    Z_{d-2} formed first, then the three-core kernels) and by LDS tiles (the
+    left chain per tile)."""
+    if layout == "lds":
+        monkeypatch.setenv("LRC_TT_WAVE", "0")
+    cores = synth.random_tt_cores(dims, ranks, tag=7 * len(dims) + sum(ranks))
+    _check(lrc, cores, prec, f"{layout}{dims}")
