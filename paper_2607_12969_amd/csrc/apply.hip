@@ -462,15 +462,12 @@ __global__ __launch_bounds__(C::NT) void k_atb_finish(
     const int64_t qs = (int64_t)NF * C::NT;      // stride between splits
     AccV acc = zero_accv<AccV>();
     int q = 0;
-    for (; q + 4 <= splits; q += 4) {
-        const AccV p0 = __builtin_nontemporal_load(src + (q + 0) * qs);
-        const AccV p1 = __builtin_nontemporal_load(src + (q + 1) * qs);
-        const AccV p2 = __builtin_nontemporal_load(src + (q + 2) * qs);
-        const AccV p3 = __builtin_nontemporal_load(src + (q + 3) * qs);
-        acc += p0;
-        acc += p1;
-        acc += p2;
-        acc += p3;
+    for (; q + 8 <= splits; q += 8) {   // eight partials fetched at a time, added in split order
+        AccV pv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) pv[u] = __builtin_nontemporal_load(src + (q + u) * qs);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc += pv[u];
     }
     for (; q < splits; ++q) acc += __builtin_nontemporal_load(src + q * qs);
     const int64_t m0 = (tile % tiles_m) * C::BM, n0 = (tile / tiles_m) * C::BN;
@@ -649,7 +646,8 @@ __global__ __launch_bounds__(256) void k_p1_stream(
     int64_t n, int64_t k, int64_t b, int64_t chunk, int splits) {
     using Acc = typename PrecTraits<T>::acc;
     __shared__ Acc red[4][64][NB];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: X rows load once per wave
     const int jg = blockIdx.x, sp = blockIdx.y;
     const int64_t j = (int64_t)jg * 64 + lane;
     const int64_t i0 = (int64_t)sp * chunk;
@@ -659,11 +657,28 @@ __global__ __launch_bounds__(256) void k_p1_stream(
 #pragma unroll
     for (int c = 0; c < NB; ++c) acc[c] = 0;
     if (j < k) {
-        for (int64_t i = i0 + wave; i < i1; i += 4) {
-            const Acc vij = to_acc(V[i * k + j]);
+        // rows i0 + wave + 4 rho in order, RB of them per batch: the batch's loads
+        // come from clamped rows and are issued together, the rows past the
+        // chunk add nothing
+        constexpr int RB = 16;
+        for (int64_t ib = i0 + wave; ib < i1; ib += 4 * RB) {
+            T v[RB], x[RB][NB];
 #pragma unroll
-            for (int c = 0; c < NB; ++c)
-                if (c < b) acc[c] += vij * to_acc(X[i * b + c]);
+            for (int rho = 0; rho < RB; ++rho) {
+                const int64_t i = ib + 4 * rho;
+                const int64_t ic = i < i1 ? i : i1 - 1;
+                v[rho] = V[ic * k + j];
+#pragma unroll
+                for (int c = 0; c < NB; ++c) x[rho][c] = X[ic * b + (c < b ? c : 0)];
+            }
+#pragma unroll
+            for (int rho = 0; rho < RB; ++rho) {
+                if (ib + 4 * rho >= i1) break;
+                const Acc vij = to_acc(v[rho]);
+#pragma unroll
+                for (int c = 0; c < NB; ++c)
+                    if (c < b) acc[c] += vij * to_acc(x[rho][c]);
+            }
         }
     }
 #pragma unroll
@@ -692,8 +707,18 @@ __global__ __launch_bounds__(256) void k_p1_stream_finish(
         if (c >= b || jj >= ldt) continue;
         Acc sum = 0;
         if (jj < k) {
-            for (int q = 0; q < splits; ++q)
-                sum += __builtin_nontemporal_load(&part[(((int64_t)jg * splits + q) * 64 + jl) * NB + c]);
+            // the split partials in order, fetched 16 at a time
+            const Acc* src = part + ((int64_t)jg * splits * 64 + jl) * NB + c;
+            const int64_t qs = 64 * NB;
+            int q = 0;
+            for (; q + 16 <= splits; q += 16) {
+                Acc v[16];
+#pragma unroll
+                for (int u = 0; u < 16; ++u) v[u] = __builtin_nontemporal_load(src + (q + u) * qs);
+#pragma unroll
+                for (int u = 0; u < 16; ++u) sum += v[u];
+            }
+            for (; q < splits; ++q) sum += __builtin_nontemporal_load(src + q * qs);
         }
         const Acc sj = (jj < k) ? to_acc(s[jj]) : Acc(0);
         Tt[(int64_t)c * ldt + jj] = to_storage<T>(sj * sum);
@@ -821,7 +846,9 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         const int64_t base = (int64_t)p.tiles_m * p.tiles_n;
         const int64_t target = p.big1 ? kBigTarget : kSmallTarget;
         int64_t splits = (target + base - 1) / base;
-        int64_t max_splits = n / (4 * BK);
+        // at least 16 K steps per split: with few tiles, more splits only
+        // lengthen the finish kernel's sums
+        int64_t max_splits = n / (16 * BK);
         if (max_splits < 1) max_splits = 1;
         if (splits > max_splits) splits = max_splits;
         if (splits < 1) splits = 1;

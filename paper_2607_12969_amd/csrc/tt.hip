@@ -58,6 +58,7 @@ struct TTArgs {
     TTSet set[kTTMaxSets];
     void* out;
     int vec4;
+    int ifast;               // wave tiles: consecutive tiles take consecutive middle indices
 };
 
 // Staged copies of the middle core G_{d-1} [rL][n_mid][rM] and the last core
@@ -111,25 +112,66 @@ __global__ __launch_bounds__(256) void k_stage_rows(const T* __restrict__ g1, T*
     }
 }
 
-// Left interface of a train with d >= 4 for the wave tiles, one level per
-// launch: Z_c(p n_c + i, t) = sum_s Z_{c-1}(p, s) G_c(s, i, t) with Z_0 = G_1,
-// summed over s in order in the accumulation precision (the arithmetic of the
-// LDS tiles' chain); the last level is rounded once to the storage type.  Its
-// rows are the left indices (i_1 .. i_{d-2}) in C order, so it takes the place
-// of G_1 of a three-core train.
-template <typename In, typename G, typename Out>
-__global__ __launch_bounds__(256) void k_tt_left(const In* __restrict__ z, const G* __restrict__ g,
-                                                 Out* __restrict__ zo, int64_t P, int rin, int64_t n, int rout) {
-    using Acc = typename PrecTraits<G>::acc;
-    const int64_t tot = P * n * rout;
-    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < tot; idx += (int64_t)gridDim.x * 256) {
-        const int t = (int)(idx % rout);
-        const int64_t q = idx / rout;
-        const int64_t i = q % n, pr = q / n;
-        const In* zr = z + pr * rin;
+// Left interface of a train with d >= 4 for the wave tiles:
+// Z(p n + i, t) = sum_s z_p(s) G_{d-2}(s, i, t) for every prefix p = (i_1 .. i_{d-3})
+// and n = n_{d-2}, where z_p = G_1(i_1, :) G_2(:, i_2, :) ... is the prefix's
+// row vector.  One workgroup per prefix forms z_p level by level in LDS (sums
+// over s in order in the accumulation precision, as the LDS tiles' chain) and
+// then the n r_{d-2} entries of its rows, rounded once to the storage type.
+// Its rows are the left indices (i_1 .. i_{d-2}) in C order, so it takes the
+// place of G_1 of a three-core train.
+struct LeftChain {
+    const void* core[kMaxD];
+    int64_t dims[kMaxD];
+    int64_t ranks[kMaxD + 1];
+    int d;
+    int rmax;   // largest rank among r_1 .. r_{d-3} (LDS vectors)
+};
+template <typename T>
+__global__ __launch_bounds__(256) void k_tt_left(LeftChain lc, T* __restrict__ zo) {
+    using Acc = typename PrecTraits<T>::acc;
+    extern __shared__ double4_t lsm[];
+    Acc* va = reinterpret_cast<Acc*>(lsm);
+    Acc* vb = va + lc.rmax;
+    const int tid = threadIdx.x;
+    const int64_t pfx = blockIdx.x;
+    // the prefix digits i_1 .. i_{d-3}, last digit fastest
+    int64_t rest = pfx;
+    int64_t dig[kMaxD];
+    for (int c = lc.d - 4; c >= 0; --c) {
+        dig[c] = rest % lc.dims[c];
+        rest /= lc.dims[c];
+    }
+    const T* g0 = static_cast<const T*>(lc.core[0]);
+    for (int t = tid; t < lc.ranks[1]; t += 256) va[t] = static_cast<Acc>(g0[dig[0] * lc.ranks[1] + t]);
+    __syncthreads();
+    for (int c = 1; c <= lc.d - 4; ++c) {
+        const T* g = static_cast<const T*>(lc.core[c]);
+        const int rin = (int)lc.ranks[c], rout = (int)lc.ranks[c + 1];
+        const int64_t n = lc.dims[c];
+        for (int t = tid; t < rout; t += 256) {
+            Acc sum = 0;
+#pragma unroll 8
+            for (int s2 = 0; s2 < rin; ++s2) sum += va[s2] * static_cast<Acc>(g[((int64_t)s2 * n + dig[c]) * rout + t]);
+            vb[t] = sum;
+        }
+        __syncthreads();
+        Acc* tmp = va;
+        va = vb;
+        vb = tmp;
+    }
+    const int c = lc.d - 3;
+    const T* g = static_cast<const T*>(lc.core[c]);
+    const int rin = (int)lc.ranks[c], rout = (int)lc.ranks[c + 1];
+    const int64_t n = lc.dims[c];
+    T* dst = zo + pfx * n * rout;
+    for (int64_t e = tid; e < n * rout; e += 256) {
+        const int64_t i = e / rout;
+        const int t = (int)(e % rout);
         Acc sum = 0;
-        for (int s2 = 0; s2 < rin; ++s2) sum += static_cast<Acc>(zr[s2]) * static_cast<Acc>(g[((int64_t)s2 * n + i) * rout + t]);
-        zo[idx] = static_cast<Out>(sum);
+#pragma unroll 8
+        for (int s2 = 0; s2 < rin; ++s2) sum += va[s2] * static_cast<Acc>(g[((int64_t)s2 * n + i) * rout + t]);
+        dst[e] = static_cast<T>(sum);
     }
 }
 
@@ -934,7 +976,8 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
 }
 
 // FP64 reconstruction for d = 3 by wave tiles: a tile is 16 NPB rows of G_1
-// for one middle index i (tile = i * ceil(n_1 / (16 NPB)) + row block), the
+// for one middle index i (tile = i * ceil(n_1 / (16 NPB)) + row block, or
+// row block * n_2 + i for short output rows, TTArgs::ifast), the
 // interfaces Z_2 of its row blocks held in registers as the A fragments of
 // the last product (see the wave-tile certificate below).  The core ring is
 // 8 steps deep (4 for four row blocks, whose steps are twice as long).
@@ -946,7 +989,8 @@ __global__ __launch_bounds__(256) void k_tt_wave(TTArgs a, int64_t ntiles) {
     const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
     const int64_t wl = xcd_tile(gridDim.x);
     for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
-        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16 * NPB;
+        const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
+        const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
         double zf[NPB][NKB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) {
@@ -1081,7 +1125,8 @@ __global__ __launch_bounds__(256) void k_tt_wave32(TTArgs a, int64_t ntiles) {
     const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
     const int64_t wl = xcd_tile(gridDim.x);
     for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
-        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16 * NPB;
+        const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
+        const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
         float zf[NPB][NKB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) {
@@ -1256,7 +1301,8 @@ __global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
     const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
     const int64_t wl = xcd_tile(gridDim.x);
     for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
-        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16 * NPB;
+        const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
+        const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
         half8_t zf[NPB][NKB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) {
@@ -1297,7 +1343,8 @@ static int64_t wave_grid(const TTPlan& p) {
 
 // ntiles = n_2 * ceil(n_1 / 16) wave tiles, tile = i * ceil(n_1 / 16) + L
 // block (the four waves of a workgroup, and consecutive workgroups of one
-// XCD, share i and so the middle core slice in L2).  The grid is a multiple
+// XCD, share i and so the middle core slice in L2), or L block * n_2 + i for
+// short output rows (TTArgs::ifast).  The grid is a multiple
 // of 8; workgroup w writes part[s * gridDim.x + w] (sums as in k_tt_cert).
 template <int NKB>
 __global__ __launch_bounds__(256) void k_tt_cert_w(TTArgs a, const double* __restrict__ Tref,
@@ -1310,7 +1357,8 @@ __global__ __launch_bounds__(256) void k_tt_cert_w(TTArgs a, const double* __res
     double sum[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
     const int64_t wl = xcd_tile(gridDim.x);
     for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
-        const int64_t i = tile / nLb, L0 = (tile % nLb) * 16;
+        const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
+        const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16;
         double zf[3][NKB];
 #pragma unroll
         for (int q = 0; q < 3; ++q) {
@@ -1432,6 +1480,12 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     for (int q = 0; q < nsets && wave_ok; ++q) {
         const TTPlanSet& ps = p.set[q];
         wave_ok = (double)ps.rL * p.n_mid * ps.rM * e < 4294967296.0 && (double)ps.rM * p.n_last * e < 4294967296.0;
+        // d >= 4: one workgroup per prefix (i_1 .. i_{d-3}) forms the left interface, its
+        // row vectors (ranks r_1 .. r_{d-3}) in 2 x 32 KB of LDS
+        int64_t npfx = 1;
+        for (int c = 0; c <= d - 4; ++c) npfx *= dims[c];
+        for (int c = 1; c <= d - 3 && wave_ok; ++c) wave_ok = rank_sets[q][c] * acc_b <= 32768;
+        wave_ok = wave_ok && npfx < 2147483647;
     }
     if (wave_ok) {
         int nkb = 0;
@@ -1478,18 +1532,8 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
             p.stage_bytes = prec == P16 ? stage_bytes() + (size_t)round_up(p.NL * p.set[0].Kp2 * e, 256) : 0;
             // d >= 4: the left interface of every set (storage type) and two
             // chain buffers (accumulation type) for its levels
-            if (d >= 4) {
-                int64_t lev = 0;
-                for (int q = 0; q < nsets; ++q) {
-                    int64_t P = dims[0];
-                    for (int c = 1; c <= d - 4; ++c) {
-                        P *= dims[c];
-                        lev = std::max<int64_t>(lev, P * rank_sets[q][c + 1]);
-                    }
-                    p.stage_bytes += (size_t)round_up(p.NL * p.set[q].rL * e, 256);
-                }
-                p.stage_bytes += 2 * (size_t)round_up(lev * acc_b, 256);
-            }
+            if (d >= 4)
+                for (int q = 0; q < nsets; ++q) p.stage_bytes += (size_t)round_up(p.NL * p.set[q].rL * e, 256);
             return 0;
         }
     }
@@ -1569,54 +1613,35 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
     a.ncp = (int)round_up(p.n_last, 32);
     a.out = out;
     a.vec4 = out && (p.n_last % 4 == 0) && (reinterpret_cast<uintptr_t>(out) % (4 * sizeof(T)) == 0);
+    // short output rows (n_d e < 1 KB): wave tiles of consecutive middle indices
+    // write neighbouring segments of the same rows, so the rows fill up together
+    a.ifast = p.wave_nkb && p.n_last * (int64_t)sizeof(T) < 1024;
     // the staging copy is timed under the kernel's label with a "_stage" suffix
     char stage_label[64];
     std::snprintf(stage_label, sizeof(stage_label), "%s_stage", label);
     // wave tiles of a train with d >= 4: its left interface takes the place of
-    // G_1 (formed here level by level, timed with the staging)
-    using Acc = typename PrecTraits<T>::acc;
+    // G_1 (formed here, timed with the staging)
     const void* left[kTTMaxSets] = {};
     if (p.wave_nkb && p.d >= 4) {
-        int64_t lev = 0;
-        for (int q = 0; q < p.nsets; ++q) {
-            int64_t P = p.dims[0];
-            for (int c = 1; c <= p.d - 4; ++c) {
-                P *= p.dims[c];
-                lev = std::max<int64_t>(lev, P * p.set[q].ranks[c + 1]);
-            }
-        }
-        Acc* buf[2] = {nullptr, nullptr};
-        if (lev > 0) {
-            buf[0] = static_cast<Acc*>(ws.take((size_t)lev * sizeof(Acc)));
-            buf[1] = static_cast<Acc*>(ws.take((size_t)lev * sizeof(Acc)));
-        }
         KernelTimer ts(stage_label, stream);
         for (int q = 0; q < p.nsets; ++q) {
             T* fin = static_cast<T*>(ws.take((size_t)p.NL * p.set[q].rL * sizeof(T)));
-            if (ws.overrun || !fin || (lev > 0 && (!buf[0] || !buf[1]))) return hipErrorOutOfMemory;
-            const int64_t* rk = p.set[q].ranks;
-            int64_t P = p.dims[0];   // rows of the level's input
-            for (int c = 1; c <= p.d - 3; ++c) {
-                const int64_t tot = P * p.dims[c] * rk[c + 1];
-                const unsigned gs = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
-                const T* g = static_cast<const T*>(cores[q][c]);
-                const bool last = c == p.d - 3;
-                if (c == 1 && last)
-                    hipLaunchKernelGGL((k_tt_left<T, T, T>), dim3(gs), dim3(256), 0, stream,
-                                       static_cast<const T*>(cores[q][0]), g, fin, P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
-                else if (c == 1)   // writes buf[0]
-                    hipLaunchKernelGGL((k_tt_left<T, T, Acc>), dim3(gs), dim3(256), 0, stream,
-                                       static_cast<const T*>(cores[q][0]), g, buf[0], P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
-                else if (last)   // level c reads buf[c % 2] (written by level c - 1)
-                    hipLaunchKernelGGL((k_tt_left<Acc, T, T>), dim3(gs), dim3(256), 0, stream,
-                                       (const Acc*)buf[c % 2], g, fin, P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
-                else             // and writes buf[(c + 1) % 2]
-                    hipLaunchKernelGGL((k_tt_left<Acc, T, Acc>), dim3(gs), dim3(256), 0, stream,
-                                       (const Acc*)buf[c % 2], g, buf[(c + 1) % 2], P, (int)rk[c], p.dims[c], (int)rk[c + 1]);
-                hipError_t e = hipGetLastError();
-                if (e != hipSuccess) return e;
-                P *= p.dims[c];
+            if (ws.overrun || !fin) return hipErrorOutOfMemory;
+            LeftChain lc{};
+            lc.d = p.d;
+            lc.rmax = 1;
+            for (int c = 0; c < p.d; ++c) {
+                lc.core[c] = cores[q][c];
+                lc.dims[c] = p.dims[c];
             }
+            for (int c = 0; c <= p.d; ++c) lc.ranks[c] = p.set[q].ranks[c];
+            for (int c = 1; c <= p.d - 3; ++c) lc.rmax = (int)std::max<int64_t>(lc.rmax, p.set[q].ranks[c]);
+            int64_t npfx = 1;
+            for (int c = 0; c <= p.d - 4; ++c) npfx *= p.dims[c];
+            const size_t lds = 2 * (size_t)lc.rmax * sizeof(typename PrecTraits<T>::acc);
+            hipLaunchKernelGGL(k_tt_left<T>, dim3((unsigned)npfx), dim3(256), lds, stream, lc, fin);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
             left[q] = fin;
         }
     }
