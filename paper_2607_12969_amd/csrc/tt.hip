@@ -1214,6 +1214,49 @@ __device__ __forceinline__ void middle_w16(const TTArgs& a, const TTSet& S, int6
     if (kb < nkb) step(x0, b0);
 }
 
+// The FP16 middle products of all NPB row blocks of a tile (one middle index,
+// so the same G_2 fragments): the NT x NKB2 A fragments are fetched once and
+// kept, then each row block needs only its rows of G_1 (Kp2 <= 32 NKB2).
+template <int NT, int NKB2, int NPB, class OutF>
+__device__ __forceinline__ void middle_w16_tile(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
+                                                OutF emit) {
+    const half_t* mid = static_cast<const half_t*>(S.st_mid) + i * S.Rt * S.Kp2;   // uniform
+    const uint32_t moff = (uint32_t)(r * S.Kp2 + 8 * g) * 2u;
+    const int64_t tstep = 16 * (int64_t)S.Kp2;
+    const int nkb = S.Kp2 / 32;   // <= NKB2
+    half8_t x[NKB2][NT];
+#pragma unroll
+    for (int kb = 0; kb < NKB2; ++kb) {
+        const half_t* mk = mid + (kb < nkb ? kb : nkb - 1) * 32;
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) x[kb][tb] = ld_off(reinterpret_cast<const half8_t*>(mk + tb * tstep), moff);
+    }
+    auto rows = [&](int pb, half8_t (&b)[NKB2]) {
+        const int64_t row = (L0 + 16 * pb + r < a.NL) ? L0 + 16 * pb + r : a.NL - 1;
+        const half_t* zr = static_cast<const half_t*>(S.st_left) + row * S.Kp2 + 8 * g;
+#pragma unroll
+        for (int kb = 0; kb < NKB2; ++kb) b[kb] = *reinterpret_cast<const half8_t*>(zr + (kb < nkb ? kb : nkb - 1) * 32);
+    };
+    half8_t bc[NKB2], bn[NKB2];
+    rows(0, bc);
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+        if (pb + 1 < NPB) rows(pb + 1, bn);   // next row block's rows, fetched ahead
+        float4_t acc[NT];
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<float4_t>();
+#pragma unroll
+        for (int kb = 0; kb < NKB2; ++kb) {
+            if (kb >= nkb) break;
+#pragma unroll
+            for (int tb = 0; tb < NT; ++tb) acc[tb] = mfma(x[kb][tb], bc[kb], acc[tb]);
+        }
+        emit(pb, acc);
+#pragma unroll
+        for (int kb = 0; kb < NKB2; ++kb) bc[kb] = bn[kb];
+    }
+}
+
 // Round the FP32 accumulators of column blocks 2 kb and 2 kb + 1 to FP16 and
 // regroup them into the A fragment of K step kb of the last product: lane
 // group g needs Z_2(L0 + r, 32 kb + 8 g .. 8 g + 7), held as four values by
@@ -1293,9 +1336,63 @@ __device__ __forceinline__ void last_store_w16(const TTArgs& a, int64_t i, int64
     }
 }
 
+// As last_store_w16 with the staged last core resident in LDS (rows of
+// pitch ldp halves): the fragments are LDS reads, which do not wait for the
+// output stores (global loads would, as loads and stores complete in order).
 template <int NKB, int NPB>
+__device__ __forceinline__ void last_store_w16l(const TTArgs& a, const half_t* Ls, int ldp, int64_t i, int64_t L0,
+                                                int r, int g, const half8_t (&zf)[NPB][NKB]) {
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    half_t* out = static_cast<half_t*>(a.out);
+    for (int cp = 0; cp < n_cb; ++cp) {
+        const half_t* lrow = Ls + (16 * cp + r) * ldp + 8 * g;
+        half8_t f[NKB];
+#pragma unroll
+        for (int s2 = 0; s2 < NKB; ++s2) f[s2] = *reinterpret_cast<const half8_t*>(lrow + 32 * s2);
+        float4_t acc[NPB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<float4_t>();
+#pragma unroll
+        for (int s2 = 0; s2 < NKB; ++s2)
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f[s2], zf[pb][s2], acc[pb]);
+        const int64_t c0 = (int64_t)cp * 16 + 4 * g;
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            const int64_t L = L0 + 16 * pb + r;
+            if (L >= a.NL) continue;
+            half_t* dst = out + (L * a.n_mid + i) * a.n_last + c0;
+            if (a.vec4 && c0 + 3 < a.n_last) {
+                typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
+                *reinterpret_cast<h4_t*>(dst) = h4_t{(half_t)acc[pb][0], (half_t)acc[pb][1], (half_t)acc[pb][2],
+                                                     (half_t)acc[pb][3]};
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (c0 + v < a.n_last) dst[v] = (half_t)acc[pb][v];
+            }
+        }
+    }
+}
+
+// LDSB: the staged last core [ncp][Kp3] is first copied into LDS at pitch
+// Kp3 + 8 halves (16-byte fragment reads of 16 rows fall on distinct banks).
+template <int NKB, int NPB, bool LDSB>
 __global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
     constexpr int NT = 2 * NKB;
+    extern __shared__ double4_t smem_v[];
+    half_t* Ls = reinterpret_cast<half_t*>(smem_v);
+    const int ldp = a.set[0].Kp3 + 8;
+    if constexpr (LDSB) {
+        typedef unsigned u4_t __attribute__((ext_vector_type(4)));
+        const u4_t* src = static_cast<const u4_t*>(a.set[0].st_last);   // rows of Kp3 / 8 chunks
+        const int cpr = a.set[0].Kp3 / 8;
+        for (int idx = threadIdx.x; idx < a.ncp * cpr; idx += 256) {
+            const int row = idx / cpr, ch = idx % cpr;
+            *reinterpret_cast<u4_t*>(Ls + row * ldp + 8 * ch) = src[idx];
+        }
+        __syncthreads();
+    }
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
@@ -1304,23 +1401,41 @@ __global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
         const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
         const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
         half8_t zf[NPB][NKB];
-#pragma unroll
-        for (int pb = 0; pb < NPB; ++pb) {
+        if (a.set[0].Kp2 <= 32 * 3) {
+            // every row block's middle product from one fetch of the G_2 fragments
             int ln = lane;
             asm volatile("" : "+v"(ln));
-            float4_t acc[NT];
-            middle_w16<NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+            middle_w16_tile<NT, 3, NPB>(a, a.set[0], i, L0, ln & 15, ln >> 4, [&](int pb, float4_t (&acc)[NT]) {
 #pragma unroll
-            for (int kb = 0; kb < NKB; ++kb) zf[pb][kb] = regroup16(acc[2 * kb], acc[2 * kb + 1]);
+                for (int kb = 0; kb < NKB; ++kb) zf[pb][kb] = regroup16(acc[2 * kb], acc[2 * kb + 1]);
+            });
+        } else {
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) {
+                int ln = lane;
+                asm volatile("" : "+v"(ln));
+                float4_t acc[NT];
+                middle_w16<NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb) zf[pb][kb] = regroup16(acc[2 * kb], acc[2 * kb + 1]);
+            }
         }
         int ln = lane;
         asm volatile("" : "+v"(ln));
-        last_store_w16<NKB, NPB>(a, i, L0, ln & 15, ln >> 4, zf);
+        if constexpr (LDSB) last_store_w16l<NKB, NPB>(a, Ls, ldp, i, L0, ln & 15, ln >> 4, zf);
+        else last_store_w16<NKB, NPB>(a, i, L0, ln & 15, ln >> 4, zf);
     }
 }
 
+// The last core goes to LDS when it fits 64 KB at the padded pitch.
 static void launch_wave16(int nkb, int npb, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
-#define LRC_TW(K, P) hipLaunchKernelGGL((k_tt_wave16<K, P>), grid, dim3(256), 0, st, a, ntiles)
+    const size_t lds = (size_t)a.ncp * (a.set[0].Kp3 + 8) * sizeof(half_t);
+    const bool in_lds = lds <= 65536;
+#define LRC_TW(K, P)                                                                                  \
+    do {                                                                                              \
+        if (in_lds) hipLaunchKernelGGL((k_tt_wave16<K, P, true>), grid, dim3(256), lds, st, a, ntiles); \
+        else hipLaunchKernelGGL((k_tt_wave16<K, P, false>), grid, dim3(256), 0, st, a, ntiles);        \
+    } while (0)
 #define LRC_TWK(K) \
     do {                                 \
         if (npb == 1) LRC_TW(K, 1);      \
