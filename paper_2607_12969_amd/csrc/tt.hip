@@ -840,6 +840,80 @@ __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_
     if (kb + 2 < nkb) step(y0, by0, kb + 2);
 }
 
+// The middle products of all NPB row blocks of a tile (FP64 or FP32) in one
+// chain: each K step multiplies the step's G_2 fragments (fetched once, for
+// every row block) with each row block's G_1 fragments, NPB NT products per
+// step; operands, clamping and masking as in middle_w.
+template <typename T, int NT, int NPB>
+__device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
+                                              typename PrecTraits<T>::accv (&acc)[NPB][NT]) {
+    using AccV = typename PrecTraits<T>::accv;
+    const T* g2 = static_cast<const T*>(S.core[0]) + i * S.rM;   // uniform
+    const uint32_t ld2 = (uint32_t)(a.n_mid * S.rM);
+    const T* zr[NPB];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+        const int64_t row = (L0 + 16 * pb + r < a.NL) ? L0 + 16 * pb + r : a.NL - 1;
+        zr[pb] = static_cast<const T*>(S.core[2]) + row * S.rL;
+    }
+    const int klast = S.rL - 1, tlast = S.rM - 1;
+    const int nkb = (S.rL + 3) / 4;
+    uint32_t tcol[NT];
+    unsigned tok = 0;
+#pragma unroll
+    for (int tb = 0; tb < NT; ++tb) {
+        const int t = 16 * tb + r;
+        tcol[tb] = (uint32_t)(t < tlast ? t : tlast);
+        tok |= (t <= tlast ? 1u : 0u) << tb;
+    }
+    auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
+    auto fetch = [&](T (&x)[NT], T (&b)[NPB], int kb) {
+        const int sk = 4 * cl(kb) + g;
+        const int sc = sk < klast ? sk : klast;
+        const uint32_t ro = (uint32_t)sc * ld2;
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) x[tb] = ld_off(g2, (ro + tcol[tb]) * (uint32_t)sizeof(T));
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) b[pb] = zr[pb][sc];
+    };
+    auto step = [&](const T (&x)[NT], const T (&b)[NPB], int kb) {
+        const bool sok = 4 * kb + g <= klast;
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) {
+            const T xa = (sok && ((tok >> tb) & 1u)) ? x[tb] : T(0);
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[pb][tb] = mfma(xa, b[pb], acc[pb][tb]);
+        }
+    };
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) acc[pb][tb] = zero_accv<AccV>();
+    T x0[NT], x1[NT], y0[NT], y1[NT], b0[NPB], b1[NPB], c0[NPB], c1[NPB];
+    fetch(x0, b0, 0);
+    fetch(x1, b1, 1);
+    fetch(y0, c0, 2);
+    fetch(y1, c1, 3);
+    int kb = 0;
+    for (; kb + 3 < nkb; kb += 4) {
+        step(x0, b0, kb);
+        fetch(x0, b0, kb + 4);
+        __builtin_amdgcn_sched_barrier(0);
+        step(x1, b1, kb + 1);
+        fetch(x1, b1, kb + 5);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y0, c0, kb + 2);
+        fetch(y0, c0, kb + 6);
+        __builtin_amdgcn_sched_barrier(0);
+        step(y1, c1, kb + 3);
+        fetch(y1, c1, kb + 7);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kb < nkb) step(x0, b0, kb);
+    if (kb + 1 < nkb) step(x1, b1, kb + 1);
+    if (kb + 2 < nkb) step(y0, c0, kb + 2);
+}
+
 // Byte offset of the last core's entry G_3(t, c) (row t clamped to the
 // rank: the matching A values, the Z_2 columns past the rank, are zero; c is
 // clamped by the caller, its outputs are discarded).
@@ -992,17 +1066,18 @@ __global__ __launch_bounds__(256) void k_tt_wave(TTArgs a, int64_t ntiles) {
         const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
         const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
         double zf[NPB][NKB];
-#pragma unroll
-        for (int pb = 0; pb < NPB; ++pb) {
+        {
             int ln = lane;
             asm volatile("" : "+v"(ln));
-            double4_t acc[NT];
-            middle_w<double, NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+            double4_t acc[NPB][NT];
+            middle_w_tile<double, NT, NPB>(a, a.set[0], i, L0, ln & 15, ln >> 4, acc);
 #pragma unroll
-            for (int tb = 0; tb < NT; ++tb)
+            for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (4 * tb + v < NKB) zf[pb][4 * tb + v] = acc[tb][v];
+                for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        if (4 * tb + v < NKB) zf[pb][4 * tb + v] = acc[pb][tb][v];
         }
         int ln = lane;
         asm volatile("" : "+v"(ln));
@@ -1128,19 +1203,20 @@ __global__ __launch_bounds__(256) void k_tt_wave32(TTArgs a, int64_t ntiles) {
         const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
         const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
         float zf[NPB][NKB];
-#pragma unroll
-        for (int pb = 0; pb < NPB; ++pb) {
+        {
             int ln = lane;
             asm volatile("" : "+v"(ln));
-            float4_t acc[NT];
-            middle_w<float, NT>(a, a.set[0], i, L0 + 16 * pb, ln & 15, ln >> 4, acc);
+            float4_t acc[NPB][NT];
+            middle_w_tile<float, NT, NPB>(a, a.set[0], i, L0, ln & 15, ln >> 4, acc);
 #pragma unroll
-            for (int tb = 0; tb < NT; ++tb) {
-                transpose_groups(acc[tb]);
+            for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (4 * tb + v < NKB) zf[pb][4 * tb + v] = acc[tb][v];
-            }
+                for (int tb = 0; tb < NT; ++tb) {
+                    transpose_groups(acc[pb][tb]);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        if (4 * tb + v < NKB) zf[pb][4 * tb + v] = acc[pb][tb][v];
+                }
         }
         int ln = lane;
         asm volatile("" : "+v"(ln));
