@@ -21,6 +21,7 @@
 // are first copied to K-contiguous, zero-padded layouts (KBs to MBs) so a
 // lane loads its 8 K values at once.
 #include <algorithm>
+#include <type_traits>
 #include <cstdio>
 #include <cstdlib>
 
@@ -803,11 +804,21 @@ __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_
 #pragma unroll
     for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<AccV>();
     T x0[NT], x1[NT], y0[NT], y1[NT];
+    T bx0, bx1 = T(0), by0 = T(0), by1 = T(0);
     af(x0, 0);
-    af(x1, 1);
-    af(y0, 2);
-    af(y1, 3);
-    T bx0 = bf(0), bx1 = bf(1), by0 = bf(2), by1 = bf(3);
+    bx0 = bf(0);
+    if (nkb > 1) {
+        af(x1, 1);
+        bx1 = bf(1);
+    }
+    if (nkb > 2) {
+        af(y0, 2);
+        by0 = bf(2);
+    }
+    if (nkb > 3) {
+        af(y1, 3);
+        by1 = bf(3);
+    }
     auto step = [&](const T (&x)[NT], T b, int kb) {
         const bool sok = 4 * kb + g <= klast;
 #pragma unroll
@@ -817,7 +828,7 @@ __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_
         }
     };
     int kb = 0;
-    for (; kb + 3 < nkb; kb += 4) {
+    for (; kb + 7 < nkb; kb += 4) {   // every refill lies inside the chain
         step(x0, bx0, kb);
         af(x0, kb + 4);
         bx0 = bf(kb + 4);
@@ -834,6 +845,25 @@ __device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_
         af(y1, kb + 7);
         by1 = bf(kb + 7);
         __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kb + 3 < nkb) {   // the last full group, refilling only what remains
+        step(x0, bx0, kb);
+        if (kb + 4 < nkb) {
+            af(x0, kb + 4);
+            bx0 = bf(kb + 4);
+        }
+        step(x1, bx1, kb + 1);
+        if (kb + 5 < nkb) {
+            af(x1, kb + 5);
+            bx1 = bf(kb + 5);
+        }
+        step(y0, by0, kb + 2);
+        if (kb + 6 < nkb) {
+            af(y0, kb + 6);
+            by0 = bf(kb + 6);
+        }
+        step(y1, by1, kb + 3);
+        kb += 4;
     }
     if (kb < nkb) step(x0, bx0, kb);
     if (kb + 1 < nkb) step(x1, bx1, kb + 1);
@@ -890,12 +920,13 @@ __device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, i
 #pragma unroll
         for (int tb = 0; tb < NT; ++tb) acc[pb][tb] = zero_accv<AccV>();
     T x0[NT], x1[NT], y0[NT], y1[NT], b0[NPB], b1[NPB], c0[NPB], c1[NPB];
+    // steps past the end are neither fetched nor computed (uniform branches)
     fetch(x0, b0, 0);
-    fetch(x1, b1, 1);
-    fetch(y0, c0, 2);
-    fetch(y1, c1, 3);
+    if (nkb > 1) fetch(x1, b1, 1);
+    if (nkb > 2) fetch(y0, c0, 2);
+    if (nkb > 3) fetch(y1, c1, 3);
     int kb = 0;
-    for (; kb + 3 < nkb; kb += 4) {
+    for (; kb + 7 < nkb; kb += 4) {   // every refill lies inside the chain
         step(x0, b0, kb);
         fetch(x0, b0, kb + 4);
         __builtin_amdgcn_sched_barrier(0);
@@ -908,6 +939,16 @@ __device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, i
         step(y1, c1, kb + 3);
         fetch(y1, c1, kb + 7);
         __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kb + 3 < nkb) {   // the last full group, refilling only what remains
+        step(x0, b0, kb);
+        if (kb + 4 < nkb) fetch(x0, b0, kb + 4);
+        step(x1, b1, kb + 1);
+        if (kb + 5 < nkb) fetch(x1, b1, kb + 5);
+        step(y0, c0, kb + 2);
+        if (kb + 6 < nkb) fetch(y0, c0, kb + 6);
+        step(y1, c1, kb + 3);
+        kb += 4;
     }
     if (kb < nkb) step(x0, b0, kb);
     if (kb + 1 < nkb) step(x1, b1, kb + 1);
@@ -967,6 +1008,9 @@ __device__ __forceinline__ void last_w(const TTArgs& a, const double* __restrict
         double4_t acc[3];
 #pragma unroll
         for (int q = 0; q < 3; ++q) acc[q] = zero_accv<double4_t>();
+        // (the last block's fetches of a next block reread its own first
+        // steps: a second copy of the unrolled block would not fit the
+        // registers of the three sets)
 #pragma unroll
         for (int s = 0; s < NKB; ++s) {
 #pragma unroll
@@ -1025,16 +1069,23 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
         double4_t acc[NPB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<double4_t>();
+        // MORE: a next block exists, whose first steps the last steps fetch
+        // (one copy of the unrolled block each way, chosen once per block)
+        auto block = [&](auto more) {
 #pragma unroll
-        for (int s = 0; s < NKB; ++s) {
-            const double f = s < D ? N[s] : R[s % D];
+            for (int s = 0; s < NKB; ++s) {
+                const double f = s < D ? N[s] : R[s % D];
 #pragma unroll
-            for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(zf[pb][s], f, acc[pb]);
-            const int k = s + D;
-            if (k < NKB) R[k % D] = ld_off(b0, last_off<double>(4 * k + gg, tl, nl, c));
-            else N[k - NKB] = ld_off(b0, last_off<double>(4 * (k - NKB) + gg, tl, nl, cn));
-            __builtin_amdgcn_sched_barrier(0);
-        }
+                for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(zf[pb][s], f, acc[pb]);
+                const int k = s + D;
+                if (k < NKB) R[k % D] = ld_off(b0, last_off<double>(4 * k + gg, tl, nl, c));
+                else if constexpr (decltype(more)::value)
+                    N[k - NKB] = ld_off(b0, last_off<double>(4 * (k - NKB) + gg, tl, nl, cn));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        if (cp + 1 < n_cb) block(std::true_type{});
+        else block(std::false_type{});
         const int64_t col = (int64_t)cp * 16 + r;
         if (col < a.n_last) {
 #pragma unroll
@@ -1161,16 +1212,23 @@ __device__ __forceinline__ void last_store_w32(const TTArgs& a, int64_t i, int64
         float4_t acc[NPB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<float4_t>();
+        // MORE: a next block exists, whose first steps the last steps fetch
+        // (one copy of the unrolled block each way, chosen once per block)
+        auto block = [&](auto more) {
 #pragma unroll
-        for (int s = 0; s < NKB; ++s) {
-            const float f = s < D ? N[s] : R[s % D];
+            for (int s = 0; s < NKB; ++s) {
+                const float f = s < D ? N[s] : R[s % D];
 #pragma unroll
-            for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f, zf[pb][s], acc[pb]);
-            const int k = s + D;
-            if (k < NKB) R[k % D] = ld_off(b0, last_off<float>(4 * k + gg, tl, nl, c));
-            else N[k - NKB] = ld_off(b0, last_off<float>(4 * (k - NKB) + gg, tl, nl, cn));
-            __builtin_amdgcn_sched_barrier(0);
-        }
+                for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f, zf[pb][s], acc[pb]);
+                const int k = s + D;
+                if (k < NKB) R[k % D] = ld_off(b0, last_off<float>(4 * k + gg, tl, nl, c));
+                else if constexpr (decltype(more)::value)
+                    N[k - NKB] = ld_off(b0, last_off<float>(4 * (k - NKB) + gg, tl, nl, cn));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        if (cp + 1 < n_cb) block(std::true_type{});
+        else block(std::false_type{});
         const int64_t c0 = (int64_t)cp * 16 + 4 * g;
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) {
