@@ -476,6 +476,72 @@ __global__ __launch_bounds__(C::NT) void k_atb_finish(
 
 enum { ABT_STORE = 0, ABT_ERR = 1 };
 
+// Output tile of k_abt rounded to T and written through LDS: the MFMA
+// layout leaves each lane with 4 elements of one row, so direct stores
+// would cover 16 rows x 32-64 bytes per instruction; staged, every lane
+// writes 16 bytes and a wave writes whole row segments of the tile
+// (BN * sizeof(T) bytes each), marked nontemporal since nothing here reads
+// Y again.  The tile goes through in bands of rows
+// (all BM rows at once when they fit the operand buffers that `stg` spans,
+// else one wave row of WTM rows per band).  Rows >= M and columns >= N are not
+// written.  vec16: Y and its pitch allow 16-byte stores.
+template <typename T, class C>
+__device__ __forceinline__ void abt_store_staged(const typename C::AccV (&acc)[C::FN][C::FM], T* stg, int tid,
+                                                 int wm, int wn, int64_t m0, int64_t n0, int64_t M, int64_t N,
+                                                 T* __restrict__ Y, int64_t ldy, int vec16) {
+    constexpr int VEC = C::VEC;
+    constexpr int LDS_ = C::BN + VEC;   // staged row pitch, 16-byte aligned
+    constexpr bool kWhole = C::BM * LDS_ <= 2 * (C::BM + C::BN) * C::LDK;
+    constexpr int RB = kWhole ? C::BM : C::WTM;   // rows per band
+    static_assert(RB * LDS_ <= 2 * (C::BM + C::BN) * C::LDK, "staging band exceeds the operand buffers");
+    static_assert(C::NT % (C::BN / VEC) == 0 && RB % (C::NT / (C::BN / VEC)) == 0, "band must split evenly");
+    constexpr int CPR = C::BN / VEC;       // 16-byte chunks per row
+    constexpr int RPP = C::NT / CPR;       // rows per pass
+    const int lane = tid & 63, r = lane & 15, g = lane >> 4;
+    typedef T vec_t __attribute__((ext_vector_type(VEC)));
+#pragma unroll
+    for (int band = 0; band < C::BM / RB; ++band) {
+        if (band > 0) __syncthreads();   // the previous band has been read
+        if (kWhole || wm == band) {
+            const int rbase = kWhole ? wm * C::WTM : 0;
+#pragma unroll
+            for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+                for (int fm = 0; fm < C::FM; ++fm) {
+                    T* d = stg + (rbase + fm * 16 + r) * LDS_ + wn * C::WTN + fn * 16;
+                    if (AccRowsContiguous<T>::value) {
+                        typedef T v4_t __attribute__((ext_vector_type(4)));
+                        v4_t w;
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[fn][fm][v]);
+                        *reinterpret_cast<v4_t*>(d + 4 * g) = w;
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) d[acc_row<T>(g, v)] = to_storage<T>(acc[fn][fm][v]);
+                    }
+                }
+        }
+        __syncthreads();
+        const int c = (tid % CPR) * VEC;
+        const int64_t nn = n0 + c;
+#pragma unroll
+        for (int p = 0; p < RB / RPP; ++p) {
+            const int row = p * RPP + tid / CPR;
+            const int64_t mm = m0 + band * RB + row;
+            if (mm >= M) break;
+            const T* srow = stg + row * LDS_ + c;
+            T* dst = Y + mm * ldy + nn;
+            if (vec16 && nn + VEC <= N) {
+                __builtin_nontemporal_store(*reinterpret_cast<const vec_t*>(srow), reinterpret_cast<vec_t*>(dst));
+            } else {
+#pragma unroll
+                for (int v = 0; v < VEC; ++v)
+                    if (nn + v < N) dst[v] = srow[v];
+            }
+        }
+    }
+}
+
 // C[m][n] = sum_k A[m][k] B[n][k]  (both sources with K contiguous).
 // One workgroup per tile, in the order of AbtOrder.
 //   ABT_STORE: Y[m][ldy] = C rounded to T.
@@ -484,11 +550,12 @@ template <typename T, class C, int MODE>
 __global__ __launch_bounds__(C::NT) void k_abt(
     const T* __restrict__ Asrc, int64_t lda, int64_t M, int64_t Ka,
     const T* __restrict__ Bsrc, int64_t ldb, int64_t N, int64_t Kb, int64_t K, int tiles_m, int tiles_n,
-    T* __restrict__ Y, int64_t ldy, int vec4,
+    T* __restrict__ Y, int64_t ldy, int vec16,
     const double* __restrict__ Aref, int64_t ldr, double* __restrict__ part) {
     using AccV = typename C::AccV;
-    __shared__ alignas(16) T As[2][C::BM * C::LDK];
-    __shared__ alignas(16) T Bs[2][C::BN * C::LDK];
+    // both operand double buffers in one array: the store epilogue reuses it
+    constexpr int kAs = C::BM * C::LDK, kBs = C::BN * C::LDK;
+    __shared__ alignas(16) T smem[2 * kAs + 2 * kBs];
     __shared__ double wsum[C::NT / 64];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -526,35 +593,16 @@ __global__ __launch_bounds__(C::NT) void k_abt(
         },
         [&](int st, int buf, int j) {
             const int64_t k0 = (int64_t)j * C::BK;
-            ta[st].stash(As[buf], ga, k0, k0 + C::BK > Ka, Ka);
-            tb[st].stash(Bs[buf], gb, k0, k0 + C::BK > Kb, Kb);
+            ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > Ka, Ka);
+            tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > Kb, Kb);
         },
-        [&](int buf) { mma_k<C>(As[buf], Bs[buf], acc, wm, wn, lane, nfm, nfn); });
+        [&](int buf) { mma_k<C>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane, nfm, nfn); });
 
     const int r = lane & 15, g = lane >> 4;
     if (MODE == ABT_STORE) {
-#pragma unroll
-        for (int fn = 0; fn < C::FN; ++fn)
-#pragma unroll
-            for (int fm = 0; fm < C::FM; ++fm) {
-                const int64_t mm = m0 + wm * C::WTM + fm * 16 + r;
-                const int64_t nb = n0 + wn * C::WTN + fn * 16;
-                if (mm >= M) continue;
-                T* dst = Y + mm * ldy + nb;
-                if (AccRowsContiguous<T>::value && vec4 && nb + 4 * g + 3 < N) {
-                    typedef T vec_t __attribute__((ext_vector_type(4)));
-                    vec_t w;
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) w[v] = to_storage<T>(acc[fn][fm][v]);
-                    *reinterpret_cast<vec_t*>(dst + 4 * g) = w;
-                } else {
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int row = acc_row<T>(g, v);
-                        if (nb + row < N) dst[row] = to_storage<T>(acc[fn][fm][v]);
-                    }
-                }
-            }
+        // pipeline2 ends on a barrier after the last MFMA step, so the
+        // operand buffers are free for staging the output tile
+        abt_store_staged<T, C>(acc, smem, tid, wm, wn, m0, n0, M, N, Y, ldy, vec16);
     } else {
         double sum = 0.0;
 #pragma unroll
@@ -975,17 +1023,17 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     KernelTimer t2(p2_mfma_label<T>(), stream);
-    const int vec4 = (b % 4 == 0) && ((reinterpret_cast<uintptr_t>(Y) % (4 * sizeof(T))) == 0);
+    const int vec16 = vec_ok<T>(Y, b) ? 1 : 0;
     const TileDims d2 = cfg_dims(PrecCode<T>::value, p.big2);
     const int tm = (int)((m + d2.bm - 1) / d2.bm), tn = (int)((b + d2.bn - 1) / d2.bn);
     const dim3 g2(xcd_grid(AbtOrder(tm, tn).total));
     if (p.big2)
         launch_abt<T, typename BigCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt, ldt,
-                                                        tm, tn, Y, b, vec4, (const double*)nullptr, (int64_t)0,
+                                                        tm, tn, Y, b, vec16, (const double*)nullptr, (int64_t)0,
                                                         (double*)nullptr);
     else
         launch_abt<T, typename SmallCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt,
-                                                          ldt, tm, tn, Y, b, vec4, (const double*)nullptr,
+                                                          ldt, tm, tn, Y, b, vec16, (const double*)nullptr,
                                                           (int64_t)0, (double*)nullptr);
     return hipGetLastError();
 }

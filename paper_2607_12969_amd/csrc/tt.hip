@@ -1093,7 +1093,9 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int64_t L = L0 + 16 * pb + g + 4 * v;
-                    if (L < a.NL) out[(L * a.n_mid + i) * a.n_last + col] = acc[pb][v];
+                    // each instruction covers whole 128-byte lines (16 lanes
+                    // of one row): written around the caches
+                    if (L < a.NL) __builtin_nontemporal_store(acc[pb][v], out + (L * a.n_mid + i) * a.n_last + col);
                 }
         }
         c = cn;
