@@ -58,6 +58,7 @@ extern "C" {
 #define LRC_EHIP (-3)       /* HIP runtime or launch error */
 #define LRC_ENOMEM (-4)     /* device workspace allocation failed */
 #define LRC_ENODEV (-5)     /* no gfx950 device is current */
+#define LRC_ENUMERIC (-6)   /* a factorization met a numerically rank-deficient matrix */
 
 /* apply kernels (regime dispatch, Sec. 4.4: the speedup depends strongly on
  * the batch size) */
@@ -211,6 +212,58 @@ typedef struct lrc_cert_result {
 } lrc_cert_result;
 
 int lrc_certify(const lrc_cert_args* args, lrc_cert_result* res);
+
+/*
+ * lrc_round -- stored values from binary64 values: y[i] = round(x[i])
+ * (Sec. 3.2 formats; Remark after Thm thm:matrix_rank_compensation: every
+ * factor entry is rounded on its own; Algorithm alg:tt_compensation,
+ * rounding step for the TT cores)
+ *   x           device, count binary64 values
+ *   y           device, count values in `prec`; must not overlap x
+ *   count       >= 0 (0: nothing is launched; x and y may then be NULL)
+ *   prec        LRC_FP32 or LRC_FP16 (LRC_FP64 copies x)
+ *   n_overflow  host, or NULL.  When given, the call waits for the result
+ *               and stores the number of finite inputs that rounded to
+ *               +-infinity.
+ * One round-to-nearest-even step from binary64 (never through binary32 on
+ * the way to binary16); subnormal results are kept; finite values from the
+ * midpoint above the largest finite value up become +-infinity; +-infinity
+ * stays; NaN becomes the quiet NaN of the same sign (payload not kept).
+ * Enqueued on the calling thread's stream; without n_overflow it returns
+ * without synchronizing.
+ * Errors: LRC_EINVAL for NULL x or y with count > 0, count < 0, an unknown
+ * prec or y overlapping x; LRC_EOVERFLOW if 8 count overflows; LRC_EHIP /
+ * LRC_ENODEV from the runtime.
+ */
+int lrc_round(const void* x, void* y, int64_t count, int prec, int64_t* n_overflow);
+
+/*
+ * lrc_tt_left_orthogonalize -- left-orthogonal gauge of FP64 TT cores, in
+ * place (Sec. 6.1; Algorithm alg:tt_compensation, gauge step)
+ *   For l = 1..d-1 the left unfolding of core l, A_l of size
+ *   (r_{l-1} n_l) x r_l, is factored A_l = Q_l R_l with Q_l^T Q_l = I and
+ *   diag(R_l) > 0; core l becomes Q_l and the left unfolding of core l+1
+ *   (r_l x n_{l+1} r_{l+1}) is replaced by R_l times itself.  The tensor
+ *   the train represents is unchanged up to rounding.
+ *   cores  host array of d device pointers to binary64 cores (ranks[l] x
+ *          dims[l] x ranks[l+1], row-major), overwritten; no two overlap
+ *   dims, ranks, d  as for lrc_tt_reconstruct, with ranks[l] <=
+ *          LRC_GAUGE_MAX_RANK and ranks[l-1] dims[l-1] >= ranks[l] for
+ *          1 <= l <= d-1
+ * Each QR is computed as CholeskyQR2 (two passes of: Gram matrix on the
+ * FP64 matrix cores, Cholesky, triangular right product), which with
+ * positive diagonals gives the same factors as a Householder QR up to
+ * rounding while the unfolding's condition number stays below about 1e7.
+ * Synchronizes the calling thread's stream before it returns.
+ * Errors: LRC_EINVAL for NULL pointers, an invalid shape, a rank above
+ * LRC_GAUGE_MAX_RANK, an unfolding with fewer rows than columns or
+ * overlapping cores; LRC_ENUMERIC when an unfolding is numerically rank
+ * deficient for this method (a Cholesky pivot at or below 2^-46 of its
+ * column's squared norm; the cores are then unspecified); LRC_EOVERFLOW,
+ * LRC_ENOMEM, LRC_EHIP, LRC_ENODEV as elsewhere.
+ */
+#define LRC_GAUGE_MAX_RANK 96
+int lrc_tt_left_orthogonalize(void* const* cores, const int64_t* dims, const int64_t* ranks, int d);
 
 /* Stored bytes of rank-k factors in `prec`: (b/8) k (m+n+1)  (Sec. 4.2).
  * Returns LRC_EINVAL for bad arguments or LRC_EOVERFLOW on overflow. */

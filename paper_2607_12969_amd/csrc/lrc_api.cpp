@@ -330,6 +330,96 @@ int lrc_tt_reconstruct(const void* const* cores, const int64_t* dims, const int6
     return tt_reconstruct_impl(cores, dims, ranks, d, out, prec);
 }
 
+int lrc_round(const void* x, void* y, int64_t count, int prec, int64_t* n_overflow) {
+    if (count > 0 && (!x || !y)) return fail(LRC_EINVAL, "NULL array argument");
+    if (!valid_prec(prec)) return fail(LRC_EINVAL, "unknown precision code %d", prec);
+    if (count < 0) return fail(LRC_EINVAL, "count = %lld < 0", (long long)count);
+    int64_t nx;
+    if (!mul_ok(count, 8, &nx)) return fail(LRC_EOVERFLOW, "byte count overflows");
+    const size_t ny = (size_t)count * elem_bytes(prec);
+    if (count > 0 && overlaps(y, ny, x, (size_t)nx)) return fail(LRC_EINVAL, "output y overlaps the input x");
+    int dev;
+    int rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    if (count == 0) {
+        if (n_overflow) *n_overflow = 0;
+        return LRC_OK;
+    }
+    if (prec == LRC_FP64) {
+        hipError_t e = hipMemcpyAsync(y, x, (size_t)nx, hipMemcpyDeviceToDevice, st);
+        if (e != hipSuccess) return fail_hip(e, "copy");
+        if (n_overflow) *n_overflow = 0;
+        return LRC_OK;
+    }
+    unsigned long long* ovf = nullptr;
+    Workspace* ws = nullptr;
+    if (n_overflow) {
+        ws = &workspace_for(dev, st);
+        ws->reset();
+        hipError_t e = ws->reserve(256, st);
+        if (e != hipSuccess) return fail_hip(e, "workspace");
+        ovf = static_cast<unsigned long long*>(ws->take(sizeof(unsigned long long)));
+    }
+    hipError_t e = launch_round(static_cast<const double*>(x), y, count, prec, ovf, st);
+    if (e != hipSuccess) return fail_hip(e, "rounding launch");
+    if (n_overflow) {
+        unsigned long long host = 0;
+        e = hipMemcpyAsync(&host, ovf, sizeof(host), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return fail_hip(e, "overflow count");
+        *n_overflow = (int64_t)host;
+    }
+    return LRC_OK;
+}
+
+int lrc_tt_left_orthogonalize(void* const* cores, const int64_t* dims, const int64_t* ranks, int d) {
+    if (!cores) return fail(LRC_EINVAL, "NULL array argument");
+    int64_t N;
+    int rc = check_tt_shape(dims, ranks, d, &N);
+    if (rc) return rc;
+    std::vector<size_t> bytes(d);
+    for (int l = 0; l < d; ++l) {
+        if (!cores[l]) return fail(LRC_EINVAL, "cores[%d] is NULL", l);
+        bytes[l] = (size_t)ranks[l] * dims[l] * ranks[l + 1] * 8;
+        for (int q = 0; q < l; ++q)
+            if (overlaps(cores[l], bytes[l], cores[q], bytes[q]))
+                return fail(LRC_EINVAL, "cores[%d] overlaps cores[%d]", l, q);
+    }
+    for (int l = 0; l + 1 < d; ++l) {
+        if (ranks[l + 1] > LRC_GAUGE_MAX_RANK)
+            return fail(LRC_EINVAL, "ranks[%d] = %lld above the gauge's limit %d", l + 1, (long long)ranks[l + 1],
+                        LRC_GAUGE_MAX_RANK);
+        if (ranks[l] * dims[l] < ranks[l + 1])
+            return fail(LRC_EINVAL, "unfolding of core %d has %lld rows for rank %lld", l,
+                        (long long)(ranks[l] * dims[l]), (long long)ranks[l + 1]);
+    }
+    if (d == 1) return LRC_OK;
+    int dev;
+    rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t e = ws.reserve(gauge_workspace_bytes(dims, ranks, d), st);
+    if (e != hipSuccess) return fail_hip(e, "workspace");
+    int* flags = static_cast<int*>(ws.take(sizeof(int) * (size_t)d));
+    std::vector<double*> cs(d);
+    for (int l = 0; l < d; ++l) cs[l] = static_cast<double*>(cores[l]);
+    e = launch_gauge(cs.data(), dims, ranks, d, flags, ws, st);
+    if (e != hipSuccess) return fail_hip(e, "gauge launch");
+    std::vector<int> hf(d, 0);
+    e = hipMemcpyAsync(hf.data(), flags, sizeof(int) * (size_t)d, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail_hip(e, "gauge status");
+    for (int l = 0; l + 1 < d; ++l)
+        if (hf[l])
+            return fail(LRC_ENUMERIC,
+                        "unfolding of core %d is numerically rank deficient (Cholesky pivot %d of its Gram matrix)",
+                        l, hf[l] - 1);
+    return LRC_OK;
+}
+
 int64_t lrc_storage_bytes(int64_t m, int64_t n, int64_t k, int prec) {
     if (!valid_prec(prec) || m < 1 || n < 1 || k < 0) return fail(LRC_EINVAL, "bad storage arguments");
     int64_t s, t;

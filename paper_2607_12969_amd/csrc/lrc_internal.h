@@ -69,6 +69,19 @@ hipError_t launch_apply(const ApplyPlan& p, const void* U, const void* s, const 
                         const void* X, void* Y, int64_t m, int64_t n, int64_t k, int64_t b,
                         int prec, Workspace& ws, hipStream_t stream);
 
+// ------------------------------------------------------------ quantization
+// y[i] = x[i] rounded from binary64 to prec (P32 / P16) with one
+// round-to-nearest-even step; finite inputs that overflow are counted into
+// *ovf (zeroed first) when ovf is not null.
+hipError_t launch_round(const double* x, void* y, int64_t n, int prec, unsigned long long* ovf,
+                        hipStream_t stream);
+
+// Left-orthogonal gauge of FP64 cores in place (CholeskyQR2 per unfolding);
+// flags[l] becomes 1 + pivot when the QR of unfolding l broke down.
+size_t gauge_workspace_bytes(const int64_t* dims, const int64_t* ranks, int d);
+hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t* ranks, int d, int* flags,
+                        Workspace& ws, hipStream_t stream);
+
 // ------------------------------------------------------- certificate (matrix)
 // G = P^T P for P (rows x cols, row-major, FP64): a split-sum Gram product.
 size_t gram_workspace_bytes(int64_t rows, int64_t cols);

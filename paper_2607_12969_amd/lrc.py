@@ -23,7 +23,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "lrc.h")
 FP64, FP32, FP16 = 0, 1, 2
 PATH_AUTO, PATH_STREAM, PATH_MFMA = 0, 1, 2
 CERT_MATRIX, CERT_TT = 0, 1
-ERRORS = {-1: "EINVAL", -2: "EOVERFLOW", -3: "EHIP", -4: "ENOMEM", -5: "ENODEV"}
+ERRORS = {-1: "EINVAL", -2: "EOVERFLOW", -3: "EHIP", -4: "ENOMEM", -5: "ENODEV", -6: "ENUMERIC"}
 PREC_NAMES = {"fp64": FP64, "fp32": FP32, "fp16": FP16}
 
 
@@ -87,6 +87,11 @@ def lib():
     L.lrc_tt_reconstruct.restype = ctypes.c_int
     L.lrc_certify.argtypes = [ctypes.POINTER(CertArgs), ctypes.POINTER(CertResult)]
     L.lrc_certify.restype = ctypes.c_int
+    L.lrc_round.argtypes = [_vp, _vp, _i64, ctypes.c_int, ctypes.POINTER(_i64)]
+    L.lrc_round.restype = ctypes.c_int
+    L.lrc_tt_left_orthogonalize.argtypes = [ctypes.POINTER(_vp), ctypes.POINTER(_i64), ctypes.POINTER(_i64),
+                                            ctypes.c_int]
+    L.lrc_tt_left_orthogonalize.restype = ctypes.c_int
     L.lrc_storage_bytes.argtypes = [_i64, _i64, _i64, ctypes.c_int]
     L.lrc_storage_bytes.restype = _i64
     L.lrc_tt_storage_bytes.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.c_int, ctypes.c_int]
@@ -215,6 +220,46 @@ def tt_reconstruct(cores, out=None):
     _bind_stream(cores[0].device)
     _check(lib().lrc_tt_reconstruct(ptrs, D, R, d, out.data_ptr(), prec))
     return out
+
+
+def round_to(x, prec, out=None, count_overflow: bool = False):
+    """Stored values of a float64 tensor: one round-to-nearest-even step to
+    `prec` ("fp32" / "fp16", or a torch dtype).  Returns the rounded tensor,
+    and with count_overflow=True also the number of finite values that
+    became infinite (this waits for the result)."""
+    import torch
+    _dev(x)
+    if x.dtype != torch.float64:
+        raise TypeError("x must be float64")
+    dt = {"fp64": torch.float64, "fp32": torch.float32, "fp16": torch.float16}.get(prec, prec)
+    p = {torch.float64: FP64, torch.float32: FP32, torch.float16: FP16}[dt]
+    if out is None:
+        out = torch.empty(x.shape, dtype=dt, device=x.device)
+    _dev(out)
+    if out.dtype != dt or out.numel() != x.numel():
+        raise ValueError("out must have the target dtype and x's size")
+    _bind_stream(x.device)
+    n = _i64(0)
+    _check(lib().lrc_round(x.data_ptr(), out.data_ptr(), x.numel(), p, ctypes.byref(n) if count_overflow else None))
+    return (out, int(n.value)) if count_overflow else out
+
+
+def tt_left_orthogonalize(cores):
+    """Left-orthogonal gauge of float64 TT cores (r_{l-1}, n_l, r_l), in
+    place; returns the same list."""
+    import torch
+    _dev(*cores)
+    for c in cores:
+        if c.dtype != torch.float64:
+            raise TypeError("the gauge takes float64 cores")
+    dims, ranks = tt_shape(cores)
+    d = len(cores)
+    ptrs = (_vp * d)(*[c.data_ptr() for c in cores])
+    D = (_i64 * d)(*dims)
+    R = (_i64 * (d + 1))(*ranks)
+    _bind_stream(cores[0].device)
+    _check(lib().lrc_tt_left_orthogonalize(ptrs, D, R, d))
+    return cores
 
 
 def _result(res: CertResult) -> dict:

@@ -129,3 +129,34 @@ def test_valid_call_without_gpu_reports_no_device():
         pass
     good = [0x10000, 0x20000, 0x30000, 0x40000, 0x90000000]
     assert _apply(good, 10, 10, 3, 4, 0) == -5
+
+
+def test_round_argument_errors():
+    n = ctypes.c_int64(0)
+    assert L.lrc_round(None, 0x20000, 8, 1, None) == -1                  # NULL x
+    assert L.lrc_round(0x10000, None, 8, 1, None) == -1                  # NULL y
+    assert L.lrc_round(0x10000, 0x20000, -1, 1, None) == -1              # count < 0
+    assert L.lrc_round(0x10000, 0x20000, 8, 7, None) == -1               # bad precision
+    assert L.lrc_round(0x10000, 0x10010, 8, 2, ctypes.byref(n)) == -1    # y overlaps x
+    assert L.lrc_round(0x10000, 0x20000, 2 ** 61, 2, None) == -2         # byte count overflow
+
+
+def _gauge(dims, ranks, d, cores=None):
+    D = (ctypes.c_int64 * max(1, len(dims)))(*dims)
+    R = (ctypes.c_int64 * max(1, len(ranks)))(*ranks)
+    if cores is None:
+        cores = [0x1000000 * (i + 1) for i in range(max(1, d))]
+    P = (ctypes.c_void_p * len(cores))(*cores)
+    return L.lrc_tt_left_orthogonalize(P, D, R, d)
+
+
+def test_gauge_argument_errors():
+    assert _gauge((4, 5), (1, 3, 1), 0) == -1                 # d < 1
+    assert _gauge((4, 5), (2, 3, 1), 2) == -1                 # ranks[0] != 1
+    assert _gauge((4, 5), (1, 3, 1), 2, cores=[0x1000000, 0]) == -1
+    assert _gauge((200, 200), (1, 97, 1), 2) == -1            # rank above the gauge's limit
+    assert _gauge((4, 3, 60), (1, 3, 13, 1), 3) == -1         # core 1: 3 * 3 = 9 rows < 13 columns
+    assert b"rows" in L.lrc_last_error()
+    assert _gauge((4, 5), (1, 3, 1), 2, cores=[0x1000000, 0x1000008]) == -1   # cores overlap
+    assert b"overlaps" in L.lrc_last_error()
+    assert _gauge((2 ** 40, 2 ** 40), (1, 3, 1), 2) == -2     # entry count overflow
