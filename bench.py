@@ -17,6 +17,7 @@ same apply and TT work.
 
   python bench.py [--steps K] [--warmup W] [--k 256] [--no-cpu-baseline]
   python bench.py --sweep FILE      per-kernel table over the workload grid
+  python bench.py --quant FILE      device rounding and TT gauge cells
 """
 from __future__ import annotations
 
@@ -262,6 +263,28 @@ def measured_traffic(label):
     return val
 
 
+def round_counts(count, e):
+    """Rounding of `count` binary64 values to e-byte storage: no flops to
+    speak of; 8 bytes read and e written per value."""
+    return 0.0, float(count * (8 + e))
+
+
+def gauge_counts(dims, ranks):
+    """Left-orthogonal gauge by CholeskyQR2, per unfolding l < d (m = r_{l-1}
+    n_l rows, r = r_l columns, c = n_{l+1} r_{l+1} columns of the next
+    core): two Gram products counted in full (2 m r^2 each), two triangular
+    right products (m r^2 each), one triangular left product (r^2 c).
+    Bytes: every core read and written once as Q, the next core read and
+    written once for the R product."""
+    f = by = 0.0
+    for l in range(len(dims) - 1):
+        m, r = ranks[l] * dims[l], ranks[l + 1]
+        c = dims[l + 1] * ranks[l + 2]
+        f += 4.0 * m * r * r + 2.0 * m * r * r + 1.0 * r * r * c
+        by += 8.0 * (2 * m * r + 2 * r * c)
+    return f, by
+
+
 # ----------------------------------------------------------------- sweep ---
 
 def _time_cell(lrc, fn, reps, labels):
@@ -360,6 +383,51 @@ def sweep(path, dev, lrc):
         fh.write("\n".join(rows) + "\n")
 
 
+def quant_sweep(path, dev, lrc):
+    """Device rounding of the stored factors / cores and the FP64 gauge of
+    the TT workloads, each against its own bound (kernel time from the
+    library's event timers; the gauge's calls synchronize, so its wall time
+    is the call's)."""
+    import torch
+    from paper_2607_12969_amd import synth
+    rows = ["| cell | prec | GFLOP | MB | flop/B | bound | t* us | kernels us | call us | GFLOP/s | GB/s | "
+            "frac of bound | per kernel (us) |", "|" + "---|" * 13]
+    rng = np.random.default_rng([12969, 98])
+    for name, (m, n, k) in (("factors 8192x8192 k=257", (8192, 8192, 257)),
+                            ("factors 65536x4096 k=513", (65536, 4096, 513))):
+        host = [rng.standard_normal((m, k)), rng.standard_normal((n, k))]
+        for p, dt in (("f32", torch.float32), ("f16", torch.float16)):
+            f, by = round_counts(sum(a.size for a in host), EBYTES[p])
+            copies = max(1, min(4, math.ceil(512e6 / by)))
+            sets = [([torch.from_numpy(a).to(dev) for a in host],
+                     [torch.empty(a.shape, dtype=dt, device=dev) for a in host]) for _ in range(copies)]
+
+            def call(r):
+                xs, ys = sets[r % copies]
+                for x, y in zip(xs, ys):
+                    lrc.round_to(x, p.replace("f", "fp"), out=y)
+            wall, km = _time_cell(lrc, call, 50, None)
+            km = {k2: v * 2 for k2, v in km.items()}   # two launches (U and V) per call
+            rows.append(_row(f"round {name}", p, km, wall, max(f, 1.0), by).replace(
+                f"| {p} | 0.000 |", f"| {p} | 0 |"))
+            log(rows[-1])
+            del sets
+            torch.cuda.empty_cache()
+    for name, dims, ranks in (("256^3 r(15,15)", (256, 256, 256), (1, 15, 15, 1)),
+                              ("256^3 r(25,25)", (256, 256, 256), (1, 25, 25, 1)),
+                              ("16^6 r(9,17,25,17,9)", (16,) * 6, (1, 9, 17, 25, 17, 9, 1)),
+                              ("512x512x224 r(33,33)", (512, 512, 224), (1, 33, 33, 1)),
+                              ("512x512x224 r(65,65)", (512, 512, 224), (1, 65, 65, 1))):
+        cores = [torch.from_numpy(c).to(dev) for c in synth.random_tt_cores(dims, ranks, tag=2)]
+        f, by = gauge_counts(dims, ranks)
+        wall, km = _time_cell(lrc, lambda r: lrc.tt_left_orthogonalize(cores), 10, None)
+        km = {"gauge_qr_f64": km["gauge_qr_f64"] * (len(dims) - 1)}   # one timed span per unfolding
+        rows.append(_row(f"gauge {name}", "f64", km, wall, f, by))
+        log(rows[-1])
+    with open(path, "w") as fh:
+        fh.write("\n".join(rows) + "\n")
+
+
 # ------------------------------------------------------------------ main ---
 
 def main():
@@ -371,6 +439,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-certs", action="store_true", help="leave the certificates out of the step")
     ap.add_argument("--sweep", default=None, help="write a per-kernel table over the workload grid")
+    ap.add_argument("--quant", default=None, help="write the device rounding and TT gauge cells")
     ap.add_argument("--copy-calibration", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -395,6 +464,9 @@ def main():
 
     if args.sweep:
         sweep(args.sweep, dev, lrc)
+        return
+    if args.quant:
+        quant_sweep(args.quant, dev, lrc)
         return
 
     wl = Workload(args.k, dev)

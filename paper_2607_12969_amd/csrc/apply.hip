@@ -1065,7 +1065,10 @@ static void gram_plan(int64_t rows, int64_t cols, int* tiles, int* splits, int64
     const int t = (int)((cols + GramC::BM - 1) / GramC::BM);
     const int64_t base = (int64_t)t * t;
     int64_t sp = (1536 + base - 1) / base;
-    int64_t mx = rows / 64;
+    // at least 64 rows per split, 256 for Grams of at most 2 x 2 tiles
+    // (those would otherwise spend more on their partial tiles than on the
+    // product)
+    int64_t mx = rows / (base <= 4 ? 256 : 64);
     if (mx < 1) mx = 1;
     if (sp > mx) sp = mx;
     if (sp < 1) sp = 1;

@@ -16,10 +16,11 @@
 //
 // Work per unfolding (m rows, r columns): two Gram products on the FP64
 // matrix cores (launch_gram: 2 m r^2 flop each, half of it computed), two
-// row products with a triangular r x r matrix (m r^2 flop each), and the
-// product R G_{l+1} (2 r^2 n_{l+1} r_{l+1} flop).  All of it is small next
-// to the reconstruction; the kernels are plain FP64 vector code except the
-// Gram.
+// triangular solves x R = a per row (forward substitution, m r^2 flop
+// each; no inverse is formed), and R G_{l+1} applied as R_2 (R_1 G_{l+1})
+// (two triangular products, r^2 n_{l+1} r_{l+1} flop each).  All of it is
+// small next to the reconstruction; the kernels are plain FP64 vector code
+// except the Gram.
 #include <hip/hip_runtime.h>
 
 #include "../../include/lrc.h"
@@ -40,134 +41,227 @@ __global__ __launch_bounds__(256) void k_gauge_pad(const double* __restrict__ sr
 }
 
 // One workgroup.  G (r x r inside pitch ld, symmetric, upper triangle used)
-// = R^T R with R upper triangular, diag(R) > 0 (right-looking Cholesky in
-// LDS).  Writes R and its inverse Rinv (both upper, zero below the diagonal
-// and in the pad columns up to ld) and, when Rprev is given, Rout = R Rprev.
-// flag: set to 1 + (pivot index) when a pivot is not above 2^-46 of the
-// column's original diagonal (or not a number); the outputs are then
-// unspecified.
+// = R^T R with R upper triangular, diag(R) > 0: right-looking Cholesky in
+// LDS with one barrier per pivot (the trailing update uses the unscaled
+// pivot row, S[i][j] -= S[k][i] S[k][j] / S[k][k], while row k of R goes to
+// a matrix of its own).  R is written with pitch ld, zero below the diagonal and in
+// the pad rows and columns.  flag: set to 1 + (pivot index) when a pivot is
+// not above 2^-46 of the column's original diagonal (or not a number); R is
+// then unspecified.
 constexpr int kGaugeMaxRank = LRC_GAUGE_MAX_RANK;
+constexpr int kFillPerThread = (kGaugeMaxRank * kGaugeMaxRank + 255) / 256;
+
+// S[i][j] = M[i][j] (pitch ld) for j >= i, 0 below the diagonal, i, j < r,
+// by 256 threads: every thread issues all its global loads before it
+// writes LDS, so their latencies overlap.
+template <int LDP>
+__device__ __forceinline__ void fill_upper(double (*S)[LDP], const double* __restrict__ M, int r, int ld,
+                                           int tid) {
+    double v[kFillPerThread];
+#pragma unroll
+    for (int q = 0; q < kFillPerThread; ++q) {
+        const int idx = tid + q * 256;
+        const int i = idx / r, j = idx - i * r;
+        v[q] = (idx < r * r && j >= i) ? M[(int64_t)i * ld + j] : 0.0;
+    }
+#pragma unroll
+    for (int q = 0; q < kFillPerThread; ++q) {
+        const int idx = tid + q * 256;
+        const int i = idx / r, j = idx - i * r;
+        if (idx < r * r) S[i][j] = v[q];
+    }
+}
+
 __global__ __launch_bounds__(256) void k_gauge_chol(const double* __restrict__ G, int r, int ld,
-                                                    double* __restrict__ R, double* __restrict__ Rinv,
-                                                    const double* __restrict__ Rprev, double* __restrict__ Rout,
-                                                    int* __restrict__ flag) {
+                                                    double* __restrict__ R, int* __restrict__ flag) {
     __shared__ double S[kGaugeMaxRank][kGaugeMaxRank + 1];
+    __shared__ double Rm[kGaugeMaxRank][kGaugeMaxRank + 1];   // R, written out at the end
     __shared__ double diag0[kGaugeMaxRank];
     __shared__ int bad;
-    const int tid = threadIdx.x;
-    for (int idx = tid; idx < r * r; idx += 256) {
-        const int i = idx / r, j = idx - i * r;
-        S[i][j] = j >= i ? G[(int64_t)i * ld + j] : 0.0;
-    }
+    constexpr int kBlk = (kGaugeMaxRank + 15) / 16;
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    fill_upper(S, G, r, ld, tid);
     if (tid == 0) bad = 0;
     __syncthreads();
     for (int i = tid; i < r; i += 256) diag0[i] = S[i][i];
     __syncthreads();
     for (int k = 0; k < r; ++k) {
-        if (tid == 0) {
-            const double d = S[k][k];
-            // a pivot that is not positive relative to its column (NaN fails too)
-            if (!(d > 0x1p-46 * diag0[k]) && bad == 0) bad = 1 + k;
-            S[k][k] = __builtin_sqrt(d > 0.0 ? d : 0.0);
+        const double d = S[k][k];
+        const double dk = d > 0.0 ? d : 0.0;
+        const double sq = __builtin_sqrt(dk), inv = 1.0 / dk;
+        if (tid == 0 && !(d > 0x1p-46 * diag0[k]) && bad == 0) bad = 1 + k;
+        // row k of R (row k of S is not written in this step); global
+        // stores here would make every barrier wait for them
+        for (int j = k + tid; j < r; j += 256) Rm[k][j] = j == k ? sq : S[k][j] / sq;
+        // trailing update of the upper triangle, k < i <= j: thread (ty, tx)
+        // of a 16 x 16 grid takes rows ty + 16 a and columns tx + 16 b;
+        // each row's reads are issued together before its writes
+        double rk[kBlk];
+#pragma unroll
+        for (int b = 0; b < kBlk; ++b) {
+            const int j = b * 16 + tx;
+            rk[b] = (j > k && j < r) ? S[k][j] : 0.0;
         }
-        __syncthreads();
-        const double rkk = S[k][k];
-        for (int j = k + 1 + tid; j < r; j += 256) S[k][j] = S[k][j] / rkk;
-        __syncthreads();
-        // trailing update of the upper triangle: S[i][j] -= R[k][i] R[k][j], k < i <= j
-        const int t = r - k - 1;
-        for (int idx = tid; idx < t * t; idx += 256) {
-            const int i = k + 1 + idx / t, j = k + 1 + idx % t;
-            if (j >= i) S[i][j] -= S[k][i] * S[k][j];
+#pragma unroll
+        for (int a = 0; a < kBlk; ++a) {
+            const int i = a * 16 + ty;
+            if (i > k && i < r) {
+                const double ski = S[k][i] * inv;
+                double cur[kBlk];
+#pragma unroll
+                for (int b = 0; b < kBlk; ++b) {
+                    const int j = b * 16 + tx;
+                    cur[b] = (j >= i && j < r) ? S[i][j] : 0.0;
+                }
+#pragma unroll
+                for (int b = 0; b < kBlk; ++b) {
+                    const int j = b * 16 + tx;
+                    if (j >= i && j < r) S[i][j] = cur[b] - ski * rk[b];
+                }
+            }
         }
         __syncthreads();
     }
     if (tid == 0 && bad) *flag = bad;
-    for (int idx = tid; idx < r * ld; idx += 256) {
+    for (int idx = tid; idx < ld * ld; idx += 256) {
         const int i = idx / ld, j = idx - i * ld;
-        R[(int64_t)i * ld + j] = (j < r && j >= i) ? S[i][j] : 0.0;
-    }
-    // Rinv column j by back substitution (thread j); entries below the
-    // diagonal and in the pad are zero
-    for (int j = tid; j < ld; j += 256) {
-        for (int i = ld - 1; i >= 0; --i) {
-            double v = 0.0;
-            if (j < r && i <= j) {
-                double acc = (i == j) ? 1.0 : 0.0;
-                for (int q = i + 1; q <= j; ++q) acc -= S[i][q] * Rinv[(int64_t)q * ld + j];
-                v = acc / S[i][i];
-            }
-            Rinv[(int64_t)i * ld + j] = v;
-        }
-    }
-    if (Rprev) {
-        __syncthreads();
-        // Rout = R Rprev, both upper triangular
-        for (int idx = tid; idx < r * ld; idx += 256) {
-            const int i = idx / ld, j = idx - i * ld;
-            double acc = 0.0;
-            if (j < r && j >= i)
-                for (int q = i; q <= j; ++q) acc += S[i][q] * Rprev[(int64_t)q * ld + j];
-            Rout[(int64_t)i * ld + j] = acc;
-        }
+        R[idx] = (i < r && j < r && j >= i) ? Rm[i][j] : 0.0;
     }
 }
 
-// C[i][j] = sum_{t <= j} A[i][t] B[t][j] for j < r (B upper triangular,
-// pitch ldb); C has pitch ldc, and pad columns r <= j < ldc are zeroed.
-// One wave per row, lane j (and j + 64) per output column; lane t holds
-// A[i][t] (and A[i][t + 64]) and hands it to the wave by a lane shuffle, so
-// B's rows are read coalesced and A once.
-__global__ __launch_bounds__(256) void k_gauge_rmul(const double* __restrict__ A, int64_t rows, int r, int lda,
-                                                    const double* __restrict__ B, int ldb,
+__device__ __forceinline__ double lane_value(double v, int lane) {
+    const long long b = __builtin_bit_cast(long long, v);
+    const int lo = __builtin_amdgcn_readlane((int)(b & 0xFFFFFFFFll), lane);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
+    return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned int)lo);
+}
+
+// C = A R^{-1} row by row (R upper triangular r x r with pitch ldr, A with
+// pitch lda, C with pitch ldc whose pad columns r <= j < ldc are zeroed):
+// forward substitution x R = a, x_t = a'_t / R[t][t], a'_j -= x_t R[t][j].
+// One wave per group of kTrsmRows rows; lane j keeps a'_j (and, for TWO,
+// that is r > 64, a'_{j+64}); the pivot value a'_t reaches the wave through
+// a uniform readlane, and R sits in LDS, its next row read one step ahead.
+// Lanes at or past r work on values that are never stored (R's entries
+// there are not initialized), so the loop needs no masks.
+constexpr int kTrsmRows = 4;
+template <bool TWO>
+__global__ __launch_bounds__(256) void k_gauge_trsm(const double* __restrict__ A, int64_t rows, int r, int lda,
+                                                    const double* __restrict__ R, int ldr,
                                                     double* __restrict__ C, int ldc) {
+    // one spare row and column: the prefetch of row t + 1 and the lanes
+    // j + 64 < 128 stay inside the array
+    __shared__ double Rs[kGaugeMaxRank + 1][kGaugeMaxRank + 1];
+    __shared__ double inv[kGaugeMaxRank + 1];
+    fill_upper(Rs, R, r, ldr, threadIdx.x);
+    __syncthreads();
+    for (int t = threadIdx.x; t < r; t += 256) inv[t] = 1.0 / Rs[t][t];
+    __syncthreads();
     const int lane = threadIdx.x & 63;
-    const int64_t w0 = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int64_t ws = (int64_t)gridDim.x * 4;
-    for (int64_t i = w0; i < rows; i += ws) {
-        const double* a = A + i * lda;
-        const double a0 = lane < r ? a[lane] : 0.0;
-        const double a1 = lane + 64 < r ? a[lane + 64] : 0.0;
-        double c0 = 0.0, c1 = 0.0;
-        for (int t = 0; t < r; ++t) {
-            const double at = t < 64 ? __shfl(a0, t, 64) : __shfl(a1, t - 64, 64);
-            const double* b = B + (int64_t)t * ldb;
-            if (lane < r && t <= lane) c0 += at * b[lane];
-            if (lane + 64 < r && t <= lane + 64) c1 += at * b[lane + 64];
+    const bool l0 = lane < r, l1 = lane + 64 < r;
+    const int c1 = lane + 64 < kGaugeMaxRank + 1 ? lane + 64 : 0;   // column of a'_{j+64} (clamped)
+    const int r0 = r < 64 ? r : 64;
+    const int64_t w0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kTrsmRows;
+    const int64_t ws = (int64_t)gridDim.x * 4 * kTrsmRows;
+    for (int64_t i0 = w0; i0 < rows; i0 += ws) {
+        double a0[kTrsmRows], a1[kTrsmRows], x0[kTrsmRows], x1[kTrsmRows];
+#pragma unroll
+        for (int u = 0; u < kTrsmRows; ++u) {
+            const int64_t i = i0 + u < rows ? i0 + u : rows - 1;
+            const double* a = A + i * lda;
+            a0[u] = l0 ? a[lane] : 0.0;
+            a1[u] = (TWO && l1) ? a[lane + 64] : 0.0;
+            x0[u] = x1[u] = 0.0;
         }
-        double* c = C + i * ldc;
-        if (lane < ldc) c[lane] = lane < r ? c0 : 0.0;
-        if (lane + 64 < ldc) c[lane + 64] = lane + 64 < r ? c1 : 0.0;
+        double rt0 = Rs[0][lane], rt1 = TWO ? Rs[0][c1] : 0.0, it = inv[0];
+        for (int t = 0; t < r0; ++t) {
+            const double n0 = Rs[t + 1][lane];
+            const double n1 = TWO ? Rs[t + 1][c1] : 0.0;
+            const double nit = inv[t + 1];
+#pragma unroll
+            for (int u = 0; u < kTrsmRows; ++u) {
+                const double xt = lane_value(a0[u], t) * it;
+                x0[u] = lane == t ? xt : x0[u];
+                a0[u] -= xt * rt0;
+                if (TWO) a1[u] -= xt * rt1;
+            }
+            rt0 = n0;
+            rt1 = n1;
+            it = nit;
+        }
+        if (TWO) {
+            rt1 = Rs[64][c1];
+            it = inv[64];
+            for (int t = 64; t < r; ++t) {
+                const double n1 = Rs[t + 1][c1];
+                const double nit = inv[t + 1];
+#pragma unroll
+                for (int u = 0; u < kTrsmRows; ++u) {
+                    const double xt = lane_value(a1[u], t - 64) * it;
+                    x1[u] = lane + 64 == t ? xt : x1[u];
+                    a1[u] -= xt * rt1;
+                }
+                rt1 = n1;
+                it = nit;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kTrsmRows; ++u) {
+            if (i0 + u >= rows) break;
+            double* c = C + (i0 + u) * ldc;
+            if (lane < ldc) c[lane] = l0 ? x0[u] : 0.0;
+            if (lane + 64 < ldc) c[lane + 64] = l1 ? x1[u] : 0.0;
+        }
     }
 }
 
 // C[i][c] = sum_{t >= i} R[i][t] X[t][c] for i < r, c < ncols (R upper
-// triangular with pitch ldr, X and C r x ncols dense).  One thread per
-// column c: the column of X is read once (coalesced across threads) into
-// registers in chunks of 32 rows, and R is read at uniform addresses.
+// triangular with pitch ldr, X and C r x ncols dense).  Workgroup (x, y)
+// takes columns 256 x .. 256 x + 255 (one per thread, read coalesced) and
+// output rows 32 y .. 32 y + 31, whose rows of R it keeps in LDS (zero
+// below the diagonal, so the loop has no masks).
+constexpr int kLmulRows = 32;
 __global__ __launch_bounds__(256) void k_gauge_lmul(const double* __restrict__ R, int r, int ldr,
                                                     const double* __restrict__ X, int64_t ncols,
                                                     double* __restrict__ C) {
+    __shared__ double Rs[LRC_GAUGE_MAX_RANK][kLmulRows];   // Rs[t][u] = R[i0 + u][t]
+    const int i0 = blockIdx.y * kLmulRows;
+    // all loads first, then the LDS writes (their latencies overlap)
+    constexpr int kPer = LRC_GAUGE_MAX_RANK * kLmulRows / 256;
+    double v[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int idx = threadIdx.x + q * 256;
+        const int t = idx / kLmulRows, i = i0 + idx % kLmulRows;
+        v[q] = (t < r && i < r && t >= i) ? R[(int64_t)i * ldr + t] : 0.0;
+    }
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int idx = threadIdx.x + q * 256;
+        Rs[idx / kLmulRows][idx % kLmulRows] = v[q];
+    }
+    __syncthreads();
     const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (c >= ncols) return;
-    for (int i0 = 0; i0 < r; i0 += 32) {
-        double acc[32];
+    double acc[kLmulRows];
 #pragma unroll
-        for (int u = 0; u < 32; ++u) acc[u] = 0.0;
-        // rows t >= i0 contribute to outputs i0 .. i0 + 31
-        for (int t = i0; t < r; ++t) {
-            const double x = X[(int64_t)t * ncols + c];
-            const double* rt = R + t;   // R[i][t] = rt[i * ldr]
+    for (int u = 0; u < kLmulRows; ++u) acc[u] = 0.0;
+    // columns of X in batches of 8 rows: the loads of a batch overlap
+    for (int t0 = i0; t0 < r; t0 += 8) {
+        double xv[8];
 #pragma unroll
-            for (int u = 0; u < 32; ++u) {
-                const int i = i0 + u;
-                if (i < r && i <= t) acc[u] += rt[(int64_t)i * ldr] * x;
+        for (int q = 0; q < 8; ++q) xv[q] = t0 + q < r ? X[(int64_t)(t0 + q) * ncols + c] : 0.0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (t0 + q < r) {
+#pragma unroll
+                for (int u = 0; u < kLmulRows; ++u) acc[u] += Rs[t0 + q][u] * xv[q];
             }
         }
-#pragma unroll
-        for (int u = 0; u < 32; ++u)
-            if (i0 + u < r) C[(int64_t)(i0 + u) * ncols + c] = acc[u];
     }
+#pragma unroll
+    for (int u = 0; u < kLmulRows; ++u)
+        if (i0 + u < r) C[(int64_t)(i0 + u) * ncols + c] = acc[u];
 }
 
 static unsigned gauge_grid(int64_t items, int per_block) {
@@ -184,9 +278,9 @@ size_t gauge_workspace_bytes(const int64_t* dims, const int64_t* ranks, int d) {
         const int64_t ncols = dims[l + 1] * ranks[l + 2];
         size_t b = 0;
         b += round_up((int64_t)(rows * rp * 8), 256) * 2;                   // W1, W2
-        b += round_up((int64_t)(rp * rp * 8), 256) * 6;                     // G, R1, Rinv1, R2, Rinv2, R
+        b += round_up((int64_t)(rp * rp * 8), 256) * 3;                     // G, R1, R2
         b += round_up((int64_t)gram_workspace_bytes(rows, rp), 256);        // Gram partials
-        b += round_up((int64_t)(r * ncols * 8), 256);                       // R G_{l+1}
+        b += round_up((int64_t)(r * ncols * 8), 256);                       // R1 G_{l+1}
         need = b > need ? b : need;
     }
     return need + 256 + (size_t)round_up(4 * (int64_t)d, 256);
@@ -194,6 +288,24 @@ size_t gauge_workspace_bytes(const int64_t* dims, const int64_t* ranks, int d) {
 
 __global__ void k_gauge_zero(int* p, int n) {
     for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
+}
+
+static unsigned trsm_grid(int64_t rows) {
+    // enough waves to cover the rows in a few passes without reloading R
+    // into LDS more often than needed
+    int64_t g = (rows + 4 * kTrsmRows - 1) / (4 * kTrsmRows);
+    if (g > 1024) g = 1024;
+    return (unsigned)(g < 1 ? 1 : g);
+}
+
+static void launch_trsm(const double* A, int64_t rows, int r, int lda, const double* R, int ldr, double* C,
+                        int ldc, hipStream_t stream) {
+    if (r > 64)
+        hipLaunchKernelGGL(k_gauge_trsm<true>, dim3(trsm_grid(rows)), dim3(256), 0, stream, A, rows, r, lda, R, ldr,
+                           C, ldc);
+    else
+        hipLaunchKernelGGL(k_gauge_trsm<false>, dim3(trsm_grid(rows)), dim3(256), 0, stream, A, rows, r, lda, R,
+                           ldr, C, ldc);
 }
 
 hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t* ranks, int d, int* flags,
@@ -209,10 +321,7 @@ hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t
         double* W2 = static_cast<double*>(ws.take((size_t)rows * rp * 8));
         double* G = static_cast<double*>(ws.take((size_t)rp * rp * 8));
         double* R1 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
-        double* I1 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
         double* R2 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
-        double* I2 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
-        double* Rt = static_cast<double*>(ws.take((size_t)rp * rp * 8));
         double* NX = static_cast<double*>(ws.take((size_t)r * ncols * 8));
         if (ws.overrun) return hipErrorOutOfMemory;
         KernelTimer tm("gauge_qr_f64", stream);
@@ -223,22 +332,18 @@ hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t
         hipError_t e = launch_gram(W1, rows, rp, G, ws, stream);
         if (e != hipSuccess) return e;
         ws.used = gmark;
-        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R1, I1, (const double*)nullptr,
-                           (double*)nullptr, flags + l);
-        hipLaunchKernelGGL(k_gauge_rmul, dim3(gauge_grid(rows, 4)), dim3(256), 0, stream, W1, rows, r, rp, I1, rp,
-                           W2, rp);
-        // second pass on W2: R = R2 R1, core l = W2 R2^{-1}
+        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R1, flags + l);
+        launch_trsm(W1, rows, r, rp, R1, rp, W2, rp, stream);
+        // second pass on W2: core l = W2 R2^{-1}; R = R2 R1
         e = launch_gram(W2, rows, rp, G, ws, stream);
         if (e != hipSuccess) return e;
         ws.used = gmark;
-        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R2, I2, R1, Rt, flags + l);
-        hipLaunchKernelGGL(k_gauge_rmul, dim3(gauge_grid(rows, 4)), dim3(256), 0, stream, W2, rows, r, rp, I2, rp,
-                           cores[l], r);
-        // core l+1 <- R core l+1 (left unfolding r x ncols)
-        hipLaunchKernelGGL(k_gauge_lmul, dim3(gauge_grid(ncols, 256)), dim3(256), 0, stream, Rt, r, rp,
-                           cores[l + 1], ncols, NX);
-        e = hipMemcpyAsync(cores[l + 1], NX, (size_t)r * ncols * 8, hipMemcpyDeviceToDevice, stream);
-        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R2, flags + l);
+        launch_trsm(W2, rows, r, rp, R2, rp, cores[l], r, stream);
+        // core l+1 <- R2 (R1 core l+1) on its left unfolding (r x ncols)
+        const dim3 gl((unsigned)((ncols + 255) / 256), (unsigned)((r + kLmulRows - 1) / kLmulRows));
+        hipLaunchKernelGGL(k_gauge_lmul, gl, dim3(256), 0, stream, R1, r, rp, cores[l + 1], ncols, NX);
+        hipLaunchKernelGGL(k_gauge_lmul, gl, dim3(256), 0, stream, R2, r, rp, NX, ncols, cores[l + 1]);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         ws.used = mark;
