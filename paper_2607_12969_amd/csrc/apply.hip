@@ -661,25 +661,38 @@ static void launch_abt(dim3 grid, hipStream_t st, Args... args) {
     hipLaunchKernelGGL((k_abt<T, C, MODE>), grid, dim3(C::NT), 0, st, args...);
 }
 
-// dst[i][j] = src[i][j] for j < cols, 0 for cols <= j < ldd: a copy of an
-// operand whose pitch or base rules out 16-byte moves.
+// Padded copies of the operands whose pitch or base rule out 16-byte moves,
+// all in one launch: job q copies src (rows x cols, pitch lds) into dst
+// (rows x ldd, ldd a multiple of the 16-byte chunk, dst 16-byte aligned),
+// with zeros in columns cols <= j < ldd.  Each thread fills whole 16-byte
+// chunks of dst from element loads of the source (adjacent threads read
+// adjacent elements, so the loads coalesce).
 template <typename T>
-__global__ __launch_bounds__(256) void k_pitch_copy(const T* __restrict__ src, int64_t rows, int64_t cols,
-                                                    int64_t lds, T* __restrict__ dst, int64_t ldd) {
-    const int64_t total = rows * ldd;
-    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (int64_t)gridDim.x * 256) {
-        const int64_t i = idx / ldd, j = idx % ldd;
-        dst[idx] = (j < cols) ? src[i * lds + j] : T(0);
-    }
-}
+struct StageJobs {
+    const T* src[3];
+    T* dst[3];
+    int64_t rows[3], cols[3], lds[3];
+    int cpr[3];              // 16-byte chunks per destination row
+    int64_t end[3];          // running total of chunks up to and including job q
+    int n;
+};
 
 template <typename T>
-static void pitch_copy(const T* src, int64_t rows, int64_t cols, int64_t lds, T* dst, int64_t ldd,
-                       hipStream_t stream) {
-    int64_t g = (rows * ldd + 255) / 256;
-    if (g > 8192) g = 8192;
-    if (g < 1) g = 1;
-    hipLaunchKernelGGL(k_pitch_copy<T>, dim3((unsigned)g), dim3(256), 0, stream, src, rows, cols, lds, dst, ldd);
+__global__ __launch_bounds__(256) void k_pitch_copy(StageJobs<T> J) {
+    constexpr int VEC = 16 / (int)sizeof(T);
+    typedef T vec_t __attribute__((ext_vector_type(VEC)));
+    const int64_t total = J.end[J.n - 1];
+    for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < total; c += (int64_t)gridDim.x * 256) {
+        const int q = c < J.end[0] ? 0 : (c < J.end[1] ? 1 : 2);
+        const int64_t cj = q == 0 ? c : c - J.end[q - 1];
+        const int64_t i = cj / J.cpr[q];
+        const int64_t j0 = (cj - i * J.cpr[q]) * VEC;
+        const T* src = J.src[q] + i * J.lds[q];
+        vec_t w;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) w[v] = j0 + v < J.cols[q] ? src[j0 + v] : T(0);
+        *reinterpret_cast<vec_t*>(J.dst[q] + i * (int64_t)J.cpr[q] * VEC + j0) = w;
+    }
 }
 
 // --------------------------------------------------------- streaming path --
@@ -987,28 +1000,42 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     const T *Ug = U, *Vg = V, *Xg = X;
     int64_t ldu = k, ldv = k, ldx = b;
     if (p.stage_u || p.stage_v || p.stage_x) {
-        KernelTimer ts("apply_stage", stream);
+        StageJobs<T> J{};
+        auto add = [&](const T* src, int64_t rows, int64_t cols, int64_t ldd) -> T* {
+            T* d = static_cast<T*>(ws.take((size_t)rows * ldd * sizeof(T)));
+            if (!d) return nullptr;
+            const int q = J.n++;
+            J.src[q] = src;
+            J.dst[q] = d;
+            J.rows[q] = rows;
+            J.cols[q] = cols;
+            J.lds[q] = cols;
+            J.cpr[q] = (int)(ldd / (16 / (int64_t)sizeof(T)));
+            J.end[q] = (q ? J.end[q - 1] : 0) + rows * J.cpr[q];
+            return d;
+        };
         if (p.stage_u) {
-            T* d = static_cast<T*>(ws.take((size_t)m * p.Kp * sizeof(T)));
+            T* d = add(U, m, k, p.Kp);
             if (!d) return hipErrorOutOfMemory;
-            pitch_copy<T>(U, m, k, k, d, p.Kp, stream);
             Ug = d;
             ldu = p.Kp;
         }
         if (p.stage_v) {
-            T* d = static_cast<T*>(ws.take((size_t)n * p.Kp * sizeof(T)));
+            T* d = add(V, n, k, p.Kp);
             if (!d) return hipErrorOutOfMemory;
-            pitch_copy<T>(V, n, k, k, d, p.Kp, stream);
             Vg = d;
             ldv = p.Kp;
         }
         if (p.stage_x) {
-            T* d = static_cast<T*>(ws.take((size_t)n * p.ldx * sizeof(T)));
+            T* d = add(X, n, b, p.ldx);
             if (!d) return hipErrorOutOfMemory;
-            pitch_copy<T>(X, n, b, b, d, p.ldx, stream);
             Xg = d;
             ldx = p.ldx;
         }
+        KernelTimer ts("apply_stage", stream);
+        int64_t g = (J.end[J.n - 1] + 255) / 256;
+        if (g > 16384) g = 16384;
+        hipLaunchKernelGGL(k_pitch_copy<T>, dim3((unsigned)(g < 1 ? 1 : g)), dim3(256), 0, stream, J);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -59,6 +59,7 @@ struct TTArgs {
     TTSet set[kTTMaxSets];
     void* out;
     int vec4;
+    int lines;               // output rows start on 128-byte lines (n_last * sizeof(T) % 128 == 0)
     int ifast;               // wave tiles: consecutive tiles take consecutive middle indices
 };
 
@@ -1093,9 +1094,15 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int64_t L = L0 + 16 * pb + g + 4 * v;
-                    // each instruction covers whole 128-byte lines (16 lanes
-                    // of one row): written around the caches
-                    if (L < a.NL) __builtin_nontemporal_store(acc[pb][v], out + (L * a.n_mid + i) * a.n_last + col);
+                    // where rows start on 128-byte lines, each instruction
+                    // covers whole lines (16 lanes of one row) and is written
+                    // around the caches; a partial line is not (measured:
+                    // nontemporal partial lines cost several times more)
+                    if (L < a.NL) {
+                        double* dst = out + (L * a.n_mid + i) * a.n_last + col;
+                        if (a.lines) __builtin_nontemporal_store(acc[pb][v], dst);
+                        else *dst = acc[pb][v];
+                    }
                 }
         }
         c = cn;
@@ -1864,6 +1871,7 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
     a.ncp = (int)round_up(p.n_last, 32);
     a.out = out;
     a.vec4 = out && (p.n_last % 4 == 0) && (reinterpret_cast<uintptr_t>(out) % (4 * sizeof(T)) == 0);
+    a.lines = out && ((p.n_last * (int64_t)sizeof(T)) % 128 == 0) && (reinterpret_cast<uintptr_t>(out) % 128 == 0);
     // short output rows (n_d e < 1 KB): wave tiles of consecutive middle indices
     // write neighbouring segments of the same rows, so the rows fill up together
     a.ifast = p.wave_nkb && p.n_last * (int64_t)sizeof(T) < 1024;

@@ -163,3 +163,19 @@ def test_unaligned_operands_are_staged(lrc, prec):
     assert "apply_stage" in labels
     u, s, v, x = [o for _, o in hs]
     assert rel_fro(Y.cpu().numpy().astype(np.float64), O.apply(u, s, v, x)) <= TOL[prec]
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("m,n,b", [(494, 494, 256), (494, 494, 8192), (640, 192, 2048), (96, 96, 8192),
+                                   (1536, 1536, 2048)])
+@pytest.mark.parametrize("inc", [0, 1])
+def test_timing_grid_shapes(lrc, prec, m, n, b, inc):
+    """Shapes of the paper's matrix timing grid (base rank 40, compensated
+    rank 41, batches 256 / 2048 / 8192, unit-norm samples), same-rank
+    controls included; every output compared."""
+    k = 40 + inc
+    d = synth.random_factors(m, n, k, b, tag=900 + m + b + inc)
+    X = d["X"] / np.linalg.norm(d["X"], axis=0, keepdims=True)
+    print(f"apply grid prec={prec} m={m} n={n} k={k} b={b}", flush=True)
+    Y, (u, s, v, x) = _run(lrc, d["U"], d["s"], d["V"], X, prec)
+    assert rel_fro(Y, O.apply(u, s, v, x)) <= TOL[prec]

@@ -167,3 +167,20 @@ def test_many_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
         monkeypatch.setenv("LRC_TT_WAVE", "0")
     cores = synth.random_tt_cores(dims, ranks, tag=7 * len(dims) + sum(ranks))
     _check(lrc, cores, prec, f"{layout}{dims}")
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("dims,nominal", [
+    ((83, 86, 204), 32), ((83, 86, 204), 36), ((145, 145, 200), 36), ((610, 340, 103), 36),
+    ((128, 24, 64, 64), 20), ((192, 24, 64, 16), 16), ((16,) * 6, 12),
+])
+def test_timing_grid_shapes(lrc, prec, dims, nominal):
+    """Shapes and rank schedules of the paper's TT timing grid (hyperspectral
+    cubes 32 -> 36, four-way subtensors 16 -> 20, six-way 8 -> 12; ranks
+    capped by the unfolding dimensions); the full tensor compared."""
+    ranks = [1]
+    for l in range(len(dims) - 1):
+        ranks.append(int(min(nominal, ranks[-1] * dims[l], np.prod(dims[l + 1:]))))
+    ranks.append(1)
+    cores = synth.random_tt_cores(dims, ranks, tag=700 + nominal + len(dims))
+    _check(lrc, cores, prec, f"grid{dims}")
