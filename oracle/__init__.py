@@ -465,3 +465,78 @@ def tt_compensation(T, R=None, R_plus=None, prec: str = "fp16", eps=None, delta=
     res = tt_certificate(T, base, aug, prec)
     res["base_cores"], res["aug_cores"] = base, aug
     return res
+
+
+# ---------------------------------------------------------------------------
+# Fixed-memory comparison (Sec. sec:hyperspectral_application): quality
+# measures of a reconstruction and the memory-matched FP64 rank.
+# ---------------------------------------------------------------------------
+
+def band_range(xb) -> float:
+    """L_b of one reference band: max - min, or max(max|X_b|, 1) for a
+    constant band."""
+    lo, hi = float(np.min(xb)), float(np.max(xb))
+    if hi > lo:
+        return hi - lo
+    return max(max(abs(lo), abs(hi)), 1.0)
+
+
+def band_quality(X, Xh) -> dict:
+    """Quality of Xh against the reference X, both FP64 with the spectral
+    bands along the last axis and the pixels along the others:
+      rel_err  ||X - Xh||_F / ||X||_F
+      psnr     mean over bands of 20 log10(L_b / sqrt(MSE_b))
+      ssim     mean over bands of the SSIM variant evaluated once per whole
+               band with population means, variances and covariance,
+               C1 = (0.01 L_b)^2, C2 = (0.03 L_b)^2
+      sam      mean over pixels with ||x|| ||xh|| > 0 of the angle between
+               the reference and reconstructed spectra (radians)."""
+    X = np.asarray(X, dtype=np.float64)
+    Xh = np.asarray(Xh, dtype=np.float64)
+    B = X.shape[-1]
+    Xm = X.reshape(-1, B)
+    Ym = Xh.reshape(-1, B)
+    psnr, ssim = [], []
+    for b in range(B):
+        x, y = Xm[:, b], Ym[:, b]
+        L = band_range(x)
+        mse = float(np.mean((x - y) ** 2))
+        with np.errstate(divide="ignore"):
+            psnr.append(20.0 * math.log10(L / math.sqrt(mse)) if mse > 0 else math.inf)
+        mx, my = float(np.mean(x)), float(np.mean(y))
+        vx, vy = float(np.mean((x - mx) ** 2)), float(np.mean((y - my) ** 2))
+        cxy = float(np.mean((x - mx) * (y - my)))
+        c1, c2 = (0.01 * L) ** 2, (0.03 * L) ** 2
+        ssim.append((2 * mx * my + c1) * (2 * cxy + c2) / ((mx * mx + my * my + c1) * (vx + vy + c2)))
+    nx = np.sqrt(np.sum(Xm * Xm, axis=1))
+    ny = np.sqrt(np.sum(Ym * Ym, axis=1))
+    keep = nx * ny > 0
+    cos = np.sum(Xm * Ym, axis=1)[keep] / (nx[keep] * ny[keep])
+    angles = np.arccos(np.clip(cos, -1.0, 1.0))
+    return dict(rel_err=fro_diff(X, Xh) / fro(X), psnr=float(np.mean(psnr)), ssim=float(np.mean(ssim)),
+                sam=float(np.mean(angles)) if angles.size else math.nan, sam_pixels=int(np.count_nonzero(keep)))
+
+
+def capped_ranks(dims, nominal):
+    """Uniform nominal TT ranks capped by the unfolding dimensions,
+    r_l <= min(R, r_{l-1} n_l, prod_{i>l} n_i) (Sec. 7.4)."""
+    ranks = [1]
+    for l in range(len(dims) - 1):
+        ranks.append(int(min(int(nominal), ranks[-1] * int(dims[l]), int(np.prod([int(n) for n in dims[l + 1:]])))))
+    return ranks + [1]
+
+
+def memory_matched_rank(dims, budget_bytes: int):
+    """The largest uniform FP64 TT rank (capped as above) whose exact TT
+    storage does not exceed budget_bytes, with its rank vector; (0, None)
+    if even rank 1 does not fit (Sec. sec:hyperspectral_application)."""
+    best = (0, None)
+    R = 1
+    while True:
+        ranks = capped_ranks(dims, R)
+        if tt_storage_bytes(dims, ranks, "fp64") > budget_bytes:
+            return best
+        best = (R, ranks)
+        if ranks == capped_ranks(dims, R + 1):   # every rank capped: storage stops growing
+            return best
+        R += 1
