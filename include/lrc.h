@@ -265,6 +265,56 @@ int lrc_round(const void* x, void* y, int64_t count, int prec, int64_t* n_overfl
 #define LRC_GAUGE_MAX_RANK 96
 int lrc_tt_left_orthogonalize(void* const* cores, const int64_t* dims, const int64_t* ranks, int d);
 
+/*
+ * Fixed-memory comparison tools (Sec. sec:hyperspectral_application).
+ *
+ * Quality of a reconstruction Xh against its FP64 reference X, both with
+ * the spectral bands as the last (contiguous) mode:
+ *   rel_err     ||X - Xh||_F / ||X||_F
+ *   psnr        mean over bands b of 20 log10(L_b / sqrt(MSE_b)), L_b the
+ *               band's range (max(max|X_b|, 1) for a constant band);
+ *               +infinity when a band is reproduced exactly
+ *   ssim        mean over bands of the SSIM variant evaluated once per whole
+ *               band with population means, variances and covariance,
+ *               C1 = (0.01 L_b)^2, C2 = (0.03 L_b)^2
+ *   sam         mean spectral angle (radians) over the sam_pixels pixels
+ *               whose reference and reconstructed spectra both have
+ *               positive norm (NaN if there are none)
+ * Sums are added in a fixed order: results are bitwise reproducible.
+ */
+typedef struct {
+    double rel_err, psnr, ssim, sam;
+    int64_t sam_pixels;
+    int64_t pixels, bands;
+} lrc_quality;
+
+/* Dense pair: X device FP64 and Xh device in `prec`, both pixels x bands
+ * row-major; Xh is multiplied by `scale` as it is read (1.0: as stored;
+ * the norm of a normalized tensor undoes the normalization).  Synchronizes
+ * the calling thread's stream.  Errors: LRC_EINVAL (NULL pointer, pixels or
+ * bands < 1, unknown prec), LRC_EOVERFLOW, LRC_ENOMEM, LRC_EHIP, LRC_ENODEV. */
+int lrc_band_quality(const void* X, const void* Xh, int64_t pixels, int64_t bands, int prec, double scale,
+                     lrc_quality* q);
+
+/* TT cores (as for lrc_tt_reconstruct, stored in `prec`, d >= 2) against the
+ * device FP64 reference X: the stored cores are widened exactly and
+ * contracted in FP64 (the paper's evaluation of rounded cores), the result
+ * multiplied by `scale`, and measured as lrc_band_quality does, with
+ * bands = dims[d-1] and pixels = the product of the other modes.  The dense
+ * FP64 reconstruction lives in the library's workspace.  Synchronizes.
+ * Errors as lrc_tt_reconstruct, plus LRC_EINVAL for d < 2 or a NULL X. */
+int lrc_tt_quality(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, int prec,
+                   const void* X, double scale, lrc_quality* q);
+
+/* Memory-matched FP64 rank: the largest uniform nominal TT rank R whose
+ * exact FP64 storage (8 sum_l r_{l-1} n_l r_l, ranks capped by the
+ * unfolding dimensions, r_l <= min(R, r_{l-1} n_l, prod_{i>l} n_i)) does
+ * not exceed budget_bytes.  Writes the d+1 capped ranks to ranks_out (host)
+ * and returns R, or returns 0 (ranks_out all 0) if rank 1 does not fit.
+ * Pure host function.  Errors: LRC_EINVAL for NULL pointers, d outside
+ * [1, LRC_TT_MAX_D] or a dimension < 1. */
+int64_t lrc_tt_memory_matched_rank(const int64_t* dims, int d, int64_t budget_bytes, int64_t* ranks_out);
+
 /* Stored bytes of rank-k factors in `prec`: (b/8) k (m+n+1)  (Sec. 4.2).
  * Returns LRC_EINVAL for bad arguments or LRC_EOVERFLOW on overflow. */
 int64_t lrc_storage_bytes(int64_t m, int64_t n, int64_t k, int prec);

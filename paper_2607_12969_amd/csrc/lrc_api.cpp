@@ -590,7 +590,7 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
 // FP64 reconstruction into a caller-provided buffer on the calling thread's
 // stream (the FP64 kernel takes no workspace); used by the TT certificate.
 static int tt_into(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, double* out,
-                   Workspace& ws) {
+                   Workspace& ws, const char* label = "cert_tt_fused_f64") {
     hipStream_t st = g_stream;
     if (d == 1) {
         hipError_t e = hipMemcpyAsync(out, cores[0], (size_t)dims[0] * 8, hipMemcpyDeviceToDevice, st);
@@ -607,7 +607,7 @@ static int tt_into(const void* const* cores, const int64_t* dims, const int64_t*
     // the staged cores live only until this launch has run: the next
     // reconstruction on the stream reuses their workspace
     const size_t mark = ws.used;
-    hipError_t e = launch_tt(plan, cores, out, ws, st, "cert_tt_fused_f64");
+    hipError_t e = launch_tt(plan, cores, out, ws, st, label);
     ws.used = mark;
     return e == hipSuccess ? LRC_OK : fail_hip(e, "TT reconstruction launch");
 }
@@ -743,3 +743,128 @@ int lrc_certify(const lrc_cert_args* args, lrc_cert_result* res) {
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------ fixed-memory tools --
+static void quality_result(const double* h, int64_t P, int64_t B, lrc_quality* q) {
+    q->rel_err = h[0];
+    q->psnr = h[1];
+    q->ssim = h[2];
+    q->sam = h[3];
+    q->sam_pixels = (int64_t)h[4];
+    q->pixels = P;
+    q->bands = B;
+}
+
+int lrc_band_quality(const void* X, const void* Xh, int64_t pixels, int64_t bands, int prec, double scale,
+                     lrc_quality* q) {
+    if (!X || !Xh || !q) return fail(LRC_EINVAL, "NULL argument");
+    if (!valid_prec(prec)) return fail(LRC_EINVAL, "unknown precision code %d", prec);
+    if (pixels < 1 || bands < 1) return fail(LRC_EINVAL, "pixels and bands must be >= 1");
+    int64_t N, nb;
+    if (!mul_ok(pixels, bands, &N) || !mul_ok(N, 8, &nb)) return fail(LRC_EOVERFLOW, "entry count overflows");
+    int dev;
+    int rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t e = ws.reserve(quality_workspace_bytes(pixels, bands) + 256, st);
+    if (e != hipSuccess) return fail_hip(e, "workspace");
+    double* out = static_cast<double*>(ws.take(5 * 8));
+    e = launch_quality(static_cast<const double*>(X), Xh, prec, scale, pixels, bands, out, ws, st);
+    double h[5];
+    if (e == hipSuccess) e = hipMemcpyAsync(h, out, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail_hip(e, "quality");
+    quality_result(h, pixels, bands, q);
+    return LRC_OK;
+}
+
+int lrc_tt_quality(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, int prec,
+                   const void* X, double scale, lrc_quality* q) {
+    if (!cores || !X || !q) return fail(LRC_EINVAL, "NULL argument");
+    if (!valid_prec(prec)) return fail(LRC_EINVAL, "unknown precision code %d", prec);
+    int64_t N;
+    int rc = check_tt_shape(dims, ranks, d, &N);
+    if (rc) return rc;
+    if (d < 2) return fail(LRC_EINVAL, "need d >= 2 (pixels and a band mode)");
+    for (int l = 0; l < d; ++l)
+        if (!cores[l]) return fail(LRC_EINVAL, "cores[%d] is NULL", l);
+    const int64_t B = dims[d - 1], P = N / B;
+    int dev;
+    rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    const int64_t cnt = tt_count(dims, ranks, d);
+    size_t need = (size_t)N * 8 + (size_t)cnt * 8 + (size_t)(d + 4) * 256 + quality_workspace_bytes(P, B) + 256;
+    need += tt_stage_need(dims, ranks, d) + 512;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t e = ws.reserve(need, st);
+    if (e != hipSuccess) return fail_hip(e, "workspace");
+    double* Xh = static_cast<double*>(ws.take((size_t)N * 8));
+    // the stored cores, widened exactly to FP64 (Sec. 3.4: FP64 contraction of the rounded cores)
+    std::vector<const void*> wide(d);
+    for (int l = 0; l < d; ++l) {
+        const int64_t c = ranks[l] * dims[l] * ranks[l + 1];
+        if (prec == LRC_FP64) {
+            wide[l] = cores[l];
+            continue;
+        }
+        double* w = static_cast<double*>(ws.take((size_t)c * 8));
+        if (ws.overrun || !w) return fail(LRC_ENOMEM, "quality workspace too small");
+        e = launch_widen(cores[l], prec, c, w, st);
+        if (e != hipSuccess) return fail_hip(e, "widen launch");
+        wide[l] = w;
+    }
+    double* out = static_cast<double*>(ws.take(5 * 8));
+    if (ws.overrun) return fail(LRC_ENOMEM, "quality workspace too small");
+    rc = tt_into(wide.data(), dims, ranks, d, Xh, ws, "quality_tt_f64");
+    if (rc) return rc;
+    e = launch_quality(static_cast<const double*>(X), Xh, LRC_FP64, scale, P, B, out, ws, st);
+    double h[5];
+    if (e == hipSuccess) e = hipMemcpyAsync(h, out, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail_hip(e, "quality");
+    quality_result(h, P, B, q);
+    return LRC_OK;
+}
+
+int64_t lrc_tt_memory_matched_rank(const int64_t* dims, int d, int64_t budget_bytes, int64_t* ranks_out) {
+    if (!dims || !ranks_out) return fail(LRC_EINVAL, "NULL argument");
+    if (d < 1 || d > LRC_TT_MAX_D) return fail(LRC_EINVAL, "d = %d outside [1, %d]", d, LRC_TT_MAX_D);
+    for (int l = 0; l < d; ++l)
+        if (dims[l] < 1) return fail(LRC_EINVAL, "dims[%d] = %lld < 1", l, (long long)dims[l]);
+    // ranks capped by the unfolding dimensions: r_l <= min(R, r_{l-1} n_l, prod_{i>l} n_i)
+    auto sat_mul = [](int64_t a, int64_t b) { return a > INT64_MAX / b ? INT64_MAX : a * b; };
+    auto capped = [&](int64_t R, std::vector<int64_t>& r) {
+        r.assign(d + 1, 1);
+        for (int l = 0; l + 1 < d; ++l) {
+            int64_t right = 1;
+            for (int i = l + 1; i < d; ++i) right = sat_mul(right, dims[i]);
+            r[l + 1] = std::min(R, std::min(sat_mul(r[l], dims[l]), right));
+        }
+    };
+    auto bytes = [&](const std::vector<int64_t>& r) {
+        int64_t tot = 0;
+        for (int l = 0; l < d; ++l) {
+            int64_t a, b;
+            if (!mul_ok(r[l], dims[l], &a) || !mul_ok(a, r[l + 1], &b) || tot > INT64_MAX / 8 - b) return INT64_MAX;
+            tot += b;
+        }
+        return tot * 8;
+    };
+    std::vector<int64_t> r, next, best;
+    int64_t R = 1, bestR = 0;
+    for (;;) {
+        capped(R, r);
+        if (bytes(r) > budget_bytes) break;
+        bestR = R;
+        best = r;
+        capped(R + 1, next);
+        if (next == r) break;   // every rank capped: storage stops growing
+        ++R;
+    }
+    for (int l = 0; l <= d; ++l) ranks_out[l] = bestR ? best[l] : 0;
+    return bestR;
+}

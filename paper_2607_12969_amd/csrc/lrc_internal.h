@@ -98,6 +98,14 @@ hipError_t launch_widen_scaled(const void* h, const void* hs, int prec, int64_t 
 // out[i] = widen(src[i])
 hipError_t launch_widen(const void* src, int prec, int64_t count, double* out, hipStream_t stream);
 
+// --------------------------------------------------------- quality measures
+// out[0..4] = relative error, mean band PSNR, mean band SSIM variant, mean
+// spectral angle, pixels in that mean; X (P x B, FP64) against scale * Xh
+// (P x B in prec).
+size_t quality_workspace_bytes(int64_t P, int64_t B);
+hipError_t launch_quality(const double* X, const void* Xh, int prec, double scale, int64_t P, int64_t B,
+                          double* out, Workspace& ws, hipStream_t stream);
+
 // Partial sums of (A - W Vw^T)^2 over m x n, one per workgroup; returns the
 // number of partials written to `part` via *nparts.
 size_t err_workspace_bytes(int64_t m, int64_t n);

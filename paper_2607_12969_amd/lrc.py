@@ -65,6 +65,11 @@ class CertResult(ctypes.Structure):
     ]
 
 
+class Quality(ctypes.Structure):
+    _fields_ = [("rel_err", ctypes.c_double), ("psnr", ctypes.c_double), ("ssim", ctypes.c_double),
+                ("sam", ctypes.c_double), ("sam_pixels", _i64), ("pixels", _i64), ("bands", _i64)]
+
+
 _lib = None
 
 
@@ -92,6 +97,13 @@ def lib():
     L.lrc_tt_left_orthogonalize.argtypes = [ctypes.POINTER(_vp), ctypes.POINTER(_i64), ctypes.POINTER(_i64),
                                             ctypes.c_int]
     L.lrc_tt_left_orthogonalize.restype = ctypes.c_int
+    L.lrc_band_quality.argtypes = [_vp, _vp, _i64, _i64, ctypes.c_int, ctypes.c_double, ctypes.POINTER(Quality)]
+    L.lrc_band_quality.restype = ctypes.c_int
+    L.lrc_tt_quality.argtypes = [ctypes.POINTER(_vp), ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.c_int,
+                                 ctypes.c_int, _vp, ctypes.c_double, ctypes.POINTER(Quality)]
+    L.lrc_tt_quality.restype = ctypes.c_int
+    L.lrc_tt_memory_matched_rank.argtypes = [ctypes.POINTER(_i64), ctypes.c_int, _i64, ctypes.POINTER(_i64)]
+    L.lrc_tt_memory_matched_rank.restype = _i64
     L.lrc_storage_bytes.argtypes = [_i64, _i64, _i64, ctypes.c_int]
     L.lrc_storage_bytes.restype = _i64
     L.lrc_tt_storage_bytes.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.c_int, ctypes.c_int]
@@ -260,6 +272,56 @@ def tt_left_orthogonalize(cores):
     _bind_stream(cores[0].device)
     _check(lib().lrc_tt_left_orthogonalize(ptrs, D, R, d))
     return cores
+
+
+def _quality(q: Quality) -> dict:
+    return {f: getattr(q, f) for f, _ in Quality._fields_}
+
+
+def band_quality(X, Xh, scale: float = 1.0) -> dict:
+    """Quality of Xh (any storage dtype) against the float64 reference X,
+    bands along the last axis (relative error, mean band PSNR, mean band
+    SSIM variant, mean spectral angle)."""
+    import torch
+    _dev(X, Xh)
+    if X.dtype != torch.float64 or X.shape != Xh.shape or X.dim() < 2:
+        raise ValueError("X must be float64 with at least two axes, Xh of the same shape")
+    B = int(X.shape[-1])
+    _bind_stream(X.device)
+    q = Quality()
+    _check(lib().lrc_band_quality(X.data_ptr(), Xh.data_ptr(), X.numel() // B, B, _prec_of(Xh), float(scale),
+                                  ctypes.byref(q)))
+    return _quality(q)
+
+
+def tt_quality(cores, X, scale: float = 1.0) -> dict:
+    """Quality of the FP64 contraction of the stored cores (times scale)
+    against the float64 reference X of the full tensor shape."""
+    import torch
+    _dev(*cores, X)
+    if X.dtype != torch.float64:
+        raise TypeError("X must be float64")
+    dims, ranks = tt_shape(cores)
+    if list(X.shape) != dims:
+        raise ValueError("X must have the tensor's shape")
+    d = len(cores)
+    ptrs = (_vp * d)(*[c.data_ptr() for c in cores])
+    D = (_i64 * d)(*dims)
+    R = (_i64 * (d + 1))(*ranks)
+    _bind_stream(X.device)
+    q = Quality()
+    _check(lib().lrc_tt_quality(ptrs, D, R, d, _prec_of(cores[0]), X.data_ptr(), float(scale), ctypes.byref(q)))
+    return _quality(q)
+
+
+def memory_matched_rank(dims, budget_bytes: int):
+    """(R, capped rank vector) of the largest uniform FP64 TT rank within
+    budget_bytes; (0, None) if rank 1 does not fit."""
+    d = len(dims)
+    D = (_i64 * d)(*dims)
+    out = (_i64 * (d + 1))()
+    R = _check(lib().lrc_tt_memory_matched_rank(D, d, int(budget_bytes), out))
+    return (int(R), [int(v) for v in out]) if R > 0 else (0, None)
 
 
 def _result(res: CertResult) -> dict:

@@ -160,3 +160,29 @@ def test_gauge_argument_errors():
     assert _gauge((4, 5), (1, 3, 1), 2, cores=[0x1000000, 0x1000008]) == -1   # cores overlap
     assert b"overlaps" in L.lrc_last_error()
     assert _gauge((2 ** 40, 2 ** 40), (1, 3, 1), 2) == -2     # entry count overflow
+
+
+def test_memory_matched_rank_matches_oracle():
+    """Pure host function: equal to the oracle's search (integers, exact),
+    including the paper's (17, 17) at its four budgets."""
+    cases = [((145, 145, 200), 36), ((610, 340, 103), 36), ((83, 86, 204), 36), ((512, 217, 204), 36),
+             ((4, 5, 6), 3), ((16,) * 6, 12), ((128, 24, 64, 64), 20), ((3, 3), 5)]
+    for dims, Rc in cases:
+        for prec in ("fp16", "fp32"):
+            budget = O.tt_storage_bytes(dims, O.capped_ranks(dims, Rc), prec)
+            for b in (budget, budget - 1, budget + 1, 8, 10 ** 12):
+                assert lrc.memory_matched_rank(dims, b) == O.memory_matched_rank(dims, b), (dims, b)
+
+
+def test_quality_argument_errors():
+    q = lrc.Quality()
+    assert L.lrc_band_quality(None, 0x10000, 4, 4, 0, 1.0, ctypes.byref(q)) == -1
+    assert L.lrc_band_quality(0x10000, 0x20000, 0, 4, 0, 1.0, ctypes.byref(q)) == -1
+    assert L.lrc_band_quality(0x10000, 0x20000, 4, 4, 9, 1.0, ctypes.byref(q)) == -1
+    assert L.lrc_band_quality(0x10000, 0x20000, 2 ** 40, 2 ** 40, 0, 1.0, ctypes.byref(q)) == -2
+    D = (ctypes.c_int64 * 1)(5)
+    R = (ctypes.c_int64 * 2)(1, 1)
+    P = (ctypes.c_void_p * 1)(0x10000)
+    assert L.lrc_tt_quality(P, D, R, 1, 0, 0x20000, 1.0, ctypes.byref(q)) == -1     # d < 2
+    out = (ctypes.c_int64 * 2)()
+    assert L.lrc_tt_memory_matched_rank(D, 0, 100, out) == -1
