@@ -19,6 +19,7 @@ same apply and TT work.
   python bench.py --sweep FILE      per-kernel table over the workload grid
   python bench.py --quant FILE      device rounding and TT gauge cells
   python bench.py --grid FILE       the paper's resident timing grid on synthetic stand-ins
+  python bench.py --fixed-memory FILE   fixed-memory comparison on hyperspectral-shaped stand-ins
 """
 from __future__ import annotations
 
@@ -425,6 +426,19 @@ def quant_sweep(path, dev, lrc):
         km = {"gauge_qr_f64": km["gauge_qr_f64"] * (len(dims) - 1)}   # one timed span per unfolding
         rows.append(_row(f"gauge {name}", "f64", km, wall, f, by))
         log(rows[-1])
+    # quality measures of a reconstruction against its reference: two passes
+    # over the FP64 pair (band sums, spectral angles), 32 bytes per entry
+    for name, dims in (("512x512x224", (512, 512, 224)), ("512x217x204", (512, 217, 204))):
+        N = int(np.prod(dims))
+        rng = np.random.default_rng([12969, 99])
+        Xh_ = rng.standard_normal(N).reshape(dims)
+        X = torch.from_numpy(Xh_).to(dev)
+        Y = X * 1.001
+        wall, km = _time_cell(lrc, lambda r: lrc.band_quality(X, Y), 10, None)
+        rows.append(_row(f"quality {name} (dense FP64 pair)", "f64", km, wall, 10.0 * N, 32.0 * N))
+        log(rows[-1])
+        del X, Y
+        torch.cuda.empty_cache()
     with open(path, "w") as fh:
         fh.write("\n".join(rows) + "\n")
 
@@ -595,6 +609,59 @@ def grid(path, dev, lrc):
         fh.write("\n".join(out) + "\n")
 
 
+# ---------------------------------------------------- fixed-memory study ---
+FM_CUBES = [("145x145x200", (145, 145, 200)), ("610x340x103", (610, 340, 103)), ("83x86x204", (83, 86, 204)),
+            ("512x217x204", (512, 217, 204))]
+
+
+def fixed_memory(path, dev, lrc):
+    """The fixed-memory comparison (Sec. sec:hyperspectral_application) on
+    hyperspectral-shaped stand-ins of the four cube shapes: FP64 TT-SVD at
+    rank R, its cores rounded to FP32 / FP16, the rank-(R + delta) cores
+    left-orthogonalized and rounded on the device, and the memory-matched
+    FP64 rank for the FP16 compensated budget; quality measured on the
+    device.  TT-SVD itself (host, numpy) is the untimed offline step."""
+    import torch
+    from paper_2607_12969_amd import synth
+    R, delta = 32, 4
+    out = ["# Fixed-memory comparison on hyperspectral-shaped stand-ins (one MI355X)", "",
+           "Command: `python -u bench.py --fixed-memory FILE`. Per cube shape: a synthetic hyperspectral stand-in",
+           "(smooth nonnegative endmember spectra times softmax abundance maps, 1e-3 noise, unit Frobenius norm);",
+           f"FP64 TT-SVD (host) at rank R = {R} and R + delta = {R + delta}; the augmented cores left-orthogonalized",
+           "(`lrc_tt_left_orthogonalize`) and every low-precision core rounded on the device (`lrc_round`); the",
+           "FP64 memory-matched rank for the FP16 compensated budget from `lrc_tt_memory_matched_rank`; every",
+           "measure from `lrc_tt_quality` (FP64 contraction of the stored cores against the FP64 cube). PSNR,",
+           "SSIM and SAM do not depend on the cube's overall scale, so the normalization needs no undoing here.", "",
+           "| cube | method | ranks | storage MiB | compression | rel. error | PSNR dB | SSIM | SAM rad |",
+           "|---|---|---|---|---|---|---|---|---|"]
+    for name, dims in FM_CUBES:
+        T = synth.hyperspectral(shape=dims)
+        Td = torch.from_numpy(T).to(dev)
+        rb, ra = capped_ranks(dims, R), capped_ranks(dims, R + delta)
+        budget = lrc.tt_storage_bytes(dims, ra, "fp16")
+        Rmm, rmm = lrc.memory_matched_rank(dims, budget)
+        base = [torch.from_numpy(c).to(dev) for c in tt_svd_fixed(T, rb[1:3])]
+        aug = lrc.tt_left_orthogonalize([torch.from_numpy(c).to(dev) for c in tt_svd_fixed(T, ra[1:3])])
+        mm = [torch.from_numpy(c).to(dev) for c in tt_svd_fixed(T, rmm[1:3])]
+        methods = [("FP64, R", base, rb, "fp64"),
+                   ("FP32, R", [lrc.round_to(c, "fp32") for c in base], rb, "fp32"),
+                   ("FP16, R", [lrc.round_to(c, "fp16") for c in base], rb, "fp16"),
+                   ("FP32, R + delta", [lrc.round_to(c, "fp32") for c in aug], ra, "fp32"),
+                   ("FP16, R + delta", [lrc.round_to(c, "fp16") for c in aug], ra, "fp16"),
+                   (f"FP64 memory-matched (R = {Rmm})", mm, rmm, "fp64")]
+        dense = 8 * int(np.prod(dims))
+        for label, cores, ranks, p in methods:
+            q = lrc.tt_quality(cores, Td)
+            sb = lrc.tt_storage_bytes(dims, ranks, p)
+            out.append(f"| {name} | {label} | {tuple(ranks[1:-1])} | {sb / 2 ** 20:.3f} | {dense / sb:.1f} | "
+                       f"{q['rel_err']:.3e} | {q['psnr']:.2f} | {q['ssim']:.5f} | {q['sam']:.4e} |")
+            log(out[-1])
+        del Td, base, aug, mm
+        torch.cuda.empty_cache()
+    with open(path, "w") as fh:
+        fh.write("\n".join(out) + "\n")
+
+
 # ------------------------------------------------------------------ main ---
 
 def main():
@@ -608,6 +675,7 @@ def main():
     ap.add_argument("--sweep", default=None, help="write a per-kernel table over the workload grid")
     ap.add_argument("--quant", default=None, help="write the device rounding and TT gauge cells")
     ap.add_argument("--grid", default=None, help="write the paper's resident timing grid (synthetic stand-ins)")
+    ap.add_argument("--fixed-memory", default=None, help="write the fixed-memory comparison (synthetic stand-ins)")
     ap.add_argument("--copy-calibration", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -638,6 +706,9 @@ def main():
         return
     if args.grid:
         grid(args.grid, dev, lrc)
+        return
+    if args.fixed_memory:
+        fixed_memory(args.fixed_memory, dev, lrc)
         return
 
     wl = Workload(args.k, dev)

@@ -12,8 +12,9 @@
 //                 band's minimum and maximum;
 //   k_sam         one wave per pixel: dot product and squared norms over the
 //                 bands, the angle, summed per workgroup.
-// k_quality_finish adds the partials in a fixed order (bitwise reproducible
-// results) and forms the per-band measures and their means.
+// k_quality_reduce adds the row blocks' partials (one wave per statistic
+// and band) and k_quality_finish forms the per-band measures and their
+// means, both in a fixed order (bitwise reproducible results).
 #include <hip/hip_runtime.h>
 
 #include "lrc_device.h"
@@ -128,8 +129,35 @@ __global__ __launch_bounds__(256) void k_sam(const double* __restrict__ X, const
     }
 }
 
-// out: rel_err, mean PSNR, mean SSIM, mean SAM, SAM pixel count
-__global__ __launch_bounds__(256) void k_quality_finish(const double* __restrict__ part, int64_t nblk,
+// red[q * B + b] = the band sums (minimum / maximum for QS_MIN / QS_MAX)
+// over the nblk row blocks: one wave per (q, b), lane j taking blocks
+// j, j + 64, ... in order, then a fixed butterfly.
+__global__ __launch_bounds__(256) void k_quality_reduce(const double* __restrict__ part, int64_t nblk, int64_t B,
+                                                        double* __restrict__ red) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= QS_N * B) return;
+    const int q = (int)(w / B);
+    const int64_t b = w - (int64_t)q * B;
+    const double* src = part + (int64_t)q * B + b;
+    const int64_t stride = (int64_t)QS_N * B;
+    const bool mn = q == QS_MIN, mxq = q == QS_MAX;
+    double v = (mn || mxq) ? src[0] : 0.0;
+    for (int64_t k = lane; k < nblk; k += 64) {
+        const double o = src[k * stride];
+        v = mn ? (o < v ? o : v) : (mxq ? (o > v ? o : v) : v + o);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const double o = __shfl_xor(v, off, 64);
+        v = mn ? (o < v ? o : v) : (mxq ? (o > v ? o : v) : v + o);
+    }
+    if (lane == 0) red[w] = v;
+}
+
+// out: rel_err, mean PSNR, mean SSIM, mean SAM, SAM pixel count (red: the
+// band sums of k_quality_reduce)
+__global__ __launch_bounds__(256) void k_quality_finish(const double* __restrict__ red,
                                                         const double* __restrict__ part2, int64_t nblk2,
                                                         const double* __restrict__ X, int64_t P, int64_t B,
                                                         double* __restrict__ out) {
@@ -139,13 +167,7 @@ __global__ __launch_bounds__(256) void k_quality_finish(const double* __restrict
     const double np = (double)P;
     for (int64_t b = t; b < B; b += 256) {
         double v[QS_N];
-        for (int q = 0; q < QS_N; ++q) v[q] = q == QS_MIN || q == QS_MAX ? part[q * B + b] : 0.0;
-        for (int64_t k = 0; k < nblk; ++k) {
-            const double* o = part + k * QS_N * B + b;
-            for (int q = 0; q < QS_MIN; ++q) v[q] += o[q * B];
-            v[QS_MIN] = o[QS_MIN * B] < v[QS_MIN] ? o[QS_MIN * B] : v[QS_MIN];
-            v[QS_MAX] = o[QS_MAX * B] > v[QS_MAX] ? o[QS_MAX * B] : v[QS_MAX];
-        }
+        for (int q = 0; q < QS_N; ++q) v[q] = red[q * B + b];
         // L_b: range of the reference band, max(max|X_b|, 1) when constant
         double L = v[QS_MAX] - v[QS_MIN];
         if (!(L > 0.0)) {
@@ -204,7 +226,7 @@ static void quality_grid(int64_t P, int64_t* nblk, int64_t* rows, int64_t* nblk2
 size_t quality_workspace_bytes(int64_t P, int64_t B) {
     int64_t nblk, rows, nblk2;
     quality_grid(P, &nblk, &rows, &nblk2);
-    return round_up(nblk * QS_N * B * 8, 256) + round_up(nblk2 * 2 * 8, 256) + 256;
+    return round_up(nblk * QS_N * B * 8, 256) + round_up(QS_N * B * 8, 256) + round_up(nblk2 * 2 * 8, 256) + 256;
 }
 
 template <typename Y>
@@ -213,13 +235,16 @@ static hipError_t quality_typed(const double* X, const Y* Xh, double scale, int6
     int64_t nblk, rows, nblk2;
     quality_grid(P, &nblk, &rows, &nblk2);
     double* part = static_cast<double*>(ws.take((size_t)(nblk * QS_N * B * 8)));
+    double* red = static_cast<double*>(ws.take((size_t)(QS_N * B * 8)));
     double* part2 = static_cast<double*>(ws.take((size_t)(nblk2 * 2 * 8)));
     if (ws.overrun) return hipErrorOutOfMemory;
     KernelTimer t("quality_f64", stream);
     hipLaunchKernelGGL((k_band_stats<Y>), dim3((unsigned)nblk), dim3(256), 0, stream, X, Xh, scale, P, B, rows,
                        part);
     hipLaunchKernelGGL((k_sam<Y>), dim3((unsigned)nblk2), dim3(256), 0, stream, X, Xh, scale, P, B, part2);
-    hipLaunchKernelGGL(k_quality_finish, dim3(1), dim3(256), 0, stream, part, nblk, part2, nblk2, X, P, B, out);
+    hipLaunchKernelGGL(k_quality_reduce, dim3((unsigned)((QS_N * B + 3) / 4)), dim3(256), 0, stream, part, nblk, B,
+                       red);
+    hipLaunchKernelGGL(k_quality_finish, dim3(1), dim3(256), 0, stream, red, part2, nblk2, X, P, B, out);
     return hipGetLastError();
 }
 
