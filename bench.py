@@ -482,19 +482,31 @@ def capped_ranks(dims, nominal):
     return ranks + [1]
 
 
-def _grid_task(lrc, calls, rounds=3, blocks=5, samples=20, warmup=30, seed=0):
+def _grid_task(lrc, calls, rounds=3, blocks=5, samples=4, warmup=30, seed=0):
     """Times of every method of one task: calls[i]() launches method i.
-    Returns per-method medians (ms) and the block medians per method."""
+    Each sample is one event pair around `reps` back-to-back calls, reps
+    calibrated per method so that a sample lasts about 2 ms (at most 256).
+    Returns per-method medians (ms per call) and the block medians."""
     import torch
     nm = len(calls)
     for _ in range(warmup):
         for c in calls:
             c()
     torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    reps = []
+    for c in calls:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        for _ in range(8):
+            c()
+        b.record(st)
+        torch.cuda.synchronize()
+        t1 = a.elapsed_time(b) / 8
+        reps.append(int(max(1, min(256, round(2.0 / max(t1, 1e-4))))))
     rng = np.random.default_rng([12969, 77, seed])
     allt = [[] for _ in range(nm)]
     bmed = [[] for _ in range(nm)]
-    st = torch.cuda.current_stream()
     for _ in range(rounds):
         for _ in range(blocks):
             order = rng.permutation(nm)
@@ -503,12 +515,13 @@ def _grid_task(lrc, calls, rounds=3, blocks=5, samples=20, warmup=30, seed=0):
                 for i in order:
                     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     a.record(st)
-                    calls[i]()
+                    for _ in range(reps[i]):
+                        calls[i]()
                     b.record(st)
                     ev[i].append((a, b))
             torch.cuda.synchronize()
             for i in range(nm):
-                ts = [a.elapsed_time(b) for a, b in ev[i]]
+                ts = [a.elapsed_time(b) / reps[i] for a, b in ev[i]]
                 allt[i] += ts
                 bmed[i].append(float(np.median(ts)))
     return [float(np.median(t)) for t in allt], bmed
@@ -527,8 +540,10 @@ def grid(path, dev, lrc):
     out = ["# The paper's resident timing grid on one MI355X (synthetic stand-ins)", "",
            "Command: `python -u bench.py --grid FILE`. Inputs resident in HBM and reused across calls (the",
            "paper's resident protocol, so small tasks run from the Infinity Cache); per task 30 warmups, then",
-           "3 rounds x 5 blocks x 20 samples per method in a seeded shuffled order, each sample timed with HIP",
-           "events; time = geometric mean over tasks of the per-task medians; speedup = geometric mean over tasks",
+           "3 rounds x 5 blocks x 4 samples per method in a seeded shuffled order (the paper takes 20 samples",
+           "per block; 4 keep the run near a minute), each sample one HIP event pair around back-to-back calls",
+           "calibrated to about 2 ms (at most 256 calls); time = geometric mean over tasks of the per-task",
+           "medians per call; speedup = geometric mean over tasks",
            "of the median paired (FP64 / method) block-median ratio, with a 10,000-resample bootstrap interval",
            "over tasks; storage = stored bytes relative to the FP64 base.", ""]
     # ---- matrix application

@@ -64,53 +64,54 @@ struct TTArgs {
 };
 
 // Staged copies of the middle core G_{d-1} [rL][n_mid][rM] and the last core
-// G_d [rM][n_last], zero padded to Kp2 x Rt and Kp3 x ncp (layouts at TTSet).
-template <typename T>
+// G_d [rM][n_last], zero padded to Kp2 x Rt and Kp3 x ncp (layouts at TTSet),
+// and, when g1 is given, the rows of G_1 [n_1][r_1] at pitch Kp2, zero padded
+// (FP16 wave tiles load a lane's eight K values of a row with one aligned
+// 16-byte load): one launch for all three.  IDX is the index type: 32-bit
+// when every segment is below 2^31 elements (the divisions are much cheaper).
+template <typename T, typename IDX>
 __global__ __launch_bounds__(256) void k_stage(const T* __restrict__ gmid, const T* __restrict__ glast,
-                                               T* __restrict__ smid, T* __restrict__ slast, int64_t n_mid,
-                                               int64_t n_last, int rL, int rM, int Kp2, int Kp3, int Rt, int ncp) {
+                                               const T* __restrict__ g1, T* __restrict__ smid,
+                                               T* __restrict__ slast, T* __restrict__ srows, int64_t n_mid,
+                                               int64_t n_last, int64_t n1, int rL, int rM, int r1, int Kp2, int Kp3,
+                                               int Rt, int ncp) {
     constexpr bool kcontig = PrecTraits<T>::KPL > 1;
     const int64_t tot_mid = n_mid * Rt * Kp2;
     const int64_t tot_last = (int64_t)ncp * Kp3;
+    const int64_t tot_rows = g1 ? n1 * Kp2 : 0;
     const int64_t stride = (int64_t)gridDim.x * 256;
-    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < tot_mid + tot_last; idx += stride) {
+    const int64_t total = tot_mid + tot_last + tot_rows;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += stride) {
         if (idx < tot_mid) {
-            int64_t s, t, i;
+            const IDX x = (IDX)idx;
+            IDX s, t, i;
             if (kcontig) {
-                s = idx % Kp2;
-                t = (idx / Kp2) % Rt;
-                i = idx / ((int64_t)Kp2 * Rt);
+                s = x % (IDX)Kp2;
+                t = (x / (IDX)Kp2) % (IDX)Rt;
+                i = x / ((IDX)Kp2 * (IDX)Rt);
             } else {
-                t = idx % Rt;
-                s = (idx / Rt) % Kp2;
-                i = idx / ((int64_t)Kp2 * Rt);
+                t = x % (IDX)Rt;
+                s = (x / (IDX)Rt) % (IDX)Kp2;
+                i = x / ((IDX)Kp2 * (IDX)Rt);
             }
-            smid[idx] = (t < rM && s < rL) ? gmid[(s * n_mid + i) * rM + t] : T(0);
+            smid[idx] = ((int)t < rM && (int)s < rL) ? gmid[((int64_t)s * n_mid + (int64_t)i) * rM + (int64_t)t] : T(0);
+        } else if (idx < tot_mid + tot_last) {
+            const IDX j = (IDX)(idx - tot_mid);
+            IDX t, c;
+            if (kcontig) {
+                t = j % (IDX)Kp3;
+                c = j / (IDX)Kp3;
+            } else {
+                c = j % (IDX)ncp;
+                t = j / (IDX)ncp;
+            }
+            slast[(int64_t)j] = ((int)t < rM && (int64_t)c < n_last) ? glast[(int64_t)t * n_last + (int64_t)c] : T(0);
         } else {
-            const int64_t j = idx - tot_mid;
-            int64_t t, c;
-            if (kcontig) {
-                t = j % Kp3;
-                c = j / Kp3;
-            } else {
-                c = j % ncp;
-                t = j / ncp;
-            }
-            slast[j] = (t < rM && c < n_last) ? glast[t * n_last + c] : T(0);
+            const IDX j = (IDX)(idx - tot_mid - tot_last);
+            const IDX L = j / (IDX)Kp2;
+            const int sc = (int)(j - L * (IDX)Kp2);
+            srows[(int64_t)j] = sc < r1 ? g1[(int64_t)L * r1 + sc] : T(0);
         }
-    }
-}
-
-// Rows of G_1 [n_1][r_1] at pitch Kp2, zero padded (FP16 wave tiles load a
-// lane's eight K values of a row with one aligned 16-byte load).
-template <typename T>
-__global__ __launch_bounds__(256) void k_stage_rows(const T* __restrict__ g1, T* __restrict__ dst, int64_t n1,
-                                                    int r1, int Kp2) {
-    const int64_t tot = n1 * Kp2;
-    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < tot; idx += (int64_t)gridDim.x * 256) {
-        const int64_t L = idx / Kp2;
-        const int s = (int)(idx % Kp2);
-        dst[idx] = s < r1 ? g1[L * r1 + s] : T(0);
     }
 }
 
@@ -1155,7 +1156,9 @@ static void launch_wave(int nkb, int npb, dim3 grid, hipStream_t st, const TTArg
     } while (0)
     switch (nkb) {
     case 4: LRC_TWK(4); break;
+    case 5: LRC_TWK(5); break;
     case 8: LRC_TWK(8); break;
+    case 9: LRC_TWK(9); break;
     case 12: LRC_TWK(12); break;
     case 16: LRC_TWK(16); break;
     default: LRC_TWK(17); break;
@@ -1193,18 +1196,59 @@ __device__ __forceinline__ void transpose_groups(float4_t& a) {
     a = float4_t{v0, v1, v2, v3};
 }
 
+// Output of one 16 x 16 block of a reconstruction wave tile (lane (r, g)
+// holding row L0 + 16 pb + r, columns cbase + 4 g .. + 3) in storage type T.
+// Rows that allow it take one vector store per lane (TS false, the kernel
+// variant for TTArgs::vec4).  Otherwise (TS: n_last not a multiple of 4, or
+// a misaligned output) the block goes through the
+// wave's own 16 x 17 LDS tile `stl`, so that each store instruction writes
+// 16 consecutive elements of each of 4 rows instead of four scattered
+// elements per lane.  The wavefront-scope fences keep the exchange in order
+// (LDS operations of one wave complete in order).
+template <typename T, int NPB, bool TS>
+__device__ __forceinline__ void store_block(const TTArgs& a, float* stl, int64_t i, int64_t L0, int64_t cbase,
+                                            int r, int g, const float4_t (&acc)[NPB]) {
+    T* out = static_cast<T*>(a.out);
+    if constexpr (!TS) {
+        const int64_t c0 = cbase + 4 * g;
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            const int64_t L = L0 + 16 * pb + r;
+            if (L >= a.NL || c0 + 3 >= a.n_last) continue;
+            T* dst = out + (L * a.n_mid + i) * a.n_last + c0;
+            typedef T v4_t __attribute__((ext_vector_type(4)));
+            *reinterpret_cast<v4_t*>(dst) = v4_t{(T)acc[pb][0], (T)acc[pb][1], (T)acc[pb][2], (T)acc[pb][3]};
+        }
+    } else {
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+        for (int v = 0; v < 4; ++v) stl[r * 17 + 4 * g + v] = acc[pb][v];
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        const int64_t col = cbase + r;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int rr = 4 * j + g;
+            const float v = stl[rr * 17 + r];
+            const int64_t L = L0 + 16 * pb + rr;
+            if (L < a.NL && col < a.n_last) out[(L * a.n_mid + i) * a.n_last + col] = (T)v;
+        }
+    }
+    }
+}
+
 // FP32 last product of a reconstruction wave tile, computed transposed
 // (core fragment as A, so that lane (r, g), value v holds row L0 + 16 pb + r,
 // column 16 cp + 4 g + v: four consecutive columns, stored as one 16-byte
 // vector where the row allows it).  Core ring as in last_store_w.
-template <int NKB, int NPB, int D>
-__device__ __forceinline__ void last_store_w32(const TTArgs& a, int64_t i, int64_t L0, int r, int g,
+template <int NKB, int NPB, int D, bool TS>
+__device__ __forceinline__ void last_store_w32(const TTArgs& a, float* stl, int64_t i, int64_t L0, int r, int g,
                                                const float (&zf)[NPB][NKB]) {
     static_assert(D <= NKB, "ring deeper than a block");
     const int n_cb = (int)((a.n_last + 15) / 16);
     const float* b0 = static_cast<const float*>(a.set[0].core[1]);
     const int tl = a.set[0].rM - 1;
-    float* out = static_cast<float*>(a.out);
     const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
     auto colc = [&](int cp) {
         const uint32_t c = (uint32_t)(16 * cp + r);
@@ -1238,30 +1282,18 @@ __device__ __forceinline__ void last_store_w32(const TTArgs& a, int64_t i, int64
         };
         if (cp + 1 < n_cb) block(std::true_type{});
         else block(std::false_type{});
-        const int64_t c0 = (int64_t)cp * 16 + 4 * g;
-#pragma unroll
-        for (int pb = 0; pb < NPB; ++pb) {
-            const int64_t L = L0 + 16 * pb + r;
-            if (L >= a.NL) continue;
-            float* dst = out + (L * a.n_mid + i) * a.n_last + c0;
-            if (a.vec4 && c0 + 3 < a.n_last) {
-                *reinterpret_cast<float4_t*>(dst) = acc[pb];
-            } else {
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (c0 + v < a.n_last) dst[v] = acc[pb][v];
-            }
-        }
+        store_block<float, NPB, TS>(a, stl, i, L0, (int64_t)cp * 16, r, g, acc);
         c = cn;
     }
 }
 
 // FP32 reconstruction for d = 3 by wave tiles (as k_tt_wave, with the
 // accumulators of the middle product transposed into A-fragment order).
-template <int NKB, int NPB>
+template <int NKB, int NPB, bool TS>
 __global__ __launch_bounds__(256) void k_tt_wave32(TTArgs a, int64_t ntiles) {
     constexpr int NT = (NKB + 3) / 4;
     constexpr int D = NKB < 8 ? NKB : 8;
+    __shared__ float st_tile[4][16 * 17];   // per wave: rows not fit for vector stores
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
@@ -1287,12 +1319,16 @@ __global__ __launch_bounds__(256) void k_tt_wave32(TTArgs a, int64_t ntiles) {
         }
         int ln = lane;
         asm volatile("" : "+v"(ln));
-        last_store_w32<NKB, NPB, D>(a, i, L0, ln & 15, ln >> 4, zf);
+        last_store_w32<NKB, NPB, D, TS>(a, st_tile[wave], i, L0, ln & 15, ln >> 4, zf);
     }
 }
 
 static void launch_wave32(int nkb, int npb, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
-#define LRC_TW(K, P) hipLaunchKernelGGL((k_tt_wave32<K, P>), grid, dim3(256), 0, st, a, ntiles)
+#define LRC_TW(K, P)                                                                              \
+    do {                                                                                          \
+        if (a.vec4) hipLaunchKernelGGL((k_tt_wave32<K, P, false>), grid, dim3(256), 0, st, a, ntiles); \
+        else hipLaunchKernelGGL((k_tt_wave32<K, P, true>), grid, dim3(256), 0, st, a, ntiles);        \
+    } while (0)
 #define LRC_TWK(K) \
     do {                                 \
         if (npb == 1) LRC_TW(K, 1);      \
@@ -1301,7 +1337,9 @@ static void launch_wave32(int nkb, int npb, dim3 grid, hipStream_t st, const TTA
     } while (0)
     switch (nkb) {
     case 4: LRC_TWK(4); break;
+    case 5: LRC_TWK(5); break;
     case 8: LRC_TWK(8); break;
+    case 9: LRC_TWK(9); break;
     case 12: LRC_TWK(12); break;
     case 16: LRC_TWK(16); break;
     default: LRC_TWK(17); break;
@@ -1436,13 +1474,12 @@ __device__ __forceinline__ half8_t regroup16(const float4_t& X, const float4_t& 
 // column 16 cp + 4 g + v (four consecutive columns, one 8-byte store where
 // the row allows it).  Each core fragment is refetched for the next column
 // block right after its use.
-template <int NKB, int NPB>
-__device__ __forceinline__ void last_store_w16(const TTArgs& a, int64_t i, int64_t L0, int r, int g,
+template <int NKB, int NPB, bool TS>
+__device__ __forceinline__ void last_store_w16(const TTArgs& a, float* stl, int64_t i, int64_t L0, int r, int g,
                                                const half8_t (&zf)[NPB][NKB]) {
     const int n_cb = (int)((a.n_last + 15) / 16);
     const int Kp3 = a.set[0].Kp3;
     const half8_t* b0 = static_cast<const half8_t*>(a.set[0].st_last);   // [ncp][Kp3], 16-byte units
-    half_t* out = static_cast<half_t*>(a.out);
     uint32_t off = (uint32_t)(r * Kp3 + 8 * g) * 2u;
     const uint32_t cstep = 16u * (uint32_t)Kp3 * 2u;
     half8_t N[NKB];
@@ -1459,22 +1496,7 @@ __device__ __forceinline__ void last_store_w16(const TTArgs& a, int64_t i, int64
             for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(N[s], zf[pb][s], acc[pb]);
             N[s] = ld_off(b0 + 4 * s, offn);
         }
-        const int64_t c0 = (int64_t)cp * 16 + 4 * g;
-#pragma unroll
-        for (int pb = 0; pb < NPB; ++pb) {
-            const int64_t L = L0 + 16 * pb + r;
-            if (L >= a.NL) continue;
-            half_t* dst = out + (L * a.n_mid + i) * a.n_last + c0;
-            if (a.vec4 && c0 + 3 < a.n_last) {
-                typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
-                *reinterpret_cast<h4_t*>(dst) = h4_t{(half_t)acc[pb][0], (half_t)acc[pb][1], (half_t)acc[pb][2],
-                                                     (half_t)acc[pb][3]};
-            } else {
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (c0 + v < a.n_last) dst[v] = (half_t)acc[pb][v];
-            }
-        }
+        store_block<half_t, NPB, TS>(a, stl, i, L0, (int64_t)cp * 16, r, g, acc);
         off = offn;
     }
 }
@@ -1482,11 +1504,10 @@ __device__ __forceinline__ void last_store_w16(const TTArgs& a, int64_t i, int64
 // As last_store_w16 with the staged last core resident in LDS (rows of
 // pitch ldp halves): the fragments are LDS reads, which do not wait for the
 // output stores (global loads would, as loads and stores complete in order).
-template <int NKB, int NPB>
-__device__ __forceinline__ void last_store_w16l(const TTArgs& a, const half_t* Ls, int ldp, int64_t i, int64_t L0,
-                                                int r, int g, const half8_t (&zf)[NPB][NKB]) {
+template <int NKB, int NPB, bool TS>
+__device__ __forceinline__ void last_store_w16l(const TTArgs& a, float* stl, const half_t* Ls, int ldp, int64_t i,
+                                                int64_t L0, int r, int g, const half8_t (&zf)[NPB][NKB]) {
     const int n_cb = (int)((a.n_last + 15) / 16);
-    half_t* out = static_cast<half_t*>(a.out);
     for (int cp = 0; cp < n_cb; ++cp) {
         const half_t* lrow = Ls + (16 * cp + r) * ldp + 8 * g;
         half8_t f[NKB];
@@ -1499,31 +1520,17 @@ __device__ __forceinline__ void last_store_w16l(const TTArgs& a, const half_t* L
         for (int s2 = 0; s2 < NKB; ++s2)
 #pragma unroll
             for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f[s2], zf[pb][s2], acc[pb]);
-        const int64_t c0 = (int64_t)cp * 16 + 4 * g;
-#pragma unroll
-        for (int pb = 0; pb < NPB; ++pb) {
-            const int64_t L = L0 + 16 * pb + r;
-            if (L >= a.NL) continue;
-            half_t* dst = out + (L * a.n_mid + i) * a.n_last + c0;
-            if (a.vec4 && c0 + 3 < a.n_last) {
-                typedef _Float16 h4_t __attribute__((ext_vector_type(4)));
-                *reinterpret_cast<h4_t*>(dst) = h4_t{(half_t)acc[pb][0], (half_t)acc[pb][1], (half_t)acc[pb][2],
-                                                     (half_t)acc[pb][3]};
-            } else {
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (c0 + v < a.n_last) dst[v] = (half_t)acc[pb][v];
-            }
-        }
+        store_block<half_t, NPB, TS>(a, stl, i, L0, (int64_t)cp * 16, r, g, acc);
     }
 }
 
 // LDSB: the staged last core [ncp][Kp3] is first copied into LDS at pitch
 // Kp3 + 8 halves (16-byte fragment reads of 16 rows fall on distinct banks).
-template <int NKB, int NPB, bool LDSB>
+template <int NKB, int NPB, bool LDSB, bool TS>
 __global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
     constexpr int NT = 2 * NKB;
     extern __shared__ double4_t smem_v[];
+    __shared__ float st_tile[4][16 * 17];   // per wave: rows not fit for vector stores
     half_t* Ls = reinterpret_cast<half_t*>(smem_v);
     const int ldp = a.set[0].Kp3 + 8;
     if constexpr (LDSB) {
@@ -1565,8 +1572,8 @@ __global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
         }
         int ln = lane;
         asm volatile("" : "+v"(ln));
-        if constexpr (LDSB) last_store_w16l<NKB, NPB>(a, Ls, ldp, i, L0, ln & 15, ln >> 4, zf);
-        else last_store_w16<NKB, NPB>(a, i, L0, ln & 15, ln >> 4, zf);
+        if constexpr (LDSB) last_store_w16l<NKB, NPB, TS>(a, st_tile[wave], Ls, ldp, i, L0, ln & 15, ln >> 4, zf);
+        else last_store_w16<NKB, NPB, TS>(a, st_tile[wave], i, L0, ln & 15, ln >> 4, zf);
     }
 }
 
@@ -1576,8 +1583,13 @@ static void launch_wave16(int nkb, int npb, dim3 grid, hipStream_t st, const TTA
     const bool in_lds = lds <= 65536;
 #define LRC_TW(K, P)                                                                                  \
     do {                                                                                              \
-        if (in_lds) hipLaunchKernelGGL((k_tt_wave16<K, P, true>), grid, dim3(256), lds, st, a, ntiles); \
-        else hipLaunchKernelGGL((k_tt_wave16<K, P, false>), grid, dim3(256), 0, st, a, ntiles);        \
+        if (in_lds && a.vec4)                                                                         \
+            hipLaunchKernelGGL((k_tt_wave16<K, P, true, false>), grid, dim3(256), lds, st, a, ntiles);  \
+        else if (in_lds)                                                                              \
+            hipLaunchKernelGGL((k_tt_wave16<K, P, true, true>), grid, dim3(256), lds, st, a, ntiles);   \
+        else if (a.vec4)                                                                              \
+            hipLaunchKernelGGL((k_tt_wave16<K, P, false, false>), grid, dim3(256), 0, st, a, ntiles);   \
+        else hipLaunchKernelGGL((k_tt_wave16<K, P, false, true>), grid, dim3(256), 0, st, a, ntiles);   \
     } while (0)
 #define LRC_TWK(K) \
     do {                                 \
@@ -1750,10 +1762,16 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         if (prec == P16) {
             if (kp3 <= 96) nkb = kp3 / 32;
         } else {
-            static const int kNkb[] = {4, 8, 12, 16, 17};
-            for (int c : kNkb)
-                if (4 * c >= kp3) {
-                    nkb = c;
+            // the certificate's kernel exists for the first list only; one set
+            // (reconstruction) also has K extents 20 and 36 (ranks 17-20 and
+            // 33-36, the paper's TT timing schedules) without padding
+            static const int kNkb3[] = {4, 8, 12, 16, 17};
+            static const int kNkb1[] = {4, 5, 8, 9, 12, 16, 17};
+            const int* lst = nsets == 1 ? kNkb1 : kNkb3;
+            const int cnt = nsets == 1 ? 7 : 5;
+            for (int c = 0; c < cnt; ++c)
+                if (4 * lst[c] >= kp3) {
+                    nkb = lst[c];
                     break;
                 }
         }
@@ -1772,7 +1790,10 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
             }
             int npb = 1;
             if (nsets == 1) {
-                const int dflt = prec == P64 ? 2 : 4;
+                // fewer row blocks per wave where the tiles would not give
+                // every SIMD two waves (2048 tiles)
+                int dflt = prec == P64 ? 2 : 4;
+                while (dflt > 1 && p.n_mid * ((p.NL + 16 * dflt - 1) / (16 * dflt)) < 2048) dflt /= 2;
                 npb = tune_env("LRC_TT_WAVE_NPB", dflt);
                 if (npb != 1 && npb != 2 && npb != 4) npb = dflt;
             }
@@ -1932,28 +1953,31 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
             T* smid = static_cast<T*>(ws.take((size_t)p.n_mid * ps.Rt * ps.Kp2 * sizeof(T)));
             T* slast = static_cast<T*>(ws.take((size_t)a.ncp * ps.Kp3 * sizeof(T)));
             if (ws.overrun || !smid || !slast) return hipErrorOutOfMemory;
-            const int64_t tot = p.n_mid * ps.Rt * ps.Kp2 + (int64_t)a.ncp * ps.Kp3;
+            // FP16 wave tiles also take the rows of G_1 at pitch Kp2
+            const bool rows = sizeof(T) == 2 && p.wave_nkb;
+            T* sl = nullptr;
+            if (rows) {
+                sl = static_cast<T*>(ws.take((size_t)p.NL * ps.Kp2 * sizeof(T)));
+                if (ws.overrun || !sl) return hipErrorOutOfMemory;
+            }
+            const int64_t tmid = p.n_mid * ps.Rt * ps.Kp2, tlast = (int64_t)a.ncp * ps.Kp3;
+            const int64_t trows = rows ? p.NL * ps.Kp2 : 0;
+            const int64_t tot = tmid + tlast + trows;
             int64_t gs = (tot + 255) / 256;
             if (gs > 4096) gs = 4096;
+            const bool narrow = tmid < 2147483647LL && tlast < 2147483647LL && trows < 2147483647LL;
             KernelTimer ts(stage_label, stream);
-            hipLaunchKernelGGL(k_stage<T>, dim3((unsigned)gs), dim3(256), 0, stream, (const T*)cores[q][p.d - 2],
-                               (const T*)cores[q][p.d - 1], smid, slast, p.n_mid, p.n_last, ps.rL, ps.rM, ps.Kp2,
-                               ps.Kp3, ps.Rt, a.ncp);
+#define LRC_STAGE(IDX)                                                                                       \
+    hipLaunchKernelGGL((k_stage<T, IDX>), dim3((unsigned)gs), dim3(256), 0, stream, (const T*)cores[q][p.d - 2], \
+                       (const T*)cores[q][p.d - 1], rows ? (const T*)S.core[2] : (const T*)nullptr, smid, slast, sl, \
+                       p.n_mid, p.n_last, p.NL, ps.rL, ps.rM, ps.rL, ps.Kp2, ps.Kp3, ps.Rt, a.ncp)
+            if (narrow) LRC_STAGE(uint32_t);
+            else LRC_STAGE(int64_t);
+#undef LRC_STAGE
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
             S.st_mid = smid;
             S.st_last = slast;
-        }
-        if (sizeof(T) == 2 && p.wave_nkb) {
-            T* sl = static_cast<T*>(ws.take((size_t)p.NL * ps.Kp2 * sizeof(T)));
-            if (ws.overrun || !sl) return hipErrorOutOfMemory;
-            int64_t gs = (p.NL * ps.Kp2 + 255) / 256;
-            if (gs > 4096) gs = 4096;
-            KernelTimer ts(stage_label, stream);
-            hipLaunchKernelGGL(k_stage_rows<T>, dim3((unsigned)gs), dim3(256), 0, stream, (const T*)S.core[2], sl,
-                               p.NL, ps.rL, ps.Kp2);
-            hipError_t e = hipGetLastError();
-            if (e != hipSuccess) return e;
             S.st_left = sl;
         }
     }

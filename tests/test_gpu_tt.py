@@ -131,7 +131,11 @@ def test_hyperspectral_shape(lrc, ranks_fp64, ranks_low):
 @pytest.mark.parametrize("layout", ["npb1", "npb2", "npb4", "lds"])
 @pytest.mark.parametrize("dims,ranks", [
     ((37, 23, 45), (1, 12, 13, 1)),     # last-product K extent 16
+    ((33, 5, 45), (1, 17, 17, 1)),      # 20 (ranks 17-20)
+    ((30, 7, 50), (1, 12, 20, 1)),      # 20
     ((64, 7, 40), (1, 20, 30, 1)),      # 32
+    ((50, 4, 33), (1, 33, 33, 1)),      # 36 (ranks 33-36)
+    ((40, 6, 60), (1, 30, 36, 1)),      # 36
     ((48, 5, 100), (1, 40, 44, 1)),     # 48
     ((70, 3, 90), (1, 62, 62, 1)),      # 64
     ((80, 6, 70), (1, 64, 65, 1)),      # 68
@@ -143,7 +147,8 @@ def test_three_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
     wave tiles of 16, 32 and 64 rows (each register layout of the last
     product; FP16 takes K steps of 32, so ranks up to 96 fit) and the LDS
     tiles, with ragged n_1 and n_3 (odd n_3: the rows are not aligned for
-    the vector stores, which fall back to scalar ones)."""
+    the vector stores, which fall back to scalar ones); FP64 and FP32 also
+    have K extents 20 and 36 without padding."""
     if layout == "lds":
         monkeypatch.setenv("LRC_TT_WAVE", "0")
     else:
