@@ -1792,7 +1792,7 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
             if (nsets == 1) {
                 // fewer row blocks per wave where the tiles would not give
                 // every SIMD two waves (2048 tiles)
-                int dflt = prec == P64 ? 2 : 4;
+                int dflt = 4;
                 while (dflt > 1 && p.n_mid * ((p.NL + 16 * dflt - 1) / (16 * dflt)) < 2048) dflt /= 2;
                 npb = tune_env("LRC_TT_WAVE_NPB", dflt);
                 if (npb != 1 && npb != 2 && npb != 4) npb = dflt;
