@@ -754,33 +754,29 @@ __global__ __launch_bounds__(256) void k_p1_stream(
     }
 }
 
-// One workgroup per column group: the columns of the group, including the
-// zero rows j in [k, ldt) of T'^T.
+// One wave per output (j, c) of T'^T, including the zero rows j in [k, ldt):
+// lane l adds the split partials l, l + 64, ... in order, then a fixed
+// butterfly over the wave (one round of loads instead of a chain over all
+// splits per thread).
 template <typename T, int NB>
 __global__ __launch_bounds__(256) void k_p1_stream_finish(
     const typename PrecTraits<T>::acc* __restrict__ part, const T* __restrict__ s, T* __restrict__ Tt,
     int64_t ldt, int64_t k, int64_t b, int splits) {
     using Acc = typename PrecTraits<T>::acc;
-    const int tid = threadIdx.x, jg = blockIdx.x;
-    for (int idx = tid; idx < 64 * NB; idx += 256) {
-        const int jl = idx / NB, c = idx % NB;
-        const int64_t jj = (int64_t)jg * 64 + jl;
-        if (c >= b || jj >= ldt) continue;
-        Acc sum = 0;
-        if (jj < k) {
-            // the split partials in order, fetched 16 at a time
-            const Acc* src = part + ((int64_t)jg * splits * 64 + jl) * NB + c;
-            const int64_t qs = 64 * NB;
-            int q = 0;
-            for (; q + 16 <= splits; q += 16) {
-                Acc v[16];
-#pragma unroll
-                for (int u = 0; u < 16; ++u) v[u] = __builtin_nontemporal_load(src + (q + u) * qs);
-#pragma unroll
-                for (int u = 0; u < 16; ++u) sum += v[u];
-            }
-            for (; q < splits; ++q) sum += __builtin_nontemporal_load(src + q * qs);
-        }
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= ldt * NB) return;
+    const int64_t jj = w / NB;
+    const int c = (int)(w - jj * NB);
+    if (c >= b) return;
+    Acc sum = 0;
+    if (jj < k) {
+        const int64_t jg = jj / 64, jl = jj - jg * 64;
+        const Acc* src = part + (jg * splits * 64 + jl) * NB + c;
+        for (int q = lane; q < splits; q += 64) sum += __builtin_nontemporal_load(src + (int64_t)q * 64 * NB);
+        sum = wave_sum(sum);
+    }
+    if (lane == 0) {
         const Acc sj = (jj < k) ? to_acc(s[jj]) : Acc(0);
         Tt[(int64_t)c * ldt + jj] = to_storage<T>(sj * sum);
     }
@@ -980,8 +976,8 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     do {                                                                                                  \
         hipLaunchKernelGGL((k_p1_stream<T, NB>), g1, dim3(256), 0, stream, V, X, part, n, k, b, p.chunk,  \
                            p.splits);                                                                     \
-        hipLaunchKernelGGL((k_p1_stream_finish<T, NB>), dim3(p.tiles_m), dim3(256), 0, stream, part, s,  \
-                           Tt, ldt, k, b, p.splits);                                                      \
+        hipLaunchKernelGGL((k_p1_stream_finish<T, NB>), dim3((unsigned)((ldt * NB + 3) / 4)), dim3(256), 0, \
+                           stream, part, s, Tt, ldt, k, b, p.splits);                                     \
     } while (0)
             if (b <= 1) LRC_P1S(1); else if (b <= 2) LRC_P1S(2); else if (b <= 4) LRC_P1S(4); else LRC_P1S(8);
 #undef LRC_P1S
