@@ -540,3 +540,65 @@ def memory_matched_rank(dims, budget_bytes: int):
         if ranks == capped_ranks(dims, R + 1):   # every rank capped: storage stops growing
             return best
         R += 1
+
+
+# ---------------------------------------------------------------------------
+# Randomized factorizations (the end-to-end decomposition that Sec.
+# sec:conclusion leaves to future work).  The paper fixes no GPU method for
+# it; these follow the randomized range finder of Halko, Martinsson and Tropp
+# (SIAM Review 2011: Gaussian sketch, optional subspace iterations with
+# re-orthonormalization, then the exact SVD of the small projected matrix),
+# and TT-SVD (Sec. 5.1) with every truncated SVD replaced by that.  The
+# Gaussian test vectors are inputs: the caller draws them.
+# ---------------------------------------------------------------------------
+
+def randomized_svd(A, Omega, k: int, power_iters: int = 0):
+    """Rank-k randomized SVD of A (m x n) with the l test vectors given as
+    the rows of Omega (l x n), k <= l <= min(m, n):
+      Y = A Omega^T, Q = orth(Y);  q times: Q = orth(A orth(A^T Q));
+      B = Q^T A = Ub S Vt (exact SVD);  U = Q Ub[:, :k].
+    Returns U (m x k), S (k), Vt (k x n).  U diag(S) Vt = Q_k Q_k^T A with
+    Q_k = U: an orthogonal projection of A's columns."""
+    A = _c(A)
+    Om = _c(Omega)
+    m, n = A.shape
+    l = Om.shape[0]
+    if Om.shape[1] != n or not (1 <= k <= l <= min(m, n)):
+        raise ValueError("randomized_svd: need Omega l x n with k <= l <= min(m, n)")
+    Q, _ = qr(matmul(A, Om.T))
+    for _ in range(int(power_iters)):
+        Z, _ = qr(matmul(A.T, Q))
+        Q, _ = qr(matmul(A, Z))
+    B = matmul(Q.T, A)
+    Ub, S, Vt = svd(B)
+    return matmul(Q, Ub[:, :k]), S[:k].copy(), np.ascontiguousarray(Vt[:k])
+
+
+def tt_svd_randomized(T: np.ndarray, ranks, omegas, power_iters: int = 0):
+    """TT-SVD (Sec. 5.1) with the truncated SVD of unfolding l replaced by
+    randomized_svd(C_l, omegas[l], ranks[l]); C_l is (r_{l-1} n_l) x
+    prod_{i>l} n_i and omegas[l] holds l_l test vectors of that length as
+    rows.  Ranks are used as given (r_l <= l_l <= both unfolding sizes).
+    Returns the FP64 cores and, per step, the r_l singular values kept and
+    the step's truncation error eps_l = ||C_l - U S Vt||_F (the terms of
+    eq. tt_svd_error)."""
+    dims = [int(x) for x in T.shape]
+    d = len(dims)
+    ranks = [int(r) for r in ranks]
+    if len(ranks) != d - 1 or len(omegas) != d - 1:
+        raise ValueError("need d-1 ranks and test matrices")
+    C = _c(T).reshape(dims[0], -1)
+    r_prev = 1
+    cores, sigma, step_err = [], [], []
+    for l in range(d - 1):
+        C = C.reshape(r_prev * dims[l], -1)
+        U, S, Vt = randomized_svd(C, omegas[l], ranks[l], power_iters)
+        r = ranks[l]
+        nxt = S[:, None] * Vt
+        step_err.append(fro_diff(C, matmul(U, nxt)))
+        sigma.append(S)
+        cores.append(np.ascontiguousarray(U.reshape(r_prev, dims[l], r)))
+        C = nxt
+        r_prev = r
+    cores.append(np.ascontiguousarray(C.reshape(r_prev, dims[-1], 1)))
+    return cores, {"sigma": sigma, "step_err": step_err}

@@ -273,3 +273,25 @@ def random_tt_cores(dims, ranks, tag: int = 0):
             mat = rng.standard_normal((r0, n)) * scale[:, None]
             cores.append(np.ascontiguousarray(mat.reshape(r0, n, 1)))
     return cores
+
+
+# --------------------------------------------------------------------------
+# Factorization inputs
+# --------------------------------------------------------------------------
+
+W_FACTOR = 8              # test vectors and dense matrices of the randomized factorizations
+
+
+def test_vectors(l: int, n: int, tag: int = 0) -> np.ndarray:
+    """l Gaussian test vectors of length n as the rows of an l x n matrix
+    (the sketch of a randomized range finder)."""
+    return rng_for(W_FACTOR, 0, tag).standard_normal((int(l), int(n)))
+
+
+def spectral_matrix(m: int, n: int, sigma: np.ndarray, tag: int = 0) -> np.ndarray:
+    """Dense m x n matrix with Haar singular vectors and the given singular
+    values (len(sigma) <= min(m, n)), formed as (P * sigma) Q^T."""
+    sigma = np.asarray(sigma, dtype=np.float64)
+    P = haar(rng_for(W_FACTOR, 1, tag), m, sigma.size)
+    Q = haar(rng_for(W_FACTOR, 2, tag), n, sigma.size)
+    return np.ascontiguousarray((P * sigma) @ Q.T)
