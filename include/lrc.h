@@ -315,6 +315,49 @@ int lrc_tt_quality(const void* const* cores, const int64_t* dims, const int64_t*
  * [1, LRC_TT_MAX_D] or a dimension < 1. */
 int64_t lrc_tt_memory_matched_rank(const int64_t* dims, int d, int64_t budget_bytes, int64_t* ranks_out);
 
+/* ---- Randomized FP64 factorization (the end-to-end decomposition left to
+ * future work in Sec. sec:conclusion): the randomized range finder of
+ * Halko, Martinsson and Tropp (2011) with an exact SVD of the projected
+ * matrix, and TT-SVD (Sec. 5.1, eq. tt_svd_error) built on it.  The test
+ * vectors are drawn by the caller (Gaussian in the intended use). */
+#define LRC_RSVD_MAX_SAMPLES 96
+#define LRC_RSVD_MAX_POWER_ITERS 8
+
+/* Rank-k randomized SVD of the device FP64 matrix A (m x n, row-major) with
+ * the l test vectors given as the rows of omega (l x n, device FP64):
+ *   Y = A omega^T, Q = orth(Y); power_iters times Q = orth(A orth(A^T Q));
+ *   B = Q^T A = Ub diag(s) Vt (exact SVD of the small matrix);
+ *   U = Q Ub[:, :k], V = Vt[:k]^T,
+ * so that U diag(s) V^T = U U^T A.  Outputs (device, FP64, written whole):
+ * U (m x k), s (k, non-increasing), V (n x k), all row-major.  The factors
+ * are unique up to the sign of each singular pair when the singular values
+ * are distinct; a singular value that is exactly zero gets a zero column in
+ * U.  Orthonormalizations are CholeskyQR2 (as lrc_tt_left_orthogonalize);
+ * the small SVD is one-sided Jacobi.  Synchronizes the calling thread's
+ * stream.  Errors: LRC_EINVAL (NULL pointer, sizes outside 1 <= k <= l <=
+ * min(m, n), l > LRC_RSVD_MAX_SAMPLES, power_iters outside [0,
+ * LRC_RSVD_MAX_POWER_ITERS], an output overlapping an input or another
+ * output), LRC_ENUMERIC (a sketch or projected matrix numerically rank
+ * deficient for CholeskyQR2, i.e. condition number above about 1e7, or a
+ * Jacobi sweep limit reached), LRC_EOVERFLOW, LRC_ENOMEM, LRC_EHIP,
+ * LRC_ENODEV. */
+int lrc_rsvd(const double* A, int64_t m, int64_t n, const double* omega, int64_t l, int power_iters, int64_t k,
+             double* U, double* s, double* V);
+
+/* Randomized TT-SVD of the device FP64 tensor T (dims[0..d-1], C order,
+ * d >= 2): step l = 0..d-2 factors C_l ((ranks[l] dims[l]) x prod_{i>l}
+ * dims[i], C_0 = T) as lrc_rsvd does with samples[l] test vectors
+ * omegas[l] (samples[l] x prod_{i>l} dims[i], device FP64) at rank
+ * ranks[l+1]; core l = U (ranks[l] x dims[l] x ranks[l+1]) and C_{l+1} =
+ * diag(s) V^T, whose last value is the last core.  ranks has d+1 entries
+ * with ranks[0] = ranks[d] = 1 and 1 <= ranks[l+1] <= samples[l] <= both
+ * sizes of C_l, samples[l] <= LRC_RSVD_MAX_SAMPLES.  cores: d device FP64
+ * buffers (written whole).  sigma (device, may be NULL): the kept singular
+ * values of every step, concatenated (sum of ranks[1..d-1] values).
+ * Synchronizes.  Errors as lrc_rsvd (LRC_ENUMERIC names the step). */
+int lrc_tt_rsvd(const double* T, const int64_t* dims, const int64_t* ranks, int d, const double* const* omegas,
+                const int64_t* samples, int power_iters, double* const* cores, double* sigma);
+
 /* Stored bytes of rank-k factors in `prec`: (b/8) k (m+n+1)  (Sec. 4.2).
  * Returns LRC_EINVAL for bad arguments or LRC_EOVERFLOW on overflow. */
 int64_t lrc_storage_bytes(int64_t m, int64_t n, int64_t k, int prec);

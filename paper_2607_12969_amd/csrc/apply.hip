@@ -355,7 +355,7 @@ __device__ __forceinline__ void atb_store(const typename C::AccV& a, int tid, in
         const int64_t nn = n0 + wn * C::WTN + fn * 16 + acc_row<T>(g, v);
         if (MODE == ATB_APPLY) {
             if (nn < N && mm < Mout) {
-                const Acc val = (mm < M) ? to_acc(svals[mm]) * a[v] : Acc(0);
+                const Acc val = (mm < M) ? (svals ? to_acc(svals[mm]) * a[v] : a[v]) : Acc(0);
                 static_cast<T*>(out)[nn * ldo + mm] = to_storage<T>(val);
             }
         } else {
@@ -373,7 +373,8 @@ __device__ __forceinline__ void atb_store(const typename C::AccV& a, int tid, in
 // and k_atb_finish, launched next on the same stream, sums them.  Kernel
 // boundaries order the partials: no device-scope fences, which on this
 // chip write back and invalidate the L2 of the XCD.
-//   ATB_APPLY: out is T'^T[n][ldo] in T, value s[m] * C (s[m] = 0 for m >= M),
+//   ATB_APPLY: out is T'^T[n][ldo] in T, value s[m] * C (s[m] = 0 for m >= M;
+//              factor 1 when s is null),
 //              written for m < Mout (zero padding rows included).
 //   ATB_GRAM : out is G[m][ldo] in double (T = double).
 template <typename T, class C, int MODE>
@@ -1133,6 +1134,133 @@ hipError_t launch_err_dense(const double* A, const double* W, const double* Vw, 
     KernelTimer tm_("cert_err_dense_f64", stream);
     launch_abt<double, GramC, ABT_ERR>(dim3(xcd_grid(AbtOrder(tm, tn).total)), stream, W, ldw, m, r, Vw, ldw, n, r, K, tm, tn,
                                        (double*)nullptr, (int64_t)0, 0, A, n, part);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------- factorization GEMMs (FP64)
+// Split-K partial tiles of C[m][n] = sum_{k in split} A[m][k] B[n][k] (both
+// sources K-contiguous, 16-byte aligned with even pitches), in the layout of
+// k_atb's partials (tile = n tile * tiles_m + m tile): k_atb_finish in
+// ATB_APPLY mode sums them in split order and stores C transposed.
+template <class C>
+__global__ __launch_bounds__(C::NT) void k_abt_part(const double* __restrict__ Asrc, int64_t lda, int64_t M,
+                                                    const double* __restrict__ Bsrc, int64_t ldb, int64_t N,
+                                                    int64_t K, int64_t chunk, int tiles_m, int tiles_n, int splits,
+                                                    double* __restrict__ part) {
+    using AccV = typename C::AccV;
+    constexpr int kAs = C::BM * C::LDK, kBs = C::BN * C::LDK;
+    __shared__ alignas(16) double smem[2 * kAs + 2 * kBs];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / C::WN, wn = wave % C::WN;
+    const int64_t ntile = (int64_t)tiles_m * tiles_n;
+    const int64_t lt = xcd_tile(ntile * splits);
+    if (lt >= ntile * splits) return;
+    const int64_t tile = lt % ntile;
+    const int sp = (int)(lt / ntile);
+    const int64_t m0 = (tile % tiles_m) * C::BM, n0 = (tile / tiles_m) * C::BN;
+    const int nfm = live_frags<C::FM>(m0 + wm * C::WTM, M), nfn = live_frags<C::FN>(n0 + wn * C::WTN, N);
+    const int64_t kbeg = (int64_t)sp * chunk;
+    const int64_t kend = (kbeg + chunk < K) ? kbeg + chunk : K;
+    AccV acc[C::FN][C::FM];
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = zero_accv<AccV>();
+    using TA = KTile<C, C::BM, double>;
+    using TB = KTile<C, C::BN, double>;
+    const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid);
+    const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
+    TA ta[2];
+    TB tb[2];
+    const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
+    pipeline2(
+        nsteps,
+        [&](int st, int j) {
+            const int64_t k0 = kbeg + (int64_t)j * C::BK;
+            ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
+            tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
+        },
+        [&](int st, int buf, int j) {
+            const int64_t k0 = kbeg + (int64_t)j * C::BK;
+            ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > kend, kend);
+            tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > kend, kend);
+        },
+        [&](int buf) { mma_k<C>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane, nfm, nfn); });
+    constexpr int NF = C::FN * C::FM;
+    AccV* mine = reinterpret_cast<AccV*>(part) + ((tile * splits + sp) * NF) * C::NT + tid;
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) mine[(fn * C::FM + fm) * C::NT] = acc[fn][fm];
+}
+
+// Splits of a K range over `tiles` output tiles: about 1536 workgroups, at
+// least 256 K values per split (chunk a multiple of the K step).
+static void split_plan(int64_t tiles, int64_t K, int* splits, int64_t* chunk) {
+    int64_t sp = (1536 + tiles - 1) / tiles;
+    int64_t mx = K / 256;
+    if (mx < 1) mx = 1;
+    if (sp > mx) sp = mx;
+    if (sp < 1) sp = 1;
+    *chunk = round_up((K + sp - 1) / sp, GramC::BK);
+    *splits = (int)((K + *chunk - 1) / *chunk);
+}
+
+static int64_t tiles_of(int64_t n, int b) { return (n + b - 1) / b; }
+
+size_t gemm_nt_workspace_bytes(int64_t nw, int64_t rows, int64_t K) {
+    const int64_t tiles = tiles_of(nw, GramC::BM) * tiles_of(rows, GramC::BN);
+    int sp;
+    int64_t ch;
+    split_plan(tiles, K, &sp, &ch);
+    return (size_t)tiles * sp * GramC::BM * GramC::BN * sizeof(double);
+}
+
+hipError_t launch_gemm_nt(const double* W, int64_t ldw, int64_t nw, const double* A, int64_t lda, int64_t rows,
+                          int64_t K, const double* svals, double* out, int64_t ldo, int64_t mout, Workspace& ws,
+                          hipStream_t stream, const char* label) {
+    const int tm = (int)tiles_of(nw, GramC::BM), tn = (int)tiles_of(rows, GramC::BN);
+    if (!vec_ok<double>(W, ldw) || !vec_ok<double>(A, lda) || mout < nw || mout > (int64_t)tm * GramC::BM)
+        return hipErrorInvalidValue;
+    int sp;
+    int64_t ch;
+    split_plan((int64_t)tm * tn, K, &sp, &ch);
+    double* part = static_cast<double*>(ws.take(gemm_nt_workspace_bytes(nw, rows, K)));
+    if (ws.overrun) return hipErrorOutOfMemory;
+    KernelTimer t(label, stream);
+    hipLaunchKernelGGL(k_abt_part<GramC>, dim3(xcd_grid((int64_t)tm * tn * sp)), dim3(GramC::NT), 0, stream, W, ldw,
+                       nw, A, lda, rows, K, ch, tm, tn, sp, part);
+    hipLaunchKernelGGL((k_atb_finish<double, GramC, ATB_APPLY>), dim3((unsigned)((int64_t)tm * tn * GramC::FN * GramC::FM)),
+                       dim3(GramC::NT), 0, stream, reinterpret_cast<const GramC::AccV*>(part), nw, rows, tm, sp, svals,
+                       (void*)out, ldo, mout);
+    return hipGetLastError();
+}
+
+size_t gemm_tn_workspace_bytes(int64_t nq, int64_t cols, int64_t K) {
+    const int64_t tiles = tiles_of(nq, GramC::BM) * tiles_of(cols, GramC::BN);
+    int sp;
+    int64_t ch;
+    split_plan(tiles, K, &sp, &ch);
+    return sp > 1 ? (size_t)tiles * sp * GramC::BM * GramC::BN * sizeof(double) : 0;
+}
+
+hipError_t launch_gemm_tn(const double* Q, int64_t ldq, int64_t nq, const double* A, int64_t lda, int64_t cols,
+                          int64_t K, double* out, int64_t ldo, int64_t mout, Workspace& ws, hipStream_t stream,
+                          const char* label, const char* finish_label) {
+    const int tm = (int)tiles_of(nq, GramC::BM), tn = (int)tiles_of(cols, GramC::BN);
+    if (!vec_ok<double>(Q, ldq) || !vec_ok<double>(A, lda) || mout < nq || mout > (int64_t)tm * GramC::BM)
+        return hipErrorInvalidValue;
+    int sp;
+    int64_t ch;
+    split_plan((int64_t)tm * tn, K, &sp, &ch);
+    double* part = nullptr;
+    if (sp > 1) {
+        part = static_cast<double*>(ws.take(gemm_tn_workspace_bytes(nq, cols, K)));
+        if (ws.overrun) return hipErrorOutOfMemory;
+    }
+    run_atb<double, GramC, ATB_APPLY>(label, finish_label, stream, Q, ldq, A, lda, nq, cols, K, ch, tm, tn, sp, part,
+                                      (const double*)nullptr, (void*)out, ldo, mout);
     return hipGetLastError();
 }
 

@@ -308,6 +308,41 @@ static void launch_trsm(const double* A, int64_t rows, int r, int lda, const dou
                            ldr, C, ldc);
 }
 
+size_t cholqr2_workspace_bytes(int64_t rows, int r) {
+    const int64_t rp = round_up(r, 2);
+    return (size_t)round_up(rows * rp * 8, 256) + 3 * (size_t)round_up(rp * rp * 8, 256) +
+           (size_t)round_up((int64_t)gram_workspace_bytes(rows, rp), 256);
+}
+
+hipError_t launch_cholqr2(const double* A, int64_t rows, int r, double* Q, double* R, int* flag, Workspace& ws,
+                          hipStream_t stream, const char* label) {
+    const int rp = (int)round_up(r, 2);
+    double* W2 = static_cast<double*>(ws.take((size_t)rows * rp * 8));
+    double* G = static_cast<double*>(ws.take((size_t)rp * rp * 8));
+    double* R1 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
+    double* R2 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
+    if (ws.overrun) return hipErrorOutOfMemory;
+    KernelTimer tm(label, stream);
+    const size_t gmark = ws.used;
+    hipError_t e = launch_gram(A, rows, rp, G, ws, stream);
+    if (e != hipSuccess) return e;
+    ws.used = gmark;
+    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R1, flag);
+    launch_trsm(A, rows, r, rp, R1, rp, W2, rp, stream);
+    e = launch_gram(W2, rows, rp, G, ws, stream);
+    if (e != hipSuccess) return e;
+    ws.used = gmark;
+    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R2, flag);
+    launch_trsm(W2, rows, r, rp, R2, rp, Q, rp, stream);
+    if (R) {
+        // R = R2 R1: rows 0..r-1 of the triangular product, R1 taken as an r x rp block
+        const dim3 gl((unsigned)((rp + 255) / 256), (unsigned)((r + kLmulRows - 1) / kLmulRows));
+        hipLaunchKernelGGL(k_gauge_lmul, gl, dim3(256), 0, stream, R2, r, rp, R1, (int64_t)rp, R);
+    }
+    return hipGetLastError();
+}
+
+
 hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t* ranks, int d, int* flags,
                         Workspace& ws, hipStream_t stream) {
     hipLaunchKernelGGL(k_gauge_zero, dim3(1), dim3(64), 0, stream, flags, d);

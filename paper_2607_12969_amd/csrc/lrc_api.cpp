@@ -868,3 +868,114 @@ int64_t lrc_tt_memory_matched_rank(const int64_t* dims, int d, int64_t budget_by
     for (int l = 0; l <= d; ++l) ranks_out[l] = bestR ? best[l] : 0;
     return bestR;
 }
+
+// ------------------------------------------------- randomized factorization
+static int check_rsvd_sizes(int64_t rows, int64_t cols, int64_t l, int64_t k, const char* what) {
+    if (l < 1 || l > LRC_RSVD_MAX_SAMPLES)
+        return fail(LRC_EINVAL, "%s: %lld test vectors outside [1, %d]", what, (long long)l, LRC_RSVD_MAX_SAMPLES);
+    if (k < 1 || k > l) return fail(LRC_EINVAL, "%s: rank %lld outside [1, l = %lld]", what, (long long)k, (long long)l);
+    if (l > rows || l > cols)
+        return fail(LRC_EINVAL, "%s: %lld test vectors exceed the matrix size %lld x %lld", what, (long long)l,
+                    (long long)rows, (long long)cols);
+    int64_t t;
+    if (!mul_ok(rows, cols, &t) || !mul_ok(t, 16, &t)) return fail(LRC_EOVERFLOW, "%s: size overflows", what);
+    return LRC_OK;
+}
+
+static int factor_status(const int* dflags, int nsteps, hipStream_t st, bool tt) {
+    std::vector<int> hf(3 * (size_t)nsteps, 0);
+    hipError_t e = hipMemcpyAsync(hf.data(), dflags, sizeof(int) * hf.size(), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail_hip(e, "factorization status");
+    static const char* what[3] = {"the range finder's sketch", "the projected matrix B^T", "the small Jacobi SVD"};
+    for (int s = 0; s < nsteps; ++s)
+        for (int q = 0; q < 3; ++q)
+            if (hf[3 * s + q]) {
+                if (tt)
+                    return fail(LRC_ENUMERIC, "TT-SVD step %d: %s is numerically rank deficient or did not converge",
+                                s, what[q]);
+                return fail(LRC_ENUMERIC, "%s is numerically rank deficient or did not converge", what[q]);
+            }
+    return LRC_OK;
+}
+
+int lrc_rsvd(const double* A, int64_t m, int64_t n, const double* omega, int64_t l, int power_iters, int64_t k,
+             double* U, double* s, double* V) {
+    if (!A || !omega || !U || !s || !V) return fail(LRC_EINVAL, "NULL array argument");
+    if (m < 1 || n < 1) return fail(LRC_EINVAL, "matrix size %lld x %lld", (long long)m, (long long)n);
+    if (power_iters < 0 || power_iters > LRC_RSVD_MAX_POWER_ITERS)
+        return fail(LRC_EINVAL, "power_iters = %d outside [0, %d]", power_iters, LRC_RSVD_MAX_POWER_ITERS);
+    int rc = check_rsvd_sizes(m, n, l, k, "rsvd");
+    if (rc) return rc;
+    const size_t bA = (size_t)m * n * 8, bO = (size_t)l * n * 8;
+    const size_t bU = (size_t)m * k * 8, bS = (size_t)k * 8, bV = (size_t)n * k * 8;
+    const void* outs[3] = {U, s, V};
+    const size_t nb[3] = {bU, bS, bV};
+    for (int i = 0; i < 3; ++i) {
+        if (overlaps(outs[i], nb[i], A, bA) || overlaps(outs[i], nb[i], omega, bO))
+            return fail(LRC_EINVAL, "an output overlaps an input");
+        for (int j = 0; j < i; ++j)
+            if (overlaps(outs[i], nb[i], outs[j], nb[j])) return fail(LRC_EINVAL, "two outputs overlap");
+    }
+    int dev;
+    rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t e = ws.reserve(matrix_rsvd_workspace_bytes(m, n, (int)l, (int)k, power_iters), st);
+    if (e != hipSuccess) return fail_hip(e, "workspace");
+    int* flags = static_cast<int*>(ws.take(3 * sizeof(int)));
+    e = launch_matrix_rsvd(A, m, n, omega, (int)l, power_iters, (int)k, U, s, V, flags, ws, st);
+    if (e != hipSuccess) return fail_hip(e, "rsvd launch");
+    return factor_status(flags, 1, st, false);
+}
+
+int lrc_tt_rsvd(const double* T, const int64_t* dims, const int64_t* ranks, int d, const double* const* omegas,
+                const int64_t* samples, int power_iters, double* const* cores, double* sigma) {
+    if (!T || !omegas || !samples || !cores) return fail(LRC_EINVAL, "NULL array argument");
+    int64_t N;
+    int rc = check_tt_shape(dims, ranks, d, &N);
+    if (rc) return rc;
+    if (d < 2) return fail(LRC_EINVAL, "TT-SVD needs d >= 2 (got %d)", d);
+    if (power_iters < 0 || power_iters > LRC_RSVD_MAX_POWER_ITERS)
+        return fail(LRC_EINVAL, "power_iters = %d outside [0, %d]", power_iters, LRC_RSVD_MAX_POWER_ITERS);
+    int64_t cols = N / dims[0], nsig = 0;
+    std::vector<std::pair<const void*, size_t>> ins{{T, (size_t)N * 8}}, outs;
+    for (int l = 0; l + 1 < d; ++l) {
+        const int64_t rows = ranks[l] * dims[l];
+        char what[48];
+        snprintf(what, sizeof(what), "TT-SVD step %d", l);
+        rc = check_rsvd_sizes(rows, cols, samples[l], ranks[l + 1], what);
+        if (rc) return rc;
+        if (!omegas[l]) return fail(LRC_EINVAL, "omegas[%d] is NULL", l);
+        ins.emplace_back(omegas[l], (size_t)samples[l] * cols * 8);
+        nsig += ranks[l + 1];
+        cols /= dims[l + 1];
+    }
+    for (int l = 0; l < d; ++l) {
+        if (!cores[l]) return fail(LRC_EINVAL, "cores[%d] is NULL", l);
+        outs.emplace_back(cores[l], (size_t)ranks[l] * dims[l] * ranks[l + 1] * 8);
+    }
+    if (sigma) outs.emplace_back(sigma, (size_t)nsig * 8);
+    for (size_t i = 0; i < outs.size(); ++i) {
+        for (auto& in : ins)
+            if (overlaps(outs[i].first, outs[i].second, in.first, in.second))
+                return fail(LRC_EINVAL, "an output overlaps an input");
+        for (size_t j = 0; j < i; ++j)
+            if (overlaps(outs[i].first, outs[i].second, outs[j].first, outs[j].second))
+                return fail(LRC_EINVAL, "two outputs overlap");
+    }
+    int dev;
+    rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    hipStream_t st = g_stream;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    hipError_t e = ws.reserve(tt_rsvd_workspace_bytes(dims, ranks, samples, d, power_iters), st);
+    if (e != hipSuccess) return fail_hip(e, "workspace");
+    int* flags = static_cast<int*>(ws.take(3 * sizeof(int) * (size_t)d));
+    e = launch_tt_rsvd(T, dims, ranks, samples, d, omegas, power_iters, cores, sigma, flags, ws, st);
+    if (e != hipSuccess) return fail_hip(e, "TT-SVD launch");
+    return factor_status(flags, d - 1, st, true);
+}

@@ -82,6 +82,39 @@ size_t gauge_workspace_bytes(const int64_t* dims, const int64_t* ranks, int d);
 hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t* ranks, int d, int* flags,
                         Workspace& ws, hipStream_t stream);
 
+// Thin QR of A (rows x r inside pitch rp = r rounded to 2, 16-byte aligned,
+// rows >= r) by CholeskyQR2 (the gauge's kernels): Q (pitch rp, pad column
+// zeroed) with Q^T Q = I and, when R is not null, R = R2 R1 (rows 0..r-1 of an
+// rp x rp block, upper triangular, diag > 0); *flag becomes 1 + pivot when a
+// Cholesky factorization breaks down (left unchanged otherwise).
+size_t cholqr2_workspace_bytes(int64_t rows, int r);
+hipError_t launch_cholqr2(const double* A, int64_t rows, int r, double* Q, double* R, int* flag, Workspace& ws,
+                          hipStream_t stream, const char* label);
+// ------------------------------------------------------ FP64 factor GEMMs ---
+// out[i][j] = s_j sum_{t<K} W[j][t] A[i][t] for i < rows, j < nw (s = 1 when
+// svals is null); out[i][j] = 0 for nw <= j < mout (mout <= nw rounded up to
+// 64).  W, A: 16-byte aligned with even pitches.  Split-K MFMA partials
+// summed in split order.
+size_t gemm_nt_workspace_bytes(int64_t nw, int64_t rows, int64_t K);
+hipError_t launch_gemm_nt(const double* W, int64_t ldw, int64_t nw, const double* A, int64_t lda, int64_t rows,
+                          int64_t K, const double* svals, double* out, int64_t ldo, int64_t mout, Workspace& ws,
+                          hipStream_t stream, const char* label);
+// out[c][j] = sum_{i<K} Q[i][j] A[i][c] for c < cols, j < nq; zero for
+// nq <= j < mout.  Same operand rules.
+size_t gemm_tn_workspace_bytes(int64_t nq, int64_t cols, int64_t K);
+hipError_t launch_gemm_tn(const double* Q, int64_t ldq, int64_t nq, const double* A, int64_t lda, int64_t cols,
+                          int64_t K, double* out, int64_t ldo, int64_t mout, Workspace& ws, hipStream_t stream,
+                          const char* label, const char* finish_label);
+// ------------------------------------------------ randomized factorization
+// flags: 3 ints (matrix) or 3 per step (TT), 0 on success; [0] range-finder
+// QR, [1] QR of B^T, [2] Jacobi sweep limit.
+size_t matrix_rsvd_workspace_bytes(int64_t m, int64_t n, int l, int k, int q);
+hipError_t launch_matrix_rsvd(const double* A, int64_t m, int64_t n, const double* Om, int l, int q, int k, double* U,
+                              double* s, double* V, int* flags, Workspace& ws, hipStream_t st);
+size_t tt_rsvd_workspace_bytes(const int64_t* dims, const int64_t* ranks, const int64_t* samples, int d, int q);
+hipError_t launch_tt_rsvd(const double* T, const int64_t* dims, const int64_t* ranks, const int64_t* samples, int d,
+                          const double* const* omegas, int q, double* const* cores, double* sigma, int* flags,
+                          Workspace& ws, hipStream_t st);
 // ------------------------------------------------------- certificate (matrix)
 // G = P^T P for P (rows x cols, row-major, FP64): a split-sum Gram product.
 size_t gram_workspace_bytes(int64_t rows, int64_t cols);

@@ -104,6 +104,11 @@ def lib():
     L.lrc_tt_quality.restype = ctypes.c_int
     L.lrc_tt_memory_matched_rank.argtypes = [ctypes.POINTER(_i64), ctypes.c_int, _i64, ctypes.POINTER(_i64)]
     L.lrc_tt_memory_matched_rank.restype = _i64
+    L.lrc_rsvd.argtypes = [_vp, _i64, _i64, _vp, _i64, ctypes.c_int, _i64, _vp, _vp, _vp]
+    L.lrc_rsvd.restype = ctypes.c_int
+    L.lrc_tt_rsvd.argtypes = [_vp, ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.c_int, ctypes.POINTER(_vp),
+                              ctypes.POINTER(_i64), ctypes.c_int, ctypes.POINTER(_vp), _vp]
+    L.lrc_tt_rsvd.restype = ctypes.c_int
     L.lrc_storage_bytes.argtypes = [_i64, _i64, _i64, ctypes.c_int]
     L.lrc_storage_bytes.restype = _i64
     L.lrc_tt_storage_bytes.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64), ctypes.c_int, ctypes.c_int]
@@ -322,6 +327,61 @@ def memory_matched_rank(dims, budget_bytes: int):
     out = (_i64 * (d + 1))()
     R = _check(lib().lrc_tt_memory_matched_rank(D, d, int(budget_bytes), out))
     return (int(R), [int(v) for v in out]) if R > 0 else (0, None)
+
+
+def rsvd(A, omega, k: int, power_iters: int = 0):
+    """Rank-k randomized SVD of the float64 device matrix A (m x n) with the
+    test vectors as the rows of omega (l x n): returns U (m x k), s (k),
+    V (n x k), float64 on A's device, with U diag(s) V^T = U U^T A."""
+    import torch
+    _dev(A, omega)
+    if A.dtype != torch.float64 or omega.dtype != torch.float64 or A.dim() != 2 or omega.dim() != 2:
+        raise ValueError("A and omega must be float64 matrices")
+    m, n = (int(x) for x in A.shape)
+    l = int(omega.shape[0])
+    if int(omega.shape[1]) != n:
+        raise ValueError("omega must have n columns")
+    A = A.contiguous()
+    omega = omega.contiguous()
+    U = torch.empty((m, k), dtype=torch.float64, device=A.device)
+    s = torch.empty(k, dtype=torch.float64, device=A.device)
+    V = torch.empty((n, k), dtype=torch.float64, device=A.device)
+    _bind_stream(A.device)
+    _check(lib().lrc_rsvd(A.data_ptr(), m, n, omega.data_ptr(), l, int(power_iters), int(k), U.data_ptr(),
+                          s.data_ptr(), V.data_ptr()))
+    return U, s, V
+
+
+def tt_rsvd(T, ranks, omegas, power_iters: int = 0):
+    """Randomized TT-SVD of the float64 device tensor T at TT ranks
+    `ranks` (d-1 values), omegas[l] holding the test vectors of step l as
+    rows.  Returns (cores, sigmas): float64 cores (r_{l-1}, n_l, r_l) and
+    the kept singular values of every step."""
+    import torch
+    _dev(T, *omegas)
+    if T.dtype != torch.float64 or any(o.dtype != torch.float64 for o in omegas):
+        raise ValueError("T and the test matrices must be float64")
+    dims = [int(x) for x in T.shape]
+    d = len(dims)
+    rk = [1] + [int(r) for r in ranks] + [1]
+    if len(rk) != d + 1 or len(omegas) != d - 1:
+        raise ValueError("need d-1 ranks and d-1 test matrices")
+    T = T.contiguous()
+    oms = [o.contiguous() for o in omegas]
+    cores = [torch.empty((rk[l], dims[l], rk[l + 1]), dtype=torch.float64, device=T.device) for l in range(d)]
+    sig = torch.empty(sum(rk[1:d]), dtype=torch.float64, device=T.device)
+    D = (_i64 * d)(*dims)
+    R = (_i64 * (d + 1))(*rk)
+    S = (_i64 * (d - 1))(*[int(o.shape[0]) for o in oms])
+    O = (_vp * (d - 1))(*[o.data_ptr() for o in oms])
+    C = (_vp * d)(*[c.data_ptr() for c in cores])
+    _bind_stream(T.device)
+    _check(lib().lrc_tt_rsvd(T.data_ptr(), D, R, d, O, S, int(power_iters), C, sig.data_ptr()))
+    sigmas, o = [], 0
+    for r in rk[1:d]:
+        sigmas.append(sig[o:o + r])
+        o += r
+    return cores, sigmas
 
 
 def _result(res: CertResult) -> dict:

@@ -186,3 +186,46 @@ def test_quality_argument_errors():
     assert L.lrc_tt_quality(P, D, R, 1, 0, 0x20000, 1.0, ctypes.byref(q)) == -1     # d < 2
     out = (ctypes.c_int64 * 2)()
     assert L.lrc_tt_memory_matched_rank(D, 0, 100, out) == -1
+
+
+def _rsvd(m, n, l, k, q=0, A=0x100000, Om=0x8000000, U=0x10000000, s=0x20000000, V=0x30000000):
+    return L.lrc_rsvd(A, m, n, Om, l, q, k, U, s, V)
+
+
+def test_rsvd_argument_errors():
+    """Checked on the host before any device call (no GPU here)."""
+    assert _rsvd(100, 80, 10, 5, A=0) == -1                    # NULL input
+    assert _rsvd(0, 80, 10, 5) == -1                           # empty matrix
+    assert _rsvd(100, 80, 10, 11) == -1                        # k > l
+    assert _rsvd(100, 80, 10, 0) == -1                         # k < 1
+    assert _rsvd(100, 80, 97, 5) == -1                         # above LRC_RSVD_MAX_SAMPLES
+    assert _rsvd(100, 8, 10, 5) == -1                          # l > n
+    assert b"exceed" in L.lrc_last_error()
+    assert _rsvd(100, 80, 10, 5, q=9) == -1                    # too many power iterations
+    assert _rsvd(100, 80, 10, 5, U=0x100000 + 8) == -1         # U overlaps A
+    assert b"overlaps" in L.lrc_last_error()
+    assert _rsvd(100, 80, 10, 5, V=0x10000000 + 16) == -1      # V overlaps U
+    assert _rsvd(2 ** 40, 2 ** 40, 10, 5) == -2                # size overflow
+
+
+def test_tt_rsvd_argument_errors():
+    def call(dims, ranks, samples, omegas=None, cores=None, T=0x100000, q=0):
+        d = len(dims)
+        D = (ctypes.c_int64 * d)(*dims)
+        R = (ctypes.c_int64 * (d + 1))(*ranks)
+        S = (ctypes.c_int64 * max(d - 1, 1))(*samples)
+        om = omegas or [0x4000000 * (l + 1) for l in range(d - 1)]
+        co = cores or [0x40000000 + 0x4000000 * l for l in range(d)]
+        O_ = (ctypes.c_void_p * max(d - 1, 1))(*om)
+        C_ = (ctypes.c_void_p * d)(*co)
+        return L.lrc_tt_rsvd(T, D, R, d, O_, S, q, C_, None)
+    assert call((8, 9, 10), (1, 4, 5, 1), (6, 7), T=0) == -1
+    assert call((8,), (1, 1), ()) == -1                           # d < 2
+    assert call((8, 9, 10), (1, 4, 5, 1), (3, 7)) == -1           # rank 4 > 3 test vectors
+    assert call((8, 9, 10), (1, 4, 5, 1), (6, 11)) == -1          # 11 test vectors > 10 columns of step 1
+    assert b"step 1" in L.lrc_last_error()
+    assert call((8, 9, 10), (1, 4, 5, 1), (6, 7), q=-1) == -1
+    assert call((8, 9, 10), (1, 4, 5, 1), (6, 7), omegas=[0x4000000, 0]) == -1
+    assert call((8, 9, 10), (1, 4, 5, 1), (6, 7), cores=[0x40000000, 0x40000000 + 64, 0x48000000]) == -1
+    assert b"overlap" in L.lrc_last_error()
+    assert call((8, 9, 10), (1, 4, 5, 1), (6, 7), cores=[0x100000 + 8, 0x44000000, 0x48000000]) == -1
