@@ -20,6 +20,7 @@ same apply and TT work.
   python bench.py --quant FILE      device rounding and TT gauge cells
   python bench.py --grid FILE       the paper's resident timing grid on synthetic stand-ins
   python bench.py --fixed-memory FILE   fixed-memory comparison on hyperspectral-shaped stand-ins
+  python bench.py --factor FILE         randomized FP64 SVD / TT-SVD cells
 """
 from __future__ import annotations
 
@@ -443,6 +444,79 @@ def quant_sweep(path, dev, lrc):
         fh.write("\n".join(rows) + "\n")
 
 
+def factor_sweep(path, dev, lrc):
+    """Randomized FP64 factorizations (lrc_rsvd, lrc_tt_rsvd): wall time per
+    call (the calls synchronize) and the library's event spans per stage,
+    summed per call.  Algorithmic flop: the sketch and projection GEMMs over
+    the matrix (2 m n l each, (1 + q) of each), the Gram products of the two
+    or more CholeskyQR2 runs (2 rows l^2 each), the forward substitutions
+    (rows l^2 each) and the singular-vector products (2 (m + n) l k).  The
+    dominant kernel is the sketch GEMM (one read of the matrix per pass,
+    l / 4 flop per byte: above the FP64 ridge for l > 40)."""
+    import torch
+    from paper_2607_12969_amd import synth
+    PK = PEAK_TFLOPS["f64"]
+    rows = ["| cell | GFLOP | call us | stages us (sum) | GFLOP/s | sketch GEMM us | sketch TFLOP/s | "
+            "frac of FP64 MFMA | per stage (us per call) |", "|" + "---|" * 9]
+
+    def flops(m, n, l, k, q):
+        qr = 0.0
+        for it in range(1 + q):
+            qr += 2 * (2.0 * m * l * l + m * l * l)   # range finder: two Grams, two substitutions
+            qr += 2 * (2.0 * n * l * l + n * l * l)   # projection (or its iteration counterpart)
+        return 4.0 * m * n * l * (1 + q) + qr + 2.0 * (m + n) * l * k
+
+    def run(name, fn, f, sketch_flop, reps):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        lrc.profile_reset()
+        lrc.profile_enable(True)
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) / reps * 1e3
+        lrc.profile_enable(False)
+        kt = lrc.profile_read()
+        # CholeskyQR2 spans contain the Gram launches' own spans: those are left out of the sum
+        per = {lab: kt[lab][1] / reps for lab in kt if lab.startswith("factor_")}
+        tot = sum(per.values())
+        sk = per.get("factor_sketch_f64", float("nan"))
+        sk_tf = sketch_flop / (sk * 1e-3) / 1e12
+        stages = ", ".join(f"{k} {v * 1e3:.0f}" for k, v in sorted(per.items(), key=lambda kv: -kv[1]))
+        rows.append(f"| {name} | {f / 1e9:.2f} | {wall * 1e3:.0f} | {tot * 1e3:.0f} | {f / (wall * 1e-3) / 1e9:.0f} | "
+                    f"{sk * 1e3:.0f} | {sk_tf:.1f} | {sk_tf / PK:.3f} | {stages} |")
+        log(rows[-1])
+
+    for (m, n), l, k, q in (((8192, 8192), 75, 65, 0), ((8192, 8192), 75, 65, 1), ((8192, 8192), 96, 65, 0),
+                            ((65536, 4096), 75, 65, 0)):
+        sigma = np.arange(1, 601, dtype=np.float64) ** -1.5
+        A = torch.from_numpy(synth.spectral_matrix(m, n, sigma, tag=m + n)).to(dev)
+        Om = torch.from_numpy(synth.test_vectors(l, n, m)).to(dev)
+        f = flops(m, n, l, k, q)
+        run(f"rsvd {m}x{n} k={k} l={l} q={q}", lambda: lrc.rsvd(A, Om, k, q), f, 2.0 * m * n * l * (1 + q), 5)
+        del A, Om
+        torch.cuda.empty_cache()
+    for dims, r, l in (((512, 512, 224), 65, 75), ((512, 512, 224), 33, 43), ((145, 145, 200), 36, 46)):
+        T = synth.hyperspectral(shape=dims)
+        Td = torch.from_numpy(T).to(dev)
+        oms, f, skf, rp, cols = [], 0.0, 0.0, 1, int(np.prod(dims[1:]))
+        for step in range(2):
+            oms.append(torch.from_numpy(synth.test_vectors(l, cols, 60 + step)).to(dev))
+            rows_ = rp * dims[step]
+            f += flops(rows_, cols, l, r, 0)
+            skf += 2.0 * rows_ * cols * l
+            rp = r
+            cols //= dims[step + 1]
+        run(f"tt_rsvd {'x'.join(map(str, dims))} ranks=({r},{r}) l={l}",
+            lambda: lrc.tt_rsvd(Td, (r, r), oms, 0), f, skf, 5)
+        del Td, oms
+        torch.cuda.empty_cache()
+    with open(path, "w") as fh:
+        fh.write("\n".join(rows) + "\n")
+
+
 # ------------------------------------------------------------ timing grid ---
 # The paper's resident timing protocol (Sec. 4.4 matrix application, Sec. 7.5
 # TT reconstruction; its timing paragraph): per task, warmups, then rounds of
@@ -691,6 +765,7 @@ def main():
     ap.add_argument("--quant", default=None, help="write the device rounding and TT gauge cells")
     ap.add_argument("--grid", default=None, help="write the paper's resident timing grid (synthetic stand-ins)")
     ap.add_argument("--fixed-memory", default=None, help="write the fixed-memory comparison (synthetic stand-ins)")
+    ap.add_argument("--factor", default=None, help="write the randomized FP64 factorization cells")
     ap.add_argument("--copy-calibration", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -724,6 +799,9 @@ def main():
         return
     if args.fixed_memory:
         fixed_memory(args.fixed_memory, dev, lrc)
+        return
+    if args.factor:
+        factor_sweep(args.factor, dev, lrc)
         return
 
     wl = Workload(args.k, dev)

@@ -62,33 +62,47 @@ __global__ void k_fact_zero(int* p, int n) {
     for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
 }
 
-// Sums of three values over the wave by the same butterfly (every lane ends
-// with identical totals, so branches on them stay uniform).
-__device__ __forceinline__ void wave_sum3(double& a, double& b, double& c) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        const double xa = __shfl_xor(a, off, 64), xb = __shfl_xor(b, off, 64), xc = __shfl_xor(c, off, 64);
-        a += xa;
-        b += xb;
-        c += xc;
-    }
+// Value of lane `ctl` (a DPP row permutation) for a double: its two halves
+// moved by the same data-parallel-primitive move.
+template <int CTL>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const long long b = __builtin_bit_cast(long long, v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(b & 0xFFFFFFFFll), CTL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTL, 0xF, 0xF, false);
+    return __builtin_bit_cast(double, ((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Sums of three values over each group of 16 lanes: butterfly by lane
+// swaps within quads (xor 1, xor 2), then the mirror within each half row
+// (lane i with 7 - i) and within the row (i with 15 - i).  Each step adds
+// two equal-ordered partial sums, so all 16 lanes end with identical
+// totals (branches on them stay uniform within the group).
+__device__ __forceinline__ void group16_sum3(double& a, double& b, double& c) {
+    constexpr int kXor1 = 0xB1, kXor2 = 0x4E, kHalfMirror = 0x141, kMirror = 0x140;
+    a += dpp_f64<kXor1>(a); b += dpp_f64<kXor1>(b); c += dpp_f64<kXor1>(c);
+    a += dpp_f64<kXor2>(a); b += dpp_f64<kXor2>(b); c += dpp_f64<kXor2>(c);
+    a += dpp_f64<kHalfMirror>(a); b += dpp_f64<kHalfMirror>(b); c += dpp_f64<kHalfMirror>(c);
+    a += dpp_f64<kMirror>(a); b += dpp_f64<kMirror>(b); c += dpp_f64<kMirror>(c);
 }
 
 // One workgroup: SVD of M = R^T (R upper triangular, l x l inside pitch ldr)
 // by one-sided (Hestenes) Jacobi.  The columns of M (rows of R) and of the
 // accumulated rotation Z sit in LDS; a sweep visits every column pair once
 // in l' - 1 rounds of the round-robin (circle) ordering, l' = l rounded up to
-// even, the l'/2 disjoint pairs of a round spread over the 16 waves (one
-// pair per wave at a time, lanes over the l entries).  A pair (p, q) is
-// rotated when |m_p . m_q| > tol ||m_p|| ||m_q||, tol = max(l, 8) 2^-53,
-// by the rotation that makes the two columns orthogonal (the smaller root of
-// t^2 + 2 zeta t - 1 = 0, zeta = (|m_q|^2 - |m_p|^2) / (2 m_p . m_q)).  The
-// sweeps stop when one rotates nothing; *flag = 1 if 40 sweeps do not get
-// there.  Then sigma_j = ||m_j||, and the columns are written in
-// non-increasing order of sigma (ties by index): sv[pos] = sigma,
-// Wt[pos][:] = m_j / sigma_j (zero when sigma_j = 0), Zt[pos][:] = z_j, and,
-// when Zts is not null, Zts[pos][:] = sigma_j z_j; rows of pitch ldw with
-// zeros in columns l..ldw-1; s_out[pos] = sigma for pos < k when not null.
+// even.  The l'/2 <= 48 disjoint pairs of a round run at once, one per
+// group of 16 lanes (64 groups), each lane holding entries e = lane + 16 u
+// of the two columns.  A pair (p, q) is rotated when |m_p . m_q| > tol
+// ||m_p|| ||m_q||, tol = max(l, 8) 2^-53, by the rotation that makes the two
+// columns orthogonal (the smaller root of t^2 + 2 zeta t - 1 = 0, zeta =
+// (|m_q|^2 - |m_p|^2) / (2 m_p . m_q)).  The sweeps stop when one rotates
+// nothing; *flag = 1 if 40 sweeps do not get there.  Then sigma_j = ||m_j||,
+// and the columns are written in non-increasing order of sigma (ties by
+// index): sv[pos] = sigma, Wt[pos][:] = m_j / sigma_j (zero when sigma_j =
+// 0), Zt[pos][:] = z_j, and, when Zts is not null, Zts[pos][:] = sigma_j z_j;
+// rows of pitch ldw with zeros in columns l..ldw-1; s_out[pos] = sigma for
+// pos < k when not null.
+constexpr int kJacPer = kFactMaxL / 16;   // entries of a column per lane
+static_assert(kFactMaxL % 16 == 0 && kFactMaxL / 2 <= kJacThreads / 16, "one group of 16 lanes per pair");
 __global__ __launch_bounds__(kJacThreads) void k_fact_jacobi(const double* __restrict__ R, int l, int ldr, int k,
                                                              double* __restrict__ sv, double* __restrict__ s_out,
                                                              double* __restrict__ Wt, double* __restrict__ Zt,
@@ -98,8 +112,8 @@ __global__ __launch_bounds__(kJacThreads) void k_fact_jacobi(const double* __res
     __shared__ double sig[kFactMaxL];
     __shared__ int pos[kFactMaxL];
     __shared__ int rotated;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tid = threadIdx.x;
+    const int grp = tid >> 4, gl = tid & 15;
     for (int idx = tid; idx < l * l; idx += kJacThreads) {
         const int j = idx / l, i = idx - j * l;
         Mc[j][i] = i >= j ? R[(int64_t)j * ldr + i] : 0.0;
@@ -109,47 +123,54 @@ __global__ __launch_bounds__(kJacThreads) void k_fact_jacobi(const double* __res
     __syncthreads();
     const int L = l + (l & 1);
     const double tol = (double)(l > 8 ? l : 8) * 0x1p-53;
-    const bool in0 = lane < l, in1 = lane + 64 < l;
-    const int e1 = in1 ? lane + 64 : 0;
     bool converged = false;
     for (int sweep = 0; sweep < kJacSweeps; ++sweep) {
+        int a = grp, b = L - 1;   // round 0's pair of this group (pair s = grp)
         for (int t = 0; t + 1 < L; ++t) {
-            for (int s = wave; s < L / 2; s += kJacWaves) {
-                int a, b;
-                if (s == 0) {
+            if (grp < L / 2) {
+                if (grp == 0) {
                     a = t;
                     b = L - 1;
                 } else {
-                    a = (t + s) % (L - 1);
-                    b = (t - s + L - 1) % (L - 1);
+                    a = t + grp;
+                    a = a >= L - 1 ? a - (L - 1) : a;
+                    b = t - grp;
+                    b = b < 0 ? b + (L - 1) : b;
                 }
                 const int p = a < b ? a : b, q = a < b ? b : a;
-                if (q >= l) continue;
-                const double mp0 = in0 ? Mc[p][lane] : 0.0, mq0 = in0 ? Mc[q][lane] : 0.0;
-                const double mp1 = in1 ? Mc[p][e1] : 0.0, mq1 = in1 ? Mc[q][e1] : 0.0;
-                double al = mp0 * mp0 + mp1 * mp1, be = mq0 * mq0 + mq1 * mq1, ga = mp0 * mq0 + mp1 * mq1;
-                wave_sum3(al, be, ga);
-                if (ga == 0.0 || !(__builtin_fabs(ga) > tol * __builtin_sqrt(al) * __builtin_sqrt(be))) continue;
-                const double zeta = (be - al) / (2.0 * ga);
-                const double az = __builtin_fabs(zeta);
-                double tt = az > 1e150 ? 0.5 / az : 1.0 / (az + __builtin_sqrt(1.0 + zeta * zeta));
-                tt = zeta < 0.0 ? -tt : tt;
-                const double c = 1.0 / __builtin_sqrt(1.0 + tt * tt), sn = c * tt;
-                if (in0) {
-                    Mc[p][lane] = c * mp0 - sn * mq0;
-                    Mc[q][lane] = sn * mp0 + c * mq0;
-                    const double jp = Jc[p][lane], jq = Jc[q][lane];
-                    Jc[p][lane] = c * jp - sn * jq;
-                    Jc[q][lane] = sn * jp + c * jq;
+                if (q < l) {
+                    double mp[kJacPer], mq[kJacPer];
+                    double al = 0.0, be = 0.0, ga = 0.0;
+#pragma unroll
+                    for (int u = 0; u < kJacPer; ++u) {
+                        const int e = gl + 16 * u;
+                        mp[u] = e < l ? Mc[p][e] : 0.0;
+                        mq[u] = e < l ? Mc[q][e] : 0.0;
+                        al += mp[u] * mp[u];
+                        be += mq[u] * mq[u];
+                        ga += mp[u] * mq[u];
+                    }
+                    group16_sum3(al, be, ga);
+                    if (ga != 0.0 && __builtin_fabs(ga) > tol * __builtin_sqrt(al) * __builtin_sqrt(be)) {
+                        const double zeta = (be - al) / (2.0 * ga);
+                        const double az = __builtin_fabs(zeta);
+                        double tt = az > 1e150 ? 0.5 / az : 1.0 / (az + __builtin_sqrt(1.0 + zeta * zeta));
+                        tt = zeta < 0.0 ? -tt : tt;
+                        const double c = 1.0 / __builtin_sqrt(1.0 + tt * tt), sn = c * tt;
+#pragma unroll
+                        for (int u = 0; u < kJacPer; ++u) {
+                            const int e = gl + 16 * u;
+                            if (e < l) {
+                                Mc[p][e] = c * mp[u] - sn * mq[u];
+                                Mc[q][e] = sn * mp[u] + c * mq[u];
+                                const double jp = Jc[p][e], jq = Jc[q][e];
+                                Jc[p][e] = c * jp - sn * jq;
+                                Jc[q][e] = sn * jp + c * jq;
+                            }
+                        }
+                        if (gl == 0) rotated = 1;
+                    }
                 }
-                if (in1) {
-                    Mc[p][e1] = c * mp1 - sn * mq1;
-                    Mc[q][e1] = sn * mp1 + c * mq1;
-                    const double jp = Jc[p][e1], jq = Jc[q][e1];
-                    Jc[p][e1] = c * jp - sn * jq;
-                    Jc[q][e1] = sn * jp + c * jq;
-                }
-                if (lane == 0) rotated = 1;
             }
             __syncthreads();
         }
@@ -163,12 +184,17 @@ __global__ __launch_bounds__(kJacThreads) void k_fact_jacobi(const double* __res
         }
     }
     if (tid == 0 && !converged) *flag = 1;
-    // singular values: one wave per column
-    for (int j = wave; j < l; j += kJacWaves) {
-        const double v0 = in0 ? Mc[j][lane] : 0.0, v1 = in1 ? Mc[j][e1] : 0.0;
-        double x = v0 * v0 + v1 * v1, y = 0.0, z = 0.0;
-        wave_sum3(x, y, z);
-        if (lane == 0) sig[j] = __builtin_sqrt(x);
+    // singular values: one group of 16 lanes per column
+    for (int j = grp; j < l; j += kJacThreads / 16) {
+        double x = 0.0, y = 0.0, z = 0.0;
+#pragma unroll
+        for (int u = 0; u < kJacPer; ++u) {
+            const int e = gl + 16 * u;
+            const double v = e < l ? Mc[j][e] : 0.0;
+            x += v * v;
+        }
+        group16_sum3(x, y, z);
+        if (gl == 0) sig[j] = __builtin_sqrt(x);
     }
     __syncthreads();
     if (tid < l) {
