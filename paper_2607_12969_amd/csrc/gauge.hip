@@ -49,41 +49,43 @@ __global__ __launch_bounds__(256) void k_gauge_pad(const double* __restrict__ sr
 // not above 2^-46 of the column's original diagonal (or not a number); R is
 // then unspecified.
 constexpr int kGaugeMaxRank = LRC_GAUGE_MAX_RANK;
-constexpr int kFillPerThread = (kGaugeMaxRank * kGaugeMaxRank + 255) / 256;
+constexpr int kCholSide = 32;                          // the Cholesky's thread grid is kCholSide^2
+constexpr int kCholThreads = kCholSide * kCholSide;
 
 // S[i][j] = M[i][j] (pitch ld) for j >= i, 0 below the diagonal, i, j < r,
-// by 256 threads: every thread issues all its global loads before it
+// by NTH threads: every thread issues all its global loads before it
 // writes LDS, so their latencies overlap.
-template <int LDP>
+template <int LDP, int NTH = 256>
 __device__ __forceinline__ void fill_upper(double (*S)[LDP], const double* __restrict__ M, int r, int ld,
                                            int tid) {
+    constexpr int kFillPerThread = (kGaugeMaxRank * kGaugeMaxRank + NTH - 1) / NTH;
     double v[kFillPerThread];
 #pragma unroll
     for (int q = 0; q < kFillPerThread; ++q) {
-        const int idx = tid + q * 256;
+        const int idx = tid + q * NTH;
         const int i = idx / r, j = idx - i * r;
         v[q] = (idx < r * r && j >= i) ? M[(int64_t)i * ld + j] : 0.0;
     }
 #pragma unroll
     for (int q = 0; q < kFillPerThread; ++q) {
-        const int idx = tid + q * 256;
+        const int idx = tid + q * NTH;
         const int i = idx / r, j = idx - i * r;
         if (idx < r * r) S[i][j] = v[q];
     }
 }
 
-__global__ __launch_bounds__(256) void k_gauge_chol(const double* __restrict__ G, int r, int ld,
-                                                    double* __restrict__ R, int* __restrict__ flag) {
+__global__ __launch_bounds__(kCholThreads) void k_gauge_chol(const double* __restrict__ G, int r, int ld,
+                                                             double* __restrict__ R, int* __restrict__ flag) {
     __shared__ double S[kGaugeMaxRank][kGaugeMaxRank + 1];
     __shared__ double Rm[kGaugeMaxRank][kGaugeMaxRank + 1];   // R, written out at the end
     __shared__ double diag0[kGaugeMaxRank];
     __shared__ int bad;
-    constexpr int kBlk = (kGaugeMaxRank + 15) / 16;
-    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-    fill_upper(S, G, r, ld, tid);
+    constexpr int kBlk = (kGaugeMaxRank + kCholSide - 1) / kCholSide;
+    const int tid = threadIdx.x, tx = tid % kCholSide, ty = tid / kCholSide;
+    fill_upper<kGaugeMaxRank + 1, kCholThreads>(S, G, r, ld, tid);
     if (tid == 0) bad = 0;
     __syncthreads();
-    for (int i = tid; i < r; i += 256) diag0[i] = S[i][i];
+    for (int i = tid; i < r; i += kCholThreads) diag0[i] = S[i][i];
     __syncthreads();
     for (int k = 0; k < r; ++k) {
         const double d = S[k][k];
@@ -92,30 +94,31 @@ __global__ __launch_bounds__(256) void k_gauge_chol(const double* __restrict__ G
         if (tid == 0 && !(d > 0x1p-46 * diag0[k]) && bad == 0) bad = 1 + k;
         // row k of R (row k of S is not written in this step); global
         // stores here would make every barrier wait for them
-        for (int j = k + tid; j < r; j += 256) Rm[k][j] = j == k ? sq : S[k][j] / sq;
+        for (int j = k + tid; j < r; j += kCholThreads) Rm[k][j] = j == k ? sq : S[k][j] / sq;
         // trailing update of the upper triangle, k < i <= j: thread (ty, tx)
-        // of a 16 x 16 grid takes rows ty + 16 a and columns tx + 16 b;
+        // of the square thread grid takes rows ty + kCholSide a and columns
+        // tx + kCholSide b;
         // each row's reads are issued together before its writes
         double rk[kBlk];
 #pragma unroll
         for (int b = 0; b < kBlk; ++b) {
-            const int j = b * 16 + tx;
+            const int j = b * kCholSide + tx;
             rk[b] = (j > k && j < r) ? S[k][j] : 0.0;
         }
 #pragma unroll
         for (int a = 0; a < kBlk; ++a) {
-            const int i = a * 16 + ty;
+            const int i = a * kCholSide + ty;
             if (i > k && i < r) {
                 const double ski = S[k][i] * inv;
                 double cur[kBlk];
 #pragma unroll
                 for (int b = 0; b < kBlk; ++b) {
-                    const int j = b * 16 + tx;
+                    const int j = b * kCholSide + tx;
                     cur[b] = (j >= i && j < r) ? S[i][j] : 0.0;
                 }
 #pragma unroll
                 for (int b = 0; b < kBlk; ++b) {
-                    const int j = b * 16 + tx;
+                    const int j = b * kCholSide + tx;
                     if (j >= i && j < r) S[i][j] = cur[b] - ski * rk[b];
                 }
             }
@@ -123,7 +126,7 @@ __global__ __launch_bounds__(256) void k_gauge_chol(const double* __restrict__ G
         __syncthreads();
     }
     if (tid == 0 && bad) *flag = bad;
-    for (int idx = tid; idx < ld * ld; idx += 256) {
+    for (int idx = tid; idx < ld * ld; idx += kCholThreads) {
         const int i = idx / ld, j = idx - i * ld;
         R[idx] = (i < r && j < r && j >= i) ? Rm[i][j] : 0.0;
     }
@@ -327,12 +330,12 @@ hipError_t launch_cholqr2(const double* A, int64_t rows, int r, double* Q, doubl
     hipError_t e = launch_gram(A, rows, rp, G, ws, stream);
     if (e != hipSuccess) return e;
     ws.used = gmark;
-    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R1, flag);
+    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R1, flag);
     launch_trsm(A, rows, r, rp, R1, rp, W2, rp, stream);
     e = launch_gram(W2, rows, rp, G, ws, stream);
     if (e != hipSuccess) return e;
     ws.used = gmark;
-    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R2, flag);
+    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R2, flag);
     launch_trsm(W2, rows, r, rp, R2, rp, Q, rp, stream);
     if (R) {
         // R = R2 R1: rows 0..r-1 of the triangular product, R1 taken as an r x rp block
@@ -367,13 +370,13 @@ hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t
         hipError_t e = launch_gram(W1, rows, rp, G, ws, stream);
         if (e != hipSuccess) return e;
         ws.used = gmark;
-        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R1, flags + l);
+        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R1, flags + l);
         launch_trsm(W1, rows, r, rp, R1, rp, W2, rp, stream);
         // second pass on W2: core l = W2 R2^{-1}; R = R2 R1
         e = launch_gram(W2, rows, rp, G, ws, stream);
         if (e != hipSuccess) return e;
         ws.used = gmark;
-        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(256), 0, stream, G, r, rp, R2, flags + l);
+        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R2, flags + l);
         launch_trsm(W2, rows, r, rp, R2, rp, cores[l], r, stream);
         // core l+1 <- R2 (R1 core l+1) on its left unfolding (r x ncols)
         const dim3 gl((unsigned)((ncols + 255) / 256), (unsigned)((r + kLmulRows - 1) / kLmulRows));
