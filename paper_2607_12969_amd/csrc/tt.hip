@@ -965,88 +965,13 @@ __device__ __forceinline__ uint32_t last_off(int t, int tlast, uint32_t nl, uint
     return ((uint32_t)(t < tlast ? t : tlast) * nl + c) * (uint32_t)sizeof(T);
 }
 
-// Last products of the three sets for the wave's tile and the five sums.
-// The fragments of G_3 [r_2][n_3] (lane (r, g) of step kb, block cp:
-// G_3(4 kb + g, 16 cp + r)) run four steps ahead: N holds steps 0..3 of a
-// block, R the later steps in turn, and the last four steps of a block
-// fetch the first four of the next.
-template <int NKB>
-__device__ __forceinline__ void last_w(const TTArgs& a, const double* __restrict__ Tref, int64_t i, int64_t L0,
-                                       int r, int g, const double (&zf)[3][NKB], double (&sum)[5]) {
-    const int n_cb = (int)((a.n_last + 15) / 16);
-    const double* b0 = static_cast<const double*>(a.set[0].core[1]);
-    const double* b1 = static_cast<const double*>(a.set[1].core[1]);
-    const double* b2 = static_cast<const double*>(a.set[2].core[1]);
-    const int tl0 = a.set[0].rM - 1, tl1 = a.set[1].rM - 1, tl2 = a.set[2].rM - 1;
-    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
-    auto colc = [&](int cp) {
-        const uint32_t c = (uint32_t)(16 * cp + r);
-        return c < clast ? c : clast;
-    };
-    auto ld = [&](double (&f)[3], int gg, int kb, uint32_t c) {
-        const int t = 4 * kb + gg;
-        f[0] = ld_off(b0, last_off<double>(t, tl0, nl, c));
-        f[1] = ld_off(b1, last_off<double>(t, tl1, nl, c));
-        f[2] = ld_off(b2, last_off<double>(t, tl2, nl, c));
-    };
-    double N[4][3], R[4][3];
-    uint32_t c = colc(0);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) ld(N[s], g, s, c);
-    for (int cp = 0; cp < n_cb; ++cp) {
-        // per-block copy of the lane group: the step offsets are formed here
-        // rather than all kept live across the loop
-        int gg = g;
-        asm volatile("" : "+v"(gg));
-        const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
-        const int64_t col = (int64_t)cp * 16 + r;
-        double tv[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t L = L0 + g + 4 * v;
-            const bool ok = L < a.NL && col < a.n_last;
-            tv[v] = Tref[ok ? (L * a.n_mid + i) * a.n_last + col : 0];
-        }
-        double4_t acc[3];
-#pragma unroll
-        for (int q = 0; q < 3; ++q) acc[q] = zero_accv<double4_t>();
-        // (the last block's fetches of a next block reread its own first
-        // steps: a second copy of the unrolled block would not fit the
-        // registers of the three sets)
-#pragma unroll
-        for (int s = 0; s < NKB; ++s) {
-#pragma unroll
-            for (int q = 0; q < 3; ++q) acc[q] = mfma(zf[q][s], s < 4 ? N[s][q] : R[s % 4][q], acc[q]);
-            const int k = s + 4;
-            if (k < NKB) ld(R[k % 4], gg, k, c);
-            else ld(N[k - NKB], gg, k - NKB, cn);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        // lane holds rows L0 + g + 4v of column col
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const bool ok = L0 + g + 4 * v < a.NL && col < a.n_last;
-            const double t = ok ? tv[v] : 0.0;
-            const double r0 = ok ? acc[0][v] : 0.0;
-            const double r1 = ok ? acc[1][v] : 0.0;
-            const double r2 = ok ? acc[2][v] : 0.0;
-            const double d0 = t - r0, d1 = t - r1, d2 = r1 - r2, d3 = t - r2;
-            sum[0] += d0 * d0;
-            sum[1] += d1 * d1;
-            sum[2] += d2 * d2;
-            sum[3] += d3 * d3;
-            sum[4] += t * t;
-        }
-        c = cn;
-    }
-}
-
 // Last product of a reconstruction wave tile: NPB row blocks of 16 rows,
 // stored straight from the accumulators (lane (r, g), value v: row
 // L0 + 16 pb + g + 4 v of column 16 cp + r, so that each store instruction
-// writes 128-byte row segments).  The core fragments run D steps ahead in
-// the ring of last_w (N: steps 0 .. D-1 of a block, R: the later steps;
-// the last D steps of a block fetch the first D of the next).
+// writes 128-byte row segments).  The core fragments (lane (r, g) of step
+// kb, block cp: G_3(4 kb + g, 16 cp + r)) run D steps ahead in a ring (N:
+// steps 0 .. D-1 of a block, R: the later steps; the last D steps of a
+// block fetch the first D of the next).
 template <int NKB, int NPB, int D>
 __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t L0, int r, int g,
                                              const double (&zf)[NPB][NKB]) {
@@ -1114,8 +1039,12 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
 // for one middle index i (tile = i * ceil(n_1 / (16 NPB)) + row block, or
 // row block * n_2 + i for short output rows, TTArgs::ifast), the
 // interfaces Z_2 of its row blocks held in registers as the A fragments of
-// the last product (see the wave-tile certificate below).  The core ring is
-// 8 steps deep (4 for four row blocks, whose steps are twice as long).
+// the last product (the FP64 MFMA leaves value v of column block tb of Z_2
+// in the lanes and order that the last product's K step 4 tb + v takes as
+// its A operand).  The four waves of a workgroup, and consecutive
+// workgroups of one XCD, share i and so the middle core slice in L2.  The
+// core ring is 8 steps deep (4 for four row blocks, whose steps are twice
+// as long).
 template <int NKB, int NPB>
 __global__ __launch_bounds__(256) void k_tt_wave(TTArgs a, int64_t ntiles) {
     constexpr int NT = (NKB + 3) / 4;
@@ -1611,52 +1540,153 @@ static int64_t wave_grid(const TTPlan& p) {
     return xcd_grid(std::min<int64_t>((p.wave_tiles + 3) / 4, 4096));
 }
 
-// ntiles = n_2 * ceil(n_1 / 16) wave tiles, tile = i * ceil(n_1 / 16) + L
-// block (the four waves of a workgroup, and consecutive workgroups of one
-// XCD, share i and so the middle core slice in L2), or L block * n_2 + i for
-// short output rows (TTArgs::ifast).  The grid is a multiple
-// of 8; workgroup w writes part[s * gridDim.x + w] (sums as in k_tt_cert).
-template <int NKB>
-__global__ __launch_bounds__(256) void k_tt_cert_w(TTArgs a, const double* __restrict__ Tref,
-                                                   double* __restrict__ part, int64_t ntiles) {
+// The certificate split by what its sums couple: set 0 (the base train)
+// only meets T (sums 0 and 4), sets 1 and 2 (the augmented train in FP64 and
+// as stored) meet T and each other (sums 1, 2, 3).  Each part runs as
+// NPB-row-block wave tiles like the reconstruction, so every G_3 fragment
+// feeds NS NPB products and every G_2 fragment NPB.  Last products of the NS
+// sets for a tile, with T read once per column block before its products;
+// the core ring runs D steps ahead as in last_store_w.
+template <int NKB, int NPB, int NS, int D>
+__device__ __forceinline__ void last_cert_s(const TTArgs& a, const double* __restrict__ Tref, int64_t i, int64_t L0,
+                                            int r, int g, const double (&zf)[NS][NPB][NKB],
+                                            double (&sum)[NS == 1 ? 2 : 3]) {
+    static_assert(D <= NKB, "ring deeper than a block");
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    const double* bq[NS];
+    int tl[NS];
+#pragma unroll
+    for (int q = 0; q < NS; ++q) {
+        const TTSet& S = a.set[NS == 1 ? 0 : 1 + q];
+        bq[q] = static_cast<const double*>(S.core[1]);
+        tl[q] = S.rM - 1;
+    }
+    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
+    auto colc = [&](int cp) {
+        const uint32_t c = (uint32_t)(16 * cp + r);
+        return c < clast ? c : clast;
+    };
+    double N[D][NS], R[D][NS];
+    uint32_t c = colc(0);
+#pragma unroll
+    for (int s = 0; s < D; ++s)
+#pragma unroll
+        for (int q = 0; q < NS; ++q) N[s][q] = ld_off(bq[q], last_off<double>(4 * s + g, tl[q], nl, c));
+    for (int cp = 0; cp < n_cb; ++cp) {
+        int gg = g;
+        asm volatile("" : "+v"(gg));
+        const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
+        const int64_t col = (int64_t)cp * 16 + r;
+        double tv[NPB][4];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t L = L0 + 16 * pb + g + 4 * v;
+                const bool ok = L < a.NL && col < a.n_last;
+                tv[pb][v] = Tref[ok ? (L * a.n_mid + i) * a.n_last + col : 0];
+            }
+        double4_t acc[NS][NPB];
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[q][pb] = zero_accv<double4_t>();
+        auto block = [&](auto more) {
+#pragma unroll
+            for (int s = 0; s < NKB; ++s) {
+#pragma unroll
+                for (int q = 0; q < NS; ++q) {
+                    const double f = s < D ? N[s][q] : R[s % D][q];
+#pragma unroll
+                    for (int pb = 0; pb < NPB; ++pb) acc[q][pb] = mfma(zf[q][pb][s], f, acc[q][pb]);
+                }
+                const int k = s + D;
+#pragma unroll
+                for (int q = 0; q < NS; ++q) {
+                    if (k < NKB) R[k % D][q] = ld_off(bq[q], last_off<double>(4 * k + gg, tl[q], nl, c));
+                    else if constexpr (decltype(more)::value)
+                        N[k - NKB][q] = ld_off(bq[q], last_off<double>(4 * (k - NKB) + gg, tl[q], nl, cn));
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        if (cp + 1 < n_cb) block(std::true_type{});
+        else block(std::false_type{});
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const bool ok = L0 + 16 * pb + g + 4 * v < a.NL && col < a.n_last;
+                const double t = ok ? tv[pb][v] : 0.0;
+                if constexpr (NS == 1) {
+                    const double d0 = t - (ok ? acc[0][pb][v] : 0.0);
+                    sum[0] += d0 * d0;
+                    sum[1] += t * t;
+                } else {
+                    const double r1 = ok ? acc[0][pb][v] : 0.0, r2 = ok ? acc[1][pb][v] : 0.0;
+                    const double d1 = t - r1, d2 = r1 - r2, d3 = t - r2;
+                    sum[0] += d1 * d1;
+                    sum[1] += d2 * d2;
+                    sum[2] += d3 * d3;
+                }
+            }
+        c = cn;
+    }
+}
+
+// One part of the split certificate (see last_cert_s): tiles of 16 NPB rows
+// of G_1 for one middle index, ordered as in k_tt_wave.  Workgroup w writes
+// its sums to part[row * G + w] (rows 0, 4 for NS = 1; 1, 2, 3 for NS = 2)
+// and zeros to the entries w + gridDim.x, w + 2 gridDim.x, ... < G, so both
+// parts fill the same [5][G] layout whatever their grids.
+template <int NKB, int NPB, int NS>
+__global__ __launch_bounds__(256) void k_tt_cert_s(TTArgs a, const double* __restrict__ Tref,
+                                                   double* __restrict__ part, int64_t ntiles, int64_t G) {
     constexpr int NT = (NKB + 3) / 4;
-    __shared__ double red[4][5];
+    constexpr int NSUM = NS == 1 ? 2 : 3;
+    constexpr int D = NKB < (NPB * NS >= 4 ? 4 : 8) ? NKB : (NPB * NS >= 4 ? 4 : 8);
+    __shared__ double red[4][NSUM];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t nLb = (a.NL + 15) / 16;
-    double sum[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
+    double sum[NSUM];
+#pragma unroll
+    for (int q = 0; q < NSUM; ++q) sum[q] = 0.0;
     const int64_t wl = xcd_tile(gridDim.x);
     for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
         const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
-        const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16;
-        double zf[3][NKB];
+        const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
+        double zf[NS][NPB][NKB];
 #pragma unroll
-        for (int q = 0; q < 3; ++q) {
-            // per-set copy of the lane index: the set's addresses are formed
-            // here instead of being kept live across the tile loop
+        for (int q = 0; q < NS; ++q) {
             int ln = lane;
             asm volatile("" : "+v"(ln));
-            double4_t acc[NT];
-            middle_w<double, NT>(a, a.set[q], i, L0, ln & 15, ln >> 4, acc);
+            double4_t acc[NPB][NT];
+            middle_w_tile<double, NT, NPB>(a, a.set[NS == 1 ? 0 : 1 + q], i, L0, ln & 15, ln >> 4, acc);
 #pragma unroll
-            for (int tb = 0; tb < NT; ++tb)
+            for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    if (4 * tb + v < NKB) zf[q][4 * tb + v] = acc[tb][v];
+                for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        if (4 * tb + v < NKB) zf[q][pb][4 * tb + v] = acc[pb][tb][v];
         }
         int ln = lane;
         asm volatile("" : "+v"(ln));
-        last_w<NKB>(a, Tref, i, L0, ln & 15, ln >> 4, zf, sum);
+        last_cert_s<NKB, NPB, NS, D>(a, Tref, i, L0, ln & 15, ln >> 4, zf, sum);
     }
 #pragma unroll
-    for (int s = 0; s < 5; ++s) {
-        const double w = wave_sum(sum[s]);
-        if (lane == 0) red[wave][s] = w;
+    for (int q = 0; q < NSUM; ++q) {
+        const double w = wave_sum(sum[q]);
+        if (lane == 0) red[wave][q] = w;
     }
     __syncthreads();
-    if (threadIdx.x < 5)
-        part[threadIdx.x * (int64_t)gridDim.x + blockIdx.x] =
+    if (threadIdx.x < NSUM) {
+        const int row = NS == 1 ? (threadIdx.x == 0 ? 0 : 4) : 1 + (int)threadIdx.x;
+        part[row * G + blockIdx.x] =
             ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
+        for (int64_t w = blockIdx.x + gridDim.x; w < G; w += gridDim.x) part[row * G + w] = 0.0;
+    }
 }
 
 template <typename T>
@@ -1735,7 +1765,7 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
                           round_up(ncp * p.set[q].Kp3 * e, 256));
         return b;
     };
-    // With d = 3 the kernels run by wave tiles (k_tt_cert_w for the FP64
+    // With d = 3 the kernels run by wave tiles (k_tt_cert_s for the FP64
     // certificate, k_tt_wave / k_tt_wave32 / k_tt_wave16 for the
     // reconstruction) when the last product's K extent fits one of their
     // register layouts: NKB K steps of 4 (FP64, FP32: Kp3 = 4 NKB <= 68) or of
@@ -2017,18 +2047,43 @@ hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, cons
     hipError_t e = prepare_tt<double>(p, cores, nullptr, ws, stream, "cert_tt_fused_f64", a);
     if (e != hipSuccess) return e;
     if (p.wave_nkb) {
-        const dim3 gw((unsigned)wave_grid(p));
+        // the split certificate: set 0 with two row blocks per tile (one
+        // where the tiles would not give every SIMD two waves), sets 1 and 2
+        // together with one (two would exceed the registers of two waves per
+        // SIMD), each part with the K steps of its own ranks
+        const int64_t G = wave_grid(p);
+        auto nkb_of = [](int rM) {
+            static const int lst[] = {4, 8, 12, 16, 17};
+            for (int c : lst)
+                if (4 * c >= rM) return c;
+            return 0;
+        };
+        const int nkA = nkb_of(p.set[0].rM), nkB = nkb_of(std::max(p.set[1].rM, p.set[2].rM));
+        if (!nkA || !nkB) return hipErrorInvalidValue;
+        auto tiles = [&](int npb) { return p.n_mid * ((p.NL + 16 * npb - 1) / (16 * npb)); };
+        const int npA = tiles(2) >= 2048 ? 2 : 1;
+        const int64_t ntA = tiles(npA), ntB = tiles(1);
+        const dim3 gA(xcd_grid(std::min<int64_t>((ntA + 3) / 4, 4096))), gB(xcd_grid(std::min<int64_t>((ntB + 3) / 4, 4096)));
+        if ((int64_t)gA.x > G || (int64_t)gB.x > G) return hipErrorInvalidValue;
         KernelTimer tk("cert_tt_fused_f64", stream);
-#define LRC_TTW(K) hipLaunchKernelGGL((k_tt_cert_w<K>), gw, dim3(256), 0, stream, a, Tref, part, p.wave_tiles)
-        switch (p.wave_nkb) {
-        case 4: LRC_TTW(4); break;
-        case 8: LRC_TTW(8); break;
-        case 12: LRC_TTW(12); break;
-        case 16: LRC_TTW(16); break;
-        case 17: LRC_TTW(17); break;
-        default: return hipErrorInvalidValue;
+#define LRC_TCS(K, P, S, g, nt) \
+    hipLaunchKernelGGL((k_tt_cert_s<K, P, S>), g, dim3(256), 0, stream, a, Tref, part, nt, G)
+#define LRC_TCS_K(P, S, nk, g, nt)                    \
+    switch (nk) {                                     \
+    case 4: LRC_TCS(4, P, S, g, nt); break;           \
+    case 8: LRC_TCS(8, P, S, g, nt); break;           \
+    case 12: LRC_TCS(12, P, S, g, nt); break;         \
+    case 16: LRC_TCS(16, P, S, g, nt); break;         \
+    default: LRC_TCS(17, P, S, g, nt); break;         \
+    }
+        if (npA == 2) {
+            LRC_TCS_K(2, 1, nkA, gA, ntA)
+        } else {
+            LRC_TCS_K(1, 1, nkA, gA, ntA)
         }
-#undef LRC_TTW
+        LRC_TCS_K(1, 2, nkB, gB, ntB)
+#undef LRC_TCS_K
+#undef LRC_TCS
         return hipGetLastError();
     }
     const dim3 grid((unsigned)p.num_i_blocks, (unsigned)p.grid_L);
