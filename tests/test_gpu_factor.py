@@ -156,6 +156,7 @@ def _noisy_tensor(dims, tag):
 
 
 TT_CASES = [
+    ((40, 30), (7,), 3, 0),                 # d = 2: one step, the last core is diag(s) V^T
     ((20, 18, 16), (5, 6), 4, 0),
     ((13, 11, 9), (4, 5), 3, 0),            # odd sizes: staged unfoldings
     ((6, 7, 5, 8), (4, 6, 5), 2, 1),
