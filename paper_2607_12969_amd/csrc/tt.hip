@@ -765,117 +765,15 @@ __device__ __forceinline__ T ld_off(const T* base, uint32_t byte_off) {
     return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
-// Middle product of one set for the wave's tile (FP64 or FP32, one K value
-// per lane): acc[tb] for the NT column blocks of Z_2, over ceil(r_1 / 4) K
-// steps.  A fragments come straight from G_2 [r_1][n_2][r_2] (lane (r, g) of
-// step kb reads G_2(4 kb + g, i, 16 tb + r): sixteen consecutive entries per
-// lane group), B fragments from the rows of G_1.  Indices past the ranks
-// are clamped into the cores, so the loads are unconditional; the A values
-// there are replaced by zero right before their product (the Z_2 columns
-// past r_2 are then exactly zero), the clamped rows of G_1 belong to
-// discarded rows of the tile.
-template <typename T, int NT>
-__device__ __forceinline__ void middle_w(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
-                                         typename PrecTraits<T>::accv (&acc)[NT]) {
-    using AccV = typename PrecTraits<T>::accv;
-    const T* g2 = static_cast<const T*>(S.core[0]) + i * S.rM;   // uniform
-    const uint32_t ld2 = (uint32_t)(a.n_mid * S.rM);            // stride of the first index of G_2
-    const int64_t row = (L0 + r < a.NL) ? L0 + r : a.NL - 1;
-    const T* zr = static_cast<const T*>(S.core[2]) + row * S.rL;
-    const int klast = S.rL - 1, tlast = S.rM - 1;
-    const int nkb = (S.rL + 3) / 4;
-    uint32_t tcol[NT];   // clamped column offsets of the blocks
-    unsigned tok = 0;    // bit tb: column 16 tb + r lies inside the rank
-#pragma unroll
-    for (int tb = 0; tb < NT; ++tb) {
-        const int t = 16 * tb + r;
-        tcol[tb] = (uint32_t)(t < tlast ? t : tlast);
-        tok |= (t <= tlast ? 1u : 0u) << tb;
-    }
-    auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
-    auto bf = [&](int kb) {
-        const int k = 4 * cl(kb) + g;
-        return zr[k < klast ? k : klast];
-    };
-    auto af = [&](T (&x)[NT], int kb) {
-        const int sk = 4 * cl(kb) + g;
-        const uint32_t ro = (uint32_t)(sk < klast ? sk : klast) * ld2;
-#pragma unroll
-        for (int tb = 0; tb < NT; ++tb) x[tb] = ld_off(g2, (ro + tcol[tb]) * (uint32_t)sizeof(T));
-    };
-#pragma unroll
-    for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<AccV>();
-    T x0[NT], x1[NT], y0[NT], y1[NT];
-    T bx0, bx1 = T(0), by0 = T(0), by1 = T(0);
-    af(x0, 0);
-    bx0 = bf(0);
-    if (nkb > 1) {
-        af(x1, 1);
-        bx1 = bf(1);
-    }
-    if (nkb > 2) {
-        af(y0, 2);
-        by0 = bf(2);
-    }
-    if (nkb > 3) {
-        af(y1, 3);
-        by1 = bf(3);
-    }
-    auto step = [&](const T (&x)[NT], T b, int kb) {
-        const bool sok = 4 * kb + g <= klast;
-#pragma unroll
-        for (int tb = 0; tb < NT; ++tb) {
-            const T xa = (sok && ((tok >> tb) & 1u)) ? x[tb] : T(0);
-            acc[tb] = mfma(xa, b, acc[tb]);
-        }
-    };
-    int kb = 0;
-    for (; kb + 7 < nkb; kb += 4) {   // every refill lies inside the chain
-        step(x0, bx0, kb);
-        af(x0, kb + 4);
-        bx0 = bf(kb + 4);
-        __builtin_amdgcn_sched_barrier(0);
-        step(x1, bx1, kb + 1);
-        af(x1, kb + 5);
-        bx1 = bf(kb + 5);
-        __builtin_amdgcn_sched_barrier(0);
-        step(y0, by0, kb + 2);
-        af(y0, kb + 6);
-        by0 = bf(kb + 6);
-        __builtin_amdgcn_sched_barrier(0);
-        step(y1, by1, kb + 3);
-        af(y1, kb + 7);
-        by1 = bf(kb + 7);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    if (kb + 3 < nkb) {   // the last full group, refilling only what remains
-        step(x0, bx0, kb);
-        if (kb + 4 < nkb) {
-            af(x0, kb + 4);
-            bx0 = bf(kb + 4);
-        }
-        step(x1, bx1, kb + 1);
-        if (kb + 5 < nkb) {
-            af(x1, kb + 5);
-            bx1 = bf(kb + 5);
-        }
-        step(y0, by0, kb + 2);
-        if (kb + 6 < nkb) {
-            af(y0, kb + 6);
-            by0 = bf(kb + 6);
-        }
-        step(y1, by1, kb + 3);
-        kb += 4;
-    }
-    if (kb < nkb) step(x0, bx0, kb);
-    if (kb + 1 < nkb) step(x1, bx1, kb + 1);
-    if (kb + 2 < nkb) step(y0, by0, kb + 2);
-}
-
 // The middle products of all NPB row blocks of a tile (FP64 or FP32) in one
-// chain: each K step multiplies the step's G_2 fragments (fetched once, for
-// every row block) with each row block's G_1 fragments, NPB NT products per
-// step; operands, clamping and masking as in middle_w.
+// chain: acc[pb][tb] for the NT column blocks of Z_2 over ceil(r_1 / 4) K
+// steps; each step multiplies the step's G_2 fragments (fetched once, for
+// every row block; lane (r, g) of step kb reads G_2(4 kb + g, i, 16 tb + r):
+// sixteen consecutive entries per lane group) with each row block's G_1
+// fragment.  Indices past the ranks are clamped into the cores, so the loads
+// are unconditional.  K values past r_1 occur in the last step only, whose
+// G_1 values there are replaced by zero; Z_2 columns past r_2 (formed from
+// clamped copies of the last column) are set to zero once the chain ends.
 template <typename T, int NT, int NPB>
 __device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
                                               typename PrecTraits<T>::accv (&acc)[NPB][NT]) {
@@ -891,12 +789,10 @@ __device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, i
     const int klast = S.rL - 1, tlast = S.rM - 1;
     const int nkb = (S.rL + 3) / 4;
     uint32_t tcol[NT];
-    unsigned tok = 0;
 #pragma unroll
     for (int tb = 0; tb < NT; ++tb) {
         const int t = 16 * tb + r;
         tcol[tb] = (uint32_t)(t < tlast ? t : tlast);
-        tok |= (t <= tlast ? 1u : 0u) << tb;
     }
     auto cl = [nkb](int k) { return k < nkb ? k : nkb - 1; };
     auto fetch = [&](T (&x)[NT], T (&b)[NPB], int kb) {
@@ -908,15 +804,21 @@ __device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, i
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) b[pb] = zr[pb][sc];
     };
-    auto step = [&](const T (&x)[NT], const T (&b)[NPB], int kb) {
-        const bool sok = 4 * kb + g <= klast;
+    // MASK: a step that may hold K values past r_1 (the tail of the chain)
+    auto step = [&](const T (&x)[NT], const T (&b)[NPB], int kb, auto mask) {
+        T bm[NPB];
 #pragma unroll
-        for (int tb = 0; tb < NT; ++tb) {
-            const T xa = (sok && ((tok >> tb) & 1u)) ? x[tb] : T(0);
-#pragma unroll
-            for (int pb = 0; pb < NPB; ++pb) acc[pb][tb] = mfma(xa, b[pb], acc[pb][tb]);
+        for (int pb = 0; pb < NPB; ++pb) {
+            if constexpr (decltype(mask)::value) bm[pb] = 4 * kb + g <= klast ? b[pb] : T(0);
+            else bm[pb] = b[pb];
         }
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[pb][tb] = mfma(x[tb], bm[pb], acc[pb][tb]);
     };
+    constexpr std::false_type kFull{};
+    constexpr std::true_type kTail{};
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
@@ -929,32 +831,41 @@ __device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, i
     if (nkb > 3) fetch(y1, c1, 3);
     int kb = 0;
     for (; kb + 7 < nkb; kb += 4) {   // every refill lies inside the chain
-        step(x0, b0, kb);
+        step(x0, b0, kb, kFull);
         fetch(x0, b0, kb + 4);
         __builtin_amdgcn_sched_barrier(0);
-        step(x1, b1, kb + 1);
+        step(x1, b1, kb + 1, kFull);
         fetch(x1, b1, kb + 5);
         __builtin_amdgcn_sched_barrier(0);
-        step(y0, c0, kb + 2);
+        step(y0, c0, kb + 2, kFull);
         fetch(y0, c0, kb + 6);
         __builtin_amdgcn_sched_barrier(0);
-        step(y1, c1, kb + 3);
+        step(y1, c1, kb + 3, kFull);
         fetch(y1, c1, kb + 7);
         __builtin_amdgcn_sched_barrier(0);
     }
     if (kb + 3 < nkb) {   // the last full group, refilling only what remains
-        step(x0, b0, kb);
+        step(x0, b0, kb, kTail);
         if (kb + 4 < nkb) fetch(x0, b0, kb + 4);
-        step(x1, b1, kb + 1);
+        step(x1, b1, kb + 1, kTail);
         if (kb + 5 < nkb) fetch(x1, b1, kb + 5);
-        step(y0, c0, kb + 2);
+        step(y0, c0, kb + 2, kTail);
         if (kb + 6 < nkb) fetch(y0, c0, kb + 6);
-        step(y1, c1, kb + 3);
+        step(y1, c1, kb + 3, kTail);
         kb += 4;
     }
-    if (kb < nkb) step(x0, b0, kb);
-    if (kb + 1 < nkb) step(x1, b1, kb + 1);
-    if (kb + 2 < nkb) step(y0, c0, kb + 2);
+    if (kb < nkb) step(x0, b0, kb, kTail);
+    if (kb + 1 < nkb) step(x1, b1, kb + 1, kTail);
+    if (kb + 2 < nkb) step(y0, c0, kb + 2, kTail);
+    // lane (r, g), value v of column block tb holds Z_2 column 16 tb + acc_row(g, v)
+#pragma unroll
+    for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const bool ok = 16 * tb + acc_row<T>(g, v) <= tlast;
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[pb][tb][v] = ok ? acc[pb][tb][v] : 0;
+        }
 }
 
 // Byte offset of the last core's entry G_3(t, c) (row t clamped to the
