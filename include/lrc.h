@@ -333,13 +333,15 @@ int64_t lrc_tt_memory_matched_rank(const int64_t* dims, int d, int64_t budget_by
  * are unique up to the sign of each singular pair when the singular values
  * are distinct; a singular value that is exactly zero gets a zero column in
  * U.  Orthonormalizations are CholeskyQR2 (as lrc_tt_left_orthogonalize);
- * the small SVD is one-sided Jacobi.  Synchronizes the calling thread's
- * stream.  Errors: LRC_EINVAL (NULL pointer, sizes outside 1 <= k <= l <=
- * min(m, n), l > LRC_RSVD_MAX_SAMPLES, power_iters outside [0,
+ * when one breaks down (condition number above about 1e7) the whole call is
+ * repeated once with shifted CholeskyQR3, which holds to about 1e15; the
+ * small SVD is one-sided Jacobi.  Synchronizes the calling thread's stream.
+ * Errors: LRC_EINVAL (NULL pointer, sizes outside 1 <= k <= l <= min(m, n),
+ * l > LRC_RSVD_MAX_SAMPLES, power_iters outside [0,
  * LRC_RSVD_MAX_POWER_ITERS], an output overlapping an input or another
  * output), LRC_ENUMERIC (a sketch or projected matrix numerically rank
- * deficient for CholeskyQR2, i.e. condition number above about 1e7, or a
- * Jacobi sweep limit reached), LRC_EOVERFLOW, LRC_ENOMEM, LRC_EHIP,
+ * deficient even for shifted CholeskyQR3, e.g. a matrix of rank below l, or
+ * a Jacobi sweep limit reached), LRC_EOVERFLOW, LRC_ENOMEM, LRC_EHIP,
  * LRC_ENODEV. */
 int lrc_rsvd(const double* A, int64_t m, int64_t n, const double* omega, int64_t l, int power_iters, int64_t k,
              double* U, double* s, double* V);

@@ -243,9 +243,12 @@ size_t rsvd_workspace_bytes(int64_t m, int64_t n, int l, int k, int q, bool vts)
 // pitches.  Outputs (any that are null are skipped): U (m x k, pitch ldu),
 // s_out (k), V (n x k, pitch ldv), Vts = diag(s) V^T (k x n, pitch ldvt).
 // flags[0]: range finder QR, flags[1]: QR of B^T, flags[2]: Jacobi.
+// shifted: every orthonormalization by shifted CholeskyQR3 instead of
+// CholeskyQR2 (for sketches with condition numbers between about 1e7 and
+// 1e15; half as much QR work again).
 hipError_t launch_rsvd(const double* A, int64_t m, int64_t n, int64_t lda, const double* Om, int64_t ldo, int l,
                        int q, int k, double* U, int64_t ldu, double* s_out, double* V, int64_t ldv, double* Vts,
-                       int64_t ldvt, int* flags, Workspace& ws, hipStream_t st) {
+                       int64_t ldvt, int* flags, Workspace& ws, hipStream_t st, bool shifted) {
     const int rp = (int)round_up(l, 2);
     const int64_t ldn = round_up(n, 2);
     double* Y = static_cast<double*>(ws.take((size_t)m * rp * 8));
@@ -268,22 +271,22 @@ hipError_t launch_rsvd(const double* A, int64_t m, int64_t n, int64_t lda, const
         ws.used = mark;                    \
     } while (0)
     LRC_STEP(launch_gemm_nt(Om, ldo, l, A, lda, m, n, nullptr, Y, rp, rp, ws, st, "factor_sketch_f64"));
-    LRC_STEP(launch_cholqr2(Y, m, l, Q, nullptr, flags, ws, st, "factor_cholqr2_f64"));
+    LRC_STEP(launch_cholqr2(Y, m, l, Q, nullptr, flags, ws, st, "factor_cholqr2_f64", shifted));
     for (int it = 0; it < q; ++it) {
         LRC_STEP(launch_gemm_tn(Q, rp, l, A, lda, n, m, Bt, rp, rp, ws, st, "factor_project_f64",
                                 "factor_project_finish_f64"));
-        LRC_STEP(launch_cholqr2(Bt, n, l, Q2, nullptr, flags, ws, st, "factor_cholqr2_f64"));
+        LRC_STEP(launch_cholqr2(Bt, n, l, Q2, nullptr, flags, ws, st, "factor_cholqr2_f64", shifted));
         {
             KernelTimer tm("factor_transpose_f64", st);
             hipLaunchKernelGGL(k_fact_transpose, dim3((unsigned)((ldn + 31) / 32), (unsigned)((rp + 31) / 32)),
                                dim3(256), 0, st, Q2, n, (int64_t)rp, (int64_t)rp, Qzt, ldn);
         }
         LRC_STEP(launch_gemm_nt(Qzt, ldn, l, A, lda, m, n, nullptr, Y, rp, rp, ws, st, "factor_sketch_f64"));
-        LRC_STEP(launch_cholqr2(Y, m, l, Q, nullptr, flags, ws, st, "factor_cholqr2_f64"));
+        LRC_STEP(launch_cholqr2(Y, m, l, Q, nullptr, flags, ws, st, "factor_cholqr2_f64", shifted));
     }
     LRC_STEP(launch_gemm_tn(Q, rp, l, A, lda, n, m, Bt, rp, rp, ws, st, "factor_project_f64",
                             "factor_project_finish_f64"));
-    LRC_STEP(launch_cholqr2(Bt, n, l, Q2, R, flags + 1, ws, st, "factor_cholqr2_f64"));
+    LRC_STEP(launch_cholqr2(Bt, n, l, Q2, R, flags + 1, ws, st, "factor_cholqr2_f64", shifted));
     {
         KernelTimer tm("factor_jacobi_f64", st);
         hipLaunchKernelGGL(k_fact_jacobi, dim3(1), dim3(kJacThreads), 0, st, R, l, rp, k, sv, s_out, Wt, Zt,
@@ -322,14 +325,14 @@ size_t matrix_rsvd_workspace_bytes(int64_t m, int64_t n, int l, int k, int q) {
 }
 
 hipError_t launch_matrix_rsvd(const double* A, int64_t m, int64_t n, const double* Om, int l, int q, int k, double* U,
-                              double* s, double* V, int* flags, Workspace& ws, hipStream_t st) {
+                              double* s, double* V, int* flags, Workspace& ws, hipStream_t st, bool shifted) {
     hipLaunchKernelGGL(k_fact_zero, dim3(1), dim3(64), 0, st, flags, 3);
     const double *Af, *Of;
     int64_t lda, ldo;
     hipError_t e = fit(A, m, n, ws, st, &Af, &lda);
     if (e == hipSuccess) e = fit(Om, l, n, ws, st, &Of, &ldo);
     if (e != hipSuccess) return e;
-    return launch_rsvd(Af, m, n, lda, Of, ldo, l, q, k, U, k, s, V, k, nullptr, 0, flags, ws, st);
+    return launch_rsvd(Af, m, n, lda, Of, ldo, l, q, k, U, k, s, V, k, nullptr, 0, flags, ws, st, shifted);
 }
 
 // TT-SVD, step l of d - 1: C_l ((r_{l-1} n_l) x prod_{i>l} n_i) -> core l =
@@ -352,7 +355,7 @@ size_t tt_rsvd_workspace_bytes(const int64_t* dims, const int64_t* ranks, const 
 
 hipError_t launch_tt_rsvd(const double* T, const int64_t* dims, const int64_t* ranks, const int64_t* samples, int d,
                           const double* const* omegas, int q, double* const* cores, double* sigma, int* flags,
-                          Workspace& ws, hipStream_t st) {
+                          Workspace& ws, hipStream_t st, bool shifted) {
     hipLaunchKernelGGL(k_fact_zero, dim3(1), dim3(64), 0, st, flags, 3 * (d - 1));
     int64_t cols = 1;
     for (int i = 1; i < d; ++i) cols *= dims[i];
@@ -384,7 +387,7 @@ hipError_t launch_tt_rsvd(const double* T, const int64_t* dims, const int64_t* r
         if (e == hipSuccess) e = fit(omegas[l], samples[l], cols, ws, st, &Of, &ldo);
         if (e == hipSuccess)
             e = launch_rsvd(Af, rows, cols, lda, Of, ldo, (int)samples[l], q, r, cores[l], r,
-                            sigma ? sigma + soff : nullptr, nullptr, 0, next, cols, flags + 3 * l, ws, st);
+                            sigma ? sigma + soff : nullptr, nullptr, 0, next, cols, flags + 3 * l, ws, st, shifted);
         if (e != hipSuccess) return e;
         ws.used = mark;
         soff += r;

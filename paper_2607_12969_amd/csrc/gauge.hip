@@ -47,7 +47,8 @@ __global__ __launch_bounds__(256) void k_gauge_pad(const double* __restrict__ sr
 // a matrix of its own).  R is written with pitch ld, zero below the diagonal and in
 // the pad rows and columns.  flag: set to 1 + (pivot index) when a pivot is
 // not above 2^-46 of the column's original diagonal (or not a number); R is
-// then unspecified.
+// then unspecified.  shift_rel > 0 factors G + s I instead, s = shift_rel
+// trace(G) (the shifted first pass of shifted CholeskyQR3).
 constexpr int kGaugeMaxRank = LRC_GAUGE_MAX_RANK;
 constexpr int kCholSide = 32;                          // the Cholesky's thread grid is kCholSide^2
 constexpr int kCholThreads = kCholSide * kCholSide;
@@ -75,7 +76,8 @@ __device__ __forceinline__ void fill_upper(double (*S)[LDP], const double* __res
 }
 
 __global__ __launch_bounds__(kCholThreads) void k_gauge_chol(const double* __restrict__ G, int r, int ld,
-                                                             double* __restrict__ R, int* __restrict__ flag) {
+                                                             double* __restrict__ R, int* __restrict__ flag,
+                                                             double shift_rel) {
     __shared__ double S[kGaugeMaxRank][kGaugeMaxRank + 1];
     __shared__ double Rm[kGaugeMaxRank][kGaugeMaxRank + 1];   // R, written out at the end
     __shared__ double diag0[kGaugeMaxRank];
@@ -85,6 +87,16 @@ __global__ __launch_bounds__(kCholThreads) void k_gauge_chol(const double* __res
     fill_upper<kGaugeMaxRank + 1, kCholThreads>(S, G, r, ld, tid);
     if (tid == 0) bad = 0;
     __syncthreads();
+    if (shift_rel > 0.0) {
+        // trace summed by one thread in index order (deterministic)
+        if (tid == 0) {
+            double tr = 0.0;
+            for (int i = 0; i < r; ++i) tr += S[i][i];
+            const double sh = shift_rel * tr;
+            for (int i = 0; i < r; ++i) S[i][i] += sh;
+        }
+        __syncthreads();
+    }
     for (int i = tid; i < r; i += kCholThreads) diag0[i] = S[i][i];
     __syncthreads();
     for (int k = 0; k < r; ++k) {
@@ -313,38 +325,55 @@ static void launch_trsm(const double* A, int64_t rows, int r, int lda, const dou
 
 size_t cholqr2_workspace_bytes(int64_t rows, int r) {
     const int64_t rp = round_up(r, 2);
-    return (size_t)round_up(rows * rp * 8, 256) + 3 * (size_t)round_up(rp * rp * 8, 256) +
+    return (size_t)round_up(rows * rp * 8, 256) + 5 * (size_t)round_up(rp * rp * 8, 256) +
            (size_t)round_up((int64_t)gram_workspace_bytes(rows, rp), 256);
 }
 
 hipError_t launch_cholqr2(const double* A, int64_t rows, int r, double* Q, double* R, int* flag, Workspace& ws,
-                          hipStream_t stream, const char* label) {
+                          hipStream_t stream, const char* label, bool shifted) {
     const int rp = (int)round_up(r, 2);
     double* W2 = static_cast<double*>(ws.take((size_t)rows * rp * 8));
     double* G = static_cast<double*>(ws.take((size_t)rp * rp * 8));
     double* R1 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
     double* R2 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
+    double* R3 = static_cast<double*>(ws.take((size_t)rp * rp * 8));
+    double* RX = static_cast<double*>(ws.take((size_t)rp * rp * 8));
     if (ws.overrun) return hipErrorOutOfMemory;
     KernelTimer tm(label, stream);
     const size_t gmark = ws.used;
-    hipError_t e = launch_gram(A, rows, rp, G, ws, stream);
-    if (e != hipSuccess) return e;
-    ws.used = gmark;
-    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R1, flag);
-    launch_trsm(A, rows, r, rp, R1, rp, W2, rp, stream);
-    e = launch_gram(W2, rows, rp, G, ws, stream);
-    if (e != hipSuccess) return e;
-    ws.used = gmark;
-    hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R2, flag);
-    launch_trsm(W2, rows, r, rp, R2, rp, Q, rp, stream);
-    if (R) {
-        // R = R2 R1: rows 0..r-1 of the triangular product, R1 taken as an r x rp block
+    // one pass: Gram of `in`, its Cholesky factor `Rk`, out = in Rk^{-1}
+    auto pass = [&](const double* in, double* Rk, double* out, double shift_rel) {
+        hipError_t e = launch_gram(in, rows, rp, G, ws, stream);
+        ws.used = gmark;
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, Rk, flag, shift_rel);
+        launch_trsm(in, rows, r, rp, Rk, rp, out, rp, stream);
+        return hipGetLastError();
+    };
+    // rows 0..r-1 of the triangular product dst = Ra Rb (Rb taken as an r x rp block)
+    auto tri = [&](const double* Ra, const double* Rb, double* dst) {
         const dim3 gl((unsigned)((rp + 255) / 256), (unsigned)((r + kLmulRows - 1) / kLmulRows));
-        hipLaunchKernelGGL(k_gauge_lmul, gl, dim3(256), 0, stream, R2, r, rp, R1, (int64_t)rp, R);
+        hipLaunchKernelGGL(k_gauge_lmul, gl, dim3(256), 0, stream, Ra, r, rp, Rb, (int64_t)rp, dst);
+    };
+    hipError_t e;
+    if (!shifted) {
+        if ((e = pass(A, R1, W2, 0.0)) != hipSuccess || (e = pass(W2, R2, Q, 0.0)) != hipSuccess) return e;
+        if (R) tri(R2, R1, R);
+    } else {
+        // shifted CholeskyQR3 (Fukaya, Kannan, Nakatsukasa, Yamamoto, Yanagisawa 2020): the shift
+        // s = 11 (m r + r (r + 1)) u ||A||_F^2 keeps the first factorization away from breakdown for
+        // condition numbers up to about u^-1; two plain passes restore orthogonality
+        const double shift_rel = 11.0 * ((double)rows * r + (double)r * (r + 1)) * 0x1p-53;
+        if ((e = pass(A, R1, Q, shift_rel)) != hipSuccess || (e = pass(Q, R2, W2, 0.0)) != hipSuccess ||
+            (e = pass(W2, R3, Q, 0.0)) != hipSuccess)
+            return e;
+        if (R) {
+            tri(R2, R1, RX);
+            tri(R3, RX, R);
+        }
     }
     return hipGetLastError();
 }
-
 
 hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t* ranks, int d, int* flags,
                         Workspace& ws, hipStream_t stream) {
@@ -370,13 +399,13 @@ hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t
         hipError_t e = launch_gram(W1, rows, rp, G, ws, stream);
         if (e != hipSuccess) return e;
         ws.used = gmark;
-        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R1, flags + l);
+        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R1, flags + l, 0.0);
         launch_trsm(W1, rows, r, rp, R1, rp, W2, rp, stream);
         // second pass on W2: core l = W2 R2^{-1}; R = R2 R1
         e = launch_gram(W2, rows, rp, G, ws, stream);
         if (e != hipSuccess) return e;
         ws.used = gmark;
-        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R2, flags + l);
+        hipLaunchKernelGGL(k_gauge_chol, dim3(1), dim3(kCholThreads), 0, stream, G, r, rp, R2, flags + l, 0.0);
         launch_trsm(W2, rows, r, rp, R2, rp, cores[l], r, stream);
         // core l+1 <- R2 (R1 core l+1) on its left unfolding (r x ncols)
         const dim3 gl((unsigned)((ncols + 255) / 256), (unsigned)((r + kLmulRows - 1) / kLmulRows));

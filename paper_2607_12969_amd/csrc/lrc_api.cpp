@@ -882,11 +882,21 @@ static int check_rsvd_sizes(int64_t rows, int64_t cols, int64_t l, int64_t k, co
     return LRC_OK;
 }
 
-static int factor_status(const int* dflags, int nsteps, hipStream_t st, bool tt) {
+// Reads the device flags; *qr_broke tells whether only QR breakdowns (which
+// shifted CholeskyQR3 may cure) were seen.
+static int factor_status(const int* dflags, int nsteps, hipStream_t st, bool tt, bool* qr_broke = nullptr) {
     std::vector<int> hf(3 * (size_t)nsteps, 0);
     hipError_t e = hipMemcpyAsync(hf.data(), dflags, sizeof(int) * hf.size(), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) return fail_hip(e, "factorization status");
+    if (qr_broke) {
+        bool qr = false, jac = false;
+        for (int s = 0; s < nsteps; ++s) {
+            qr = qr || hf[3 * s] || hf[3 * s + 1];
+            jac = jac || hf[3 * s + 2];
+        }
+        *qr_broke = qr && !jac;
+    }
     static const char* what[3] = {"the range finder's sketch", "the projected matrix B^T", "the small Jacobi SVD"};
     for (int s = 0; s < nsteps; ++s)
         for (int q = 0; q < 3; ++q)
@@ -926,9 +936,18 @@ int lrc_rsvd(const double* A, int64_t m, int64_t n, const double* omega, int64_t
     hipError_t e = ws.reserve(matrix_rsvd_workspace_bytes(m, n, (int)l, (int)k, power_iters), st);
     if (e != hipSuccess) return fail_hip(e, "workspace");
     int* flags = static_cast<int*>(ws.take(3 * sizeof(int)));
+    const size_t mark = ws.used;
     e = launch_matrix_rsvd(A, m, n, omega, (int)l, power_iters, (int)k, U, s, V, flags, ws, st);
     if (e != hipSuccess) return fail_hip(e, "rsvd launch");
-    return factor_status(flags, 1, st, false);
+    bool qr_broke = false;
+    rc = factor_status(flags, 1, st, false, &qr_broke);
+    if (rc == LRC_ENUMERIC && qr_broke) {   // ill-conditioned sketch: once more with shifted CholeskyQR3
+        ws.used = mark;
+        e = launch_matrix_rsvd(A, m, n, omega, (int)l, power_iters, (int)k, U, s, V, flags, ws, st, true);
+        if (e != hipSuccess) return fail_hip(e, "rsvd launch");
+        rc = factor_status(flags, 1, st, false);
+    }
+    return rc;
 }
 
 int lrc_tt_rsvd(const double* T, const int64_t* dims, const int64_t* ranks, int d, const double* const* omegas,
@@ -975,7 +994,16 @@ int lrc_tt_rsvd(const double* T, const int64_t* dims, const int64_t* ranks, int 
     hipError_t e = ws.reserve(tt_rsvd_workspace_bytes(dims, ranks, samples, d, power_iters), st);
     if (e != hipSuccess) return fail_hip(e, "workspace");
     int* flags = static_cast<int*>(ws.take(3 * sizeof(int) * (size_t)d));
+    const size_t mark = ws.used;
     e = launch_tt_rsvd(T, dims, ranks, samples, d, omegas, power_iters, cores, sigma, flags, ws, st);
     if (e != hipSuccess) return fail_hip(e, "TT-SVD launch");
-    return factor_status(flags, d - 1, st, true);
+    bool qr_broke = false;
+    rc = factor_status(flags, d - 1, st, true, &qr_broke);
+    if (rc == LRC_ENUMERIC && qr_broke) {   // ill-conditioned sketch: once more with shifted CholeskyQR3
+        ws.used = mark;
+        e = launch_tt_rsvd(T, dims, ranks, samples, d, omegas, power_iters, cores, sigma, flags, ws, st, true);
+        if (e != hipSuccess) return fail_hip(e, "TT-SVD launch");
+        rc = factor_status(flags, d - 1, st, true);
+    }
+    return rc;
 }

@@ -83,13 +83,14 @@ hipError_t launch_gauge(double* const* cores, const int64_t* dims, const int64_t
                         Workspace& ws, hipStream_t stream);
 
 // Thin QR of A (rows x r inside pitch rp = r rounded to 2, 16-byte aligned,
-// rows >= r) by CholeskyQR2 (the gauge's kernels): Q (pitch rp, pad column
-// zeroed) with Q^T Q = I and, when R is not null, R = R2 R1 (rows 0..r-1 of an
-// rp x rp block, upper triangular, diag > 0); *flag becomes 1 + pivot when a
-// Cholesky factorization breaks down (left unchanged otherwise).
+// rows >= r) by CholeskyQR2 (the gauge's kernels), or by shifted CholeskyQR3
+// when `shifted` (condition numbers up to about 1e15): Q (pitch rp, pad column
+// zeroed) with Q^T Q = I and, when R is not null, R with A = Q R (rows 0..r-1
+// of an rp x rp block, upper triangular, diag > 0); *flag becomes 1 + pivot
+// when a Cholesky factorization breaks down (left unchanged otherwise).
 size_t cholqr2_workspace_bytes(int64_t rows, int r);
 hipError_t launch_cholqr2(const double* A, int64_t rows, int r, double* Q, double* R, int* flag, Workspace& ws,
-                          hipStream_t stream, const char* label);
+                          hipStream_t stream, const char* label, bool shifted = false);
 // ------------------------------------------------------ FP64 factor GEMMs ---
 // out[i][j] = s_j sum_{t<K} W[j][t] A[i][t] for i < rows, j < nw (s = 1 when
 // svals is null); out[i][j] = 0 for nw <= j < mout (mout <= nw rounded up to
@@ -110,11 +111,11 @@ hipError_t launch_gemm_tn(const double* Q, int64_t ldq, int64_t nq, const double
 // QR, [1] QR of B^T, [2] Jacobi sweep limit.
 size_t matrix_rsvd_workspace_bytes(int64_t m, int64_t n, int l, int k, int q);
 hipError_t launch_matrix_rsvd(const double* A, int64_t m, int64_t n, const double* Om, int l, int q, int k, double* U,
-                              double* s, double* V, int* flags, Workspace& ws, hipStream_t st);
+                              double* s, double* V, int* flags, Workspace& ws, hipStream_t st, bool shifted = false);
 size_t tt_rsvd_workspace_bytes(const int64_t* dims, const int64_t* ranks, const int64_t* samples, int d, int q);
 hipError_t launch_tt_rsvd(const double* T, const int64_t* dims, const int64_t* ranks, const int64_t* samples, int d,
                           const double* const* omegas, int q, double* const* cores, double* sigma, int* flags,
-                          Workspace& ws, hipStream_t st);
+                          Workspace& ws, hipStream_t st, bool shifted = false);
 // ------------------------------------------------------- certificate (matrix)
 // G = P^T P for P (rows x cols, row-major, FP64): a split-sum Gram product.
 size_t gram_workspace_bytes(int64_t rows, int64_t cols);

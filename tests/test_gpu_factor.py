@@ -122,13 +122,47 @@ def test_rsvd_deterministic(lrc):
         np.testing.assert_array_equal(x, y)
 
 
-def test_rsvd_rank_deficient_sketch_is_reported(lrc):
-    """rank(A) = 3 < l = 10: the sketch has no full-rank QR, which
-    CholeskyQR2 reports instead of returning an unreliable basis."""
+def test_rsvd_ill_conditioned_sketch(lrc):
+    """sigma_j = 2^-j: the sketch's condition number (about 1e12) is past
+    CholeskyQR2, so the call repeats with shifted CholeskyQR3.  The unique
+    quantities match the oracle: singular values and the rank-k
+    reconstruction (the vectors of the smallest pairs are as ill-determined
+    as the sketch's small directions, for both methods)."""
+    sigma = 2.0 ** -np.arange(60, dtype=np.float64)
+    A = synth.spectral_matrix(300, 200, sigma, tag=9)
+    Om = synth.test_vectors(40, 200, 9)
+    print("rsvd ill-conditioned 300x200 l=40 k=30", flush=True)
+    U, s, V = _gpu_rsvd(lrc, A, Om, 30, 0)
+    Uo, so, Vto = O.randomized_svd(A, Om, 30)
+    assert np.max(np.abs(s - so)) <= 1e-12 * so[0]
+    rec, reco = (U * s) @ V.T, (Uo * so) @ Vto
+    assert np.linalg.norm(rec - reco) <= 1e-12 * np.linalg.norm(reco)
+    assert np.linalg.norm(U.T @ U - np.eye(30)) <= 1e-13 * 30
+    assert np.linalg.norm(V.T @ V - np.eye(30)) <= 1e-13 * 30
+
+
+def test_rsvd_rank_deficient_sketch(lrc):
+    """rank(A) = 3 < l = 10: CholeskyQR2 breaks down on the sketch and the
+    shifted CholeskyQR3 retry completes the basis with orthonormal
+    directions outside range(A) (as Householder QR does), so the leading
+    k = 3 triplets match the oracle's."""
     rng = np.random.default_rng([12969, 81])
     A = rng.standard_normal((60, 3)) @ rng.standard_normal((3, 50))
+    Om = synth.test_vectors(10, 50, 5)
+    print("rsvd rank 3, l=10", flush=True)
+    U, s, V = _gpu_rsvd(lrc, A, Om, 3, 0)
+    Uo, so, Vto = O.randomized_svd(A, Om, 3)
+    assert np.max(np.abs(s - so)) <= 1e-12 * so[0]
+    assert np.linalg.norm((U * s) @ V.T - A) <= 1e-12 * np.linalg.norm(A)
+    assert np.linalg.norm(U.T @ U - np.eye(3)) <= 1e-13 * 3
+    assert np.linalg.norm(V.T @ V - np.eye(3)) <= 1e-13 * 3
+
+
+def test_rsvd_zero_matrix_is_reported(lrc):
+    """A = 0: every Gram matrix is zero (no shift helps), which both QR
+    attempts report instead of returning a basis."""
     with pytest.raises(lrc.LrcError) as ei:
-        _gpu_rsvd(lrc, A, synth.test_vectors(10, 50, 5), 3, 0)
+        _gpu_rsvd(lrc, np.zeros((40, 30)), synth.test_vectors(5, 30, 6), 2, 0)
     assert ei.value.code == -6
 
 
