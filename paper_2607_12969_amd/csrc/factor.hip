@@ -87,7 +87,8 @@ __device__ __forceinline__ void group16_sum3(double& a, double& b, double& c) {
 
 // One workgroup: SVD of M = R^T (R upper triangular, l x l inside pitch ldr)
 // by one-sided (Hestenes) Jacobi.  The columns of M (rows of R) and of the
-// accumulated rotation Z sit in LDS; a sweep visits every column pair once
+// accumulated rotation Z sit in LDS, the columns first put in non-increasing
+// order of their norms (de Rijk's ordering); a sweep visits every column pair once
 // in l' - 1 rounds of the round-robin (circle) ordering, l' = l rounded up to
 // even.  The l'/2 <= 48 disjoint pairs of a round run at once, one per
 // group of 16 lanes (64 groups), each lane holding entries e = lane + 16 u
@@ -114,10 +115,32 @@ __global__ __launch_bounds__(kJacThreads) void k_fact_jacobi(const double* __res
     __shared__ int rotated;
     const int tid = threadIdx.x;
     const int grp = tid >> 4, gl = tid & 15;
+    // columns of M = R^T (rows of R) placed in non-increasing order of their
+    // norms (ties by index), which shortens the sweeps; the rotation
+    // accumulator starts as that permutation
+    for (int j = grp; j < l; j += kJacThreads / 16) {
+        double x = 0.0, y = 0.0, z = 0.0;
+#pragma unroll
+        for (int u = 0; u < kJacPer; ++u) {
+            const int e = gl + 16 * u;
+            const double v = (e < l && e >= j) ? R[(int64_t)j * ldr + e] : 0.0;
+            x += v * v;
+        }
+        group16_sum3(x, y, z);
+        if (gl == 0) sig[j] = x;
+    }
+    __syncthreads();
+    if (tid < l) {
+        const double sj = sig[tid];
+        int c = 0;
+        for (int i = 0; i < l; ++i) c += (sig[i] > sj || (sig[i] == sj && i < tid)) ? 1 : 0;
+        pos[tid] = c;
+    }
+    __syncthreads();
     for (int idx = tid; idx < l * l; idx += kJacThreads) {
         const int j = idx / l, i = idx - j * l;
-        Mc[j][i] = i >= j ? R[(int64_t)j * ldr + i] : 0.0;
-        Jc[j][i] = i == j ? 1.0 : 0.0;
+        Mc[pos[j]][i] = i >= j ? R[(int64_t)j * ldr + i] : 0.0;
+        Jc[pos[j]][i] = i == j ? 1.0 : 0.0;
     }
     if (tid == 0) rotated = 0;
     __syncthreads();
