@@ -1464,29 +1464,36 @@ __device__ __forceinline__ void last_cert_s(const TTArgs& a, const double* __res
                                             double (&sum)[NS == 1 ? 2 : 3]) {
     static_assert(D <= NKB, "ring deeper than a block");
     const int n_cb = (int)((a.n_last + 15) / 16);
-    const double* bq[NS];
-    int tl[NS];
+    // G_3 of each set through a buffer resource of its exact size: rows past
+    // the rank lie beyond it and read as zero (their Z_2 columns are zero), so
+    // a fragment's byte offset is the lane's offset in step 0 plus a uniform
+    // step stride, with no clamp
+    __amdgpu_buffer_rsrc_t rs[NS];
 #pragma unroll
     for (int q = 0; q < NS; ++q) {
         const TTSet& S = a.set[NS == 1 ? 0 : 1 + q];
-        bq[q] = static_cast<const double*>(S.core[1]);
-        tl[q] = S.rM - 1;
+        rs[q] = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(S.core[1]), (short)0,
+                                                  (int)((uint32_t)S.rM * (uint32_t)a.n_last * 8u), 0x00020000);
     }
-    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
+    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1, kstride = 32u * nl;   // 4 rows of 8 bytes
     auto colc = [&](int cp) {
         const uint32_t c = (uint32_t)(16 * cp + r);
         return c < clast ? c : clast;
     };
+    auto bld = [&](int q, int k, uint32_t vo) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs[q], vo + (uint32_t)k * kstride, 0, 0);
+        return __builtin_bit_cast(double, v);
+    };
     double N[D][NS], R[D][NS];
     uint32_t c = colc(0);
+    uint32_t vo = ((uint32_t)g * nl + c) * 8u;
 #pragma unroll
     for (int s = 0; s < D; ++s)
 #pragma unroll
-        for (int q = 0; q < NS; ++q) N[s][q] = ld_off(bq[q], last_off<double>(4 * s + g, tl[q], nl, c));
+        for (int q = 0; q < NS; ++q) N[s][q] = bld(q, s, vo);
     for (int cp = 0; cp < n_cb; ++cp) {
-        int gg = g;
-        asm volatile("" : "+v"(gg));
         const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
+        const uint32_t von = ((uint32_t)g * nl + cn) * 8u;
         const int64_t col = (int64_t)cp * 16 + r;
         double tv[NPB][4];
 #pragma unroll
@@ -1514,9 +1521,8 @@ __device__ __forceinline__ void last_cert_s(const TTArgs& a, const double* __res
                 const int k = s + D;
 #pragma unroll
                 for (int q = 0; q < NS; ++q) {
-                    if (k < NKB) R[k % D][q] = ld_off(bq[q], last_off<double>(4 * k + gg, tl[q], nl, c));
-                    else if constexpr (decltype(more)::value)
-                        N[k - NKB][q] = ld_off(bq[q], last_off<double>(4 * (k - NKB) + gg, tl[q], nl, cn));
+                    if (k < NKB) R[k % D][q] = bld(q, k, vo);
+                    else if constexpr (decltype(more)::value) N[k - NKB][q] = bld(q, k - NKB, von);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -1541,7 +1547,7 @@ __device__ __forceinline__ void last_cert_s(const TTArgs& a, const double* __res
                     sum[2] += d3 * d3;
                 }
             }
-        c = cn;
+        vo = von;
     }
 }
 
