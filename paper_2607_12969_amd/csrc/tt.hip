@@ -868,13 +868,26 @@ __device__ __forceinline__ void middle_w_tile(const TTArgs& a, const TTSet& S, i
         }
 }
 
-// Byte offset of the last core's entry G_3(t, c) (row t clamped to the
-// rank: the matching A values, the Z_2 columns past the rank, are zero; c is
-// clamped by the caller, its outputs are discarded).
+// Last-core fragments of the reconstruction through a buffer resource of the
+// core's exact size: rows past the rank lie beyond it and read as zero (their
+// Z_2 columns are zero), so a fragment's byte offset is the lane's offset in
+// step 0 plus a uniform stride per K step, kept in the range-checked vector
+// offset, with no clamp.
 template <typename T>
-__device__ __forceinline__ uint32_t last_off(int t, int tlast, uint32_t nl, uint32_t c) {
-    return ((uint32_t)(t < tlast ? t : tlast) * nl + c) * (uint32_t)sizeof(T);
-}
+struct LastCoreReader {
+    __amdgpu_buffer_rsrc_t rs;
+    uint32_t nl, kstride;
+    __device__ __forceinline__ LastCoreReader(const void* core, int rM, uint32_t n_last)
+        : rs(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(core), (short)0,
+                                               (int)((uint32_t)rM * n_last * (uint32_t)sizeof(T)), 0x00020000)),
+          nl(n_last), kstride(4u * n_last * (uint32_t)sizeof(T)) {}
+    __device__ __forceinline__ uint32_t lane(int g, uint32_t c) const { return ((uint32_t)g * nl + c) * (uint32_t)sizeof(T); }
+    __device__ __forceinline__ T ld(int k, uint32_t vo) const {
+        const uint32_t off = vo + (uint32_t)k * kstride;
+        if constexpr (sizeof(T) == 8) return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+        else return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0));
+    }
+};
 
 // Last product of a reconstruction wave tile: NPB row blocks of 16 rows,
 // stored straight from the accumulators (lane (r, g), value v: row
@@ -888,8 +901,7 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
                                              const double (&zf)[NPB][NKB]) {
     static_assert(D <= NKB, "ring deeper than a block");
     const int n_cb = (int)((a.n_last + 15) / 16);
-    const double* b0 = static_cast<const double*>(a.set[0].core[1]);
-    const int tl = a.set[0].rM - 1;
+    const LastCoreReader<double> lc(a.set[0].core[1], a.set[0].rM, (uint32_t)a.n_last);
     double* out = static_cast<double*>(a.out);
     const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
     auto colc = [&](int cp) {
@@ -897,13 +909,11 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
         return c < clast ? c : clast;
     };
     double N[D], R[D];
-    uint32_t c = colc(0);
+    uint32_t vo = lc.lane(g, colc(0));
 #pragma unroll
-    for (int s = 0; s < D; ++s) N[s] = ld_off(b0, last_off<double>(4 * s + g, tl, nl, c));
+    for (int s = 0; s < D; ++s) N[s] = lc.ld(s, vo);
     for (int cp = 0; cp < n_cb; ++cp) {
-        int gg = g;
-        asm volatile("" : "+v"(gg));
-        const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
+        const uint32_t von = lc.lane(g, colc(cp + 1 < n_cb ? cp + 1 : cp));
         double4_t acc[NPB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<double4_t>();
@@ -916,9 +926,8 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
 #pragma unroll
                 for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(zf[pb][s], f, acc[pb]);
                 const int k = s + D;
-                if (k < NKB) R[k % D] = ld_off(b0, last_off<double>(4 * k + gg, tl, nl, c));
-                else if constexpr (decltype(more)::value)
-                    N[k - NKB] = ld_off(b0, last_off<double>(4 * (k - NKB) + gg, tl, nl, cn));
+                if (k < NKB) R[k % D] = lc.ld(k, vo);
+                else if constexpr (decltype(more)::value) N[k - NKB] = lc.ld(k - NKB, von);
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
@@ -942,7 +951,7 @@ __device__ __forceinline__ void last_store_w(const TTArgs& a, int64_t i, int64_t
                     }
                 }
         }
-        c = cn;
+        vo = von;
     }
 }
 
@@ -1087,21 +1096,18 @@ __device__ __forceinline__ void last_store_w32(const TTArgs& a, float* stl, int6
                                                const float (&zf)[NPB][NKB]) {
     static_assert(D <= NKB, "ring deeper than a block");
     const int n_cb = (int)((a.n_last + 15) / 16);
-    const float* b0 = static_cast<const float*>(a.set[0].core[1]);
-    const int tl = a.set[0].rM - 1;
+    const LastCoreReader<float> lc(a.set[0].core[1], a.set[0].rM, (uint32_t)a.n_last);
     const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
     auto colc = [&](int cp) {
         const uint32_t c = (uint32_t)(16 * cp + r);
         return c < clast ? c : clast;
     };
     float N[D], R[D];
-    uint32_t c = colc(0);
+    uint32_t vo = lc.lane(g, colc(0));
 #pragma unroll
-    for (int s = 0; s < D; ++s) N[s] = ld_off(b0, last_off<float>(4 * s + g, tl, nl, c));
+    for (int s = 0; s < D; ++s) N[s] = lc.ld(s, vo);
     for (int cp = 0; cp < n_cb; ++cp) {
-        int gg = g;
-        asm volatile("" : "+v"(gg));
-        const uint32_t cn = colc(cp + 1 < n_cb ? cp + 1 : cp);
+        const uint32_t von = lc.lane(g, colc(cp + 1 < n_cb ? cp + 1 : cp));
         float4_t acc[NPB];
 #pragma unroll
         for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<float4_t>();
@@ -1114,16 +1120,15 @@ __device__ __forceinline__ void last_store_w32(const TTArgs& a, float* stl, int6
 #pragma unroll
                 for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f, zf[pb][s], acc[pb]);
                 const int k = s + D;
-                if (k < NKB) R[k % D] = ld_off(b0, last_off<float>(4 * k + gg, tl, nl, c));
-                else if constexpr (decltype(more)::value)
-                    N[k - NKB] = ld_off(b0, last_off<float>(4 * (k - NKB) + gg, tl, nl, cn));
+                if (k < NKB) R[k % D] = lc.ld(k, vo);
+                else if constexpr (decltype(more)::value) N[k - NKB] = lc.ld(k - NKB, von);
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
         if (cp + 1 < n_cb) block(std::true_type{});
         else block(std::false_type{});
         store_block<float, NPB, TS>(a, stl, i, L0, (int64_t)cp * 16, r, g, acc);
-        c = cn;
+        vo = von;
     }
 }
 
