@@ -1209,32 +1209,51 @@ static void split_plan(int64_t tiles, int64_t K, int* splits, int64_t* chunk) {
 
 static int64_t tiles_of(int64_t n, int b) { return (n + b - 1) / b; }
 
-size_t gemm_nt_workspace_bytes(int64_t nw, int64_t rows, int64_t K) {
-    const int64_t tiles = tiles_of(nw, GramC::BM) * tiles_of(rows, GramC::BN);
+// At most 96 rows of W (the factorization's sketches and small factors) take
+// one 96-row tile, three fragments per wave (75 test vectors leave 21 of 96
+// rows idle instead of 53 of 128); wider W takes the 64 x 64 tiles.
+using NarrowC = Cfg<double, 96, 64, 16, 2, 2>;
+
+template <class C>
+static size_t gemm_nt_bytes(int64_t nw, int64_t rows, int64_t K) {
+    const int64_t tiles = tiles_of(nw, C::BM) * tiles_of(rows, C::BN);
     int sp;
     int64_t ch;
     split_plan(tiles, K, &sp, &ch);
-    return (size_t)tiles * sp * GramC::BM * GramC::BN * sizeof(double);
+    return (size_t)tiles * sp * C::BM * C::BN * sizeof(double);
+}
+
+size_t gemm_nt_workspace_bytes(int64_t nw, int64_t rows, int64_t K) {
+    return nw <= NarrowC::BM ? gemm_nt_bytes<NarrowC>(nw, rows, K) : gemm_nt_bytes<GramC>(nw, rows, K);
+}
+
+template <class C>
+static hipError_t gemm_nt_typed(const double* W, int64_t ldw, int64_t nw, const double* A, int64_t lda, int64_t rows,
+                                int64_t K, const double* svals, double* out, int64_t ldo, int64_t mout, Workspace& ws,
+                                hipStream_t stream, const char* label) {
+    const int tm = (int)tiles_of(nw, C::BM), tn = (int)tiles_of(rows, C::BN);
+    if (!vec_ok<double>(W, ldw) || !vec_ok<double>(A, lda) || mout < nw || mout > (int64_t)tm * C::BM)
+        return hipErrorInvalidValue;
+    int sp;
+    int64_t ch;
+    split_plan((int64_t)tm * tn, K, &sp, &ch);
+    double* part = static_cast<double*>(ws.take(gemm_nt_bytes<C>(nw, rows, K)));
+    if (ws.overrun) return hipErrorOutOfMemory;
+    KernelTimer t(label, stream);
+    hipLaunchKernelGGL(k_abt_part<C>, dim3(xcd_grid((int64_t)tm * tn * sp)), dim3(C::NT), 0, stream, W, ldw, nw, A,
+                       lda, rows, K, ch, tm, tn, sp, part);
+    hipLaunchKernelGGL((k_atb_finish<double, C, ATB_APPLY>), dim3((unsigned)((int64_t)tm * tn * C::FN * C::FM)),
+                       dim3(C::NT), 0, stream, reinterpret_cast<const typename C::AccV*>(part), nw, rows, tm, sp, svals,
+                       (void*)out, ldo, mout);
+    return hipGetLastError();
 }
 
 hipError_t launch_gemm_nt(const double* W, int64_t ldw, int64_t nw, const double* A, int64_t lda, int64_t rows,
                           int64_t K, const double* svals, double* out, int64_t ldo, int64_t mout, Workspace& ws,
                           hipStream_t stream, const char* label) {
-    const int tm = (int)tiles_of(nw, GramC::BM), tn = (int)tiles_of(rows, GramC::BN);
-    if (!vec_ok<double>(W, ldw) || !vec_ok<double>(A, lda) || mout < nw || mout > (int64_t)tm * GramC::BM)
-        return hipErrorInvalidValue;
-    int sp;
-    int64_t ch;
-    split_plan((int64_t)tm * tn, K, &sp, &ch);
-    double* part = static_cast<double*>(ws.take(gemm_nt_workspace_bytes(nw, rows, K)));
-    if (ws.overrun) return hipErrorOutOfMemory;
-    KernelTimer t(label, stream);
-    hipLaunchKernelGGL(k_abt_part<GramC>, dim3(xcd_grid((int64_t)tm * tn * sp)), dim3(GramC::NT), 0, stream, W, ldw,
-                       nw, A, lda, rows, K, ch, tm, tn, sp, part);
-    hipLaunchKernelGGL((k_atb_finish<double, GramC, ATB_APPLY>), dim3((unsigned)((int64_t)tm * tn * GramC::FN * GramC::FM)),
-                       dim3(GramC::NT), 0, stream, reinterpret_cast<const GramC::AccV*>(part), nw, rows, tm, sp, svals,
-                       (void*)out, ldo, mout);
-    return hipGetLastError();
+    if (nw <= NarrowC::BM)
+        return gemm_nt_typed<NarrowC>(W, ldw, nw, A, lda, rows, K, svals, out, ldo, mout, ws, stream, label);
+    return gemm_nt_typed<GramC>(W, ldw, nw, A, lda, rows, K, svals, out, ldo, mout, ws, stream, label);
 }
 
 size_t gemm_tn_workspace_bytes(int64_t nq, int64_t cols, int64_t K) {

@@ -93,9 +93,9 @@ hipError_t launch_cholqr2(const double* A, int64_t rows, int r, double* Q, doubl
                           hipStream_t stream, const char* label, bool shifted = false);
 // ------------------------------------------------------ FP64 factor GEMMs ---
 // out[i][j] = s_j sum_{t<K} W[j][t] A[i][t] for i < rows, j < nw (s = 1 when
-// svals is null); out[i][j] = 0 for nw <= j < mout (mout <= nw rounded up to
-// 64).  W, A: 16-byte aligned with even pitches.  Split-K MFMA partials
-// summed in split order.
+// svals is null); out[i][j] = 0 for nw <= j < mout (mout <= 96 when
+// nw <= 96, else at most nw rounded up to 64).  W, A: 16-byte aligned with
+// even pitches.  Split-K MFMA partials summed in split order.
 size_t gemm_nt_workspace_bytes(int64_t nw, int64_t rows, int64_t K);
 hipError_t launch_gemm_nt(const double* W, int64_t ldw, int64_t nw, const double* A, int64_t lda, int64_t rows,
                           int64_t K, const double* svals, double* out, int64_t ldo, int64_t mout, Workspace& ws,
