@@ -1,21 +1,27 @@
 """Benchmark of the rank-compensation hot path on one MI355X.
 
-One step is one pass of the whole hot path over one batch of synthetic
-input, in method precision with every input resident in HBM:
-  - factor apply Y = U diag(s) V^T X on the 8192 x 8192 workload
-    (sigma_j = j^-1.5 + 1e-8 noise, Haar singular vectors) at batch 4096:
-    FP64 at rank k, FP32 and FP16 at the compensated rank k + 1;
-  - TT reconstruction of the 512 x 512 x 224 hyperspectral-shaped cube:
-    FP64 at ranks (64, 64), FP32 and FP16 at (65, 65);
-  - the device certificates of both compensated representations (matrix:
-    Gram-based eta and the Eckart-Young verdict; TT: E_R, E_R+, eta_TT).
+One step is one pass of the hot path over one batch of synthetic input, in
+method precision with every input resident in HBM:
+  - factor apply Y = U diag(s) V^T X on the 65536 x 4096 tail-rank stress
+    workload (sigma_j = max(exp(-j/40), 1e-6), Haar singular vectors) at
+    batch 4096: FP64 at rank k = 512, FP32 and FP16 at the compensated
+    rank k + 1 (--matrix square: the 8192 x 8192 workload instead);
+  - TT reconstruction of the normalized 512 x 512 x 224 hyperspectral-shaped
+    cube from its own fixed-rank TT-SVD: FP64 at ranks (64, 64), FP32 and
+    FP16 at (65, 65).
+The device certificates of both compensated representations run once after
+the timed steps (the paper leaves them out of its timings); their verdicts
+and kernel times are reported beside the line.
 Prints one JSON line.  `value` is the step's algorithmic GFLOP divided by
-its wall time; the `roofline` object describes the kernel with the largest
-share of the step, timed by the library's HIP-event kernel timers over the
-timed steps; `cpu_baseline` is the CPU oracle on a bounded sample of the
-same apply and TT work.
+its wall time; the `roofline` object describes the apply or TT kernel with
+the largest share of the step, timed by the library's HIP-event kernel
+timers over the timed steps; `hbm_ceilings_measured_gbps` holds plain
+read / write / copy stream rates measured in the same run;
+`cpu_baseline` is the CPU oracle on a bounded sample of the same apply and
+TT work (all host threads, with the CPU model and one-thread times of the
+small configurations).
 
-  python bench.py [--steps K] [--warmup W] [--k 256] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--k 512] [--matrix tail|square] [--no-cpu-baseline]
   python bench.py --sweep FILE      per-kernel table over the workload grid
   python bench.py --quant FILE      device rounding and TT gauge cells
   python bench.py --grid FILE       the paper's resident timing grid on synthetic stand-ins
@@ -99,12 +105,21 @@ def tt_svd_fixed(T, ranks):
 
 
 class Workload:
-    def __init__(self, k, dev):
+    """One benchmark step: the factor apply on the 65536 x 4096 tail-rank
+    workload at batch 4096 (FP64 rank k, FP32 / FP16 rank k + 1; or the
+    8192 x 8192 workload with --matrix square) and the TT reconstruction of
+    the normalized 512 x 512 x 224 cube from its own fixed-rank TT-SVD (FP64
+    (64, 64), FP32 / FP16 (65, 65)).  The certificates of both compensated
+    representations are run outside the timed steps."""
+
+    def __init__(self, k, dev, matrix="tail"):
         import torch
         from paper_2607_12969_amd import synth
         t0 = time.time()
         self.k = k
-        w = synth.matrix_square(kmax=256, batch=4096)
+        self.matrix = matrix
+        w = (synth.matrix_tail(kmax=k, batch=4096) if matrix == "tail"
+             else synth.matrix_square(kmax=k, batch=4096))
         self.m, self.n, self.b = w["m"], w["n"], 4096
         self.sigma = w["sigma"]
         r = k + 1
@@ -138,18 +153,25 @@ class Workload:
         self.host_mat = (U, s, V, w["X"])
         log(f"TT workload ready ({time.time() - t0:.1f}s)")
 
-    def step(self, lrc, certs=True):
-        res = {}
+    def describe(self):
+        mat = ("65536x4096 sigma_j=max(exp(-j/40),1e-6)" if self.matrix == "tail"
+               else "8192x8192 sigma_j=j^-1.5+1e-8 noise")
+        return (f"apply {mat} batch 4096 (FP64 k={self.k}, FP32/FP16 k={self.k + 1}) + TT reconstruct "
+                "512x512x224 hyperspectral-shaped cube from its own TT-SVD (FP64 (64,64), FP32/FP16 (65,65))")
+
+    def step(self, lrc):
         for p in ("f64", "f32", "f16"):
             dv, Y, _ = self.apply_in[p]
             lrc.matrix_apply(*dv, Y=Y)
         for p in ("f64", "f32", "f16"):
             dv, out, _ = self.tt_in[p]
             lrc.tt_reconstruct(dv, out=out)
-        if certs:
-            for p in ("f32", "f16"):
-                res[("mat", p)] = lrc.certify_matrix(self.sigma, *self.f64, *self.cert_h[p], self.k)
-                res[("tt", p)] = lrc.certify_tt(self.T, self.base, self.aug, self.tt_in[p][0])
+
+    def certify(self, lrc):
+        res = {}
+        for p in ("f32", "f16"):
+            res[("mat", p)] = lrc.certify_matrix(self.sigma, *self.f64, *self.cert_h[p], self.k)
+            res[("tt", p)] = lrc.certify_tt(self.T, self.base, self.aug, self.tt_in[p][0])
         return res
 
     def step_counts(self):
@@ -160,18 +182,10 @@ class Workload:
             kk = self.apply_in[p][2]
             out[f"apply_{p}"] = apply_counts(m, n, kk, b, EBYTES[p])
             out[f"tt_{p}"] = tt_counts(self.dims, self.tt_in[p][2] + [1], EBYTES[p])
-        r = self.k + 1
-        for p in ("f32", "f16"):
-            g1, g2 = gram_counts(m, 2 * r), gram_counts(n, 2 * r)
-            out[f"cert_matrix_{p}"] = (g1[0] + g2[0], g1[1] + g2[1] + (m + n) * r * EBYTES[p])
-            N = int(np.prod(self.dims))
-            fb = tt_counts(self.dims, [1, 64, 64, 1], 8)[0]
-            fa = tt_counts(self.dims, [1, 65, 65, 1], 8)[0]
-            out[f"cert_tt_{p}"] = (fb + 2 * fa + 9.0 * N, 8.0 * N)
         return out
 
     def kernel_counts(self):
-        """(flops, bytes, dtype) per kernel launch label."""
+        """(flops, bytes, dtype) per kernel launch label of the step."""
         m, n, b = self.m, self.n, self.b
         out = {}
         for p in ("f64", "f32", "f16"):
@@ -181,56 +195,118 @@ class Workload:
             out[f"apply_p2_mfma_{p}"] = (*p2, p)
             f, by = tt_counts(self.dims, self.tt_in[p][2] + [1], EBYTES[p])
             out[f"tt_fused_{p}"] = (f, by, p)
-        # TT certificate (FP64, one fused launch): the reconstructions of T_R
-        # (ranks 64, 64), T_R+ and of the rounded cores (65, 65) formed on
-        # chip and compared with T; bytes = T read once plus the three core sets
-        N = float(np.prod(self.dims))
-        fb, bb = tt_counts(self.dims, [1, 64, 64, 1], 8)
-        fa, ba = tt_counts(self.dims, [1, 65, 65, 1], 8)
-        out["cert_tt_fused_f64"] = (fb + 2 * fa + 9.0 * N, 8.0 * N + (bb - 8.0 * N) + 2 * (ba - 8.0 * N), "f64")
-        r2 = 2 * (self.k + 1)
-        gm, gn = gram_counts(m, r2), gram_counts(n, r2)
-        out["cert_gram_f64"] = ((gm[0] + gn[0]) / 2, (gm[1] + gn[1]) / 2, "f64")
-        out["cert_sumsq5_f64"] = (11.0 * N, 32.0 * N, "f64")
         return out
 
 
 # ----------------------------------------------------------------- CPU ---
 
-def cpu_baseline(wl, budget_s=8.0):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, budget_s=12.0):
     """The oracle's FP64 apply and TT reconstruction on a bounded sample of
     the step's work (a fraction of the batch columns and of the cube's first
-    mode), scaled to GFLOP/s with the same algorithmic flop counts."""
+    mode) on every host thread, scaled to GFLOP/s with the same algorithmic
+    flop counts; then single-thread times of the 512 x 256 apply (k = 20,
+    batch 64) and of a 256^3 reconstruction at ranks (15, 15)."""
     import oracle as O
+    from paper_2607_12969_amd import synth
+    names = {"f64": "fp64", "f32": "fp32", "f16": "fp16"}
     U, s, V, X = wl.host_mat
     base, aug = wl.host_tt["base"], wl.host_tt["aug"]
     dims = wl.dims
+    threads = len(os.sched_getaffinity(0))
+    O.set_num_threads(threads)
     res = None
-    for frac in (1 / 64, 1 / 16, 1 / 4, 1.0):
+    stored = {p: [O.stored(a, names[p]) for a in (U[:, :wl.apply_in[p][2]], s[:wl.apply_in[p][2]],
+                                                   V[:, :wl.apply_in[p][2]])] for p in names}
+    for frac in (1 / 256, 1 / 64, 1 / 16, 1 / 4):
         bs = max(1, int(round(wl.b * frac)))
         n1 = max(1, int(round(dims[0] * frac)))
         flops = 0.0
         t0 = time.time()
         for p in ("f64", "f32", "f16"):
             kk = wl.apply_in[p][2]
-            st = [O.stored(a, {"f64": "fp64", "f32": "fp32", "f16": "fp16"}[p])
-                  for a in (U[:, :kk], s[:kk], V[:, :kk], X[:, :bs])]
-            O.apply(*st)
+            O.apply(*stored[p], O.stored(X[:, :bs], names[p]))
             flops += apply_counts(wl.m, wl.n, kk, bs, 8)[0]
             cs = base if p == "f64" else aug
-            cs = [O.stored(c, {"f64": "fp64", "f32": "fp32", "f16": "fp16"}[p]) for c in cs]
+            cs = [O.stored(c, names[p]) for c in cs]
             cs[0] = np.ascontiguousarray(cs[0][:, :n1, :])
             O.tt_full(cs)
             ranks = [1, cs[0].shape[2], cs[1].shape[2], 1]
             flops += tt_counts([n1] + dims[1:], ranks, 8)[0]
         el = time.time() - t0
         res = dict(value=round(flops / el / 1e9, 3), unit="GFLOP/s", cores=O.num_threads(), kind="oracle",
+                   cpu_model=cpu_model(),
                    sample=(f"FP64 oracle apply (3 methods, batch {bs} of 4096) and TT reconstruction "
                            f"(3 methods, first {n1} of 512 slabs); {flops / 1e9:.1f} GFLOP in {el:.1f}s; "
                            "certificates not included"))
         if el >= budget_s:
             break
+    # one thread: the small configurations
+    O.set_num_threads(1)
+    try:
+        w = synth.matrix_small()
+        m1, n1_, k1 = w["m"], w["n"], 20
+        Us, ss, Vs = w["U"][:, :k1], w["sigma"][:k1], w["V"][:, :k1]
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 1.0 or reps < 3:
+            O.apply(Us, ss, Vs, w["X"])
+            reps += 1
+        c1_ms = (time.perf_counter() - t0) / reps * 1e3
+        cores4 = synth.random_tt_cores((256, 256, 256), (1, 15, 15, 1), tag=1)
+        t0 = time.perf_counter()
+        O.tt_full(cores4)
+        c4_ms = (time.perf_counter() - t0) * 1e3
+        c1_f = apply_counts(m1, n1_, k1, 64, 8)[0]
+        c4_f = tt_counts([256, 256, 256], [1, 15, 15, 1], 8)[0]
+        res["one_thread"] = {
+            "apply_512x256_k20_b64": {"ms": round(c1_ms, 4), "gflops": round(c1_f / c1_ms / 1e6, 3)},
+            "tt_256^3_ranks15": {"ms": round(c4_ms, 2), "gflops": round(c4_f / c4_ms / 1e6, 3)},
+        }
+    finally:
+        O.set_num_threads(threads)
     return res
+
+
+# ------------------------------------------------------------ HBM ceilings ---
+
+def hbm_ceilings(dev, gib=4):
+    """Read, write and copy rates of plain device-wide streams over a `gib`
+    GiB buffer (far above the 256 MB Infinity Cache): a sum reduction
+    (read), a fill (write) and a copy, each timed with torch's events on the
+    current stream (median of 5).  Context for the kernels' fractions; the
+    spec peak stays the reference."""
+    import torch
+    n = (gib << 30) // 8
+    a = torch.ones(n, dtype=torch.float64, device=dev)
+    b = torch.empty_like(a)
+    out = {}
+    for name, fn, nbytes in (("read", lambda: a.sum(), 8 * n), ("write", lambda: b.fill_(2.0), 8 * n),
+                             ("copy", lambda: b.copy_(a), 16 * n)):
+        for _ in range(2):
+            fn()
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        out[name] = round(nbytes / (sorted(ts)[2] * 1e-3) / 1e9, 1)
+    del a, b
+    torch.cuda.empty_cache()
+    return out
 
 
 # ---------------------------------------------------------------- traffic ---
@@ -758,9 +834,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--k", type=int, default=256, help="FP64 rank of the apply (compensated rank k+1)")
+    ap.add_argument("--k", type=int, default=512, help="FP64 rank of the apply (compensated rank k+1)")
+    ap.add_argument("--matrix", choices=("tail", "square"), default="tail",
+                    help="apply workload: 65536 x 4096 tail-rank stress matrix or 8192 x 8192")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-certs", action="store_true", help="leave the certificates out of the step")
     ap.add_argument("--sweep", default=None, help="write a per-kernel table over the workload grid")
     ap.add_argument("--quant", default=None, help="write the device rounding and TT gauge cells")
     ap.add_argument("--grid", default=None, help="write the paper's resident timing grid (synthetic stand-ins)")
@@ -804,11 +881,10 @@ def main():
         factor_sweep(args.factor, dev, lrc)
         return
 
-    wl = Workload(args.k, dev)
-    certs = not args.no_certs
+    wl = Workload(args.k, dev, args.matrix)
     log("warmup")
     for _ in range(args.warmup):
-        res = wl.step(lrc, certs)
+        wl.step(lrc)
     torch.cuda.synchronize()
 
     # per-kernel table: an untimed pass with every kernel's event timers on
@@ -820,7 +896,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(prof_steps):
-        wl.step(lrc, certs)
+        wl.step(lrc)
     torch.cuda.synchronize()
     prof_ms = (time.perf_counter() - t0) / prof_steps * 1e3
     lrc.profile_enable(False)
@@ -849,7 +925,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        res = wl.step(lrc, certs)
+        wl.step(lrc)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     lrc.profile_enable(False)
@@ -859,11 +935,15 @@ def main():
     log(f"timed {args.steps} steps: {ms:.3f} ms/step")
 
     counts = wl.step_counts()
-    if not certs:
-        counts = {k: v for k, v in counts.items() if not k.startswith("cert")}
     flops = sum(f for f, _ in counts.values())
     byts = sum(b for _, b in counts.values())
     value = flops / (ms * 1e-3) / 1e9
+
+    ceil = hbm_ceilings(dev)
+    log(f"measured HBM ceilings (GB/s): {ceil}")
+    for c in cells:
+        if c.get("bound") == "hbm":
+            c["frac_of_measured"] = round(c["gbs"] / ceil["copy"], 4)
 
     roofline = None
     if dom is not None:
@@ -877,13 +957,22 @@ def main():
         else:
             ach = by / avg_ms / 1e6
             roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": round(ach / PEAK_HBM_GBS, 4)}
+                        "frac": round(ach / PEAK_HBM_GBS, 4), "frac_of_measured_copy": round(ach / ceil["copy"], 4)}
         roofline["kernel"] = dom["kernel"]
         roofline["avg_ms"] = round(avg_ms, 5)
         roofline["launches_timed"] = cnt
         roofline["algorithmic_per_launch"] = {"flop": f, "bytes": by}
         roofline["traffic"] = measured_traffic(dom["kernel"])
 
+    # certificates of both compensated representations, outside the timed steps
+    lrc.profile_reset()
+    lrc.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    res = wl.certify(lrc)
+    cert_ms = (time.perf_counter() - t0) * 1e3
+    lrc.profile_enable(False)
+    cert_kernels = {lab: round(tot, 4) for lab, (cnt, tot) in lrc.profile_read().items()}
     verdicts = {f"{a}_{p}": {"certified": r["certified"], "outcome": r["outcome"], "eta": r["eta"],
                              "E_base": r["E_base"], "E_aug": r["E_aug"]} for (a, p), r in res.items()}
 
@@ -897,16 +986,14 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64/f32/f16(f32-accumulate)", "data": "synthetic",
-        "config": {"workload": (f"apply 8192x8192 sigma_j=j^-1.5 batch 4096 (FP64 k={args.k}, FP32/FP16 "
-                                f"k={args.k + 1}) + TT reconstruct 512x512x224 hyperspectral-shaped "
-                                "(FP64 (64,64), FP32/FP16 (65,65))" + (" + device certificates" if certs else "")),
-                   "parallelism": "single GPU"},
+        "config": {"workload": wl.describe(), "parallelism": "single GPU"},
         "hbm_gbps": round(byts / (ms * 1e-3) / 1e9, 2),
+        "hbm_ceilings_measured_gbps": ceil,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "step_parts": {k: {"gflop": round(f / 1e9, 4), "mb": round(b / 1e6, 2)} for k, (f, b) in counts.items()},
         "kernels": cells,
-        "certificates": verdicts,
+        "certificates": {"untimed_wall_ms": round(cert_ms, 2), "kernel_ms": cert_kernels, "verdicts": verdicts},
     }
     print(json.dumps(line), flush=True)
 

@@ -123,9 +123,18 @@ int lrc_set_apply_path(int path);
  * the partial interfaces kept on chip and the last contraction fused with
  * the output stores; intermediate sums use the accumulation precision and,
  * for FP16, the last interface is rounded once to binary16.
+ * On-chip limits.  Every rank up to LRC_TT_MAX_RANK is accepted for d <= 3
+ * in every precision, and for d >= 4 in FP32 and FP16.  FP64 trains of four
+ * or more cores whose last rank r_{d-1} exceeds 68 keep, per workgroup, 16
+ * rows of Z_{d-2} and Z_{d-1} plus two chain rows of the left interface in
+ * LDS: 128 (r_{d-2} + r_{d-1}) + 16 B max(r_1 .. r_{d-2}) bytes (B = 16,
+ * or 16 / n_{d-1} rounded down when n_{d-1} < 16), which must fit the
+ * device's 160 KB (about rank 300 with B = 16 and equal ranks); larger ones
+ * return LRC_EINVAL.
  * Errors: LRC_EINVAL for NULL pointers, d out of range, a dimension or rank
- * < 1, ranks[0] or ranks[d] != 1, a rank above LRC_TT_MAX_RANK, an unknown
- * prec or overlapping output; LRC_EOVERFLOW if prod(dims) overflows.
+ * < 1, ranks[0] or ranks[d] != 1, a rank above LRC_TT_MAX_RANK or beyond the
+ * on-chip limits above, an unknown prec or overlapping output;
+ * LRC_EOVERFLOW if prod(dims) overflows.
  */
 #define LRC_TT_MAX_D 16
 #define LRC_TT_MAX_RANK 512
@@ -137,7 +146,9 @@ int lrc_tt_reconstruct(const void* const* cores, const int64_t* dims, const int6
  *
  * Matrix (kind = LRC_CERT_MATRIX), Thm thm:matrix_rank_compensation:
  *   base rank k in FP64, compensated rank k+1 stored in `prec`.
- *   sigma       host, n_sigma >= k+1 singular values of A, non-increasing
+ *   sigma       host, all n_sigma = min(m, n) singular values of A,
+ *               non-increasing (the tails E_k, E_{k+1} sum over the whole
+ *               spectrum; a truncated spectrum is rejected)
  *   U, s, V     device FP64 rank-(k+1) factors: U m x (k+1), s (k+1), V n x (k+1)
  *   Uh, sh, Vh  device, the same factors as stored in `prec` (each rounded
  *               individually, Remark after the theorem)
@@ -166,7 +177,7 @@ int lrc_tt_reconstruct(const void* const* cores, const int64_t* dims, const int6
  * the flags follow the vocabulary of Sec. 4.1 with strict comparisons for
  * wins.  Synchronizes the stream.
  * Errors: LRC_EINVAL for missing arrays, inconsistent sizes or ranks, prec
- * not FP32/FP16/FP64, or sigma not non-increasing.
+ * not FP32/FP16/FP64, n_sigma != min(m, n), or sigma not non-increasing.
  */
 typedef struct lrc_cert_args {
     int kind;                       /* LRC_CERT_MATRIX or LRC_CERT_TT */

@@ -69,6 +69,8 @@ def _load():
     lib.orc_matmul.restype = None
     lib.orc_num_threads.argtypes = []
     lib.orc_num_threads.restype = ctypes.c_int
+    lib.orc_set_num_threads.argtypes = [ctypes.c_int]
+    lib.orc_set_num_threads.restype = None
     _lib = lib
     return lib
 
@@ -83,6 +85,11 @@ def _ptr(a: np.ndarray):
 
 def num_threads() -> int:
     return int(_load().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops; results are independent of it."""
+    _load().orc_set_num_threads(int(n))
 
 
 # ---------------------------------------------------------------------------
@@ -303,12 +310,18 @@ def svd(A):
     return U, S, Vt
 
 
-def tt_svd(T: np.ndarray, ranks=None, eps=None):
+def tt_svd(T: np.ndarray, ranks=None, eps=None, svd_memo=None):
     """TT-SVD (Oseledets 2011, as used in Sec. 5.1): sequential truncated
     SVDs of the unfoldings.  Either fixed nominal ranks (each capped by the
     valid unfolding dimension, min(R_nom, r_{l-1} n_l, prod_{i>l} n_i), as in
     Sec. 7.4) or a relative tolerance eps with per-step threshold
-    eps ||T||_F / sqrt(d-1).  Returns FP64 cores r_{l-1} x n_l x r_l."""
+    eps ||T||_F / sqrt(d-1).  Returns FP64 cores r_{l-1} x n_l x r_l.
+
+    svd_memo: optional dict shared by several runs on the same tensor.  The
+    unfolding of step l depends only on the ranks kept before it, so its SVD
+    is stored under that rank prefix and reused (the first unfolding's SVD is
+    the same for every rank choice); the cores are bit for bit those of a run
+    without the memo."""
     dims = [int(x) for x in T.shape]
     d = len(dims)
     if (ranks is None) == (eps is None):
@@ -323,9 +336,15 @@ def tt_svd(T: np.ndarray, ranks=None, eps=None):
     C = _c(T).reshape(dims[0], -1)
     r_prev = 1
     cores = []
+    kept = ()
     for l in range(d - 1):
         C = C.reshape(r_prev * dims[l], -1)
-        U, S, Vt = svd(C)
+        if svd_memo is not None and kept in svd_memo:
+            U, S, Vt = svd_memo[kept]
+        else:
+            U, S, Vt = svd(C)
+            if svd_memo is not None:
+                svd_memo[kept] = (U, S, Vt)
         cap = min(C.shape)
         if ranks is not None:
             r = min(ranks[l], cap)
@@ -339,6 +358,7 @@ def tt_svd(T: np.ndarray, ranks=None, eps=None):
         cores.append(np.ascontiguousarray(U[:, :r].reshape(r_prev, dims[l], r)))
         C = S[:r, None] * Vt[:r, :]
         r_prev = r
+        kept = kept + (r,)
     cores.append(np.ascontiguousarray(C.reshape(r_prev, dims[-1], 1)))
     return cores
 

@@ -462,6 +462,17 @@ void orc_matmul(const double* A, const double* B, double* C, int64_t m, int64_t 
     }
 }
 
+/* Thread count of later parallel loops (timing of the one-thread baseline);
+ * results do not depend on it (every loop's sums run in a fixed order). */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
+}
+
 int orc_num_threads(void)
 {
 #ifdef _OPENMP

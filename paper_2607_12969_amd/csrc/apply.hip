@@ -879,6 +879,12 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
     ApplyPlan p{};
     if (path != 1 && path != 2) path = (b <= kStreamMaxBatch) ? 1 : 2;
     if (path == 1 && b > kStreamMaxBatch) path = 2;
+    // the streaming phase 2 stages T' (k x NB in the accumulation type) in
+    // LDS: ranks whose T' exceeds 64 KB take the matrix-core path
+    if (path == 1) {
+        const int64_t nb = (b <= 1) ? 1 : (b <= 2) ? 2 : (b <= 4) ? 4 : 8;
+        if (k * nb * ((prec == P64) ? 8 : 4) > 65536) path = 2;
+    }
     p.path = path;
     p.Kp = round_up(k, 8);
     const size_t acc_b = (prec == P64) ? 8 : 4;

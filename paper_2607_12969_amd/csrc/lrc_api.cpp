@@ -213,6 +213,9 @@ namespace lrc {
 hipError_t Workspace::reserve(size_t bytes, hipStream_t stream) {
     bytes = (size_t)round_up((int64_t)bytes, 256) + 256;
     if (bytes > cap) {
+        // grow by at least half the current size, so that a sequence of
+        // slightly larger calls does not reallocate every time
+        const size_t want = std::max(bytes, cap + cap / 2);
         if (base) {
             hipError_t e = hipStreamSynchronize(stream);
             if (e != hipSuccess) return e;
@@ -220,7 +223,6 @@ hipError_t Workspace::reserve(size_t bytes, hipStream_t stream) {
             base = nullptr;
             cap = 0;
         }
-        size_t want = std::max(bytes, cap + cap / 2);
         hipError_t e = hipMalloc(reinterpret_cast<void**>(&base), want);
         if (e != hipSuccess) {
             base = nullptr;
@@ -290,8 +292,8 @@ int lrc_matrix_apply_path(int64_t m, int64_t n, int64_t k, int64_t batch, int pr
     return plan_apply(m, n, k, batch, prec, LRC_PATH_AUTO).path;
 }
 
-int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X, void* Y, int64_t m, int64_t n,
-                     int64_t k, int64_t batch, int prec) {
+static int check_apply_arrays(const void* U, const void* s, const void* V, const void* X, void* Y, int64_t m,
+                              int64_t n, int64_t k, int64_t batch, int prec) {
     if (!U || !s || !V || !X || !Y) return fail(LRC_EINVAL, "NULL array argument");
     int rc = check_apply(m, n, k, batch, prec);
     if (rc) return rc;
@@ -300,6 +302,13 @@ int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X,
     if (overlaps(Y, ny, U, (size_t)m * k * e) || overlaps(Y, ny, s, (size_t)k * e) ||
         overlaps(Y, ny, V, (size_t)n * k * e) || overlaps(Y, ny, X, (size_t)n * batch * e))
         return fail(LRC_EINVAL, "output Y overlaps an input");
+    return LRC_OK;
+}
+
+int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X, void* Y, int64_t m, int64_t n,
+                     int64_t k, int64_t batch, int prec) {
+    int rc = check_apply_arrays(U, s, V, X, Y, m, n, k, batch, prec);
+    if (rc) return rc;
     int dev;
     rc = current_device(&dev, nullptr);
     if (rc) return rc;
@@ -504,7 +513,11 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
     const int64_t m = a->m, n = a->n, k = a->k, r = k + 1;
     if (m < 1 || n < 1 || k < 1) return fail(LRC_EINVAL, "sizes must be >= 1");
     if (r > std::min(m, n)) return fail(LRC_EINVAL, "k + 1 = %lld exceeds min(m, n)", (long long)r);
-    if (!a->sigma || a->n_sigma < r) return fail(LRC_EINVAL, "sigma must hold at least k + 1 values");
+    // E_k and E_{k+1} are Eckart-Young tails over the whole spectrum: a
+    // truncated sigma would make both too small and could certify falsely
+    if (!a->sigma || a->n_sigma != std::min(m, n))
+        return fail(LRC_EINVAL, "sigma must hold all min(m, n) = %lld singular values (got %lld)",
+                    (long long)std::min(m, n), (long long)a->n_sigma);
     if (!a->U || !a->s || !a->V || !a->Uh || !a->sh || !a->Vh) return fail(LRC_EINVAL, "NULL factor argument");
     for (int64_t j = 0; j < a->n_sigma; ++j) {
         if (!(a->sigma[j] >= 0.0)) return fail(LRC_EINVAL, "sigma[%lld] is negative or NaN", (long long)j);

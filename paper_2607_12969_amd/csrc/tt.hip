@@ -1770,10 +1770,13 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     }
     // at most 64 KB of LDS per workgroup (80 KB for the three-set
     // certificate kernel), so that at least two workgroups share a compute
-    // unit
-    const size_t lds_cap = nsets > 1 ? 81920 : 65536;
-    if (max_lds > lds_cap) max_lds = lds_cap;
+    // unit; a reconstruction whose buffers do not fit that takes the whole
+    // LDS of the compute unit (160 KB on gfx950), one workgroup per unit
+    // (the certificate falls back to dense reconstructions instead)
+    const size_t lds_soft = nsets > 1 ? 81920 : 65536;
     const int P0 = tune_env("LRC_TT_P", (prec == P64) ? 32 : 64);
+    for (int pass = 0; pass < (nsets == 1 ? 2 : 1) && p.P == 0; ++pass) {
+    const size_t lds_cap = pass == 0 ? std::min(max_lds, lds_soft) : max_lds;
     for (int P = P0; P >= 16; P /= 2) {
         int BI, BL;
         if (d == 2) {
@@ -1798,13 +1801,14 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
         }
         lds += zl;
         if (d >= 4) lds += (size_t)2 * BL * p.chain_rmax * acc_b;
-        if (lds <= max_lds) {
+        if (lds <= lds_cap) {
             p.BL = BL;
             p.BI = BI;
             p.P = Peff;
             p.lds_bytes = lds;
             break;
         }
+    }
     }
     if (p.P == 0) return -1;
     p.num_i_blocks = (p.n_mid + p.BI - 1) / p.BI;

@@ -194,21 +194,32 @@ def set_apply_path(path: int):
     _check(lib().lrc_set_apply_path(path))
 
 
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
 def matrix_apply(U, s, V, X, Y=None):
-    """Y = U diag(s) (V^T X): U (m x k), s (k), V (n x k), X (n x batch)."""
+    """Y = U diag(s) (V^T X): U (m x k), s (k), V (n x k), X (n x batch).
+    A caller-supplied Y must be (m, batch), of U's dtype and on U's device."""
     import torch
-    _dev(U, s, V, X)
     prec = _prec_of(U)
     for t in (s, V, X):
         if t.dtype != U.dtype:
             raise TypeError("all factors and the batch must share one dtype")
+    _need(U.dim() == 2 and X.dim() == 2, "U and X must be matrices")
     m, k = U.shape
     n, b = X.shape
-    if V.shape != (n, k) or s.shape != (k,):
-        raise ValueError("shape mismatch")
+    _need(tuple(V.shape) == (n, k) and tuple(s.shape) == (k,),
+          f"shape mismatch: V {tuple(V.shape)} (want {(n, k)}), s {tuple(s.shape)} (want {(k,)})")
+    if Y is not None:
+        _need(tuple(Y.shape) == (m, b), f"Y has shape {tuple(Y.shape)}, want {(m, b)}")
+        _need(Y.dtype == U.dtype, f"Y has dtype {Y.dtype}, want {U.dtype}")
+    _dev(U, s, V, X)
     if Y is None:
         Y = torch.empty((m, b), dtype=U.dtype, device=U.device)
     _dev(Y)
+    _need(all(t.device == U.device for t in (s, V, X, Y)), "all tensors must be on one device")
     _bind_stream(U.device)
     _check(lib().lrc_matrix_apply(U.data_ptr(), s.data_ptr(), V.data_ptr(), X.data_ptr(), Y.data_ptr(),
                                   m, n, k, b, prec))
@@ -221,16 +232,37 @@ def tt_shape(cores):
     return dims, ranks
 
 
+def _check_train(cores):
+    """Consistent TT cores: 3-D (r_{l-1}, n_l, r_l), adjacent ranks equal,
+    boundary ranks 1, one dtype."""
+    _need(len(cores) >= 1, "need at least one core")
+    for l, c in enumerate(cores):
+        _need(c.dim() == 3, f"core {l} must be 3-D (r_prev, n, r_next)")
+        if c.dtype != cores[0].dtype:
+            raise TypeError("all cores must share one dtype")
+        if l > 0:
+            _need(int(c.shape[0]) == int(cores[l - 1].shape[2]),
+                  f"core {l} starts with rank {int(c.shape[0])}, core {l - 1} ends with {int(cores[l - 1].shape[2])}")
+    _need(int(cores[0].shape[0]) == 1 and int(cores[-1].shape[2]) == 1, "boundary ranks must be 1")
+
+
 def tt_reconstruct(cores, out=None):
-    """Dense tensor (C order) from TT cores G_l of shape (r_{l-1}, n_l, r_l)."""
+    """Dense tensor (C order) from TT cores G_l of shape (r_{l-1}, n_l, r_l).
+    A caller-supplied `out` must hold prod(dims) entries of the cores'
+    dtype on their device."""
     import torch
-    _dev(*cores)
     prec = _prec_of(cores[0])
+    _check_train(cores)
     dims, ranks = tt_shape(cores)
     d = len(cores)
+    if out is not None:
+        _need(out.numel() == math.prod(dims), f"out has {out.numel()} entries, want {math.prod(dims)}")
+        _need(out.dtype == cores[0].dtype, f"out has dtype {out.dtype}, want {cores[0].dtype}")
+    _dev(*cores)
     if out is None:
         out = torch.empty(dims, dtype=cores[0].dtype, device=cores[0].device)
     _dev(out)
+    _need(all(c.device == out.device for c in cores), "cores and out must be on one device")
     ptrs = (_vp * d)(*[c.data_ptr() for c in cores])
     D = (_i64 * d)(*dims)
     R = (_i64 * (d + 1))(*ranks)
@@ -393,16 +425,35 @@ def _result(res: CertResult) -> dict:
 
 def certify_matrix(sigma, U, s, V, Uh, sh, Vh, k: int, A=None) -> dict:
     """Matrix certificate for base rank k (FP64) vs rank k+1 stored as
-    (Uh, sh, Vh).  sigma: host sequence of singular values."""
+    (Uh, sh, Vh).  sigma: host sequence of all min(m, n) singular values;
+    U (m x k+1), s (k+1), V (n x k+1) float64; Uh, sh, Vh the same shapes
+    in float32 or float16; A (m x n, float64) or None."""
     import numpy as np
+    import torch
+    sig = np.ascontiguousarray(np.asarray(sigma, dtype=np.float64))
+    _need(U.dim() == 2 and V.dim() == 2, "U and V must be matrices")
+    m, n, r = int(U.shape[0]), int(V.shape[0]), int(k) + 1
+    _need(int(k) >= 1 and tuple(U.shape) == (m, r) and tuple(V.shape) == (n, r) and tuple(s.shape) == (r,),
+          f"FP64 factors must have k + 1 = {r} columns: U {tuple(U.shape)}, s {tuple(s.shape)}, V {tuple(V.shape)}")
+    for name, t in (("U", U), ("s", s), ("V", V)):
+        if t.dtype != torch.float64:
+            raise TypeError(f"{name} must be float64")
+    for name, t, ref in (("Uh", Uh, U), ("sh", sh, s), ("Vh", Vh, V)):
+        _need(tuple(t.shape) == tuple(ref.shape), f"{name} has shape {tuple(t.shape)}, want {tuple(ref.shape)}")
+        if t.dtype != Uh.dtype or t.dtype not in (torch.float16, torch.float32, torch.float64):
+            raise TypeError("Uh, sh, Vh must share one storage dtype")
+    _need(sig.ndim == 1 and sig.size == min(m, n), f"sigma must hold all min(m, n) = {min(m, n)} singular values")
+    if A is not None:
+        _need(tuple(A.shape) == (m, n), f"A has shape {tuple(A.shape)}, want {(m, n)}")
+        if A.dtype != torch.float64:
+            raise TypeError("A must be float64")
     _dev(U, s, V, Uh, sh, Vh)
     if A is not None:
         _dev(A)
-    sig = np.ascontiguousarray(np.asarray(sigma, dtype=np.float64))
     a = CertArgs()
     a.kind = CERT_MATRIX
     a.prec = _prec_of(Uh)
-    a.m, a.n, a.k = int(U.shape[0]), int(V.shape[0]), int(k)
+    a.m, a.n, a.k = m, n, int(k)
     a.sigma = sig.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
     a.n_sigma = len(sig)
     a.U, a.s, a.V = U.data_ptr(), s.data_ptr(), V.data_ptr()
@@ -415,12 +466,27 @@ def certify_matrix(sigma, U, s, V, Uh, sh, Vh, k: int, A=None) -> dict:
 
 
 def certify_tt(T, base_cores, aug_cores, aug_cores_h) -> dict:
-    """TT certificate: T dense FP64; FP64 base and augmented cores; the
-    augmented cores as stored (FP32 or FP16)."""
-    _dev(T, *base_cores, *aug_cores, *aug_cores_h)
+    """TT certificate: T dense FP64 of the trains' shape; FP64 base and
+    augmented cores; the augmented cores as stored (FP32 or FP16), of the
+    augmented cores' shapes."""
+    import torch
     d = len(base_cores)
+    _need(len(aug_cores) == d and len(aug_cores_h) == d, "the three trains must have the same number of cores")
+    for cs in (base_cores, aug_cores, aug_cores_h):
+        _check_train(cs)
+    for cs in (base_cores, aug_cores):
+        if cs[0].dtype != torch.float64:
+            raise TypeError("base and augmented cores must be float64")
     dims, rb = tt_shape(base_cores)
-    _, ra = tt_shape(aug_cores)
+    dims_a, ra = tt_shape(aug_cores)
+    _need(dims_a == dims, f"augmented train has dims {dims_a}, base {dims}")
+    for l in range(d):
+        _need(tuple(aug_cores_h[l].shape) == tuple(aug_cores[l].shape),
+              f"stored core {l} has shape {tuple(aug_cores_h[l].shape)}, want {tuple(aug_cores[l].shape)}")
+    _need(T.numel() == math.prod(dims), f"T has {T.numel()} entries, want {math.prod(dims)}")
+    if T.dtype != torch.float64:
+        raise TypeError("T must be float64")
+    _dev(T, *base_cores, *aug_cores, *aug_cores_h)
     a = CertArgs()
     a.kind = CERT_TT
     a.prec = _prec_of(aug_cores_h[0])

@@ -10,7 +10,8 @@ the GPU path and the CPU oracle consume what it returns.
 Seeds: every stream is ``numpy.random.default_rng([12969, workload_id,
 stream_id])`` (PCG64).  Stream ids: 0 = left factor, 1 = right factor,
 2 = spectrum noise, 3 = batch X, 4 and up = tensor cores, endmembers,
-abundances and noise.
+abundances and noise; 10 and 11 = the full orthogonal factors of the dense
+8192 x 8192 matrix.
 
 Workloads stand in for the paper's data sets, which are not available here:
 the matrix workloads replace the SuiteSparse application timings (Sec. 4.4)
@@ -101,6 +102,20 @@ def matrix_square(kmax: int = 256, batch: int = 4096, m: int = 8192, n: int = 81
     sigma = sigma_square(min(m, n))
     x = gaussian(rng_for(W_MATRIX_SQUARE, 3), (n, batch))
     return dict(m=m, n=n, U=u, V=v, sigma=sigma, X=x)
+
+
+def matrix_square_dense(kmax: int = 256, m: int = 8192, n: int = 8192):
+    """The 8192 x 8192 workload formed densely, for the error of the stored
+    representation against A itself: full Haar orthogonal Q1 (m x m) and
+    Q2 (n x n) from streams 10 and 11, A = Q1 diag(sigma) Q2^T with the
+    sigma_square law over all min(m, n) values.  Returns A with its leading
+    kmax+1 singular triplets (the first columns of Q1 and Q2)."""
+    r = kmax + 1
+    sigma = sigma_square(min(m, n))
+    q1 = haar(rng_for(W_MATRIX_SQUARE, 10), m, m)
+    q2 = haar(rng_for(W_MATRIX_SQUARE, 11), n, n)
+    a = (q1[:, :min(m, n)] * sigma) @ q2[:, :min(m, n)].T
+    return dict(m=m, n=n, A=a, sigma=sigma, U=np.ascontiguousarray(q1[:, :r]), V=np.ascontiguousarray(q2[:, :r]))
 
 
 def matrix_tail(kmax: int = 512, batch: int = 4096, m: int = 65536, n: int = 4096):

@@ -20,3 +20,20 @@ def read_golden(name):
     with open(path) as fh:
         lines = [ln for ln in fh if not ln.startswith("#")]
     return list(csv.DictReader(lines))
+
+
+@pytest.fixture(scope="session")
+def hyper():
+    """The normalized 512 x 512 x 224 hyperspectral-shaped cube and its own
+    fixed-rank TT-SVD (the oracle's, one SVD memo for every schedule): FP64
+    bases at (64, 64) and (32, 32); compensated trains at (65, 65), (33, 33)
+    and (36, 36), left-orthogonalized.  Shared by the reconstruction and
+    certificate tests (the oracle's SVD of the 512 x 114688 unfolding takes
+    tens of seconds)."""
+    import oracle as O
+    from paper_2607_12969_amd import synth
+    T = synth.hyperspectral()
+    memo = {}
+    base = {r: O.tt_svd(T, ranks=[r, r], svd_memo=memo) for r in (64, 32)}
+    aug = {r: O.left_orthogonalize(O.tt_svd(T, ranks=[r, r], svd_memo=memo)) for r in (65, 33, 36)}
+    return T, base, aug

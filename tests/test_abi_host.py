@@ -51,6 +51,9 @@ def test_apply_path_dispatch():
     assert lrc.apply_path(8192, 8192, 257, 9, "fp32") == lrc.PATH_MFMA
     assert lrc.apply_path(8192, 8192, 257, 4096, "fp16") == lrc.PATH_MFMA
     assert L.lrc_matrix_apply_path(10, 10, 11, 4, 0) == -1   # k > min(m, n)
+    # the streaming path keeps T' (k x batch, accumulation type) in 64 KB of LDS
+    assert lrc.apply_path(9000, 9000, 8192, 1, "fp64") == lrc.PATH_STREAM
+    assert lrc.apply_path(9000, 9000, 8193, 1, "fp64") == lrc.PATH_MFMA
     assert L.lrc_set_apply_path(3) == -1
     assert L.lrc_set_apply_path(0) == 0
 
@@ -110,14 +113,34 @@ def test_certify_argument_errors():
     assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
     a.k = 3
     a.U = a.s = a.V = a.Uh = a.sh = a.Vh = 0x10000
-    bad = np.array([1.0, 2.0, 0.5, 0.1])                      # not non-increasing
+    bad = np.array([1.0, 2.0, 0.5, 0.1, 0.05, 0.04, 0.03, 0.02])   # not non-increasing
     a.sigma = bad.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
-    a.n_sigma = 4
+    a.n_sigma = 8
     assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
     assert b"non-increasing" in L.lrc_last_error()
     a.kind = lrc.CERT_TT
     a.d = 0
     assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
+
+
+def test_certify_rejects_truncated_spectrum():
+    """The tails E_k, E_{k+1} of Thm thm:matrix_rank_compensation sum over
+    the whole spectrum: a spectrum cut after sigma_{k+1} (say, from a rank-k
+    factorization) would make E_{k+1} = 0 and certify on eta <= sigma_{k+1}
+    alone, so anything but min(m, n) values is rejected before any device
+    call."""
+    a = lrc.CertArgs()
+    r = lrc.CertResult()
+    a.kind = lrc.CERT_MATRIX
+    a.prec = lrc.FP16
+    a.m, a.n, a.k = 10, 8, 3
+    a.U = a.s = a.V = a.Uh = a.sh = a.Vh = 0x10000
+    sig = np.linspace(1.0, 0.1, 8)
+    a.sigma = sig.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    for n_sigma in (4, 7, 9):                                 # k + 1, one short, one too many
+        a.n_sigma = n_sigma
+        assert L.lrc_certify(ctypes.byref(a), ctypes.byref(r)) == -1
+        assert b"min(m, n)" in L.lrc_last_error()
 
 
 def test_valid_call_without_gpu_reports_no_device():

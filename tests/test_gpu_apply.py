@@ -3,15 +3,15 @@ gpu_matrix_apply) against the oracle on the same stored values.
 
 Tolerances (relative Frobenius error vs the oracle's FP64 evaluation of the
 stored factors): 1e-12 FP64, 1e-5 FP32, 2e-3 FP16 with FP32 accumulation.
-Small shapes are compared on every output; the full 8192 x 8192 and
-65536 x 4096 workloads on sampled rows and columns, which the oracle
-evaluates by the same definition restricted to those rows and columns."""
+Every output is compared, the 8192 x 8192 and 65536 x 4096 workloads
+included; those also pass a per-tile Frobenius check and the componentwise
+bound of Lemma lem:dot (Sec. 5.2) on every entry."""
 import numpy as np
 import pytest
 
 import oracle as O
 from paper_2607_12969_amd import synth
-from parity import PRECS, TOL, rel_fro, stored_pair, to_dev
+from parity import PRECS, TOL, apply_bound, componentwise_ratio, rel_fro, stored_pair, tile_rel_fro_max, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -38,6 +38,12 @@ def _run(lrc, U, s, V, X, prec, path=0):
     return Y.cpu().numpy().astype(np.float64), [o for _, o in hs]
 
 
+def _assert_parity(Y, u, s, v, x, prec):
+    ref = O.apply(u, s, v, x)
+    assert rel_fro(Y, ref) <= TOL[prec]
+    assert componentwise_ratio(Y, ref, apply_bound(u, s, v, x, prec, ref)) <= 1.0
+
+
 @pytest.mark.parametrize("prec", PRECS)
 @pytest.mark.parametrize("path", [1, 2])
 def test_small_workload(lrc, prec, path):
@@ -49,8 +55,7 @@ def test_small_workload(lrc, prec, path):
     X = w["X"] if path == 2 else w["X"][:, :5]
     print(f"apply small prec={prec} path={path}", flush=True)
     Y, (u, s, v, x) = _run(lrc, U[:, :k], S[:k], Vt[:k].T, X, prec, path)
-    ref = O.apply(u, s, v, x)
-    assert rel_fro(Y, ref) <= TOL[prec]
+    _assert_parity(Y, u, s, v, x, prec)
 
 
 @pytest.mark.parametrize("prec", PRECS)
@@ -65,7 +70,7 @@ def test_ragged_shapes_both_paths(lrc, prec, m, n, k, b):
             continue
         print(f"apply ragged prec={prec} m={m} n={n} k={k} b={b} path={path}", flush=True)
         Y, (u, s, v, x) = _run(lrc, d["U"], d["s"], d["V"], d["X"], prec, path)
-        assert rel_fro(Y, O.apply(u, s, v, x)) <= TOL[prec]
+        _assert_parity(Y, u, s, v, x, prec)
 
 
 def test_stream_and_mfma_paths_agree(lrc):
@@ -84,16 +89,28 @@ def test_deterministic(lrc):
         assert np.array_equal(y1, y2), prec
 
 
-def _sampled(lrc, U, s, V, X, prec, rows, cols):
+def _full(lrc, U, s, V, X, prec, label):
+    """Every output of the apply against the oracle on the same stored values:
+    the relative Frobenius tolerance over the whole output and over every
+    64 x 64 tile, and the componentwise bound of Lemma lem:dot on every
+    entry."""
     import torch
     hs = [stored_pair(a, prec) for a in (U, s, V, X)]
+    print(f"apply {label} prec={prec} shape={hs[0][0].shape[0]}x{hs[3][0].shape[1]} k={hs[0][0].shape[1]}",
+          flush=True)
     Y = lrc.matrix_apply(*[to_dev(h) for h, _ in hs])
     torch.cuda.synchronize()
-    got = Y[torch.as_tensor(rows, device=Y.device)][:, torch.as_tensor(cols, device=Y.device)]
-    got = got.cpu().numpy().astype(np.float64)
+    got = Y.cpu().numpy().astype(np.float64)
+    del Y
     u, s_, v, x = [o for _, o in hs]
-    ref = O.apply(u[rows], s_, v, x[:, cols])
-    return rel_fro(got, ref)
+    ref = O.apply(u, s_, v, x)
+    err = rel_fro(got, ref)
+    assert err <= TOL[prec], (label, prec, err)
+    tile = tile_rel_fro_max(got, ref)
+    assert tile <= TOL[prec], (label, prec, "worst 64 x 64 tile", tile)
+    ratio = componentwise_ratio(got, ref, apply_bound(u, s_, v, x, prec, ref))
+    assert ratio <= 1.0, (label, prec, "componentwise bound exceeded", ratio)
+    return err
 
 
 @pytest.fixture(scope="module")
@@ -103,18 +120,13 @@ def square():
 
 @pytest.mark.parametrize("k", [64, 128, 256])
 @pytest.mark.parametrize("b", [1, 64, 4096])
-def test_square_workload_sampled(lrc, square, k, b):
+def test_square_workload_full(lrc, square, k, b):
     """8192 x 8192, sigma_j = j^-1.5 (+1e-8 noise): FP64 at rank k, FP32 and
-    FP16 at rank k + 1, batches 1, 64 and 4096."""
-    rng = np.random.default_rng([12969, 50, k, b])
-    rows = np.sort(rng.choice(8192, 96, replace=False))
-    cols = np.sort(rng.choice(b, min(b, 24), replace=False))
+    FP16 at rank k + 1, batches 1, 64 and 4096; every output compared."""
     X = square["X"][:, :b]
     for prec in PRECS:
         r = k if prec == "fp64" else k + 1
-        print(f"apply 8192^2 k={r} b={b} prec={prec}", flush=True)
-        err = _sampled(lrc, square["U"][:, :r], square["sigma"][:r], square["V"][:, :r], X, prec, rows, cols)
-        assert err <= TOL[prec], (prec, err)
+        _full(lrc, square["U"][:, :r], square["sigma"][:r], square["V"][:, :r], X, prec, "8192^2")
 
 
 @pytest.fixture(scope="module")
@@ -122,18 +134,14 @@ def tail():
     return synth.matrix_tail(kmax=512, batch=4096)
 
 
-@pytest.mark.parametrize("k", [64, 512])
-def test_tail_workload_sampled(lrc, tail, k):
-    """65536 x 4096, sigma_j = max(exp(-j/40), 1e-6), batch 4096."""
+@pytest.mark.parametrize("k", [64, 256, 512])
+@pytest.mark.parametrize("prec", PRECS)
+def test_tail_workload_full(lrc, tail, k, prec):
+    """65536 x 4096, sigma_j = max(exp(-j/40), 1e-6), batch 4096: FP64 at
+    rank k, FP32/FP16 at k + 1; every one of the 268M outputs compared."""
     w = tail
-    rng = np.random.default_rng([12969, 51, k])
-    rows = np.sort(rng.choice(65536, 64, replace=False))
-    cols = np.sort(rng.choice(4096, 16, replace=False))
-    for prec in PRECS:
-        r = k if prec == "fp64" else k + 1
-        print(f"apply 65536x4096 k={r} prec={prec}", flush=True)
-        err = _sampled(lrc, w["U"][:, :r], w["sigma"][:r], w["V"][:, :r], w["X"], prec, rows, cols)
-        assert err <= TOL[prec], (prec, err)
+    r = k if prec == "fp64" else k + 1
+    _full(lrc, w["U"][:, :r], w["sigma"][:r], w["V"][:, :r], w["X"], prec, "65536x4096")
 
 
 @pytest.mark.parametrize("prec", PRECS)
@@ -179,3 +187,17 @@ def test_timing_grid_shapes(lrc, prec, m, n, b, inc):
     print(f"apply grid prec={prec} m={m} n={n} k={k} b={b}", flush=True)
     Y, (u, s, v, x) = _run(lrc, d["U"], d["s"], d["V"], X, prec)
     assert rel_fro(Y, O.apply(u, s, v, x)) <= TOL[prec]
+
+
+def test_large_rank_small_batch(lrc):
+    """A rank whose T' does not fit the streaming path's on-chip buffer at
+    batch 1 (FP64, k = 8200) is still applied correctly."""
+    m, n, k = 8300, 8250, 8200
+    rng = synth.rng_for(synth.W_RANDOM, 30, k)
+    U = synth.gaussian(rng, (m, k)) / np.sqrt(m)
+    V = synth.gaussian(rng, (n, k)) / np.sqrt(n)
+    s = 0.999 ** np.arange(k)
+    X = synth.gaussian(rng, (n, 1))
+    print("apply 8300x8250 k=8200 b=1 fp64", flush=True)
+    Y, (u, s, v, x) = _run(lrc, U, s, V, X, "fp64")
+    _assert_parity(Y, u, s, v, x, "fp64")

@@ -95,7 +95,7 @@ def _tail():
     return _CACHE["tail"]
 
 
-@pytest.mark.parametrize("k", [64, 256])
+@pytest.mark.parametrize("k", [64, 128, 256])
 @pytest.mark.parametrize("prec", ["fp32", "fp16"])
 def test_matrix_square_workload(lrc, k, prec):
     w = _square()
@@ -105,7 +105,7 @@ def test_matrix_square_workload(lrc, k, prec):
     assert abs(want["margin"]) > 1e-6 * want["E_base"]   # verdict not at the boundary
 
 
-@pytest.mark.parametrize("k", [64, 512])
+@pytest.mark.parametrize("k", [64, 256, 512])
 @pytest.mark.parametrize("prec", ["fp32", "fp16"])
 def test_matrix_tail_workload(lrc, k, prec):
     w = _tail()
@@ -113,6 +113,43 @@ def test_matrix_tail_workload(lrc, k, prec):
     got, want = _matrix(lrc, w["sigma"], w["U"][:, :k + 1], w["sigma"][:k + 1], w["V"][:, :k + 1], k, prec)
     _compare(got, want, eta_rtol=1e-6)
     assert abs(want["margin"]) > 1e-6 * want["E_base"]
+
+
+@pytest.fixture(scope="module")
+def square_dense():
+    """The 8192 x 8192 workload formed densely (full Haar singular vectors),
+    so that err_new = ||A - A_hat_{k+1}||_F is measured against A itself."""
+    return synth.matrix_square_dense(kmax=256)
+
+
+@pytest.mark.parametrize("k", [64, 256])
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+def test_matrix_square_err_new(lrc, square_dense, k, prec):
+    """err_new at the 8192 x 8192 size: the dense FP64 matrix-core pass over
+    A (512 MB) against the oracle's dense difference, plus the accuracy-win
+    flags it decides (Sec. 4.1 vocabulary)."""
+    w = square_dense
+    print(f"certify 8192^2 with A k={k} prec={prec}", flush=True)
+    got, want = _matrix(lrc, w["sigma"], w["U"][:, :k + 1], w["sigma"][:k + 1], w["V"][:, :k + 1], k, prec,
+                        A=w["A"])
+    _compare(got, want, eta_rtol=1e-6, err_rtol=1e-9)
+    # E_k^2 = E_{k+1}^2 + sigma_{k+1}^2 and err_new^2 = E_{k+1}^2 + eta^2 up to the
+    # cross term, so err_new sits within eta of E_{k+1}
+    assert abs(got["err_new"] - got["E_aug"]) <= got["eta"] * (1 + 1e-6) + 1e-12 * got["norm_ref"]
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+def test_matrix_eta_exact_on_device(lrc, prec):
+    """The device eta (Gram matrices of the exact rounding differences) on a
+    factorization whose only rounding is in s, with every rounding error
+    known: eta = h sqrt(3311) in closed form (see the oracle pin)."""
+    from test_oracle_certificate import exact_eta_case
+    U, s, V, sigma, exact = exact_eta_case(prec)
+    got, want = _matrix(lrc, sigma, U, s, V, 20, prec)
+    assert abs(got["eta"] - exact) <= 1e-14 * exact, (got["eta"], exact)
+    assert abs(want["eta"] - exact) <= 2.0 ** -52 * exact
+    for f in FLAGS:
+        assert got[f] == want[f], f
 
 
 def _tt(lrc, T, base, aug, prec):
@@ -226,3 +263,36 @@ def test_tt_certificate_unfused_fallback(lrc):
     got, want, labels = _tt_labels(lrc, T, base, aug, "fp16")
     assert labels.get("cert_tt_fused_f64") == 3 and labels.get("cert_sumsq5_f64") == 1, labels
     _compare(got, want, eta_rtol=1e-6, err_rtol=1e-6, e_atol=1e-12 * want["norm_ref"])
+
+
+@pytest.mark.parametrize("schedule", [(64, 65), (32, 33), (32, 36)])
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+def test_tt_hyperspectral_workload(lrc, hyper, schedule, prec):
+    """The benchmark's TT certificate input: the normalized 512 x 512 x 224
+    cube with its own TT-SVD, FP64 base (64,64) or (32,32) against the
+    compensated (65,65), (33,33) or (36,36) stored in FP32 / FP16.  Verdicts,
+    outcome and bytes must equal the oracle's; the sums agree to FP64
+    reduction-order rounding."""
+    T, base, aug = hyper
+    rb, ra = schedule
+    print(f"certify tt 512x512x224 ({rb},{rb})->({ra},{ra}) {prec}", flush=True)
+    got, want = _tt(lrc, T, base[rb], aug[ra], prec)
+    print(f"  eta/|T| {want['eta'] / want['norm_ref']:.3e} E_R {want['E_base']:.6e} E_R+ {want['E_aug']:.6e} "
+          f"certified {want['certified']}", flush=True)
+    assert abs(want["margin"]) > 1e-9 * want["E_base"]      # verdict not at the boundary
+    _compare(got, want, eta_rtol=1e-6, err_rtol=1e-6, e_atol=1e-12 * want["norm_ref"])
+
+
+def test_tt_certificate_on_benchmark_cores(lrc, hyper):
+    """The certificate verdicts the benchmark prints come from its own
+    fixed-rank TT-SVD of the cube (LAPACK, for speed); the device certificate
+    on exactly those cores must equal the oracle's on them."""
+    import bench
+    T = hyper[0]
+    base = bench.tt_svd_fixed(T, (64, 64))
+    aug = bench.tt_svd_fixed(T, (65, 65))
+    for prec in ("fp32", "fp16"):
+        print(f"certify tt benchmark cores (64,64)->(65,65) {prec}", flush=True)
+        got, want = _tt(lrc, T, base, aug, prec)
+        assert abs(want["margin"]) > 1e-9 * want["E_base"]
+        _compare(got, want, eta_rtol=1e-6, err_rtol=1e-6, e_atol=1e-12 * want["norm_ref"])

@@ -176,3 +176,43 @@ def test_tt_compensation_algorithm_outcomes():
     assert r16["outcome"] == 2
     r32 = O.tt_compensation(T, R=[4, 4], delta=4, prec="fp32")
     assert r32["ranks_aug"] == [1, 8, 8, 1] and r32["outcome"] == 1
+
+
+def exact_eta_case(prec):
+    """A rank-21 factorization whose stored form differs from the FP64 one
+    only through s, with every rounding error known in closed form.
+
+    U = [I; 0] (40 x 21) and V = [I; 0] (30 x 21) are exact in every format.
+    s_j = 1 + 4 (25 - j) ulp + e_j (ulp = 2^-23 for FP32, 2^-10 for FP16),
+    with e_j = (j+1) h below half an ulp (rounds down, error -(j+1) h) for
+    even j and e_j = ulp - (j+1) h (rounds up, error +(j+1) h) for odd j,
+    h = 2^-30 (FP32) or 2^-20 (FP16); all s_j are exact binary64 values.
+    Then A_hat - A_{k+1} = U diag(s_hat - s) V^T and
+    eta = h sqrt(sum_{j=1}^{21} j^2) = h sqrt(3311)."""
+    ulp, h = {"fp32": (2.0 ** -23, 2.0 ** -30), "fp16": (2.0 ** -10, 2.0 ** -20)}[prec]
+    m, n, r = 40, 30, 21
+    U = np.zeros((m, r))
+    V = np.zeros((n, r))
+    U[:r, :r] = np.eye(r)
+    V[:r, :r] = np.eye(r)
+    j = np.arange(r)
+    e = np.where(j % 2 == 0, (j + 1) * h, ulp - (j + 1) * h)
+    s = 1.0 + 4.0 * (25 - j) * ulp + e
+    sigma = np.concatenate([s, 0.5 ** np.arange(1, n - r + 1)])   # non-increasing full spectrum
+    return U, s, V, sigma, h * math.sqrt(3311.0)
+
+
+@pytest.mark.parametrize("prec", ["fp32", "fp16"])
+def test_matrix_eta_exact_when_only_sigma_rounds(prec):
+    """Remark after Thm thm:matrix_rank_compensation: U, Sigma and V are
+    rounded individually, so rounding s alone must produce exactly
+    ||s_hat - s||_2.  An oracle that left s unrounded would report 0, one
+    that rounded it to the other format a different value."""
+    U, s, V, sigma, want = exact_eta_case(prec)
+    sh = O.widen(O.round_to(s, prec))
+    ref_err = np.where(np.arange(21) % 2 == 0, -1.0, 1.0) * (np.arange(21) + 1) * (want / math.sqrt(3311.0))
+    assert np.array_equal(sh - s, ref_err)                     # every rounding error as constructed
+    c = O.matrix_certificate(sigma, U, s, V, 20, prec)
+    assert abs(c["eta"] - want) <= 2.0 ** -52 * want
+    other = "fp16" if prec == "fp32" else "fp32"
+    assert abs(O.matrix_certificate(sigma, U, s, V, 20, other)["eta"] - want) > 0.5 * want

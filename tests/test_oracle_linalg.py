@@ -232,3 +232,21 @@ def test_left_orthogonalize_properties():
     lo2 = O.left_orthogonalize(cs)
     for a, b in zip(cs, lo2):
         assert np.max(np.abs(a - b)) <= 1e-13 * max(1.0, np.max(np.abs(a)))
+
+
+def test_tt_svd_memo_is_bitwise_transparent():
+    """The SVD memo only reuses the SVD of an unfolding that an earlier run
+    on the same tensor already computed for the same kept ranks: cores are
+    identical bit for bit to fresh runs, and the first unfolding's SVD is
+    computed once for every rank choice."""
+    rng = np.random.default_rng([12969, 77])
+    T = rng.standard_normal((6, 7, 8, 5))
+    memo = {}
+    for ranks in ([3, 4, 2], [3, 5, 2], [2, 4, 2], [3, 4, 3]):
+        fresh = O.tt_svd(T, ranks=ranks)
+        memod = O.tt_svd(T, ranks=ranks, svd_memo=memo)
+        assert len(fresh) == len(memod)
+        for a, b in zip(fresh, memod):
+            assert a.shape == b.shape and np.array_equal(a.view(np.uint64), b.view(np.uint64))
+    assert sum(1 for key in memo if key == ()) == 1
+    assert {key for key in memo if len(key) == 1} == {(2,), (3,)}
