@@ -99,6 +99,28 @@ extern "C" {
 int lrc_matrix_apply(const void* U, const void* s, const void* V, const void* X, void* Y,
                      int64_t m, int64_t n, int64_t k, int64_t batch, int prec);
 
+/*
+ * lrc_matrix_apply_noalloc -- lrc_matrix_apply without any allocation
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, kernels, plan and result (bit for bit) as lrc_matrix_apply;
+ * the split sums and T' live in a fixed scratch array of
+ * LRC_NOALLOC_SCRATCH_BYTES in device memory instead of the library's
+ * grow-only workspace.  Each device holds its own array from the first call
+ * until the process ends; no hipMalloc, hipFree or allocating library
+ * routine is called (with kernel timing off, the default).
+ * Every call on one device shares that device's array and leaves its last
+ * contents there: calls that overlap in time on one device (two streams,
+ * two threads) race on it and must be serialized by the caller.
+ * Errors: those of lrc_matrix_apply, and LRC_EINVAL when the plan for these
+ * sizes needs more than LRC_NOALLOC_SCRATCH_BYTES of scratch (checked on
+ * the host before anything is launched).
+ */
+#define LRC_NOALLOC_SCRATCH_BYTES (64LL << 20)
+int lrc_matrix_apply_noalloc(const void* U, const void* s, const void* V, const void* X, void* Y,
+                             int64_t m, int64_t n, int64_t k, int64_t batch, int prec);
+
 /* The apply kernel pair LRC_PATH_AUTO selects for these sizes (pure host
  * function, no device needed).  Returns LRC_PATH_STREAM or LRC_PATH_MFMA, or
  * LRC_EINVAL for invalid sizes. */

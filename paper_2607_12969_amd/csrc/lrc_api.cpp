@@ -22,6 +22,13 @@
 
 using namespace lrc;
 
+// Scratch of lrc_matrix_apply_noalloc: one array per device, held from the
+// module's load until the process ends.  Host code never passes the array's
+// name to a kernel (on the host it is only a stand-in for the symbol); the
+// device address comes from hipGetSymbolAddress, taken once per device with
+// that device current (noalloc_scratch), and every later use goes through it.
+static __device__ __align__(256) char scratch[LRC_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_err;
@@ -78,6 +85,24 @@ int current_device(int* dev, size_t* max_lds) {
     }
     if (!it->second.first) return fail(LRC_ENODEV, "device %d is not a gfx950 (MI355X) GPU", *dev);
     if (max_lds) *max_lds = it->second.second;
+    return LRC_OK;
+}
+
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch;   // device -> device address of `scratch`
+
+int noalloc_scratch(int dev, void** out) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch.find(dev);
+    if (it == g_scratch.end()) {
+        void* p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(LRC_EHIP, "address of the scratch array on device %d: %s", dev,
+                        e != hipSuccess ? hipGetErrorString(e) : "null");
+        it = g_scratch.emplace(dev, p).first;
+    }
+    *out = it->second;
     return LRC_OK;
 }
 
@@ -302,6 +327,29 @@ static int check_apply_arrays(const void* U, const void* s, const void* V, const
     if (overlaps(Y, ny, U, (size_t)m * k * e) || overlaps(Y, ny, s, (size_t)k * e) ||
         overlaps(Y, ny, V, (size_t)n * k * e) || overlaps(Y, ny, X, (size_t)n * batch * e))
         return fail(LRC_EINVAL, "output Y overlaps an input");
+    return LRC_OK;
+}
+
+int lrc_matrix_apply_noalloc(const void* U, const void* s, const void* V, const void* X, void* Y, int64_t m,
+                             int64_t n, int64_t k, int64_t batch, int prec) {
+    int rc = check_apply_arrays(U, s, V, X, Y, m, n, k, batch, prec);
+    if (rc) return rc;
+    const ApplyPlan plan = plan_apply(m, n, k, batch, prec, g_force_path, U, V, X);
+    const size_t need = apply_workspace_bytes(plan);
+    if (need > (size_t)LRC_NOALLOC_SCRATCH_BYTES)
+        return fail(LRC_EINVAL, "this apply needs %zu bytes of scratch, above the %lld of the allocation-free entry",
+                    need, (long long)LRC_NOALLOC_SCRATCH_BYTES);
+    int dev;
+    rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    void* base = nullptr;
+    rc = noalloc_scratch(dev, &base);
+    if (rc) return rc;
+    Workspace ws;   // a view of the device's scratch array: take() only, never reserve()
+    ws.base = static_cast<char*>(base);
+    ws.cap = (size_t)LRC_NOALLOC_SCRATCH_BYTES;
+    hipError_t he = launch_apply(plan, U, s, V, X, Y, m, n, k, batch, prec, ws, g_stream);
+    if (he != hipSuccess) return fail_hip(he, "apply launch");
     return LRC_OK;
 }
 

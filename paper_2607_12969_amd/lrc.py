@@ -83,6 +83,8 @@ def lib():
     L = ctypes.CDLL(LIB_PATH)
     L.lrc_matrix_apply.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, ctypes.c_int]
     L.lrc_matrix_apply.restype = ctypes.c_int
+    L.lrc_matrix_apply_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, ctypes.c_int]
+    L.lrc_matrix_apply_noalloc.restype = ctypes.c_int
     L.lrc_matrix_apply_path.argtypes = [_i64, _i64, _i64, _i64, ctypes.c_int]
     L.lrc_matrix_apply_path.restype = ctypes.c_int
     L.lrc_set_apply_path.argtypes = [ctypes.c_int]
@@ -230,6 +232,26 @@ def tt_shape(cores):
     dims = [int(c.shape[1]) for c in cores]
     ranks = [int(cores[0].shape[0])] + [int(c.shape[2]) for c in cores]
     return dims, ranks
+
+
+def matrix_apply_noalloc(U, s, V, X, Y):
+    """matrix_apply through the allocation-free entry point: Y (m x batch)
+    must be supplied; the library's per-device scratch array holds the
+    intermediate sums (calls overlapping on one device race on it)."""
+    prec = _prec_of(U)
+    for t in (s, V, X, Y):
+        if t.dtype != U.dtype:
+            raise TypeError("all factors, the batch and Y must share one dtype")
+    _need(U.dim() == 2 and X.dim() == 2, "U and X must be matrices")
+    m, k = U.shape
+    n, b = X.shape
+    _need(tuple(V.shape) == (n, k) and tuple(s.shape) == (k,), "shape mismatch")
+    _need(tuple(Y.shape) == (m, b), f"Y has shape {tuple(Y.shape)}, want {(m, b)}")
+    _dev(U, s, V, X, Y)
+    _bind_stream(U.device)
+    _check(lib().lrc_matrix_apply_noalloc(U.data_ptr(), s.data_ptr(), V.data_ptr(), X.data_ptr(), Y.data_ptr(),
+                                          m, n, k, b, prec))
+    return Y
 
 
 def _check_train(cores):

@@ -76,6 +76,19 @@ def test_apply_argument_errors():
     assert b"overlaps" in L.lrc_last_error()
 
 
+def test_noalloc_apply_checks_on_the_host():
+    """The allocation-free apply validates like lrc_matrix_apply and rejects
+    sizes whose plan needs more than its fixed scratch before any device
+    call (T' alone of a 65536 x 4096 FP64 apply at rank 512 and batch 20000
+    is 82 MB)."""
+    good = [0x10000, 0x20000, 0x30000, 0x40000, 0x90000000]
+    f = L.lrc_matrix_apply_noalloc
+    assert f(0, *good[1:], 10, 10, 3, 4, 0) == -1                          # NULL
+    assert f(*good, 10, 10, 11, 4, 0) == -1                                # k > min(m, n)
+    assert f(*good, 65536, 4096, 512, 20000, 0) == -1
+    assert b"scratch" in L.lrc_last_error()
+
+
 def _tt(dims, ranks, d, prec=0, cores=None, out=0x90000000):
     D = (ctypes.c_int64 * max(1, len(dims)))(*dims)
     R = (ctypes.c_int64 * max(1, len(ranks)))(*ranks)
