@@ -228,12 +228,14 @@ def cpu_baseline(wl, budget_s=12.0):
     res = None
     stored = {p: [O.stored(a, names[p]) for a in (U[:, :wl.apply_in[p][2]], s[:wl.apply_in[p][2]],
                                                    V[:, :wl.apply_in[p][2]])] for p in names}
-    for frac in (1 / 256, 1 / 64, 1 / 16, 1 / 4):
-        bs = max(1, int(round(wl.b * frac)))
-        n1 = max(1, int(round(dims[0] * frac)))
+    # growing samples; past the whole batch and cube the whole step is repeated
+    for frac in (1 / 256, 1 / 64, 1 / 16, 1 / 4, 1, 2, 4, 8):
+        reps = max(1, int(frac))
+        bs = max(1, int(round(wl.b * min(frac, 1))))
+        n1 = max(1, int(round(dims[0] * min(frac, 1))))
         flops = 0.0
         t0 = time.time()
-        for p in ("f64", "f32", "f16"):
+        for p in ("f64", "f32", "f16") * reps:
             kk = wl.apply_in[p][2]
             O.apply(*stored[p], O.stored(X[:, :bs], names[p]))
             flops += apply_counts(wl.m, wl.n, kk, bs, 8)[0]
@@ -247,8 +249,8 @@ def cpu_baseline(wl, budget_s=12.0):
         res = dict(value=round(flops / el / 1e9, 3), unit="GFLOP/s", cores=O.num_threads(), kind="oracle",
                    cpu_model=cpu_model(),
                    sample=(f"FP64 oracle apply (3 methods, batch {bs} of 4096) and TT reconstruction "
-                           f"(3 methods, first {n1} of 512 slabs); {flops / 1e9:.1f} GFLOP in {el:.1f}s; "
-                           "certificates not included"))
+                           f"(3 methods, first {n1} of 512 slabs), {reps} pass(es); {flops / 1e9:.1f} GFLOP in "
+                           f"{el:.1f}s; certificates not included"))
         if el >= budget_s:
             break
     # one thread: the small configurations

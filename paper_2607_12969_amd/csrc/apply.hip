@@ -72,14 +72,73 @@ template <> struct SmallCfg<half_t> { using C = Cfg<half_t, 64, 64, 32, 2, 2>; }
 // step of a K range can be partial, and there the missing K values are
 // zeroed.
 
-// Every thread moves whole 16-byte chunks: sources have a 16-byte aligned
-// base and a pitch that is a multiple of the chunk (operands that are not
-// are first copied into a padded workspace), so a chunk that starts inside a
-// row stays inside that row's pitch.
+// Every thread moves whole 16-byte chunks.  When the source has a 16-byte
+// aligned base and a pitch that is a multiple of the chunk (MIS = false), a
+// chunk that starts inside a row stays inside that row's pitch and is read
+// directly.  Otherwise (MIS = true: odd ranks such as the compensated k + 1,
+// odd batches, offset views) a thread's chunk starts anywhere: it reads the
+// two aligned 16-byte chunks that cover it and funnel-shifts them into place
+// when it writes LDS, so the operand is read in place at any pitch.  The
+// second aligned chunk is read only when it still holds an element of the
+// matrix (else the first is read twice); an aligned chunk that holds a
+// valid element lies inside one page of the allocation.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
+// The 16 bytes that start `sh` bytes into lo, continued into hi (sh in
+// [0, 16), a multiple of the element size).  Whole dwords are picked by
+// selects over named words (no array, so nothing is promoted to memory, and
+// no 64-bit shifts); a 2-byte remainder (binary16) is taken with
+// v_alignbyte.
+template <typename T>
+__device__ __forceinline__ u32x4_t funnel16(u32x4_t lo, u32x4_t hi, int sh) {
+    const int dq = sh >> 2;
+    const unsigned d0 = lo[0], d1 = lo[1], d2 = lo[2], d3 = lo[3], d4 = hi[0], d5 = hi[1], d6 = hi[2], d7 = hi[3];
+    const bool q1 = dq == 1, q2 = dq == 2, q3 = dq == 3;
+    const unsigned w0 = q3 ? d3 : q2 ? d2 : q1 ? d1 : d0;
+    const unsigned w1 = q3 ? d4 : q2 ? d3 : q1 ? d2 : d1;
+    const unsigned w2 = q3 ? d5 : q2 ? d4 : q1 ? d3 : d2;
+    const unsigned w3 = q3 ? d6 : q2 ? d5 : q1 ? d4 : d3;
+    u32x4_t out;
+    if constexpr (sizeof(T) >= 4) {
+        out[0] = w0;
+        out[1] = w1;
+        out[2] = w2;
+        out[3] = w3;
+    } else {
+        const unsigned w4 = q3 ? d7 : q2 ? d6 : q1 ? d5 : d4;
+        const unsigned sb = (unsigned)(sh & 3);   // 0 or 2
+        out[0] = __builtin_amdgcn_alignbyte(w1, w0, sb);
+        out[1] = __builtin_amdgcn_alignbyte(w2, w1, sb);
+        out[2] = __builtin_amdgcn_alignbyte(w3, w2, sb);
+        out[3] = __builtin_amdgcn_alignbyte(w4, w3, sb);
+    }
+    return out;
+}
+
+// Loads of a chunk of 16 bytes of T that starts at element address `el`
+// (any alignment); `last` is the matrix's last element.
+template <typename T>
+struct MisChunk {
+    static constexpr int CH = 16 / (int)sizeof(T);
+    u32x4_t lo, hi;
+    int sh;
+    __device__ __forceinline__ void fetch(const T* el, const T* last) {
+        const int off = (int)(reinterpret_cast<uintptr_t>(el) & 15) / (int)sizeof(T);   // elements past the chunk start
+        const T* pa = el - off;
+        const T* ph = (pa + CH <= last) ? pa + CH : pa;
+        sh = off * (int)sizeof(T);
+        lo = *reinterpret_cast<const u32x4_t*>(pa);
+        hi = *reinterpret_cast<const u32x4_t*>(ph);
+    }
+    template <typename V>
+    __device__ __forceinline__ V value() const {
+        return __builtin_bit_cast(V, funnel16<T>(lo, hi, sh));
+    }
+};
 
 // A tile of BK x ROWS elements taken from a source laid out [K][ld] with the
 // ROWS index contiguous, into LDS [BK][ROWS + PADR].
-template <class C, int ROWS, typename T>
+template <class C, int ROWS, typename T, bool MIS = false>
 struct RowsTile {
     static constexpr int CH = C::VEC;                            // elements per move
     static constexpr int E = C::BK * ROWS / (C::NT * CH);        // moves per thread
@@ -88,7 +147,8 @@ struct RowsTile {
     static constexpr int KS = C::NT / RC;                        // K rows between a thread's moves
     static_assert(C::NT % RC == 0, "a thread keeps one column position");
     typedef T vec_t __attribute__((ext_vector_type(CH)));
-    vec_t reg[E];
+    vec_t reg[MIS ? 1 : E];
+    MisChunk<T> mc[MIS ? E : 1];
     // per-thread geometry: K row of move 0 and element offset of its column
     struct Geo {
         const T* base;   // source + r0 (uniform)
@@ -96,34 +156,36 @@ struct RowsTile {
         int kk0;         // K row of move 0 within a step
         int col;         // column offset within the tile, clamped into the matrix
         int lcol;        // LDS column of this thread
+        const T* last;   // last element of the matrix (MIS)
     };
-    __device__ __forceinline__ static Geo geo(const T* src, int64_t ld, int64_t r0, int64_t rlim, int tid) {
+    __device__ __forceinline__ static Geo geo(const T* src, int64_t ld, int64_t r0, int64_t rlim, int tid,
+                                              const T* last = nullptr) {
         Geo g;
         g.base = src + r0;
         g.ld = ld;
         g.kk0 = tid / RC;
         g.lcol = (tid % RC) * CH;
         g.col = (r0 + g.lcol < rlim) ? g.lcol : 0;
+        g.last = last;
         return g;
     }
     __device__ __forceinline__ void fetch(const Geo& g, int64_t k0, bool partial, int64_t klim) {
-        if (!partial) {
-            const T* p = g.base + (k0 + g.kk0) * g.ld + g.col;
 #pragma unroll
-            for (int e = 0; e < E; ++e) reg[e] = *reinterpret_cast<const vec_t*>(p + (int64_t)(e * KS) * g.ld);
-        } else {
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int64_t gk = k0 + g.kk0 + e * KS;
-                reg[e] = *reinterpret_cast<const vec_t*>(g.base + (gk < klim ? gk : klim - 1) * g.ld + g.col);
-            }
+        for (int e = 0; e < E; ++e) {
+            int64_t gk = k0 + g.kk0 + e * KS;
+            if (partial) gk = gk < klim ? gk : klim - 1;
+            const T* p = g.base + gk * g.ld + g.col;
+            if constexpr (MIS) mc[e].fetch(p, g.last);
+            else reg[e] = *reinterpret_cast<const vec_t*>(p);
         }
     }
     __device__ __forceinline__ void stash(T* S, const Geo& g, int64_t k0, bool partial, int64_t klim) const {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const int kk = g.kk0 + e * KS;
-            vec_t w = reg[e];
+            vec_t w;
+            if constexpr (MIS) w = mc[e].template value<vec_t>();
+            else w = reg[e];
             if (partial && k0 + kk >= klim) {
 #pragma unroll
                 for (int v = 0; v < CH; ++v) w[v] = T(0);
@@ -135,7 +197,7 @@ struct RowsTile {
 
 // A tile of ROWS x BK elements from a source laid out [rows][ld] with K
 // contiguous, into LDS [ROWS][LDK].
-template <class C, int ROWS, typename T>
+template <class C, int ROWS, typename T, bool MIS = false>
 struct KTile {
     static constexpr int CH = C::VEC;
     static constexpr int E = C::BK * ROWS / (C::NT * CH);
@@ -143,15 +205,18 @@ struct KTile {
     static constexpr int RS = C::NT / KC;                        // rows between a thread's moves
     static_assert(C::NT % KC == 0, "a thread keeps one K position");
     typedef T vec_t __attribute__((ext_vector_type(CH)));
-    vec_t reg[E];
+    vec_t reg[MIS ? 1 : E];
+    MisChunk<T> mc[MIS ? E : 1];
     struct Geo {
         const T* base;   // source + r0 * ld (uniform)
         int64_t ld;
         int rr0;         // row of move 0 within the tile
         int rmax;        // last row inside the matrix, relative to r0
         int kq;          // K offset of this thread within a step
+        const T* last;   // last element of the matrix (MIS)
     };
-    __device__ __forceinline__ static Geo geo(const T* src, int64_t ld, int64_t r0, int64_t rlim, int tid) {
+    __device__ __forceinline__ static Geo geo(const T* src, int64_t ld, int64_t r0, int64_t rlim, int tid,
+                                              const T* last = nullptr) {
         Geo g;
         g.base = src + r0 * ld;
         g.ld = ld;
@@ -159,6 +224,7 @@ struct KTile {
         g.kq = (tid % KC) * CH;
         const int64_t rm = rlim - 1 - r0;
         g.rmax = rm < ROWS ? (int)rm : ROWS;
+        g.last = last;
         return g;
     }
     __device__ __forceinline__ void fetch(const Geo& g, int64_t k0, bool partial, int64_t klim) {
@@ -168,14 +234,18 @@ struct KTile {
             rr = rr < g.rmax ? rr : g.rmax;
             int64_t gk = k0 + g.kq;
             if (partial && gk >= klim) gk = 0;
-            reg[e] = *reinterpret_cast<const vec_t*>(g.base + (int64_t)rr * g.ld + gk);
+            const T* p = g.base + (int64_t)rr * g.ld + gk;
+            if constexpr (MIS) mc[e].fetch(p, g.last);
+            else reg[e] = *reinterpret_cast<const vec_t*>(p);
         }
     }
     __device__ __forceinline__ void stash(T* S, const Geo& g, int64_t k0, bool partial, int64_t klim) const {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const int rr = g.rr0 + e * RS;
-            vec_t w = reg[e];
+            vec_t w;
+            if constexpr (MIS) w = mc[e].template value<vec_t>();
+            else w = reg[e];
             if (partial) {
                 const int64_t gk = k0 + g.kq;
 #pragma unroll
@@ -377,7 +447,7 @@ __device__ __forceinline__ void atb_store(const typename C::AccV& a, int tid, in
 //              factor 1 when s is null),
 //              written for m < Mout (zero padding rows included).
 //   ATB_GRAM : out is G[m][ldo] in double (T = double).
-template <typename T, class C, int MODE>
+template <typename T, class C, int MODE, bool MIS = false>
 __global__ __launch_bounds__(C::NT) void k_atb(
     const T* __restrict__ Asrc, int64_t lda, const T* __restrict__ Bsrc, int64_t ldb,
     int64_t M, int64_t N, int64_t K, int64_t chunk, int tiles_m, int tiles_n, int splits,
@@ -407,10 +477,10 @@ __global__ __launch_bounds__(C::NT) void k_atb(
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = zero_accv<AccV>();
 
-    using TA = RowsTile<C, C::BM, T>;
-    using TB = RowsTile<C, C::BN, T>;
-    const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid);
-    const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
+    using TA = RowsTile<C, C::BM, T, MIS>;
+    using TB = RowsTile<C, C::BN, T, MIS>;
+    const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid, Asrc + (K - 1) * lda + (M - 1));
+    const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid, Bsrc + (K - 1) * ldb + (N - 1));
     TA ta[2];
     TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
@@ -547,7 +617,7 @@ __device__ __forceinline__ void abt_store_staged(const typename C::AccV (&acc)[C
 // One workgroup per tile, in the order of AbtOrder.
 //   ABT_STORE: Y[m][ldy] = C rounded to T.
 //   ABT_ERR  : (T = double) partial sum of (Aref[m][n] - C)^2 per workgroup.
-template <typename T, class C, int MODE>
+template <typename T, class C, int MODE, bool MIS = false>
 __global__ __launch_bounds__(C::NT) void k_abt(
     const T* __restrict__ Asrc, int64_t lda, int64_t M, int64_t Ka,
     const T* __restrict__ Bsrc, int64_t ldb, int64_t N, int64_t Kb, int64_t K, int tiles_m, int tiles_n,
@@ -578,9 +648,9 @@ __global__ __launch_bounds__(C::NT) void k_abt(
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = zero_accv<AccV>();
 
-    using TA = KTile<C, C::BM, T>;
-    using TB = KTile<C, C::BN, T>;
-    const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid);
+    using TA = KTile<C, C::BM, T, MIS>;
+    using TB = KTile<C, C::BN, T>;   // T'^T (or the certificate's factors): aligned rows
+    const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid, Asrc + (M - 1) * lda + (Ka - 1));
     const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
     TA ta[2];
     TB tb[2];
@@ -639,15 +709,15 @@ static bool vec_ok(const void* p, int64_t ld) {
 }
 
 // k_atb over all (tile, split) workgroups, then k_atb_finish when the sum is split.
-template <typename T, class C, int MODE>
+template <typename T, class C, int MODE, bool MIS = false>
 static void run_atb(const char* label, const char* finish_label, hipStream_t st, const T* A, int64_t lda,
                     const T* B, int64_t ldb, int64_t M, int64_t N, int64_t K, int64_t chunk, int tiles_m, int tiles_n,
                     int splits, typename C::Acc* part, const T* svals, void* out, int64_t ldo, int64_t Mout) {
     {
         KernelTimer t(label, st);
         const dim3 grid(xcd_grid((int64_t)tiles_m * tiles_n * splits));
-        hipLaunchKernelGGL((k_atb<T, C, MODE>), grid, dim3(C::NT), 0, st, A, lda, B, ldb, M, N, K, chunk, tiles_m,
-                           tiles_n, splits, part, svals, out, ldo, Mout);
+        hipLaunchKernelGGL((k_atb<T, C, MODE, MIS>), grid, dim3(C::NT), 0, st, A, lda, B, ldb, M, N, K, chunk,
+                           tiles_m, tiles_n, splits, part, svals, out, ldo, Mout);
     }
     if (splits > 1) {
         KernelTimer t(finish_label, st);
@@ -657,110 +727,145 @@ static void run_atb(const char* label, const char* finish_label, hipStream_t st,
                            Mout);
     }
 }
-template <typename T, class C, int MODE, class... Args>
+template <typename T, class C, int MODE, bool MIS = false, class... Args>
 static void launch_abt(dim3 grid, hipStream_t st, Args... args) {
-    hipLaunchKernelGGL((k_abt<T, C, MODE>), grid, dim3(C::NT), 0, st, args...);
+    hipLaunchKernelGGL((k_abt<T, C, MODE, MIS>), grid, dim3(C::NT), 0, st, args...);
 }
 
-// Padded copies of the operands whose pitch or base rule out 16-byte moves,
-// all in one launch: job q copies src (rows x cols, pitch lds) into dst
+// Padded copies of the operands whose pitch or base rule out 16-byte moves
+// (large batches: the matrix-core tiles then read the copy many times), all
+// in one launch: job q copies src (rows x cols, pitch lds) into dst
 // (rows x ldd, ldd a multiple of the 16-byte chunk, dst 16-byte aligned),
 // with zeros in columns cols <= j < ldd.  Each thread fills whole 16-byte
-// chunks of dst from element loads of the source (adjacent threads read
-// adjacent elements, so the loads coalesce).
+// chunks of dst from the two aligned 16-byte chunks of the source that cover
+// them (funnel-shifted), so loads and stores are full 16-byte moves.
 template <typename T>
 struct StageJobs {
     const T* src[3];
     T* dst[3];
     int64_t rows[3], cols[3], lds[3];
     int cpr[3];              // 16-byte chunks per destination row
-    int64_t end[3];          // running total of chunks up to and including job q
+    int64_t chunks[3];       // chunks of job q
+    unsigned bend[3];        // workgroups up to and including job q
     int n;
 };
 
-template <typename T>
+template <typename T, typename I>
 __global__ __launch_bounds__(256) void k_pitch_copy(StageJobs<T> J) {
     constexpr int VEC = 16 / (int)sizeof(T);
     typedef T vec_t __attribute__((ext_vector_type(VEC)));
-    const int64_t total = J.end[J.n - 1];
-    for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < total; c += (int64_t)gridDim.x * 256) {
-        const int q = c < J.end[0] ? 0 : (c < J.end[1] ? 1 : 2);
-        const int64_t cj = q == 0 ? c : c - J.end[q - 1];
-        const int64_t i = cj / J.cpr[q];
-        const int64_t j0 = (cj - i * J.cpr[q]) * VEC;
-        const T* src = J.src[q] + i * J.lds[q];
-        vec_t w;
+    // the job is uniform over the workgroup: its fields come from scalar loads
+    const unsigned bid = blockIdx.x;
+    const int q = bid < J.bend[0] ? 0 : (bid < J.bend[1] ? 1 : 2);
+    const unsigned b0 = q == 0 ? 0u : J.bend[q - 1];
+    const I nb = (I)(J.bend[q] - b0);
+    const I total = (I)J.chunks[q];
+    const I cpr = (I)J.cpr[q];
+    const T* src = J.src[q];
+    T* dst = J.dst[q];
+    const int64_t lds = J.lds[q], cols = J.cols[q];
+    const T* last = src + (J.rows[q] - 1) * lds + (cols - 1);
+    for (I c = (I)(bid - b0) * 256 + threadIdx.x; c < total; c += nb * 256) {
+        const I i = c / cpr;
+        const int64_t j0 = (int64_t)(c - i * cpr) * VEC;
+        MisChunk<T> mc;   // chunks past the row's end start at its last element (their values are zeroed)
+        mc.fetch(src + (int64_t)i * lds + (j0 < cols ? j0 : cols - 1), last);
+        vec_t w = mc.template value<vec_t>();
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) w[v] = j0 + v < J.cols[q] ? src[j0 + v] : T(0);
-        *reinterpret_cast<vec_t*>(J.dst[q] + i * (int64_t)J.cpr[q] * VEC + j0) = w;
+        for (int v = 0; v < VEC; ++v)
+            if (j0 + v >= cols) w[v] = T(0);
+        *reinterpret_cast<vec_t*>(dst + (int64_t)c * VEC) = w;
     }
 }
 
 // --------------------------------------------------------- streaming path --
-// Phase 1, batch <= NB: workgroup (jg, sp) owns columns [64 jg, 64 jg + 64)
-// of V and rows [sp*chunk, (sp+1)*chunk) of V and X.  Lane j of every wave
-// accumulates column j; the four waves take interleaved rows and are summed
-// in wave order.  k_p1_stream_finish then combines the per-chunk partials
-// in chunk order, scales by s and writes T'^T.
+// Batches of at most NB = 8 columns, two launches.
+//
+// Phase 1 (k_p1_thin): workgroup (jg, sp) of 8 waves owns columns
+// [64 jg, 64 jg + 64) of V and a chunk of rows of V and X.  Lane j of every
+// wave accumulates column j over the wave's contiguous share of the chunk, in
+// batches of RW rows whose loads are all issued before the first product
+// (V element by element along its rows, which a wave reads as whole 128-byte
+// segments whatever the row pitch; the batch's X rows, contiguous in memory,
+// by one coalesced load per lane into the wave's own LDS rows, from which
+// every lane reads them).  The waves are added in wave order and the
+// workgroup writes its partial.  (A last-workgroup finish inside this kernel
+// needs a device-scope release per workgroup, which on this chip writes back
+// the L2 of its XCD each time and measured slower than a second launch.)
+constexpr int kThinWaves = 8;
+constexpr int kThinRows = 32;                    // rows per wave and batch
+
 template <typename T, int NB>
-__global__ __launch_bounds__(256) void k_p1_stream(
+__global__ __launch_bounds__(64 * kThinWaves) void k_p1_thin(
     const T* __restrict__ V, const T* __restrict__ X, typename PrecTraits<T>::acc* __restrict__ part,
     int64_t n, int64_t k, int64_t b, int64_t chunk, int splits) {
     using Acc = typename PrecTraits<T>::acc;
-    __shared__ Acc red[4][64][NB];
+    constexpr int W = kThinWaves, RW = kThinRows;
+    __shared__ Acc red[W][64][NB];
+    __shared__ Acc xs[W][RW * NB];
     const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: X rows load once per wave
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int jg = blockIdx.x, sp = blockIdx.y;
     const int64_t j = (int64_t)jg * 64 + lane;
-    const int64_t i0 = (int64_t)sp * chunk;
-    const int64_t i1 = (i0 + chunk < n) ? i0 + chunk : n;
+    const int64_t jc = j < k ? j : k - 1;        // clamped column: loads stay inside V
+    const int64_t c0 = (int64_t)sp * chunk;
+    const int64_t c1 = (c0 + chunk < n) ? c0 + chunk : n;
+    const int64_t q = (c1 - c0 + W - 1) / W;     // rows of this wave's share
+    const int64_t i0 = c0 + wave * q;
+    const int64_t i1 = (i0 + q < c1) ? i0 + q : c1;
 
     Acc acc[NB];
 #pragma unroll
     for (int c = 0; c < NB; ++c) acc[c] = 0;
-    if (j < k) {
-        // rows i0 + wave + 4 rho in order, RB of them per batch: the batch's loads
-        // come from clamped rows and are issued together, the rows past the
-        // chunk add nothing
-        constexpr int RB = 16;
-        for (int64_t ib = i0 + wave; ib < i1; ib += 4 * RB) {
-            T v[RB], x[RB][NB];
+    for (int64_t ib = i0; ib < i1; ib += RW) {
+        const int rows = (int)((i1 - ib < RW) ? i1 - ib : RW);
+        T v[RW];
 #pragma unroll
-            for (int rho = 0; rho < RB; ++rho) {
-                const int64_t i = ib + 4 * rho;
-                const int64_t ic = i < i1 ? i : i1 - 1;
-                v[rho] = V[ic * k + j];
+        for (int r = 0; r < RW; ++r) v[r] = V[(ib + (r < rows ? r : rows - 1)) * k + jc];
+        // the batch's X values, rows ib .. ib + rows - 1 (rows * b contiguous values)
+        constexpr int XL = (RW * NB + 63) / 64;
+        Acc xv[XL];
 #pragma unroll
-                for (int c = 0; c < NB; ++c) x[rho][c] = X[ic * b + (c < b ? c : 0)];
-            }
+        for (int t = 0; t < XL; ++t) {
+            const int e = t * 64 + lane;                 // (row, column) = (e / NB, e % NB)
+            const int r = e / NB, c = e - r * NB;
+            xv[t] = (r < rows && c < b) ? to_acc(X[(ib + r) * b + c]) : Acc(0);
+        }
 #pragma unroll
-            for (int rho = 0; rho < RB; ++rho) {
-                if (ib + 4 * rho >= i1) break;
-                const Acc vij = to_acc(v[rho]);
+        for (int t = 0; t < XL; ++t)
+            if (t * 64 + lane < RW * NB) xs[wave][t * 64 + lane] = xv[t];
+        __builtin_amdgcn_wave_barrier();                 // LDS writes of this wave before its reads
 #pragma unroll
-                for (int c = 0; c < NB; ++c)
-                    if (c < b) acc[c] += vij * to_acc(x[rho][c]);
+        for (int r = 0; r < RW; ++r) {
+            if (r < rows) {   // predicated, so v[] stays in registers
+                const Acc vij = to_acc(v[r]);
+#pragma unroll
+                for (int c = 0; c < NB; ++c) acc[c] += vij * xs[wave][r * NB + c];
             }
         }
+        __builtin_amdgcn_wave_barrier();                 // reads done before the next batch's writes
     }
 #pragma unroll
     for (int c = 0; c < NB; ++c) red[wave][lane][c] = acc[c];
     __syncthreads();
     if (wave == 0) {
+        Acc* dst = part + (((int64_t)jg * splits + sp) * 64 + lane) * NB;
 #pragma unroll
         for (int c = 0; c < NB; ++c) {
-            const Acc t = ((red[0][lane][c] + red[1][lane][c]) + red[2][lane][c]) + red[3][lane][c];
-            part[(((int64_t)jg * splits + sp) * 64 + lane) * NB + c] = t;
+            Acc t = red[0][lane][c];
+#pragma unroll
+            for (int w = 1; w < W; ++w) t += red[w][lane][c];
+            dst[c] = t;
         }
     }
 }
 
-// One wave per output (j, c) of T'^T, including the zero rows j in [k, ldt):
-// lane l adds the split partials l, l + 64, ... in order, then a fixed
-// butterfly over the wave (one round of loads instead of a chain over all
-// splits per thread).
+// T'[j][c] = s_j * (sum of the chunk partials of (j, c) in chunk order):
+// one wave per output (j, c) of T'^T, including the zero rows j in [k, ldt),
+// lane l adding the partials l, l + 64, ... then a fixed butterfly.  Used
+// when the batch is wider than the phase-2 kernel folds in itself.
 template <typename T, int NB>
-__global__ __launch_bounds__(256) void k_p1_stream_finish(
+__global__ __launch_bounds__(256) void k_p1_thin_finish(
     const typename PrecTraits<T>::acc* __restrict__ part, const T* __restrict__ s, T* __restrict__ Tt,
     int64_t ldt, int64_t k, int64_t b, int splits) {
     using Acc = typename PrecTraits<T>::acc;
@@ -774,7 +879,7 @@ __global__ __launch_bounds__(256) void k_p1_stream_finish(
     if (jj < k) {
         const int64_t jg = jj / 64, jl = jj - jg * 64;
         const Acc* src = part + (jg * splits * 64 + jl) * NB + c;
-        for (int q = lane; q < splits; q += 64) sum += __builtin_nontemporal_load(src + (int64_t)q * 64 * NB);
+        for (int t = lane; t < splits; t += 64) sum += src[(int64_t)t * 64 * NB];
         sum = wave_sum(sum);
     }
     if (lane == 0) {
@@ -783,58 +888,96 @@ __global__ __launch_bounds__(256) void k_p1_stream_finish(
     }
 }
 
-// Phase 2, batch <= NB: T' staged in LDS (accumulation type); every wave
-// takes 4 rows of U at a time, lanes stride over j, and a butterfly sum
-// over the wave gives each output.
-template <typename T, int NB>
-__global__ __launch_bounds__(256) void k_p2_stream(
-    const T* __restrict__ U, const T* __restrict__ Tt, int64_t ldt, T* __restrict__ Y,
-    int64_t m, int64_t k, int64_t b) {
+// Phase 2 (k_p2_thin): every wave owns RPW rows of U; lanes stride over j.
+// The U loads of the first batch of column groups are issued first; then
+// T' (k x NB) is formed in LDS, either from T'^T or (FOLD) by adding the
+// chunk partials of phase 1 in chunk order and scaling by s -- the same sum
+// and order as k_p1_thin_finish, done by every workgroup instead of by a
+// third launch; then each lane multiplies its U values by T' from LDS, and a
+// fixed butterfly over the wave gives each output.
+template <typename T, int NB, bool FOLD>
+__global__ __launch_bounds__(256) void k_p2_thin(
+    const T* __restrict__ U, const T* __restrict__ Tt, int64_t ldt, const typename PrecTraits<T>::acc* __restrict__ part,
+    const T* __restrict__ s, int splits, T* __restrict__ Y, int64_t m, int64_t k, int64_t b) {
     using Acc = typename PrecTraits<T>::acc;
+    constexpr int RPW = 4, JB = 4;
     extern __shared__ double4_t smem_v[];
-    Acc* Ts = reinterpret_cast<Acc*>(smem_v);   // [k][NB]
+    Acc* ts = reinterpret_cast<Acc*>(smem_v);    // T'[j][c], k x NB
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t row0 = ((int64_t)blockIdx.x * 4 + wave) * RPW;
+    int64_t rows[RPW];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) rows[r] = (row0 + r < m) ? row0 + r : m - 1;   // clamped: loads stay inside U
+    T u[RPW][JB];
+    auto load_u = [&](int64_t jb) {
+#pragma unroll
+        for (int t = 0; t < JB; ++t) {
+            const int64_t jj = jb + 64 * t + lane;
+            const int64_t jc = jj < k ? jj : k - 1;
+#pragma unroll
+            for (int r = 0; r < RPW; ++r) u[r][t] = U[rows[r] * k + jc];
+        }
+    };
+    load_u(0);
     for (int64_t idx = tid; idx < k * NB; idx += 256) {
         const int64_t jj = idx / NB;
-        const int c = (int)(idx % NB);
-        Ts[idx] = (c < b) ? to_acc(Tt[(int64_t)c * ldt + jj]) : Acc(0);
+        const int c = (int)(idx - jj * NB);
+        Acc val = 0;
+        if (c < b) {
+            if constexpr (FOLD) {
+                const int64_t jg = jj / 64, jl = jj - jg * 64;
+                const Acc* src = part + (jg * splits * 64 + jl) * NB + c;
+                Acc sum = 0;
+                for (int t = 0; t < splits; t += 16) {   // 16 loads in flight, added in chunk order
+                    Acc pv[16];
+#pragma unroll
+                    for (int u = 0; u < 16; ++u) pv[u] = (t + u < splits) ? src[(int64_t)(t + u) * 64 * NB] : Acc(0);
+#pragma unroll
+                    for (int u = 0; u < 16; ++u) sum += pv[u];
+                }
+                val = to_acc(to_storage<T>(to_acc(s[jj]) * sum));   // T' as stored: rounded to T
+            } else {
+                val = to_acc(Tt[(int64_t)c * ldt + jj]);
+            }
+        }
+        ts[idx] = val;
     }
     __syncthreads();
-    constexpr int RPW = 4;
-    const int64_t row0 = ((int64_t)blockIdx.x * 4 + wave) * RPW;
     Acc acc[RPW][NB];
 #pragma unroll
-    for (int q = 0; q < RPW; ++q)
+    for (int r = 0; r < RPW; ++r)
 #pragma unroll
-        for (int c = 0; c < NB; ++c) acc[q][c] = 0;
-    for (int64_t jj = lane; jj < k; jj += 64) {
+        for (int c = 0; c < NB; ++c) acc[r][c] = 0;
+    for (int64_t jb = 0; jb < k; jb += 64 * JB) {
+        if (jb > 0) load_u(jb);
 #pragma unroll
-        for (int q = 0; q < RPW; ++q) {
-            const int64_t row = row0 + q;
-            if (row < m) {
-                const Acc u = to_acc(U[row * k + jj]);
+        for (int t = 0; t < JB; ++t) {
+            const int64_t jj = jb + 64 * t + lane;
+            if (jj < k) {
 #pragma unroll
-                for (int c = 0; c < NB; ++c) acc[q][c] += u * Ts[jj * NB + c];
+                for (int r = 0; r < RPW; ++r)
+#pragma unroll
+                    for (int c = 0; c < NB; ++c) acc[r][c] += to_acc(u[r][t]) * ts[jj * NB + c];
             }
         }
     }
 #pragma unroll
-    for (int q = 0; q < RPW; ++q)
+    for (int r = 0; r < RPW; ++r)
 #pragma unroll
-        for (int c = 0; c < NB; ++c) acc[q][c] = wave_sum(acc[q][c]);
-    if (lane == 0) {
+        for (int c = 0; c < NB; ++c) acc[r][c] = wave_sum(acc[r][c]);
+    // lane r * NB + c writes output (row0 + r, c)
 #pragma unroll
-        for (int q = 0; q < RPW; ++q) {
-            const int64_t row = row0 + q;
-            if (row < m)
-                for (int c = 0; c < NB && c < b; ++c) Y[row * b + c] = to_storage<T>(acc[q][c]);
-        }
-    }
+    for (int r = 0; r < RPW; ++r)
+#pragma unroll
+        for (int c = 0; c < NB; ++c)
+            if (lane == r * NB + c && row0 + r < m && c < b) Y[(row0 + r) * b + c] = to_storage<T>(acc[r][c]);
 }
 
 // ------------------------------------------------------------------- host --
 static constexpr int kStreamMaxBatch = 8;
-static constexpr int kStreamRowsTarget = 64;     // rows of V per workgroup chunk (phase 1)
+static constexpr int kStreamRowsTarget = kThinWaves * kThinRows;   // rows of V per phase-1 chunk
+static constexpr int kStreamMaxSplits = 32;
+static constexpr int kStreamFoldBatch = 2;       // phase 2 adds the chunk partials itself up to this batch
 
 static constexpr int64_t kBigTarget = 512;       // phase-1 workgroups aimed for (128 x 128 tiles)
 static constexpr int64_t kSmallTarget = 1024;    // same for 64 x 64 tiles
@@ -879,12 +1022,13 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
     ApplyPlan p{};
     if (path != 1 && path != 2) path = (b <= kStreamMaxBatch) ? 1 : 2;
     if (path == 1 && b > kStreamMaxBatch) path = 2;
-    // the streaming phase 2 stages T' (k x NB in the accumulation type) in
-    // LDS: ranks whose T' exceeds 64 KB take the matrix-core path
+    // the streaming phase 2 keeps T' (k x batch, accumulation type) in 64 KB
+    // of LDS: ranks whose T' does not fit take the matrix-core path
     if (path == 1) {
         const int64_t nb = (b <= 1) ? 1 : (b <= 2) ? 2 : (b <= 4) ? 4 : 8;
         if (k * nb * ((prec == P64) ? 8 : 4) > 65536) path = 2;
     }
+
     p.path = path;
     p.Kp = round_up(k, 8);
     const size_t acc_b = (prec == P64) ? 8 : 4;
@@ -892,7 +1036,7 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         p.tiles_m = (int)((k + 63) / 64);
         p.tiles_n = 1;
         int64_t splits = (n + kStreamRowsTarget - 1) / kStreamRowsTarget;
-        if (splits > 256) splits = 256;
+        if (splits > kStreamMaxSplits) splits = kStreamMaxSplits;
         if (splits < 1) splits = 1;
         p.chunk = (n + splits - 1) / splits;
         p.splits = (int)((n + p.chunk - 1) / p.chunk);
@@ -934,10 +1078,16 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
     }
     p.mid_bytes = (size_t)b * p.Kp * elem_bytes(prec);
     if (path == 2) {
+        // phase 2 over one column tile reads each row of U once: a misaligned U is
+        // then read in place; with more column tiles (and for phase 1's V and X)
+        // a padded copy made once per call is cheaper than shifting every load
+        const TileDims d2 = cfg_dims(prec, p.big2);
+        const bool u_bad = needs_stage(U, k, prec);
+        p.mis2 = (u_bad && b <= d2.bn) ? 1 : 0;
+        p.stage_u = (u_bad && !p.mis2) ? 1 : 0;
+        p.stage_v = needs_stage(V, k, prec) ? 1 : 0;
+        p.stage_x = needs_stage(X, b, prec) ? 1 : 0;
         p.ldx = round_up(b, 8);
-        p.stage_u = needs_stage(U, k, prec);
-        p.stage_v = needs_stage(V, k, prec);
-        p.stage_x = needs_stage(X, b, prec);
         const size_t e = elem_bytes(prec);
         p.stage_bytes = (p.stage_u ? round_up((size_t)m * p.Kp * e, 256) : 0) +
                         (p.stage_v ? round_up((size_t)n * p.Kp * e, 256) : 0) +
@@ -976,30 +1126,40 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     if (ws.overrun || !Tt) return hipErrorOutOfMemory;
     const int64_t ldt = p.Kp;
     if (p.path == 1) {
-        dim3 g1(p.tiles_m, p.splits);
+        const int nb = b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8;
+        const bool fold = b <= kStreamFoldBatch;
+        const dim3 g1(p.tiles_m, p.splits);
         {
             KernelTimer t1(p1_stream_label<T>(), stream);
-#define LRC_P1S(NB)                                                                                       \
-    do {                                                                                                  \
-        hipLaunchKernelGGL((k_p1_stream<T, NB>), g1, dim3(256), 0, stream, V, X, part, n, k, b, p.chunk,  \
-                           p.splits);                                                                     \
-        hipLaunchKernelGGL((k_p1_stream_finish<T, NB>), dim3((unsigned)((ldt * NB + 3) / 4)), dim3(256), 0, \
-                           stream, part, s, Tt, ldt, k, b, p.splits);                                     \
-    } while (0)
-            if (b <= 1) LRC_P1S(1); else if (b <= 2) LRC_P1S(2); else if (b <= 4) LRC_P1S(4); else LRC_P1S(8);
+#define LRC_P1S(NB)                                                                                            \
+    hipLaunchKernelGGL((k_p1_thin<T, NB>), g1, dim3(64 * kThinWaves), 0, stream, V, X, part, n, k, b, p.chunk, \
+                       p.splits)
+            if (nb == 1) LRC_P1S(1); else if (nb == 2) LRC_P1S(2); else if (nb == 4) LRC_P1S(4); else LRC_P1S(8);
 #undef LRC_P1S
+        }
+        if (!fold) {
+            KernelTimer tf(p1_finish_label<T>(), stream);
+            const dim3 gf((unsigned)((ldt * nb + 3) / 4));
+#define LRC_P1F(NB) \
+    hipLaunchKernelGGL((k_p1_thin_finish<T, NB>), gf, dim3(256), 0, stream, part, s, Tt, ldt, k, b, p.splits)
+            if (nb == 4) LRC_P1F(4); else LRC_P1F(8);
+#undef LRC_P1F
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t rows_per_wg = 16;
-        dim3 g2((unsigned)((m + rows_per_wg - 1) / rows_per_wg));
+        const dim3 g2((unsigned)((m + rows_per_wg - 1) / rows_per_wg));
+        const size_t lds = (size_t)k * nb * sizeof(Acc);
         KernelTimer t2(p2_stream_label<T>(), stream);
-#define LRC_P2S(NB) hipLaunchKernelGGL((k_p2_stream<T, NB>), g2, dim3(256), (size_t)k * NB * sizeof(Acc), stream, U, Tt, ldt, Y, m, k, b)
-        if (b <= 1) LRC_P2S(1); else if (b <= 2) LRC_P2S(2); else if (b <= 4) LRC_P2S(4); else LRC_P2S(8);
+#define LRC_P2S(NB, F)                                                                                       \
+    hipLaunchKernelGGL((k_p2_thin<T, NB, F>), g2, dim3(256), lds, stream, U, Tt, ldt, part, s, p.splits, Y, m, k, \
+                       b)
+        if (nb == 1) LRC_P2S(1, true); else if (nb == 2) LRC_P2S(2, true); else if (nb == 4) LRC_P2S(4, false);
+        else LRC_P2S(8, false);
 #undef LRC_P2S
         return hipGetLastError();
     }
-    // operands whose pitch or base rule out 16-byte moves go through a padded copy
+    // operands whose pitch or base rule out 16-byte moves, unless read in place
     const T *Ug = U, *Vg = V, *Xg = X;
     int64_t ldu = k, ldv = k, ldx = b;
     if (p.stage_u || p.stage_v || p.stage_x) {
@@ -1014,7 +1174,10 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
             J.cols[q] = cols;
             J.lds[q] = cols;
             J.cpr[q] = (int)(ldd / (16 / (int64_t)sizeof(T)));
-            J.end[q] = (q ? J.end[q - 1] : 0) + rows * J.cpr[q];
+            J.chunks[q] = rows * J.cpr[q];
+            int64_t nb = (J.chunks[q] + 255) / 256;
+            if (nb > 4096) nb = 4096;
+            J.bend[q] = (q ? J.bend[q - 1] : 0u) + (unsigned)nb;
             return d;
         };
         if (p.stage_u) {
@@ -1036,20 +1199,25 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
             ldx = p.ldx;
         }
         KernelTimer ts("apply_stage", stream);
-        int64_t g = (J.end[J.n - 1] + 255) / 256;
-        if (g > 16384) g = 16384;
-        hipLaunchKernelGGL(k_pitch_copy<T>, dim3((unsigned)(g < 1 ? 1 : g)), dim3(256), 0, stream, J);
+        const dim3 grid(J.bend[J.n - 1]);
+        bool small = true;
+        for (int q = 0; q < J.n; ++q) small = small && J.chunks[q] < ((int64_t)1 << 31);
+        if (small)
+            hipLaunchKernelGGL((k_pitch_copy<T, uint32_t>), grid, dim3(256), 0, stream, J);
+        else
+            hipLaunchKernelGGL((k_pitch_copy<T, int64_t>), grid, dim3(256), 0, stream, J);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
+    using Big = typename BigCfg<T>::C;
+    using Small = typename SmallCfg<T>::C;
+    const char *l1 = p1_mfma_label<T>(), *lf = p1_finish_label<T>();
     if (p.big1)
-        run_atb<T, typename BigCfg<T>::C, ATB_APPLY>(p1_mfma_label<T>(), p1_finish_label<T>(), stream, Vg, ldv, Xg,
-                                                     ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n, p.splits, part, s,
-                                                     (void*)Tt, ldt, ldt);
+        run_atb<T, Big, ATB_APPLY>(l1, lf, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n, p.splits,
+                                   part, s, (void*)Tt, ldt, ldt);
     else
-        run_atb<T, typename SmallCfg<T>::C, ATB_APPLY>(p1_mfma_label<T>(), p1_finish_label<T>(), stream, Vg, ldv,
-                                                       Xg, ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n, p.splits,
-                                                       part, s, (void*)Tt, ldt, ldt);
+        run_atb<T, Small, ATB_APPLY>(l1, lf, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n,
+                                     p.splits, part, s, (void*)Tt, ldt, ldt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     KernelTimer t2(p2_mfma_label<T>(), stream);
@@ -1057,14 +1225,15 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     const TileDims d2 = cfg_dims(PrecCode<T>::value, p.big2);
     const int tm = (int)((m + d2.bm - 1) / d2.bm), tn = (int)((b + d2.bn - 1) / d2.bn);
     const dim3 g2(xcd_grid(AbtOrder(tm, tn).total));
-    if (p.big2)
-        launch_abt<T, typename BigCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt, ldt,
-                                                        tm, tn, Y, b, vec16, (const double*)nullptr, (int64_t)0,
-                                                        (double*)nullptr);
-    else
-        launch_abt<T, typename SmallCfg<T>::C, ABT_STORE>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt,
-                                                          ldt, tm, tn, Y, b, vec16, (const double*)nullptr,
-                                                          (int64_t)0, (double*)nullptr);
+#define LRC_P2(CFG, MISV)                                                                                       \
+    launch_abt<T, CFG, ABT_STORE, MISV>(g2, stream, Ug, ldu, m, k, (const T*)Tt, ldt, b, ldt, ldt, tm, tn, Y, b,     \
+                                        vec16, (const double*)nullptr, (int64_t)0, (double*)nullptr)
+    if (p.big2) {
+        if (p.mis2) LRC_P2(Big, true); else LRC_P2(Big, false);
+    } else {
+        if (p.mis2) LRC_P2(Small, true); else LRC_P2(Small, false);
+    }
+#undef LRC_P2
     return hipGetLastError();
 }
 

@@ -52,7 +52,11 @@ struct ApplyPlan {
     int64_t chunk;       // rows of V / X per split
     int tiles_m, tiles_n;
     int big1, big2;      // 128 x 128 tiles (else 64 x 64) for phase 1 / phase 2
-    // operands copied to a padded pitch first (MFMA path): U, V with pitch Kp, X with ldx
+    // MFMA path, operands whose base or pitch rules out aligned 16-byte moves
+    // (odd ranks such as the compensated k + 1, odd batches): U is read in
+    // place by phase 2 when the batch fits one column tile (mis2); otherwise
+    // U, V (pitch Kp) and X (pitch ldx) are copied to a padded pitch first
+    int mis2;
     int stage_u, stage_v, stage_x;
     int64_t ldx;
     size_t stage_bytes;

@@ -54,6 +54,8 @@ def test_apply_path_dispatch():
     # the streaming path keeps T' (k x batch, accumulation type) in 64 KB of LDS
     assert lrc.apply_path(9000, 9000, 8192, 1, "fp64") == lrc.PATH_STREAM
     assert lrc.apply_path(9000, 9000, 8193, 1, "fp64") == lrc.PATH_MFMA
+    assert lrc.apply_path(9000, 9000, 2048, 8, "fp32") == lrc.PATH_STREAM
+    assert lrc.apply_path(9000, 9000, 2049, 8, "fp32") == lrc.PATH_MFMA
     assert L.lrc_set_apply_path(3) == -1
     assert L.lrc_set_apply_path(0) == 0
 
