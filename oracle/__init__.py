@@ -24,7 +24,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liblrc_oracle.so")
+# LRC_ORACLE_LIBRARY selects another build of the same C file (the sanitizer build)
+_LIB_PATH = os.environ.get("LRC_ORACLE_LIBRARY") or os.path.join(_HERE, "liblrc_oracle.so")
 _lib = None
 
 PRECS = ("fp64", "fp32", "fp16")

@@ -29,15 +29,25 @@ def flags():
             "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 
-def build(verbose: bool = False, jobs: int = 4) -> str:
-    objdir = os.path.join(ROOT, "_build")
+# AddressSanitizer and UndefinedBehaviorSanitizer for the host code only (the
+# device code is built as usual): each -fsanitize= sits behind -Xarch_host.
+SAN_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+SAN_DIR = os.path.join(ROOT, "_build", "san")
+
+
+def build(verbose: bool = False, jobs: int = 4, sanitize: bool = False) -> str:
+    """Compile liblrc.so in-tree; with sanitize=True a host-sanitized copy
+    goes to _build/san/liblrc.so instead (load it with LRC_LIBRARY and the
+    clang ASan runtime preloaded)."""
+    objdir = SAN_DIR if sanitize else os.path.join(ROOT, "_build")
     os.makedirs(objdir, exist_ok=True)
     procs, objs = [], []
     for src in SOURCES:
         obj = os.path.join(objdir, src + ".o")
         objs.append(obj)
         lang = ["-x", "hip"] if src.endswith(".cpp") else []
-        cmd = [HIPCC] + flags() + lang + ["-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC] + flags() + (SAN_HOST if sanitize else []) + lang + ["-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stderr=subprocess.PIPE, stdout=subprocess.PIPE, text=True)))
@@ -45,13 +55,16 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
             _wait(procs.pop(0), verbose)
     while procs:
         _wait(procs.pop(0), verbose)
-    tmp = LIB + ".tmp"
+    lib = os.path.join(SAN_DIR, "liblrc.so") if sanitize else LIB
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs
+    if sanitize:
+        cmd += ["-fsanitize=address,undefined", "-shared-libasan"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 def _wait(item, verbose):

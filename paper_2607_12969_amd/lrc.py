@@ -17,7 +17,8 @@ import os
 import re
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liblrc.so")
+# LRC_LIBRARY selects another build of the same sources (the host-sanitized build)
+LIB_PATH = os.environ.get("LRC_LIBRARY") or os.path.join(HERE, "liblrc.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "lrc.h")
 
 FP64, FP32, FP16 = 0, 1, 2
