@@ -27,6 +27,7 @@ small configurations).
   python bench.py --grid FILE       the paper's resident timing grid on synthetic stand-ins
   python bench.py --fixed-memory FILE   fixed-memory comparison on hyperspectral-shaped stand-ins
   python bench.py --factor FILE         randomized FP64 SVD / TT-SVD cells
+  python bench.py --report FILE.jsonl   markdown tables from the records the sweeps write beside FILE
 """
 from __future__ import annotations
 
@@ -387,17 +388,50 @@ def _time_cell(lrc, fn, reps, labels):
     return wall, {lab: kt[lab][1] / kt[lab][0] for lab in kt}
 
 
-def _row(name, p, kernels_ms, wall_ms, f, by):
+ENV_KNOBS = ("LRC_APPLY_TILE", "LRC_TT_WAVE", "LRC_TT_WAVE_NPB", "LRC_TT_P", "LRC_TT_WGS")
+
+
+def env_knobs():
+    """The library's tuning overrides as set for this run (None = default)."""
+    return {k: os.environ.get(k) for k in ENV_KNOBS}
+
+
+def write_records(path, records):
+    """One JSON object per line: the machine-readable twin of a table."""
+    with open(path, "w") as fh:
+        for r in records:
+            fh.write(json.dumps(r, sort_keys=True) + "\n")
+
+
+def read_records(path):
+    with open(path) as fh:
+        return [json.loads(line) for line in fh if line.strip()]
+
+
+def _record(task, method, p, kernels_ms, wall_ms, f, by, **shape):
+    """One sweep cell: algorithmic counts, the roofline of the cell and its
+    measured times.  Parity is the tests' business (the bench never calls
+    the oracle outside its CPU baseline), so parity_error stays null."""
     ai = f / by
     ridge = PEAK_TFLOPS[p] * 1e12 / (PEAK_HBM_GBS * 1e9)
     kern = sum(kernels_ms.values())
-    gfl, gbs = f / kern / 1e6, by / kern / 1e6
-    bound = "mfma" if ai > ridge else "hbm"
     t_star = max(by / (PEAK_HBM_GBS * 1e9), f / (PEAK_TFLOPS[p] * 1e12)) * 1e3
-    frac = t_star / kern
-    ks = ", ".join(f"{k} {v * 1e3:.1f}" for k, v in kernels_ms.items())
-    return (f"| {name} | {p} | {f / 1e9:.3f} | {by / 1e6:.1f} | {ai:.1f} | {bound} | {t_star * 1e3:.1f} | "
-            f"{kern * 1e3:.1f} | {wall_ms * 1e3:.1f} | {gfl:.0f} | {gbs:.0f} | {frac:.3f} | {ks} |")
+    return dict(task=task, method=method, prec=p, **shape, flop=f, bytes=by, intensity=ai,
+                bound="mfma" if ai > ridge else "hbm", t_star_ms=t_star, kernels_ms=kern, call_ms=wall_ms,
+                gflops=f / kern / 1e6, gbs=by / kern / 1e6, frac=t_star / kern,
+                per_kernel_ms=dict(kernels_ms), counter_bytes=None, parity_error=None, certificate=None,
+                env=env_knobs())
+
+
+SWEEP_HEAD = ["| cell | prec | GFLOP | MB | flop/B | bound | t* us | kernels us | call us | GFLOP/s | GB/s | "
+              "frac of bound | per kernel (us) |", "|" + "---|" * 13]
+
+
+def render_sweep_row(r):
+    ks = ", ".join(f"{k} {v * 1e3:.1f}" for k, v in r["per_kernel_ms"].items())
+    return (f"| {r['task']} | {r['prec']} | {r['flop'] / 1e9:.3f} | {r['bytes'] / 1e6:.1f} | {r['intensity']:.1f} | "
+            f"{r['bound']} | {r['t_star_ms'] * 1e3:.1f} | {r['kernels_ms'] * 1e3:.1f} | {r['call_ms'] * 1e3:.1f} | "
+            f"{r['gflops']:.0f} | {r['gbs']:.0f} | {r['frac']:.3f} | {ks} |")
 
 
 def sweep(path, dev, lrc):
@@ -406,8 +440,7 @@ def sweep(path, dev, lrc):
     copies that consecutive calls do not hit the 256 MB Infinity Cache."""
     import torch
     from paper_2607_12969_amd import synth
-    rows = ["| cell | prec | GFLOP | MB | flop/B | bound | t* us | kernels us | call us | GFLOP/s | GB/s | "
-            "frac of bound | per kernel (us) |", "|" + "---|" * 13]
+    records = []
 
     def rotated(host_arrays, out_shape, dtype, bytes_per_call):
         copies = max(1, min(8, math.ceil(512e6 / max(bytes_per_call, 1))))
@@ -437,8 +470,9 @@ def sweep(path, dev, lrc):
                     reps = max(10, min(200, int(2e10 / max(f, 1))))
                     wall, km = _time_cell(lrc, lambda r: lrc.matrix_apply(*sets[r % len(sets)][0],
                                                                           Y=sets[r % len(sets)][1]), reps, None)
-                    rows.append(_row(f"apply {name} k={kk} b={b}", p, km, wall, f, by))
-                    log(rows[-1])
+                    records.append(_record(f"apply {name} k={kk} b={b}", "apply", p, km, wall, f, by,
+                                           config=name, m=m, n=n, k=kk, batch=b))
+                    log(render_sweep_row(records[-1]))
                     del sets
                     torch.cuda.empty_cache()
     tts = [("256^3 r(15,15)", (256, 256, 256), (15, 15), (15, 15)),
@@ -456,12 +490,14 @@ def sweep(path, dev, lrc):
             reps = max(10, min(200, int(5e9 / max(f, 1))))
             wall, km = _time_cell(lrc, lambda r: lrc.tt_reconstruct(sets[r % len(sets)][0], out=sets[r % len(sets)][1]),
                                   reps, None)
-            rows.append(_row(f"tt {name} ranks={ranks[1:-1]}", p, km, wall, f, by))
-            log(rows[-1])
+            records.append(_record(f"tt {name} ranks={ranks[1:-1]}", "tt", p, km, wall, f, by,
+                                   config=name, dims=list(dims), ranks=ranks))
+            log(render_sweep_row(records[-1]))
             del sets
             torch.cuda.empty_cache()
+    write_records(os.path.splitext(path)[0] + ".jsonl", records)
     with open(path, "w") as fh:
-        fh.write("\n".join(rows) + "\n")
+        fh.write("\n".join(SWEEP_HEAD + [render_sweep_row(r) for r in records]) + "\n")
 
 
 def quant_sweep(path, dev, lrc):
@@ -471,8 +507,7 @@ def quant_sweep(path, dev, lrc):
     is the call's)."""
     import torch
     from paper_2607_12969_amd import synth
-    rows = ["| cell | prec | GFLOP | MB | flop/B | bound | t* us | kernels us | call us | GFLOP/s | GB/s | "
-            "frac of bound | per kernel (us) |", "|" + "---|" * 13]
+    records = []
     rng = np.random.default_rng([12969, 98])
     for name, (m, n, k) in (("factors 8192x8192 k=257", (8192, 8192, 257)),
                             ("factors 65536x4096 k=513", (65536, 4096, 513))):
@@ -489,9 +524,9 @@ def quant_sweep(path, dev, lrc):
                     lrc.round_to(x, p.replace("f", "fp"), out=y)
             wall, km = _time_cell(lrc, call, 50, None)
             km = {k2: v * 2 for k2, v in km.items()}   # two launches (U and V) per call
-            rows.append(_row(f"round {name}", p, km, wall, max(f, 1.0), by).replace(
-                f"| {p} | 0.000 |", f"| {p} | 0 |"))
-            log(rows[-1])
+            records.append(_record(f"round {name}", "round", p, km, wall, max(f, 1.0), by,
+                                   config=name, m=m, n=n, k=k))
+            log(render_sweep_row(records[-1]))
             del sets
             torch.cuda.empty_cache()
     for name, dims, ranks in (("256^3 r(15,15)", (256, 256, 256), (1, 15, 15, 1)),
@@ -503,8 +538,9 @@ def quant_sweep(path, dev, lrc):
         f, by = gauge_counts(dims, ranks)
         wall, km = _time_cell(lrc, lambda r: lrc.tt_left_orthogonalize(cores), 10, None)
         km = {"gauge_qr_f64": km["gauge_qr_f64"] * (len(dims) - 1)}   # one timed span per unfolding
-        rows.append(_row(f"gauge {name}", "f64", km, wall, f, by))
-        log(rows[-1])
+        records.append(_record(f"gauge {name}", "gauge", "f64", km, wall, f, by, config=name, dims=list(dims),
+                               ranks=list(ranks)))
+        log(render_sweep_row(records[-1]))
     # quality measures of a reconstruction against its reference: two passes
     # over the FP64 pair (band sums, spectral angles), 32 bytes per entry
     for name, dims in (("512x512x224", (512, 512, 224)), ("512x217x204", (512, 217, 204))):
@@ -514,12 +550,14 @@ def quant_sweep(path, dev, lrc):
         X = torch.from_numpy(Xh_).to(dev)
         Y = X * 1.001
         wall, km = _time_cell(lrc, lambda r: lrc.band_quality(X, Y), 10, None)
-        rows.append(_row(f"quality {name} (dense FP64 pair)", "f64", km, wall, 10.0 * N, 32.0 * N))
-        log(rows[-1])
+        records.append(_record(f"quality {name} (dense FP64 pair)", "quality", "f64", km, wall, 10.0 * N, 32.0 * N,
+                               config=name, dims=list(dims)))
+        log(render_sweep_row(records[-1]))
         del X, Y
         torch.cuda.empty_cache()
+    write_records(os.path.splitext(path)[0] + ".jsonl", records)
     with open(path, "w") as fh:
-        fh.write("\n".join(rows) + "\n")
+        fh.write("\n".join(SWEEP_HEAD + [render_sweep_row(r) for r in records]) + "\n")
 
 
 def factor_sweep(path, dev, lrc):
@@ -686,9 +724,26 @@ def _geo_ci(values, n_boot=10000, seed=0):
     return float(np.exp(v.mean())), float(np.percentile(boots, 2.5)), float(np.percentile(boots, 97.5))
 
 
+def _median_ci(values, n_boot=2000, seed=0):
+    """Bootstrap 95% interval of the median of a task's block medians."""
+    v = np.asarray(values, dtype=np.float64)
+    rng = np.random.default_rng([12969, 79, seed])
+    meds = np.median(v[rng.integers(0, v.size, (n_boot, v.size))], axis=1)
+    return [float(np.percentile(meds, 2.5)), float(np.percentile(meds, 97.5))]
+
+
+def _grid_record(task, method, p, med, bmed, ratio, storage, f, by, **shape):
+    t_star = max(by / (PEAK_HBM_GBS * 1e9), f / (PEAK_TFLOPS[p] * 1e12)) * 1e3
+    return dict(task=task, method=method, prec=p, **shape, median_ms=med, ci95_ms=_median_ci(bmed),
+                speedup_vs_fp64=ratio, storage_vs_fp64=storage, flop=f, bytes=by, t_star_ms=t_star,
+                gflops=f / med / 1e6, gbs=by / med / 1e6, frac=t_star / med, counter_bytes=None,
+                parity_error=None, certificate=None, env=env_knobs())
+
+
 def grid(path, dev, lrc):
     import torch
     from paper_2607_12969_amd import synth
+    records = []
     out = ["# The paper's resident timing grid on one MI355X (synthetic stand-ins)", "",
            "Command: `python -u bench.py --grid FILE`. Inputs resident in HBM and reused across calls (the",
            "paper's resident protocol, so small tasks run from the Infinity Cache); per task 30 warmups, then",
@@ -722,6 +777,9 @@ def grid(path, dev, lrc):
                 per_method[name][0].append(med[i])
                 per_method[name][1].append(ratio)
                 per_method[name][2].append((k0 + inc) * (m + n + 1) * EBYTES[p] / base_bytes)
+                f, by = apply_counts(m, n, k0 + inc, b, EBYTES[p])
+                records.append(_grid_record(f"apply {m}x{n} b={b}", name, p, med[i], bm[i], ratio,
+                                            per_method[name][2][-1], f, by, m=m, n=n, k=k0 + inc, batch=b))
             rows.append(f"| {m}x{n} | " + " | ".join(f"{med[i] * 1e3:.1f}" for i in range(len(GRID_METHODS))) + " |")
             log(f"grid apply b={b} {m}x{n}: " + rows[-1])
             del bufs, calls
@@ -757,6 +815,9 @@ def grid(path, dev, lrc):
             per_method[name][1].append(ratio)
             per_method[name][2].append(sum(ranks[l] * dims[l] * ranks[l + 1] for l in range(len(dims)))
                                        * EBYTES[p] / base_bytes)
+            f, by = tt_counts(list(dims), ranks, EBYTES[p])
+            records.append(_grid_record(f"tt {label}", name, p, med[i], bm[i], ratio, per_method[name][2][-1],
+                                        f, by, dims=list(dims), ranks=ranks))
         rows.append(f"| {label} {rb}->{ra} | " + " | ".join(f"{med[i] * 1e3:.1f}" for i in range(len(GRID_METHODS)))
                     + " |")
         log("grid tt: " + rows[-1])
@@ -772,6 +833,7 @@ def grid(path, dev, lrc):
         out.append(f"| {name} | {_geo_ci(tm)[0]:.4f} | {g:.2f} [{lo:.2f}, {hi:.2f}] | {np.mean(sto):.4f} |")
     out += ["", "| task | " + " | ".join(n for n, _, _ in GRID_METHODS) + " |",
             "|---|" + "---|" * len(GRID_METHODS)] + rows + [""]
+    write_records(os.path.splitext(path)[0] + ".jsonl", records)
     with open(path, "w") as fh:
         fh.write("\n".join(out) + "\n")
 
@@ -829,6 +891,30 @@ def fixed_memory(path, dev, lrc):
         fh.write("\n".join(out) + "\n")
 
 
+# ---------------------------------------------------------------- report ---
+
+def render_report(records):
+    """Markdown tables from JSONL records: sweep cells (kernel-timed) and
+    grid cells (median per call with its interval) each in their own table."""
+    cells = [r for r in records if "kernels_ms" in r]
+    grid_rows = [r for r in records if "median_ms" in r]
+    out = []
+    if cells:
+        out += SWEEP_HEAD + [render_sweep_row(r) for r in cells] + [""]
+    if grid_rows:
+        out += ["| task | method | prec | median us [95% CI] | speedup vs FP64 | storage | GFLOP/s | GB/s | "
+                "frac of bound |", "|" + "---|" * 9]
+        for r in grid_rows:
+            lo, hi = r["ci95_ms"]
+            out.append(f"| {r['task']} | {r['method']} | {r['prec']} | {r['median_ms'] * 1e3:.1f} "
+                       f"[{lo * 1e3:.1f}, {hi * 1e3:.1f}] | {r['speedup_vs_fp64']:.2f} | {r['storage_vs_fp64']:.4f} | "
+                       f"{r['gflops']:.0f} | {r['gbs']:.0f} | {r['frac']:.3f} |")
+        out.append("")
+    knobs = sorted({json.dumps(r.get("env", {}), sort_keys=True) for r in records})
+    out += ["Tuning overrides in effect: " + "; ".join(knobs)]
+    return "\n".join(out) + "\n"
+
+
 # ------------------------------------------------------------------ main ---
 
 def main():
@@ -846,7 +932,11 @@ def main():
     ap.add_argument("--fixed-memory", default=None, help="write the fixed-memory comparison (synthetic stand-ins)")
     ap.add_argument("--factor", default=None, help="write the randomized FP64 factorization cells")
     ap.add_argument("--copy-calibration", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
+    ap.add_argument("--report", default=None, help="render the markdown tables of a .jsonl record file (no GPU)")
     args = ap.parse_args()
+    if args.report:
+        sys.stdout.write(render_report(read_records(args.report)))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "bench.py runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
