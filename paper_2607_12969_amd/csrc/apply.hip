@@ -447,6 +447,7 @@ __device__ __forceinline__ void atb_store(const typename C::AccV& a, int tid, in
 //              factor 1 when s is null),
 //              written for m < Mout (zero padding rows included).
 //   ATB_GRAM : out is G[m][ldo] in double (T = double).
+// MIS: A has a misaligned base or pitch and is read in place; B is aligned.
 template <typename T, class C, int MODE, bool MIS = false>
 __global__ __launch_bounds__(C::NT) void k_atb(
     const T* __restrict__ Asrc, int64_t lda, const T* __restrict__ Bsrc, int64_t ldb,
@@ -478,9 +479,9 @@ __global__ __launch_bounds__(C::NT) void k_atb(
         for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = zero_accv<AccV>();
 
     using TA = RowsTile<C, C::BM, T, MIS>;
-    using TB = RowsTile<C, C::BN, T, MIS>;
+    using TB = RowsTile<C, C::BN, T>;   // X (or the certificate's factor): aligned rows
     const typename TA::Geo ga = TA::geo(Asrc, lda, m0, M, tid, Asrc + (K - 1) * lda + (M - 1));
-    const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid, Bsrc + (K - 1) * ldb + (N - 1));
+    const typename TB::Geo gb = TB::geo(Bsrc, ldb, n0, N, tid);
     TA ta[2];
     TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
@@ -516,33 +517,49 @@ __global__ __launch_bounds__(C::NT) void k_atb(
             atb_store<T, C, MODE>(acc[fn][fm], tid, fn, fm, m0, n0, M, N, svals, out, ldo, Mout);
 }
 
-// Sum of the split partials of k_atb, in split order, then the same store.
-// One workgroup per (tile, fragment); thread t holds the vector that thread
-// t of the tile's workgroups produced.
+// Sum of the split partials of k_atb, then the same store.  Workgroup
+// (tile, fragment, slice) owns 64 consecutive thread positions of the tile's
+// workgroups; its eight waves add eight consecutive runs of splits (each in
+// split order, 16 loads in flight) and wave 0 adds the run sums in run
+// order: a fixed order, with an eighth of the serial load chain.
+constexpr int kFinishRuns = 8;
+
 template <typename T, class C, int MODE>
-__global__ __launch_bounds__(C::NT) void k_atb_finish(
+__global__ __launch_bounds__(64 * kFinishRuns) void k_atb_finish(
     const typename C::AccV* __restrict__ part, int64_t M, int64_t N, int tiles_m, int splits,
     const T* __restrict__ svals, void* __restrict__ out, int64_t ldo, int64_t Mout) {
     using AccV = typename C::AccV;
-    constexpr int NF = C::FN * C::FM;
-    const int tid = threadIdx.x;
-    const int64_t tile = blockIdx.x / NF;
-    const int f = blockIdx.x % NF;
+    constexpr int NF = C::FN * C::FM, PQ = C::NT / 64;
+    __shared__ AccV red[kFinishRuns][64];
+    const int pl = threadIdx.x & 63;
+    const int run = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t tile = blockIdx.x / (NF * PQ);
+    const int f = (int)((blockIdx.x / PQ) % NF);
+    const int pos = (int)(blockIdx.x % PQ) * 64 + pl;    // thread of the producing workgroup
     if (MODE == ATB_GRAM && tile % tiles_m > tile / tiles_m) return;   // below the diagonal
-    const AccV* src = part + (tile * splits * NF + f) * C::NT + tid;
+    const AccV* src = part + (tile * splits * NF + f) * C::NT + pos;
     const int64_t qs = (int64_t)NF * C::NT;      // stride between splits
+    const int per = (splits + kFinishRuns - 1) / kFinishRuns;
+    const int q0 = run * per < splits ? run * per : splits;
+    const int q1 = q0 + per < splits ? q0 + per : splits;
     AccV acc = zero_accv<AccV>();
-    int q = 0;
-    for (; q + 8 <= splits; q += 8) {   // eight partials fetched at a time, added in split order
-        AccV pv[8];
+    int q = q0;
+    for (; q + 16 <= q1; q += 16) {
+        AccV pv[16];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) pv[u] = __builtin_nontemporal_load(src + (q + u) * qs);
+        for (int u = 0; u < 16; ++u) pv[u] = __builtin_nontemporal_load(src + (q + u) * qs);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) acc += pv[u];
+        for (int u = 0; u < 16; ++u) acc += pv[u];
     }
-    for (; q < splits; ++q) acc += __builtin_nontemporal_load(src + q * qs);
+    for (; q < q1; ++q) acc += __builtin_nontemporal_load(src + q * qs);
+    red[run][pl] = acc;
+    __syncthreads();
+    if (run != 0) return;
+    AccV sum = red[0][pl];
+#pragma unroll
+    for (int r = 1; r < kFinishRuns; ++r) sum += red[r][pl];
     const int64_t m0 = (tile % tiles_m) * C::BM, n0 = (tile / tiles_m) * C::BN;
-    atb_store<T, C, MODE>(acc, tid, f / C::FM, f % C::FM, m0, n0, M, N, svals, out, ldo, Mout);
+    atb_store<T, C, MODE>(sum, pos, f / C::FM, f % C::FM, m0, n0, M, N, svals, out, ldo, Mout);
 }
 
 enum { ABT_STORE = 0, ABT_ERR = 1 };
@@ -721,8 +738,8 @@ static void run_atb(const char* label, const char* finish_label, hipStream_t st,
     }
     if (splits > 1) {
         KernelTimer t(finish_label, st);
-        const dim3 grid((unsigned)((int64_t)tiles_m * tiles_n * C::FN * C::FM));
-        hipLaunchKernelGGL((k_atb_finish<T, C, MODE>), grid, dim3(C::NT), 0, st,
+        const dim3 grid((unsigned)((int64_t)tiles_m * tiles_n * C::FN * C::FM * (C::NT / 64)));
+        hipLaunchKernelGGL((k_atb_finish<T, C, MODE>), grid, dim3(64 * kFinishRuns), 0, st,
                            reinterpret_cast<const typename C::AccV*>(part), M, N, tiles_m, splits, svals, out, ldo,
                            Mout);
     }
@@ -979,8 +996,11 @@ static constexpr int kStreamRowsTarget = kThinWaves * kThinRows;   // rows of V 
 static constexpr int kStreamMaxSplits = 32;
 static constexpr int kStreamFoldBatch = 2;       // phase 2 adds the chunk partials itself up to this batch
 
+static constexpr size_t kInPlaceBytes = (size_t)16 << 20;  // shifted-load budget of an in-place factor
 static constexpr int64_t kBigTarget = 512;       // phase-1 workgroups aimed for (128 x 128 tiles)
 static constexpr int64_t kSmallTarget = 1024;    // same for 64 x 64 tiles
+static constexpr int64_t kFewTiles = 16;         // phase-1 outputs of fewer tiles than this ...
+static constexpr int64_t kFewTarget = 256;       // ... aim for this many workgroups
 
 // LRC_APPLY_TILE=64 or 128 pins the MFMA tile edge of both phases (tuning aid).
 static int forced_tile() {
@@ -1059,11 +1079,16 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         p.tiles_m = (int)((k + d1.bm - 1) / d1.bm);
         p.tiles_n = (int)((b + d1.bn - 1) / d1.bn);
         const int64_t base = (int64_t)p.tiles_m * p.tiles_n;
-        const int64_t target = p.big1 ? kBigTarget : kSmallTarget;
+        // Outputs of many tiles: about kBigTarget / kSmallTarget workgroups
+        // with at least 16 K steps per split (more splits only lengthen the
+        // finish's sums).  Outputs of a few tiles (small k x batch): about one
+        // workgroup per compute unit with at least 4 K steps each, so that
+        // the few tiles still spread over the chip; the finish adds the
+        // partials in eight parallel runs.
+        const bool few = base < kFewTiles;
+        const int64_t target = few ? kFewTarget : p.big1 ? kBigTarget : kSmallTarget;
         int64_t splits = (target + base - 1) / base;
-        // at least 16 K steps per split: with few tiles, more splits only
-        // lengthen the finish kernel's sums
-        int64_t max_splits = n / (16 * BK);
+        int64_t max_splits = n / ((few ? 4 : 16) * BK);
         if (max_splits < 1) max_splits = 1;
         if (splits > max_splits) splits = max_splits;
         if (splits < 1) splits = 1;
@@ -1078,17 +1103,24 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
     }
     p.mid_bytes = (size_t)b * p.Kp * elem_bytes(prec);
     if (path == 2) {
-        // phase 2 over one column tile reads each row of U once: a misaligned U is
-        // then read in place; with more column tiles (and for phase 1's V and X)
-        // a padded copy made once per call is cheaper than shifting every load
-        const TileDims d2 = cfg_dims(prec, p.big2);
-        const bool u_bad = needs_stage(U, k, prec);
-        p.mis2 = (u_bad && b <= d2.bn) ? 1 : 0;
+        // A misaligned factor is read in place (two aligned loads and a shift
+        // per chunk) when the shifted loads add up to little: the factor's
+        // bytes times the column tiles that read it at most kInPlaceBytes
+        // (a single column tile reads each element once).  Then the copy's
+        // extra launch costs more than the shifts; otherwise the factor is
+        // copied to a padded pitch once per call (measured at 8192 x 8192,
+        // batch 4096: in place, phases 1 and 2 each lose 15-25 %, more than
+        // the copy costs).  A misaligned X is always copied.
+        const TileDims d1 = cfg_dims(prec, p.big1), d2 = cfg_dims(prec, p.big2);
+        const size_t e = elem_bytes(prec);
+        const bool u_bad = needs_stage(U, k, prec), v_bad = needs_stage(V, k, prec);
+        const size_t reads1 = (size_t)((b + d1.bn - 1) / d1.bn), reads2 = (size_t)((b + d2.bn - 1) / d2.bn);
+        p.mis1 = (v_bad && (reads1 <= 1 || (size_t)n * k * e * reads1 <= kInPlaceBytes)) ? 1 : 0;
+        p.mis2 = (u_bad && (reads2 <= 1 || (size_t)m * k * e * reads2 <= kInPlaceBytes)) ? 1 : 0;
         p.stage_u = (u_bad && !p.mis2) ? 1 : 0;
-        p.stage_v = needs_stage(V, k, prec) ? 1 : 0;
+        p.stage_v = (v_bad && !p.mis1) ? 1 : 0;
         p.stage_x = needs_stage(X, b, prec) ? 1 : 0;
         p.ldx = round_up(b, 8);
-        const size_t e = elem_bytes(prec);
         p.stage_bytes = (p.stage_u ? round_up((size_t)m * p.Kp * e, 256) : 0) +
                         (p.stage_v ? round_up((size_t)n * p.Kp * e, 256) : 0) +
                         (p.stage_x ? round_up((size_t)n * p.ldx * e, 256) : 0);
@@ -1212,12 +1244,15 @@ static hipError_t apply_typed(const ApplyPlan& p, const T* U, const T* s, const 
     using Big = typename BigCfg<T>::C;
     using Small = typename SmallCfg<T>::C;
     const char *l1 = p1_mfma_label<T>(), *lf = p1_finish_label<T>();
-    if (p.big1)
-        run_atb<T, Big, ATB_APPLY>(l1, lf, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n, p.splits,
-                                   part, s, (void*)Tt, ldt, ldt);
-    else
-        run_atb<T, Small, ATB_APPLY>(l1, lf, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n,
-                                     p.splits, part, s, (void*)Tt, ldt, ldt);
+#define LRC_P1(CFG, MISV)                                                                                        \
+    run_atb<T, CFG, ATB_APPLY, MISV>(l1, lf, stream, Vg, ldv, Xg, ldx, k, b, n, p.chunk, p.tiles_m, p.tiles_n,     \
+                                     p.splits, part, s, (void*)Tt, ldt, ldt)
+    if (p.big1) {
+        if (p.mis1) LRC_P1(Big, true); else LRC_P1(Big, false);
+    } else {
+        if (p.mis1) LRC_P1(Small, true); else LRC_P1(Small, false);
+    }
+#undef LRC_P1
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     KernelTimer t2(p2_mfma_label<T>(), stream);
@@ -1417,9 +1452,10 @@ static hipError_t gemm_nt_typed(const double* W, int64_t ldw, int64_t nw, const 
     KernelTimer t(label, stream);
     hipLaunchKernelGGL(k_abt_part<C>, dim3(xcd_grid((int64_t)tm * tn * sp)), dim3(C::NT), 0, stream, W, ldw, nw, A,
                        lda, rows, K, ch, tm, tn, sp, part);
-    hipLaunchKernelGGL((k_atb_finish<double, C, ATB_APPLY>), dim3((unsigned)((int64_t)tm * tn * C::FN * C::FM)),
-                       dim3(C::NT), 0, stream, reinterpret_cast<const typename C::AccV*>(part), nw, rows, tm, sp, svals,
-                       (void*)out, ldo, mout);
+    hipLaunchKernelGGL((k_atb_finish<double, C, ATB_APPLY>),
+                       dim3((unsigned)((int64_t)tm * tn * C::FN * C::FM * (C::NT / 64))), dim3(64 * kFinishRuns), 0,
+                       stream, reinterpret_cast<const typename C::AccV*>(part), nw, rows, tm, sp, svals, (void*)out,
+                       ldo, mout);
     return hipGetLastError();
 }
 

@@ -53,10 +53,11 @@ struct ApplyPlan {
     int tiles_m, tiles_n;
     int big1, big2;      // 128 x 128 tiles (else 64 x 64) for phase 1 / phase 2
     // MFMA path, operands whose base or pitch rules out aligned 16-byte moves
-    // (odd ranks such as the compensated k + 1, odd batches): U is read in
-    // place by phase 2 when the batch fits one column tile (mis2); otherwise
-    // U, V (pitch Kp) and X (pitch ldx) are copied to a padded pitch first
-    int mis2;
+    // (odd ranks such as the compensated k + 1, odd batches): V (phase 1,
+    // mis1) and U (phase 2, mis2) are read in place when they are small or
+    // read by a single tile of the other dimension; otherwise U, V (pitch Kp)
+    // and X (pitch ldx) are copied to a padded pitch first
+    int mis1, mis2;
     int stage_u, stage_v, stage_x;
     int64_t ldx;
     size_t stage_bytes;

@@ -59,6 +59,7 @@ struct TTArgs {
     TTSet set[kTTMaxSets];
     void* out;
     int vec4;
+    int vec8;                // FP16 rows of n_last take aligned 16-byte stores (n_last % 8 == 0)
     int lines;               // output rows start on 128-byte lines (n_last * sizeof(T) % 128 == 0)
     int ifast;               // wave tiles: consecutive tiles take consecutive middle indices
 };
@@ -113,6 +114,97 @@ __global__ __launch_bounds__(256) void k_stage(const T* __restrict__ gmid, const
             srows[(int64_t)j] = sc < r1 ? g1[(int64_t)L * r1 + sc] : T(0);
         }
     }
+}
+
+// The same staging for the FP16 wave tiles (K-contiguous layouts, Rt and
+// Kp3 at most 96, Kp2 and ncp multiples of 32), transposed through LDS so
+// that the global reads run along each core's contiguous index instead of
+// gathering along the K index:
+//   mid  [n_mid][Rt][Kp2]: workgroup (i, block sb of 32 values of s) reads
+//        the rows G_{d-1}(s, i, :) and writes the 16-byte chunks of its 32
+//        values of s for every t < Rt;
+//   last [ncp][Kp3]: workgroup (block of 32 columns c) reads the rows
+//        G_d(t, c0 .. c0 + 31) and writes the chunks of its 32 columns;
+//   rows [NL][Kp2]: one chunk of a row of G_1 (or of the left interface)
+//        per thread.
+// Every thread issues all of its loads before its first LDS write.
+constexpr int kStage16T = 96;                 // t extent held in LDS
+constexpr int kStage16Ld = kStage16T + 2;     // odd dword pitch: column reads hit distinct banks
+constexpr int kStage16Loads = 32 * kStage16T / 256;
+
+__global__ __launch_bounds__(256) void k_stage16(const half_t* __restrict__ gmid, const half_t* __restrict__ glast,
+                                                 const half_t* __restrict__ g1, half_t* __restrict__ smid,
+                                                 half_t* __restrict__ slast, half_t* __restrict__ srows,
+                                                 int64_t n_mid, int64_t n_last, int64_t n1, int rL, int rM, int Kp2,
+                                                 int Kp3, int Rt, int ncp, int64_t wg_mid, int64_t wg_last) {
+    __shared__ half_t tile[32 * kStage16Ld];
+    const int tid = threadIdx.x;
+    int64_t wg = blockIdx.x;
+    if (wg < wg_mid) {
+        const int nsb = Kp2 / 32;
+        const int64_t i = wg / nsb;
+        const int sb = (int)(wg - i * nsb);
+        const int ne = 32 * rM;
+        half_t v[kStage16Loads];
+#pragma unroll
+        for (int q = 0; q < kStage16Loads; ++q) {
+            const int e = tid + 256 * q;
+            const int r = e / rM, t = e - r * rM, sv = 32 * sb + r;
+            v[q] = (e < ne && sv < rL) ? gmid[((int64_t)sv * n_mid + i) * rM + t] : half_t(0);
+        }
+#pragma unroll
+        for (int q = 0; q < kStage16Loads; ++q) {
+            const int e = tid + 256 * q;
+            const int r = e / rM, t = e - r * rM;
+            if (e < ne) tile[r * kStage16Ld + t] = v[q];
+        }
+        __syncthreads();
+        for (int ch = tid; ch < Rt * 4; ch += 256) {
+            const int t = ch >> 2, c = ch & 3;
+            half8_t w;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) w[j] = t < rM ? tile[(8 * c + j) * kStage16Ld + t] : half_t(0);
+            *reinterpret_cast<half8_t*>(smid + ((i * Rt + t) * (int64_t)Kp2 + 32 * sb + 8 * c)) = w;
+        }
+        return;
+    }
+    wg -= wg_mid;
+    if (wg < wg_last) {
+        const int64_t c0 = wg * 32;
+        const int ne = 32 * rM;
+        half_t v[kStage16Loads];
+#pragma unroll
+        for (int q = 0; q < kStage16Loads; ++q) {
+            const int e = tid + 256 * q;
+            const int t = e >> 5, cc = e & 31;
+            v[q] = (e < ne && c0 + cc < n_last) ? glast[(int64_t)t * n_last + c0 + cc] : half_t(0);
+        }
+#pragma unroll
+        for (int q = 0; q < kStage16Loads; ++q) {
+            const int e = tid + 256 * q;
+            if (e < ne) tile[(e & 31) * kStage16Ld + (e >> 5)] = v[q];
+        }
+        __syncthreads();
+        const int tcs = Kp3 / 8;
+        for (int ch = tid; ch < 32 * tcs; ch += 256) {
+            const int cc = ch / tcs, tc = ch - cc * tcs;
+            half8_t w;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) w[j] = 8 * tc + j < rM ? tile[cc * kStage16Ld + 8 * tc + j] : half_t(0);
+            if (c0 + cc < ncp) *reinterpret_cast<half8_t*>(slast + (c0 + cc) * Kp3 + 8 * tc) = w;
+        }
+        return;
+    }
+    wg -= wg_last;
+    const int64_t q = wg * 256 + tid;           // chunk of the rows copy
+    const int cpr = Kp2 / 8;
+    if (q >= n1 * cpr) return;
+    const int64_t L = q / cpr;
+    const int s0 = 8 * (int)(q - L * cpr);
+    half8_t w;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = s0 + j < rL ? g1[L * rL + s0 + j] : half_t(0);
+    *reinterpret_cast<half8_t*>(srows + L * Kp2 + s0) = w;
 }
 
 // Left interface of a train with d >= 4 for the wave tiles:
@@ -1243,13 +1335,15 @@ __device__ __forceinline__ void middle_w16(const TTArgs& a, const TTSet& S, int6
 // The FP16 middle products of all NPB row blocks of a tile (one middle index,
 // so the same G_2 fragments): the NT x NKB2 A fragments are fetched once and
 // kept, then each row block needs only its rows of G_1 (Kp2 <= 32 NKB2).
-template <int NT, int NKB2, int NPB, class OutF>
+// EXACT: Kp2 == 32 NKB2, so no K step is skipped at run time (a skip lets
+// the compiler sink the row loads down to their use, one wait each).
+template <int NT, int NKB2, int NPB, bool EXACT, class OutF>
 __device__ __forceinline__ void middle_w16_tile(const TTArgs& a, const TTSet& S, int64_t i, int64_t L0, int r, int g,
                                                 OutF emit) {
     const half_t* mid = static_cast<const half_t*>(S.st_mid) + i * S.Rt * S.Kp2;   // uniform
     const uint32_t moff = (uint32_t)(r * S.Kp2 + 8 * g) * 2u;
     const int64_t tstep = 16 * (int64_t)S.Kp2;
-    const int nkb = S.Kp2 / 32;   // <= NKB2
+    const int nkb = EXACT ? NKB2 : S.Kp2 / 32;   // <= NKB2
     half8_t x[NKB2][NT];
 #pragma unroll
     for (int kb = 0; kb < NKB2; ++kb) {
@@ -1265,15 +1359,19 @@ __device__ __forceinline__ void middle_w16_tile(const TTArgs& a, const TTSet& S,
     };
     half8_t bc[NKB2], bn[NKB2];
     rows(0, bc);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int pb = 0; pb < NPB; ++pb) {
         if (pb + 1 < NPB) rows(pb + 1, bn);   // next row block's rows, fetched ahead
+        // keep the prefetch ahead of this block's products (the scheduler
+        // would otherwise sink each load down to its use)
+        __builtin_amdgcn_sched_barrier(0);
         float4_t acc[NT];
 #pragma unroll
         for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<float4_t>();
 #pragma unroll
         for (int kb = 0; kb < NKB2; ++kb) {
-            if (kb >= nkb) break;
+            if (!EXACT && kb >= nkb) break;
 #pragma unroll
             for (int tb = 0; tb < NT; ++tb) acc[tb] = mfma(x[kb][tb], bc[kb], acc[tb]);
         }
@@ -1353,38 +1451,90 @@ template <int NKB, int NPB, bool TS>
 __device__ __forceinline__ void last_store_w16l(const TTArgs& a, float* stl, const half_t* Ls, int ldp, int64_t i,
                                                 int64_t L0, int r, int g, const half8_t (&zf)[NPB][NKB]) {
     const int n_cb = (int)((a.n_last + 15) / 16);
-    for (int cp = 0; cp < n_cb; ++cp) {
-        const half_t* lrow = Ls + (16 * cp + r) * ldp + 8 * g;
-        half8_t f[NKB];
+    // two column blocks per step (twice the independent products), the
+    // next step's fragments read from LDS before this step's products
+    auto frags = [&](half8_t (&f)[2][NKB], int cp) {
 #pragma unroll
-        for (int s2 = 0; s2 < NKB; ++s2) f[s2] = *reinterpret_cast<const half8_t*>(lrow + 32 * s2);
-        float4_t acc[NPB];
+        for (int h = 0; h < 2; ++h) {
+            const int c = cp + h < n_cb ? cp + h : n_cb - 1;
+            const half_t* lrow = Ls + (16 * c + r) * ldp + 8 * g;
 #pragma unroll
-        for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<float4_t>();
+            for (int s2 = 0; s2 < NKB; ++s2) f[h][s2] = *reinterpret_cast<const half8_t*>(lrow + 32 * s2);
+        }
+    };
+    half8_t f[2][NKB], fn[2][NKB];
+    frags(f, 0);
+    for (int cp = 0; cp < n_cb; cp += 2) {
+        if (cp + 2 < n_cb) frags(fn, cp + 2);
+        float4_t acc[2][NPB];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) acc[h][pb] = zero_accv<float4_t>();
 #pragma unroll
         for (int s2 = 0; s2 < NKB; ++s2)
 #pragma unroll
-            for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(f[s2], zf[pb][s2], acc[pb]);
-        store_block<half_t, NPB, TS>(a, stl, i, L0, (int64_t)cp * 16, r, g, acc);
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int pb = 0; pb < NPB; ++pb) acc[h][pb] = mfma(f[h][s2], zf[pb][s2], acc[h][pb]);
+        if (!TS && a.vec8 && cp + 1 < n_cb) {
+            // the two blocks' 32 columns regrouped so that lane (r, g) holds
+            // columns 8 g .. 8 g + 7: one 16-byte store per row block, 64
+            // bytes per row and instruction
+            half_t* out = static_cast<half_t*>(a.out);
+            const int64_t c0 = (int64_t)cp * 16 + 8 * g;
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb) {
+                const half8_t v = regroup16(acc[0][pb], acc[1][pb]);
+                const int64_t L = L0 + 16 * pb + r;
+                if (L < a.NL && c0 + 8 <= a.n_last)
+                    *reinterpret_cast<half8_t*>(out + (L * a.n_mid + i) * a.n_last + c0) = v;
+            }
+        } else {
+            store_block<half_t, NPB, TS>(a, stl, i, L0, (int64_t)cp * 16, r, g, acc[0]);
+            if (cp + 1 < n_cb) store_block<half_t, NPB, TS>(a, stl, i, L0, (int64_t)(cp + 1) * 16, r, g, acc[1]);
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int s2 = 0; s2 < NKB; ++s2) f[h][s2] = fn[h][s2];
     }
 }
 
 // LDSB: the staged last core [ncp][Kp3] is first copied into LDS at pitch
 // Kp3 + 8 halves (16-byte fragment reads of 16 rows fall on distinct banks).
+// kW16 waves share one workgroup and its copy of the last core (8 and 16
+// measured no faster than 4 on a 512 x 512 x 224 train).
+constexpr int kW16 = 4;
+
 template <int NKB, int NPB, bool LDSB, bool TS>
-__global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
+__global__ __launch_bounds__(64 * kW16) void k_tt_wave16(TTArgs a, int64_t ntiles) {
     constexpr int NT = 2 * NKB;
     extern __shared__ double4_t smem_v[];
-    __shared__ float st_tile[4][16 * 17];   // per wave: rows not fit for vector stores
+    __shared__ float st_tile[kW16][16 * 17];   // per wave: rows not fit for vector stores
     half_t* Ls = reinterpret_cast<half_t*>(smem_v);
     const int ldp = a.set[0].Kp3 + 8;
     if constexpr (LDSB) {
+        // every thread issues all of its loads (at most 16 chunks: the copy
+        // is at most 64 KB) before the first LDS write, so the copy costs one
+        // load latency instead of one per chunk
         typedef unsigned u4_t __attribute__((ext_vector_type(4)));
         const u4_t* src = static_cast<const u4_t*>(a.set[0].st_last);   // rows of Kp3 / 8 chunks
-        const int cpr = a.set[0].Kp3 / 8;
-        for (int idx = threadIdx.x; idx < a.ncp * cpr; idx += 256) {
-            const int row = idx / cpr, ch = idx % cpr;
-            *reinterpret_cast<u4_t*>(Ls + row * ldp + 8 * ch) = src[idx];
+        const int cpr = a.set[0].Kp3 / 8, nch = a.ncp * cpr;
+        constexpr int kMaxChunks = 65536 / 16 / (64 * kW16);
+        u4_t buf[kMaxChunks];
+#pragma unroll
+        for (int q = 0; q < kMaxChunks; ++q) {
+            const int idx = threadIdx.x + 64 * kW16 * q;
+            if (idx < nch) buf[q] = src[idx];
+        }
+#pragma unroll
+        for (int q = 0; q < kMaxChunks; ++q) {
+            const int idx = threadIdx.x + 64 * kW16 * q;
+            if (idx < nch) {
+                const int row = idx / cpr, ch = idx - row * cpr;
+                *reinterpret_cast<u4_t*>(Ls + row * ldp + 8 * ch) = buf[q];
+            }
         }
         __syncthreads();
     }
@@ -1392,18 +1542,23 @@ __global__ __launch_bounds__(256) void k_tt_wave16(TTArgs a, int64_t ntiles) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
     const int64_t wl = xcd_tile(gridDim.x);
-    for (int64_t tile = wl * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
+    for (int64_t tile = wl * kW16 + wave; tile < ntiles; tile += (int64_t)gridDim.x * kW16) {
         const int64_t i = a.ifast ? tile % a.n_mid : tile / nLb;
         const int64_t L0 = (a.ifast ? tile / a.n_mid : tile % nLb) * 16 * NPB;
         half8_t zf[NPB][NKB];
-        if (a.set[0].Kp2 <= 32 * 3) {
+        auto keep = [&](int pb, float4_t (&acc)[NT]) {
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) zf[pb][kb] = regroup16(acc[2 * kb], acc[2 * kb + 1]);
+        };
+        if (a.set[0].Kp2 == 32 * NKB) {
             // every row block's middle product from one fetch of the G_2 fragments
             int ln = lane;
             asm volatile("" : "+v"(ln));
-            middle_w16_tile<NT, 3, NPB>(a, a.set[0], i, L0, ln & 15, ln >> 4, [&](int pb, float4_t (&acc)[NT]) {
-#pragma unroll
-                for (int kb = 0; kb < NKB; ++kb) zf[pb][kb] = regroup16(acc[2 * kb], acc[2 * kb + 1]);
-            });
+            middle_w16_tile<NT, NKB, NPB, true>(a, a.set[0], i, L0, ln & 15, ln >> 4, keep);
+        } else if (a.set[0].Kp2 <= 32 * 3) {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            middle_w16_tile<NT, 3, NPB, false>(a, a.set[0], i, L0, ln & 15, ln >> 4, keep);
         } else {
 #pragma unroll
             for (int pb = 0; pb < NPB; ++pb) {
@@ -1429,12 +1584,12 @@ static void launch_wave16(int nkb, int npb, dim3 grid, hipStream_t st, const TTA
 #define LRC_TW(K, P)                                                                                  \
     do {                                                                                              \
         if (in_lds && a.vec4)                                                                         \
-            hipLaunchKernelGGL((k_tt_wave16<K, P, true, false>), grid, dim3(256), lds, st, a, ntiles);  \
+            hipLaunchKernelGGL((k_tt_wave16<K, P, true, false>), grid, dim3(64 * kW16), lds, st, a, ntiles);  \
         else if (in_lds)                                                                              \
-            hipLaunchKernelGGL((k_tt_wave16<K, P, true, true>), grid, dim3(256), lds, st, a, ntiles);   \
+            hipLaunchKernelGGL((k_tt_wave16<K, P, true, true>), grid, dim3(64 * kW16), lds, st, a, ntiles);   \
         else if (a.vec4)                                                                              \
-            hipLaunchKernelGGL((k_tt_wave16<K, P, false, false>), grid, dim3(256), 0, st, a, ntiles);   \
-        else hipLaunchKernelGGL((k_tt_wave16<K, P, false, true>), grid, dim3(256), 0, st, a, ntiles);   \
+            hipLaunchKernelGGL((k_tt_wave16<K, P, false, false>), grid, dim3(64 * kW16), 0, st, a, ntiles);   \
+        else hipLaunchKernelGGL((k_tt_wave16<K, P, false, true>), grid, dim3(64 * kW16), 0, st, a, ntiles);   \
     } while (0)
 #define LRC_TWK(K) \
     do {                                 \
@@ -1451,9 +1606,11 @@ static void launch_wave16(int nkb, int npb, dim3 grid, hipStream_t st, const TTA
 #undef LRC_TW
 }
 
-// Workgroups of the wave-tile kernels: four tiles each, at most 4096.
+// Workgroups of the wave-tile kernels: four tiles each (kW16 for FP16), at
+// most 4096.
 static int64_t wave_grid(const TTPlan& p) {
-    return xcd_grid(std::min<int64_t>((p.wave_tiles + 3) / 4, 4096));
+    const int w = p.prec == P16 ? kW16 : 4;
+    return xcd_grid(std::min<int64_t>((p.wave_tiles + w - 1) / w, 4096));
 }
 
 // The certificate split by what its sums couple: set 0 (the base train)
@@ -1848,6 +2005,7 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
     a.ncp = (int)round_up(p.n_last, 32);
     a.out = out;
     a.vec4 = out && (p.n_last % 4 == 0) && (reinterpret_cast<uintptr_t>(out) % (4 * sizeof(T)) == 0);
+    a.vec8 = sizeof(T) == 2 && out && (p.n_last % 8 == 0) && (reinterpret_cast<uintptr_t>(out) % 16 == 0);
     a.lines = out && ((p.n_last * (int64_t)sizeof(T)) % 128 == 0) && (reinterpret_cast<uintptr_t>(out) % 128 == 0);
     // short output rows (n_d e < 1 KB): wave tiles of consecutive middle indices
     // write neighbouring segments of the same rows, so the rows fill up together
@@ -1923,6 +2081,22 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
             if (gs > 4096) gs = 4096;
             const bool narrow = tmid < 2147483647LL && tlast < 2147483647LL && trows < 2147483647LL;
             KernelTimer ts(stage_label, stream);
+            if constexpr (sizeof(T) == 2) {
+                if (rows && ps.Rt <= kStage16T && ps.Kp3 <= kStage16T && ps.rM <= kStage16T) {
+                    const int64_t wg_mid = p.n_mid * (ps.Kp2 / 32), wg_last = a.ncp / 32;
+                    const int64_t wg_rows = (p.NL * (ps.Kp2 / 8) + 255) / 256;
+                    hipLaunchKernelGGL(k_stage16, dim3((unsigned)(wg_mid + wg_last + wg_rows)), dim3(256), 0, stream,
+                                       (const half_t*)cores[q][p.d - 2], (const half_t*)cores[q][p.d - 1],
+                                       (const half_t*)S.core[2], (half_t*)smid, (half_t*)slast, (half_t*)sl, p.n_mid,
+                                       p.n_last, p.NL, ps.rL, ps.rM, ps.Kp2, ps.Kp3, ps.Rt, a.ncp, wg_mid, wg_last);
+                    hipError_t e = hipGetLastError();
+                    if (e != hipSuccess) return e;
+                    S.st_mid = smid;
+                    S.st_last = slast;
+                    S.st_left = sl;
+                    continue;
+                }
+            }
 #define LRC_STAGE(IDX)                                                                                       \
     hipLaunchKernelGGL((k_stage<T, IDX>), dim3((unsigned)gs), dim3(256), 0, stream, (const T*)cores[q][p.d - 2], \
                        (const T*)cores[q][p.d - 1], rows ? (const T*)S.core[2] : (const T*)nullptr, smid, slast, sl, \
