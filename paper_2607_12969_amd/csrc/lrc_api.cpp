@@ -853,17 +853,32 @@ int lrc_tt_quality(const void* const* cores, const int64_t* dims, const int64_t*
         if (!cores[l]) return fail(LRC_EINVAL, "cores[%d] is NULL", l);
     const int64_t B = dims[d - 1], P = N / B;
     int dev;
-    rc = current_device(&dev, nullptr);
+    size_t max_lds;
+    rc = current_device(&dev, &max_lds);
     if (rc) return rc;
     hipStream_t st = g_stream;
     const int64_t cnt = tt_count(dims, ranks, d);
-    size_t need = (size_t)N * 8 + (size_t)cnt * 8 + (size_t)(d + 4) * 256 + quality_workspace_bytes(P, B) + 256;
-    need += tt_stage_need(dims, ranks, d) + 512;
+    // Fused when the FP64 plan takes wave tiles: the measures are formed in
+    // the reconstruction's epilogue, which reads only the cores and X.
+    // Otherwise the FP64 reconstruction is written to the workspace and
+    // measured densely.
+    TTPlan plan;
+    int64_t G = 0;
+    if (d >= 3) {
+        const int64_t* rs[1] = {ranks};
+        if (plan_tt(plan, dims, rs, 1, d, LRC_FP64, max_lds) == 0) G = tt_quality_blocks(plan, max_lds);
+    }
+    size_t need = (size_t)cnt * 8 + (size_t)(d + 4) * 256 + 256;
+    if (G > 0)
+        need += plan.stage_bytes + 512 + round_up((size_t)G * QS_N * B * 8, 256) + round_up((size_t)G * 16, 256) +
+                round_up((size_t)QS_N * B * 8, 256);
+    else
+        need += (size_t)N * 8 + quality_workspace_bytes(P, B) + tt_stage_need(dims, ranks, d) + 512;
     Workspace& ws = workspace_for(dev, st);
     ws.reset();
     hipError_t e = ws.reserve(need, st);
     if (e != hipSuccess) return fail_hip(e, "workspace");
-    double* Xh = static_cast<double*>(ws.take((size_t)N * 8));
+    double* Xh = G > 0 ? nullptr : static_cast<double*>(ws.take((size_t)N * 8));
     // the stored cores, widened exactly to FP64 (Sec. 3.4: FP64 contraction of the rounded cores)
     std::vector<const void*> wide(d);
     for (int l = 0; l < d; ++l) {
@@ -880,9 +895,19 @@ int lrc_tt_quality(const void* const* cores, const int64_t* dims, const int64_t*
     }
     double* out = static_cast<double*>(ws.take(5 * 8));
     if (ws.overrun) return fail(LRC_ENOMEM, "quality workspace too small");
-    rc = tt_into(wide.data(), dims, ranks, d, Xh, ws, "quality_tt_f64");
-    if (rc) return rc;
-    e = launch_quality(static_cast<const double*>(X), Xh, LRC_FP64, scale, P, B, out, ws, st);
+    if (G > 0) {
+        double* part = static_cast<double*>(ws.take((size_t)G * QS_N * B * 8));
+        double* part2 = static_cast<double*>(ws.take((size_t)G * 16));
+        double* red = static_cast<double*>(ws.take((size_t)QS_N * B * 8));
+        if (ws.overrun) return fail(LRC_ENOMEM, "quality workspace too small");
+        e = launch_tt_quality(plan, wide.data(), static_cast<const double*>(X), scale, part, part2, max_lds, ws, st);
+        if (e == hipSuccess)
+            e = launch_quality_reduce(part, G, part2, G, static_cast<const double*>(X), P, B, red, out, st);
+    } else {
+        rc = tt_into(wide.data(), dims, ranks, d, Xh, ws, "quality_tt_f64");
+        if (rc) return rc;
+        e = launch_quality(static_cast<const double*>(X), Xh, LRC_FP64, scale, P, B, out, ws, st);
+    }
     double h[5];
     if (e == hipSuccess) e = hipMemcpyAsync(h, out, sizeof(h), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);

@@ -141,7 +141,17 @@ hipError_t launch_widen(const void* src, int prec, int64_t count, double* out, h
 // out[0..4] = relative error, mean band PSNR, mean band SSIM variant, mean
 // spectral angle, pixels in that mean; X (P x B, FP64) against scale * Xh
 // (P x B in prec).
+// Band statistics of the quality measures, in the order of their partials:
+// part[(block * QS_N + q) * B + b] (shifted sums of X and Xh, their squares
+// and cross products, squared differences, squares of X, band min and max).
+enum { QS_X = 0, QS_Y, QS_XX, QS_YY, QS_XY, QS_DD, QS_X2, QS_MIN, QS_MAX, QS_N };
 size_t quality_workspace_bytes(int64_t P, int64_t B);
+// The reductions of the band partials (nblk blocks) and the angle partials
+// part2[2 k], part2[2 k + 1] (nblk2 blocks) into the five results at `out`
+// (red: QS_N * B doubles of scratch).
+hipError_t launch_quality_reduce(const double* part, int64_t nblk, const double* part2, int64_t nblk2,
+                                 const double* X, int64_t P, int64_t B, double* red, double* out,
+                                 hipStream_t stream);
 hipError_t launch_quality(const double* X, const void* Xh, int prec, double scale, int64_t P, int64_t B,
                           double* out, Workspace& ws, hipStream_t stream);
 
@@ -214,6 +224,15 @@ hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Works
 // widened rounded augmented): part[s * tt_cert_parts(p) + w] receives the
 // five partial sums of workgroup w (order at k_tt_cert).
 int64_t tt_cert_parts(const TTPlan& p);
+
+// Quality measures of an FP64 reconstruction (one set, wave tiles) fused
+// into the reconstruction: tt_quality_blocks(p, B) is the number of
+// workgroup partials the fused kernel writes (0: the plan does not take it,
+// reconstruct densely instead); launch_tt_quality writes them at part
+// (tt_quality_blocks * QS_N * n_d doubles) and part2 (2 per block).
+int64_t tt_quality_blocks(const TTPlan& p, size_t max_lds);
+hipError_t launch_tt_quality(const TTPlan& p, const void* const* cores, const double* X, double scale,
+                             double* part, double* part2, size_t max_lds, Workspace& ws, hipStream_t stream);
 hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, const double* Tref, double* part,
                           Workspace& ws, hipStream_t stream);
 

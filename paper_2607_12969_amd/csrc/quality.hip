@@ -22,8 +22,6 @@
 
 namespace lrc {
 
-enum { QS_X = 0, QS_Y, QS_XX, QS_YY, QS_XY, QS_DD, QS_X2, QS_MIN, QS_MAX, QS_N };
-
 template <typename Y>
 __device__ __forceinline__ double widen_q(Y v) { return static_cast<double>(v); }
 
@@ -161,9 +159,14 @@ __global__ __launch_bounds__(256) void k_quality_finish(const double* __restrict
                                                         const double* __restrict__ part2, int64_t nblk2,
                                                         const double* __restrict__ X, int64_t P, int64_t B,
                                                         double* __restrict__ out) {
-    __shared__ double acc[256][4];   // per thread: sum of PSNR_b, SSIM_b, squared differences, squares
+    __shared__ double acc[256][6];   // per thread: PSNR_b, SSIM_b, squared differences, squares, angles, pixels
     const int t = threadIdx.x;
-    double ps = 0.0, ss = 0.0, dd = 0.0, x2 = 0.0;
+    double ps = 0.0, ss = 0.0, dd = 0.0, x2 = 0.0, sa = 0.0, sc = 0.0;
+    // the angle partials: thread t adds blocks t, t + 256, ... in order
+    for (int64_t k = t; k < nblk2; k += 256) {
+        sa += part2[2 * k];
+        sc += part2[2 * k + 1];
+    }
     const double np = (double)P;
     for (int64_t b = t; b < B; b += 256) {
         double v[QS_N];
@@ -190,20 +193,18 @@ __global__ __launch_bounds__(256) void k_quality_finish(const double* __restrict
     acc[t][1] = ss;
     acc[t][2] = dd;
     acc[t][3] = x2;
+    acc[t][4] = sa;
+    acc[t][5] = sc;
     __syncthreads();
+    if (t >= 64) return;
+    // wave 0: lane l adds threads l, l + 64, l + 128, l + 192, then a fixed butterfly
+    double a[6];
+#pragma unroll
+    for (int j = 0; j < 6; ++j) a[j] = wave_sum(((acc[t][j] + acc[t + 64][j]) + acc[t + 128][j]) + acc[t + 192][j]);
     if (t == 0) {
-        double a0 = 0, a1 = 0, a2 = 0, a3 = 0;
-        for (int q = 0; q < 256; ++q) {
-            a0 += acc[q][0];
-            a1 += acc[q][1];
-            a2 += acc[q][2];
-            a3 += acc[q][3];
-        }
-        double sa = 0.0, sc = 0.0;
-        for (int64_t k = 0; k < nblk2; ++k) {
-            sa += part2[2 * k];
-            sc += part2[2 * k + 1];
-        }
+        const double a0 = a[0], a1 = a[1], a2 = a[2], a3 = a[3];
+        sa = a[4];
+        sc = a[5];
         out[0] = sqrt(a2) / sqrt(a3);
         out[1] = a0 / (double)B;
         out[2] = a1 / (double)B;
@@ -242,6 +243,16 @@ static hipError_t quality_typed(const double* X, const Y* Xh, double scale, int6
     hipLaunchKernelGGL((k_band_stats<Y>), dim3((unsigned)nblk), dim3(256), 0, stream, X, Xh, scale, P, B, rows,
                        part);
     hipLaunchKernelGGL((k_sam<Y>), dim3((unsigned)nblk2), dim3(256), 0, stream, X, Xh, scale, P, B, part2);
+    hipLaunchKernelGGL(k_quality_reduce, dim3((unsigned)((QS_N * B + 3) / 4)), dim3(256), 0, stream, part, nblk, B,
+                       red);
+    hipLaunchKernelGGL(k_quality_finish, dim3(1), dim3(256), 0, stream, red, part2, nblk2, X, P, B, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_quality_reduce(const double* part, int64_t nblk, const double* part2, int64_t nblk2,
+                                 const double* X, int64_t P, int64_t B, double* red, double* out,
+                                 hipStream_t stream) {
+    KernelTimer t("quality_f64", stream);
     hipLaunchKernelGGL(k_quality_reduce, dim3((unsigned)((QS_N * B + 3) / 4)), dim3(256), 0, stream, part, nblk, B,
                        red);
     hipLaunchKernelGGL(k_quality_finish, dim3(1), dim3(256), 0, stream, red, part2, nblk2, X, P, B, out);

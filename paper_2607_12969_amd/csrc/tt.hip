@@ -1108,6 +1108,225 @@ static void launch_wave(int nkb, int npb, dim3 grid, hipStream_t st, const TTArg
 #undef LRC_TW
 }
 
+// ---------------------------------------------------------------------------
+// Quality of an FP64 reconstruction against its reference, fused into the
+// wave tiles (Sec. sec:hyperspectral_application): the last product's
+// values y = scale * T^(L, i, c) meet the reference X(L, i, c) while they
+// are in registers, and nothing of the reconstruction is written.  Pixels
+// are the rows (L, i), bands the columns c.
+//   bands:  per 16-column block, each lane adds its elements' shifted sums
+//           (shift s_c = X(0, c)), squares, cross products, squared
+//           differences and squares of X, and its minimum and maximum; the
+//           four lane groups of a column are combined in a fixed butterfly
+//           and added into the wave's own LDS accumulators [QS_N][n_d];
+//   pixels: each lane keeps the dot product and squared norms of its rows
+//           over the tile's column blocks in registers; at the tile's end
+//           they are added across the 16 column lanes and give the angles.
+// At the end the workgroup adds its four waves in wave order into one
+// partial per workgroup in the layout of the dense quality kernels, whose
+// reductions finish the measures.
+constexpr int kQualNpb = 2;   // row blocks per quality tile (register budget)
+
+template <int NKB, int NPB, int D>
+__device__ __forceinline__ void last_quality_w(const TTArgs& a, int64_t i, int64_t L0, int r, int g,
+                                               const double (&zf)[NPB][NKB], const double* __restrict__ X,
+                                               double scale, double* wacc, double (&pd)[NPB][4],
+                                               double (&px)[NPB][4], double (&py)[NPB][4]) {
+    static_assert(D <= NKB, "ring deeper than a block");
+    const int n_cb = (int)((a.n_last + 15) / 16);
+    const int64_t B = a.n_last;
+    const LastCoreReader<double> lc(a.set[0].core[1], a.set[0].rM, (uint32_t)a.n_last);
+    const uint32_t nl = (uint32_t)a.n_last, clast = nl - 1;
+    auto colc = [&](int cp) {
+        const uint32_t c = (uint32_t)(16 * cp + r);
+        return c < clast ? c : clast;
+    };
+    int64_t prow[NPB][4];   // X offsets of the lane's rows (clamped), validity in rok
+    bool rok[NPB][4];
+#pragma unroll
+    for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t L = L0 + 16 * pb + g + 4 * v;
+            rok[pb][v] = L < a.NL;
+            prow[pb][v] = ((rok[pb][v] ? L : a.NL - 1) * a.n_mid + i) * B;
+        }
+    double N[D], R[D];
+    uint32_t vo = lc.lane(g, colc(0));
+#pragma unroll
+    for (int s = 0; s < D; ++s) N[s] = lc.ld(s, vo);
+    for (int cp = 0; cp < n_cb; ++cp) {
+        const uint32_t von = lc.lane(g, colc(cp + 1 < n_cb ? cp + 1 : cp));
+        const int64_t col = (int64_t)cp * 16 + r;
+        const bool cok = col < B;
+        const int64_t cc = cok ? col : B - 1;
+        // the reference values of this block, in flight during its products
+        double xv[NPB][4];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) xv[pb][v] = X[prow[pb][v] + cc];
+        const double sh = X[cc];
+        __builtin_amdgcn_sched_barrier(0);
+        double4_t acc[NPB];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) acc[pb] = zero_accv<double4_t>();
+        auto block = [&](auto more) {
+#pragma unroll
+            for (int s = 0; s < NKB; ++s) {
+                const double f = s < D ? N[s] : R[s % D];
+#pragma unroll
+                for (int pb = 0; pb < NPB; ++pb) acc[pb] = mfma(zf[pb][s], f, acc[pb]);
+                const int k = s + D;
+                if (k < NKB) R[k % D] = lc.ld(k, vo);
+                else if constexpr (decltype(more)::value) N[k - NKB] = lc.ld(k - NKB, von);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        if (cp + 1 < n_cb) block(std::true_type{});
+        else block(std::false_type{});
+        double st[QS_N];
+#pragma unroll
+        for (int q = 0; q < QS_MIN; ++q) st[q] = 0.0;
+        st[QS_MIN] = sh;
+        st[QS_MAX] = sh;
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const bool ok = cok && rok[pb][v];
+                const double x = ok ? xv[pb][v] : 0.0, y = ok ? scale * acc[pb][v] : 0.0;
+                pd[pb][v] += x * y;
+                px[pb][v] += x * x;
+                py[pb][v] += y * y;
+                const double dx = ok ? x - sh : 0.0, dy = ok ? y - sh : 0.0, dd = x - y;
+                st[QS_X] += dx;
+                st[QS_Y] += dy;
+                st[QS_XX] += dx * dx;
+                st[QS_YY] += dy * dy;
+                st[QS_XY] += dx * dy;
+                st[QS_DD] += dd * dd;
+                st[QS_X2] += x * x;
+                if (ok) {
+                    st[QS_MIN] = x < st[QS_MIN] ? x : st[QS_MIN];
+                    st[QS_MAX] = x > st[QS_MAX] ? x : st[QS_MAX];
+                }
+            }
+        // the four lane groups of this column: a fixed butterfly
+#pragma unroll
+        for (int off = 16; off <= 32; off <<= 1) {
+#pragma unroll
+            for (int q = 0; q < QS_MIN; ++q) st[q] += __shfl_xor(st[q], off, 64);
+            const double mn = __shfl_xor(st[QS_MIN], off, 64), mx = __shfl_xor(st[QS_MAX], off, 64);
+            st[QS_MIN] = mn < st[QS_MIN] ? mn : st[QS_MIN];
+            st[QS_MAX] = mx > st[QS_MAX] ? mx : st[QS_MAX];
+        }
+        if (g == 0 && cok) {
+#pragma unroll
+            for (int q = 0; q < QS_MIN; ++q) wacc[q * B + col] += st[q];
+            const double mn = wacc[QS_MIN * B + col], mx = wacc[QS_MAX * B + col];
+            wacc[QS_MIN * B + col] = st[QS_MIN] < mn ? st[QS_MIN] : mn;
+            wacc[QS_MAX * B + col] = st[QS_MAX] > mx ? st[QS_MAX] : mx;
+        }
+        vo = von;
+    }
+}
+
+template <int NKB>
+__global__ __launch_bounds__(256) void k_tt_wave_q(TTArgs a, int64_t ntiles, const double* __restrict__ X,
+                                                   double scale, double* __restrict__ part,
+                                                   double* __restrict__ part2) {
+    constexpr int NPB = kQualNpb;
+    constexpr int NT = (NKB + 3) / 4;
+    constexpr int D = NKB < 8 ? NKB : 8;
+    extern __shared__ double4_t smem_v[];
+    __shared__ double wsam[4][2];
+    double* qacc = reinterpret_cast<double*>(smem_v);   // [4 waves][QS_N][n_d]
+    const int64_t B = a.n_last;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    double* wacc = qacc + (int64_t)wave * QS_N * B;
+    for (int64_t c = lane; c < B; c += 64) {
+        const double s = X[c];
+#pragma unroll
+        for (int q = 0; q < QS_MIN; ++q) wacc[q * B + c] = 0.0;
+        wacc[QS_MIN * B + c] = s;
+        wacc[QS_MAX * B + c] = s;
+    }
+    __syncthreads();
+    const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
+    double asum = 0.0, cnt = 0.0;
+    for (int64_t tile = (int64_t)blockIdx.x * 4 + wave; tile < ntiles; tile += (int64_t)gridDim.x * 4) {
+        const int64_t i = tile / nLb;
+        const int64_t L0 = (tile % nLb) * 16 * NPB;
+        double zf[NPB][NKB];
+        {
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            double4_t acc[NPB][NT];
+            middle_w_tile<double, NT, NPB>(a, a.set[0], i, L0, ln & 15, ln >> 4, acc);
+#pragma unroll
+            for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+                for (int tb = 0; tb < NT; ++tb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        if (4 * tb + v < NKB) zf[pb][4 * tb + v] = acc[pb][tb][v];
+        }
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int r = ln & 15, g = ln >> 4;
+        double pd[NPB][4], px[NPB][4], py[NPB][4];
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) pd[pb][v] = px[pb][v] = py[pb][v] = 0.0;
+        last_quality_w<NKB, NPB, D>(a, i, L0, r, g, zf, X, scale, wacc, pd, px, py);
+        // each row's sums over its 16 column lanes (fixed butterfly), then its angle
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) {
+                    pd[pb][v] += __shfl_xor(pd[pb][v], off, 64);
+                    px[pb][v] += __shfl_xor(px[pb][v], off, 64);
+                    py[pb][v] += __shfl_xor(py[pb][v], off, 64);
+                }
+                const int64_t L = L0 + 16 * pb + g + 4 * v;
+                const double nn = __builtin_sqrt(px[pb][v]) * __builtin_sqrt(py[pb][v]);
+                if (r == 0 && L < a.NL && nn > 0.0) {
+                    double c = pd[pb][v] / nn;
+                    c = c > 1.0 ? 1.0 : (c < -1.0 ? -1.0 : c);
+                    asum += acos(c);
+                    cnt += 1.0;
+                }
+            }
+    }
+    asum = wave_sum(asum);
+    cnt = wave_sum(cnt);
+    if (lane == 0) {
+        wsam[wave][0] = asum;
+        wsam[wave][1] = cnt;
+    }
+    __syncthreads();
+    const int64_t blk = blockIdx.x;
+    for (int64_t e = tid; e < QS_N * B; e += 256) {
+        const int q = (int)(e / B);
+        const double* w0 = qacc + e;
+        double v = w0[0];
+        for (int w = 1; w < 4; ++w) {
+            const double o = w0[(int64_t)w * QS_N * B];
+            v = q == QS_MIN ? (o < v ? o : v) : (q == QS_MAX ? (o > v ? o : v) : v + o);
+        }
+        part[blk * QS_N * B + e] = v;
+    }
+    if (tid == 0) {
+        part2[2 * blk] = ((wsam[0][0] + wsam[1][0]) + wsam[2][0]) + wsam[3][0];
+        part2[2 * blk + 1] = ((wsam[0][1] + wsam[1][1]) + wsam[2][1]) + wsam[3][1];
+    }
+}
+
 // FP32 accumulators of the transposed middle product hold, in lane (r, g),
 // value v, Z_2(L0 + r, 16 tb + 4 g + v): lane group g has the four K values
 // of step kb = 4 tb + g.  The A fragment of the FP32 last product wants
@@ -2208,6 +2427,44 @@ hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Works
     if (p.prec == P64) return tt_typed<double>(p, sets, out, ws, stream, label);
     if (p.prec == P32) return tt_typed<float>(p, sets, out, ws, stream, label);
     return tt_typed<half_t>(p, sets, out, ws, stream, label);
+}
+
+static size_t quality_lds(int64_t B) { return (size_t)4 * QS_N * B * sizeof(double); }
+
+int64_t tt_quality_blocks(const TTPlan& p, size_t max_lds) {
+    if (p.prec != P64 || p.nsets != 1 || !p.wave_nkb) return 0;
+    const size_t lds = quality_lds(p.n_last);
+    if (lds > max_lds || lds > 131072) return 0;
+    const int64_t per_cu = std::max<int64_t>(1, (int64_t)(163840 / lds));
+    const int64_t tiles = p.n_mid * ((p.NL + 16 * kQualNpb - 1) / (16 * kQualNpb));
+    return std::max<int64_t>(1, std::min<int64_t>((tiles + 3) / 4, 256 * per_cu));
+}
+
+hipError_t launch_tt_quality(const TTPlan& p, const void* const* cores, const double* X, double scale,
+                             double* part, double* part2, size_t max_lds, Workspace& ws, hipStream_t stream) {
+    const int64_t G = tt_quality_blocks(p, max_lds);
+    if (!G) return hipErrorInvalidValue;
+    TTArgs a;
+    const void* const* sets[1] = {cores};
+    hipError_t e = prepare_tt<double>(p, sets, nullptr, ws, stream, "quality_tt_f64", a);
+    if (e != hipSuccess) return e;
+    const int64_t tiles = p.n_mid * ((p.NL + 16 * kQualNpb - 1) / (16 * kQualNpb));
+    const size_t lds = quality_lds(p.n_last);
+    KernelTimer tk("quality_tt_f64", stream);
+#define LRC_TQ(K) \
+    hipLaunchKernelGGL((k_tt_wave_q<K>), dim3((unsigned)G), dim3(256), lds, stream, a, tiles, X, scale, part, part2)
+    switch (p.wave_nkb) {
+    case 4: LRC_TQ(4); break;
+    case 5: LRC_TQ(5); break;
+    case 8: LRC_TQ(8); break;
+    case 9: LRC_TQ(9); break;
+    case 12: LRC_TQ(12); break;
+    case 16: LRC_TQ(16); break;
+    case 17: LRC_TQ(17); break;
+    default: return hipErrorInvalidValue;
+    }
+#undef LRC_TQ
+    return hipGetLastError();
 }
 
 }  // namespace lrc

@@ -86,6 +86,29 @@ def test_tt_against_reference(lrc, prec, dims, rank):
     _compare(got, ref, (dims, prec))
 
 
+@pytest.mark.parametrize("dims,ranks", [((100, 100, 90), (1, 80, 80, 1)), ((300, 40), (1, 12, 1))])
+def test_tt_dense_fallback(lrc, dims, ranks):
+    """Trains whose FP64 plan takes no wave tiles (rank 80 > 68; d = 2) are
+    reconstructed densely and measured by the two-pass kernels: the same
+    measures as the oracle."""
+    T = _cube(dims, 11)
+    cores = synth.random_tt_cores(dims, ranks, tag=43)
+    got = lrc.tt_quality([to_dev(c) for c in cores], to_dev(T), scale=2.0)
+    _compare(got, O.band_quality(T, 2.0 * O.tt_full(cores)), (dims, ranks))
+
+
+def test_tt_fused_deterministic(lrc):
+    """The fused epilogue adds its partials in a fixed order: repeated calls
+    agree bitwise."""
+    dims = (145, 145, 200)
+    T = synth.hyperspectral(shape=dims)
+    cores = [to_dev(c) for c in synth.random_tt_cores(dims, (1, 17, 17, 1), tag=44)]
+    X = to_dev(T)
+    a = lrc.tt_quality(cores, X, scale=1.5)
+    b = lrc.tt_quality(cores, X, scale=1.5)
+    assert a == b
+
+
 def test_full_size_hyperspectral(lrc):
     """512 x 512 x 224 stand-in at rank (32, 32): FP16 cores against the
     FP64 reference, every measure compared with the oracle's."""
