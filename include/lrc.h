@@ -330,12 +330,17 @@ int lrc_band_quality(const void* X, const void* Xh, int64_t pixels, int64_t band
                      lrc_quality* q);
 
 /* TT cores (as for lrc_tt_reconstruct, stored in `prec`, d >= 2) against the
- * device FP64 reference X: the stored cores are widened exactly and
- * contracted in FP64 (the paper's evaluation of rounded cores), the result
- * multiplied by `scale`, and measured as lrc_band_quality does, with
- * bands = dims[d-1] and pixels = the product of the other modes.  The dense
- * FP64 reconstruction lives in the library's workspace.  Synchronizes.
- * Errors as lrc_tt_reconstruct, plus LRC_EINVAL for d < 2 or a NULL X. */
+ * device FP64 reference X (Sec. sec:hyperspectral_application): the stored
+ * cores are widened exactly and contracted in FP64 (the paper's evaluation
+ * of rounded cores), the result multiplied by `scale`, and measured as
+ * lrc_band_quality does, with bands = dims[d-1] and pixels = the product of
+ * the other modes.  When the FP64 reconstruction runs by wave tiles (d >= 3,
+ * last rank <= 68, at most 455 bands) the measures are formed in its
+ * epilogue, which reads only the cores and X; otherwise the dense FP64
+ * reconstruction is written to the library's workspace and measured in two
+ * passes.  Sums are added in a fixed order either way (bitwise reproducible
+ * for a given path).  Synchronizes.  Errors as lrc_tt_reconstruct, plus
+ * LRC_EINVAL for d < 2 or a NULL X. */
 int lrc_tt_quality(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, int prec,
                    const void* X, double scale, lrc_quality* q);
 
