@@ -1839,10 +1839,17 @@ static int64_t wave_grid(const TTPlan& p) {
 // feeds NS NPB products and every G_2 fragment NPB.  Last products of the NS
 // sets for a tile, with T read once per column block before its products;
 // the core ring runs D steps ahead as in last_store_w.
+// NS = 3: all three sets in one pass over T (sums 0 .. 4).
+template <int NS>
+struct CertSets {
+    static constexpr int nsum = NS == 1 ? 2 : (NS == 2 ? 3 : 5);
+    __host__ __device__ static constexpr int set(int q) { return NS == 1 ? 0 : (NS == 2 ? 1 + q : q); }
+};
+
 template <int NKB, int NPB, int NS, int D>
 __device__ __forceinline__ void last_cert_s(const TTArgs& a, const double* __restrict__ Tref, int64_t i, int64_t L0,
                                             int r, int g, const double (&zf)[NS][NPB][NKB],
-                                            double (&sum)[NS == 1 ? 2 : 3]) {
+                                            double (&sum)[CertSets<NS>::nsum]) {
     static_assert(D <= NKB, "ring deeper than a block");
     const int n_cb = (int)((a.n_last + 15) / 16);
     // G_3 of each set through a buffer resource of its exact size: rows past
@@ -1852,7 +1859,7 @@ __device__ __forceinline__ void last_cert_s(const TTArgs& a, const double* __res
     __amdgpu_buffer_rsrc_t rs[NS];
 #pragma unroll
     for (int q = 0; q < NS; ++q) {
-        const TTSet& S = a.set[NS == 1 ? 0 : 1 + q];
+        const TTSet& S = a.set[CertSets<NS>::set(q)];
         rs[q] = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(S.core[1]), (short)0,
                                                   (int)((uint32_t)S.rM * (uint32_t)a.n_last * 8u), 0x00020000);
     }
@@ -1920,6 +1927,15 @@ __device__ __forceinline__ void last_cert_s(const TTArgs& a, const double* __res
                     const double d0 = t - (ok ? acc[0][pb][v] : 0.0);
                     sum[0] += d0 * d0;
                     sum[1] += t * t;
+                } else if constexpr (NS == 3) {
+                    const double r0 = ok ? acc[0][pb][v] : 0.0, r1 = ok ? acc[1][pb][v] : 0.0;
+                    const double r2 = ok ? acc[2][pb][v] : 0.0;
+                    const double d0 = t - r0, d1 = t - r1, d2 = r1 - r2, d3 = t - r2;
+                    sum[0] += d0 * d0;
+                    sum[1] += d1 * d1;
+                    sum[2] += d2 * d2;
+                    sum[3] += d3 * d3;
+                    sum[4] += t * t;
                 } else {
                     const double r1 = ok ? acc[0][pb][v] : 0.0, r2 = ok ? acc[1][pb][v] : 0.0;
                     const double d1 = t - r1, d2 = r1 - r2, d3 = t - r2;
@@ -1941,8 +1957,8 @@ template <int NKB, int NPB, int NS>
 __global__ __launch_bounds__(256) void k_tt_cert_s(TTArgs a, const double* __restrict__ Tref,
                                                    double* __restrict__ part, int64_t ntiles, int64_t G) {
     constexpr int NT = (NKB + 3) / 4;
-    constexpr int NSUM = NS == 1 ? 2 : 3;
-    constexpr int D = NKB < (NPB * NS >= 4 ? 4 : 8) ? NKB : (NPB * NS >= 4 ? 4 : 8);
+    constexpr int NSUM = CertSets<NS>::nsum;
+    constexpr int D = NKB < (NPB * NS >= 3 ? 4 : 8) ? NKB : (NPB * NS >= 3 ? 4 : 8);
     __shared__ double red[4][NSUM];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1960,7 +1976,7 @@ __global__ __launch_bounds__(256) void k_tt_cert_s(TTArgs a, const double* __res
             int ln = lane;
             asm volatile("" : "+v"(ln));
             double4_t acc[NPB][NT];
-            middle_w_tile<double, NT, NPB>(a, a.set[NS == 1 ? 0 : 1 + q], i, L0, ln & 15, ln >> 4, acc);
+            middle_w_tile<double, NT, NPB>(a, a.set[CertSets<NS>::set(q)], i, L0, ln & 15, ln >> 4, acc);
 #pragma unroll
             for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
@@ -1980,7 +1996,7 @@ __global__ __launch_bounds__(256) void k_tt_cert_s(TTArgs a, const double* __res
     }
     __syncthreads();
     if (threadIdx.x < NSUM) {
-        const int row = NS == 1 ? (threadIdx.x == 0 ? 0 : 4) : 1 + (int)threadIdx.x;
+        const int row = NS == 1 ? (threadIdx.x == 0 ? 0 : 4) : (NS == 2 ? 1 + (int)threadIdx.x : (int)threadIdx.x);
         part[row * G + blockIdx.x] =
             ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
         for (int64_t w = blockIdx.x + gridDim.x; w < G; w += gridDim.x) part[row * G + w] = 0.0;
@@ -2395,12 +2411,24 @@ hipError_t launch_tt_cert(const TTPlan& p, const void* const* const* cores, cons
     case 16: LRC_TCS(16, P, S, g, nt); break;         \
     default: LRC_TCS(17, P, S, g, nt); break;         \
     }
-        if (npA == 2) {
-            LRC_TCS_K(2, 1, nkA, gA, ntA)
+        // one pass over T with the three sets in each wave (default), or
+        // (LRC_TT_CERT_SPLIT=1) the base set and the augmented pair as two
+        // kernels that each read T
+        static const bool split = [] {
+            const char* e = std::getenv("LRC_TT_CERT_SPLIT");
+            return e && e[0] == '1';
+        }();
+        if (!split) {
+            const int nk = std::max(nkA, nkB);
+            LRC_TCS_K(1, 3, nk, gB, ntB)
         } else {
-            LRC_TCS_K(1, 1, nkA, gA, ntA)
+            if (npA == 2) {
+                LRC_TCS_K(2, 1, nkA, gA, ntA)
+            } else {
+                LRC_TCS_K(1, 1, nkA, gA, ntA)
+            }
+            LRC_TCS_K(1, 2, nkB, gB, ntB)
         }
-        LRC_TCS_K(1, 2, nkB, gB, ntB)
 #undef LRC_TCS_K
 #undef LRC_TCS
         return hipGetLastError();
