@@ -2243,8 +2243,11 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
     a.vec8 = sizeof(T) == 2 && out && (p.n_last % 8 == 0) && (reinterpret_cast<uintptr_t>(out) % 16 == 0);
     a.lines = out && ((p.n_last * (int64_t)sizeof(T)) % 128 == 0) && (reinterpret_cast<uintptr_t>(out) % 128 == 0);
     // short output rows (n_d e < 1 KB): wave tiles of consecutive middle indices
-    // write neighbouring segments of the same rows, so the rows fill up together
-    a.ifast = p.wave_nkb && p.n_last * (int64_t)sizeof(T) < 1024;
+    // write neighbouring segments of the same rows, so the rows fill up
+    // together.  Not for FP16: its tiles of one middle index share the staged
+    // G_{d-1} slice, which then stays in the L2 (512 x 512 x 224 at rank 65:
+    // 40.7 -> 31.9 us; with 16-byte row stores the rows' locality matters less)
+    a.ifast = p.wave_nkb && p.n_last * (int64_t)sizeof(T) < 1024 && sizeof(T) != 2;
     // the staging copy is timed under the kernel's label with a "_stage" suffix
     char stage_label[64];
     std::snprintf(stage_label, sizeof(stage_label), "%s_stage", label);
