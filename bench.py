@@ -28,6 +28,8 @@ small configurations).
   python bench.py --fixed-memory FILE   fixed-memory comparison on hyperspectral-shaped stand-ins
   python bench.py --factor FILE         randomized FP64 SVD / TT-SVD cells
   python bench.py --report FILE.jsonl   markdown tables from the records the sweeps write beside FILE
+  python bench.py --apply-cell M N K B PREC [--reps R]   one apply configuration, R calls (for profilers)
+  python bench.py --tt-cell DIMS RANKS PREC [--reps R]   one TT reconstruction, R calls (for profilers)
 """
 from __future__ import annotations
 
@@ -555,6 +557,21 @@ def quant_sweep(path, dev, lrc):
         log(render_sweep_row(records[-1]))
         del X, Y
         torch.cuda.empty_cache()
+    # quality of stored TT cores against the reference, fused into the FP64
+    # reconstruction: reads the reference once (8 bytes per entry) and the cores
+    for name, dims, ranks in (("512x512x224 r(32,32)", (512, 512, 224), (1, 32, 32, 1)),
+                              ("512x512x224 r(65,65)", (512, 512, 224), (1, 65, 65, 1))):
+        N = int(np.prod(dims))
+        X = torch.from_numpy(synth.hyperspectral(shape=dims)).to(dev)
+        cores = [torch.from_numpy(c.astype(np.float16)).to(dev) for c in synth.random_tt_cores(dims, ranks, tag=3)]
+        f, _ = tt_counts(list(dims), list(ranks), 8)
+        by = 8.0 * N + sum(2.0 * c.numel() for c in cores)
+        wall, km = _time_cell(lrc, lambda r: lrc.tt_quality(cores, X), 10, None)
+        records.append(_record(f"tt quality {name} fused (FP16 cores)", "tt_quality", "f64", km, wall, f + 10.0 * N, by,
+                               config=name, dims=list(dims), ranks=list(ranks)))
+        log(render_sweep_row(records[-1]))
+        del X, cores
+        torch.cuda.empty_cache()
     write_records(os.path.splitext(path)[0] + ".jsonl", records)
     with open(path, "w") as fh:
         fh.write("\n".join(SWEEP_HEAD + [render_sweep_row(r) for r in records]) + "\n")
@@ -891,6 +908,36 @@ def fixed_memory(path, dev, lrc):
         fh.write("\n".join(out) + "\n")
 
 
+# ------------------------------------------------------------ single cells ---
+
+def run_cell(args, dev, lrc):
+    """One apply or TT configuration, --reps calls back to back on seeded
+    synthetic inputs (the kernels a profiler then sees are that cell's)."""
+    import torch
+    from paper_2607_12969_amd import synth
+    dt = {"fp64": np.float64, "fp32": np.float32, "fp16": np.float16}
+    if args.apply_cell:
+        m, n, k, b = (int(v) for v in args.apply_cell[:4])
+        p = args.apply_cell[4]
+        w = synth.random_factors(m, n, k, b, tag=77)
+        ins = [torch.from_numpy(np.ascontiguousarray(w[key]).astype(dt[p])).to(dev) for key in ("U", "s", "V", "X")]
+        Y = torch.empty((m, b), dtype=ins[0].dtype, device=dev)
+        log(f"apply cell {m}x{n} k={k} b={b} {p}, {args.reps} calls")
+        for _ in range(args.reps):
+            lrc.matrix_apply(*ins, Y=Y)
+    else:
+        dims = tuple(int(v) for v in args.tt_cell[0].split("x"))
+        ranks = [1] + [int(v) for v in args.tt_cell[1].split(",")] + [1]
+        p = args.tt_cell[2]
+        cores = [torch.from_numpy(c.astype(dt[p])).to(dev) for c in synth.random_tt_cores(dims, ranks, tag=1)]
+        out = torch.empty(dims, dtype=cores[0].dtype, device=dev)
+        log(f"tt cell {dims} ranks {ranks[1:-1]} {p}, {args.reps} calls")
+        for _ in range(args.reps):
+            lrc.tt_reconstruct(cores, out=out)
+    torch.cuda.synchronize()
+    print(json.dumps({"cell": args.apply_cell or args.tt_cell, "reps": args.reps}))
+
+
 # ---------------------------------------------------------------- report ---
 
 def render_report(records):
@@ -933,6 +980,11 @@ def main():
     ap.add_argument("--factor", default=None, help="write the randomized FP64 factorization cells")
     ap.add_argument("--copy-calibration", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
     ap.add_argument("--report", default=None, help="render the markdown tables of a .jsonl record file (no GPU)")
+    ap.add_argument("--apply-cell", nargs=5, default=None, metavar=("M", "N", "K", "B", "PREC"),
+                    help="run one apply configuration --reps times (for profilers)")
+    ap.add_argument("--tt-cell", nargs=3, default=None, metavar=("DIMS", "RANKS", "PREC"),
+                    help="run one TT reconstruction (e.g. 512x512x224 65,65 fp16) --reps times (for profilers)")
+    ap.add_argument("--reps", type=int, default=20)
     args = ap.parse_args()
     if args.report:
         sys.stdout.write(render_report(read_records(args.report)))
@@ -957,6 +1009,9 @@ def main():
         print(json.dumps({"copy_bytes": a.numel() * 8, "launches": 5}))
         return
 
+    if args.apply_cell or args.tt_cell:
+        run_cell(args, dev, lrc)
+        return
     if args.sweep:
         sweep(args.sweep, dev, lrc)
         return
