@@ -1796,6 +1796,235 @@ __global__ __launch_bounds__(64 * kW16) void k_tt_wave16(TTArgs a, int64_t ntile
     }
 }
 
+// ---------------------------------------------------------------------------
+// FP16 wave tiles reading the cores in place (d >= 3, no staging launch):
+//   - the last core's rows G_d(t, :) go to LDS as they lie in memory (rows
+//     t < Kp3 at pitch ldc = ncp + 16 halves, zero past r_{d-1}), and the
+//     last product takes its operand (eight consecutive t for one column c)
+//     with the transposing LDS read ds_read_b64_tr_b16;
+//   - the middle core's operand (eight consecutive s for one t) is gathered
+//     from the core in global memory: the tiles of one middle index run
+//     consecutively, so its slice is found in the L2; columns t past r_{d-1}
+//     are zero;
+//   - the rows of G_1 (or of the left interface) are read as eight values
+//     each, zero past r_{d-2}.
+// WIDE: the middle product runs three K steps of 32 (Kp2 <= 96); else NKB
+// (Kp2 <= 32 NKB).
+__device__ __forceinline__ half8_t frag_krows16(const half_t* S, int ld, int rbase, int k0, int lane) {
+    typedef short s4_t __attribute__((ext_vector_type(4)));
+    typedef short s8_t __attribute__((ext_vector_type(8)));
+    const int s = lane & 15;
+    const half_t* p = S + (k0 + (s >> 2)) * ld + rbase + 4 * (s & 3);
+    const s4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4_t*)(p));
+    const s4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4_t*)(p + 4 * ld));
+    const s8_t both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(half8_t, both);
+}
+
+template <int NKB, int NPB, bool WIDE, bool TS>
+__global__ __launch_bounds__(64 * kW16) void k_tt_wave16d(TTArgs a, int64_t ntiles) {
+    constexpr int NT = 2 * NKB;
+    constexpr int NKB2 = WIDE ? 3 : NKB;
+    extern __shared__ double4_t smem_v[];
+    __shared__ float st_tile[kW16][16 * 17];   // per wave: rows not fit for vector stores
+    half_t* Ls = reinterpret_cast<half_t*>(smem_v);
+    const TTSet& S = a.set[0];
+    const int rL = S.rL, rM = S.rM, Kp3 = S.Kp3;
+    const int ldc = a.ncp + 16;
+    {
+        // G_d rows t < Kp3 into LDS, 16-byte chunks of eight columns (whole
+        // aligned loads when the rows allow it, else eight scalar loads);
+        // rows past r_{d-1} and columns past n_d are zero
+        const half_t* g3 = static_cast<const half_t*>(S.core[1]);
+        const int cpr = a.ncp / 8, nch = Kp3 * cpr;
+        const bool vec = (a.n_last % 8 == 0) && (reinterpret_cast<uintptr_t>(g3) % 16 == 0);
+        for (int c0 = threadIdx.x; c0 < nch; c0 += 8 * 64 * kW16) {
+            half8_t buf[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int idx = c0 + 64 * kW16 * q;
+                const int t = idx / cpr, c = 8 * (idx - (idx / cpr) * cpr);
+                half8_t w;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) w[j] = half_t(0);
+                if (idx < nch && t < rM && c < a.n_last) {
+                    const half_t* src = g3 + (int64_t)t * a.n_last + c;
+                    if (vec) {
+                        w = *reinterpret_cast<const half8_t*>(src);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) w[j] = c + j < a.n_last ? src[j] : half_t(0);
+                    }
+                }
+                buf[q] = w;
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int idx = c0 + 64 * kW16 * q;
+                if (idx < nch) {
+                    const int t = idx / cpr, c = 8 * (idx - (idx / cpr) * cpr);
+                    *reinterpret_cast<half8_t*>(Ls + t * ldc + c) = buf[q];
+                }
+            }
+        }
+        __syncthreads();
+    }
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nLb = (a.NL + 16 * NPB - 1) / (16 * NPB);
+    const int64_t wl = xcd_tile(gridDim.x);
+    const half_t* g2 = static_cast<const half_t*>(S.core[0]);
+    const half_t* g1 = static_cast<const half_t*>(S.core[2]);
+    const int64_t ld2 = a.n_mid * (int64_t)rM;   // between consecutive s of G_{d-1}
+    for (int64_t tile = wl * kW16 + wave; tile < ntiles; tile += (int64_t)gridDim.x * kW16) {
+        const int64_t i = tile / nLb;
+        const int64_t L0 = (tile % nLb) * 16 * NPB;
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int r = ln & 15, g = ln >> 4;
+        // middle-core operands: lane (r, g) of step kb, block tb holds
+        // G_{d-1}(32 kb + 8 g + j, i, 16 tb + r), j = 0..7
+        half8_t x[NKB2][NT];
+        const half_t* g2i = g2 + i * rM;
+#pragma unroll
+        for (int tb = 0; tb < NT; ++tb) {
+            const int t = 16 * tb + r;
+            const bool tok = t < rM;
+            const int tc = tok ? t : rM - 1;
+#pragma unroll
+            for (int kb = 0; kb < NKB2; ++kb)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int sv = 32 * kb + 8 * g + j;
+                    const half_t v = g2i[(int64_t)(sv < rL ? sv : rL - 1) * ld2 + tc];
+                    x[kb][tb][j] = tok ? v : half_t(0);
+                }
+        }
+        auto rows = [&](int pb, half8_t (&b)[NKB2]) {
+            const int64_t L = L0 + 16 * pb + r;
+            const half_t* zr = g1 + (L < a.NL ? L : a.NL - 1) * rL;
+#pragma unroll
+            for (int kb = 0; kb < NKB2; ++kb)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int sv = 32 * kb + 8 * g + j;
+                    const half_t v = zr[sv < rL ? sv : rL - 1];
+                    b[kb][j] = sv < rL ? v : half_t(0);
+                }
+        };
+        half8_t zf[NPB][NKB];
+        half8_t bc[NKB2], bn[NKB2];
+        rows(0, bc);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int pb = 0; pb < NPB; ++pb) {
+            if (pb + 1 < NPB) rows(pb + 1, bn);
+            __builtin_amdgcn_sched_barrier(0);
+            float4_t acc[NT];
+#pragma unroll
+            for (int tb = 0; tb < NT; ++tb) acc[tb] = zero_accv<float4_t>();
+#pragma unroll
+            for (int kb = 0; kb < NKB2; ++kb)
+#pragma unroll
+                for (int tb = 0; tb < NT; ++tb) acc[tb] = mfma(x[kb][tb], bc[kb], acc[tb]);
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) zf[pb][kb] = regroup16(acc[2 * kb], acc[2 * kb + 1]);
+#pragma unroll
+            for (int kb = 0; kb < NKB2; ++kb) bc[kb] = bn[kb];
+        }
+        // last product: two column blocks per step, operands by transposing LDS reads
+        const int n_cb = (int)((a.n_last + 15) / 16);
+        auto frags = [&](half8_t (&f)[2][NKB], int cp) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int c = cp + h < n_cb ? cp + h : n_cb - 1;
+#pragma unroll
+                for (int s2 = 0; s2 < NKB; ++s2) f[h][s2] = frag_krows16(Ls, ldc, 16 * c, 32 * s2 + 8 * g, ln);
+            }
+        };
+        half8_t f[2][NKB], fn[2][NKB];
+        frags(f, 0);
+        for (int cp = 0; cp < n_cb; cp += 2) {
+            if (cp + 2 < n_cb) frags(fn, cp + 2);
+            float4_t acc[2][NPB];
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int pb = 0; pb < NPB; ++pb) acc[h][pb] = zero_accv<float4_t>();
+#pragma unroll
+            for (int s2 = 0; s2 < NKB; ++s2)
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int pb = 0; pb < NPB; ++pb) acc[h][pb] = mfma(f[h][s2], zf[pb][s2], acc[h][pb]);
+            if (!TS && a.vec8 && cp + 1 < n_cb) {
+                half_t* out = static_cast<half_t*>(a.out);
+                const int64_t c0 = (int64_t)cp * 16 + 8 * g;
+#pragma unroll
+                for (int pb = 0; pb < NPB; ++pb) {
+                    const half8_t v = regroup16(acc[0][pb], acc[1][pb]);
+                    const int64_t L = L0 + 16 * pb + r;
+                    if (L < a.NL && c0 + 8 <= a.n_last)
+                        *reinterpret_cast<half8_t*>(out + (L * a.n_mid + i) * a.n_last + c0) = v;
+                }
+            } else {
+                store_block<half_t, NPB, TS>(a, st_tile[wave], i, L0, (int64_t)cp * 16, r, g, acc[0]);
+                if (cp + 1 < n_cb)
+                    store_block<half_t, NPB, TS>(a, st_tile[wave], i, L0, (int64_t)(cp + 1) * 16, r, g, acc[1]);
+            }
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int s2 = 0; s2 < NKB; ++s2) f[h][s2] = fn[h][s2];
+        }
+    }
+}
+
+// The in-place kernel serves three-core FP16 trains whose middle product has
+// at most three K steps, whose last product at most two (three hold 259
+// VGPRs, one wave per SIMD) and whose last core fits 64 KB of LDS at its
+// pitch, when they have at most 2048 tiles: there the staging launch weighs
+// most, while with more tiles the gathered middle-core operands of each tile
+// cost more than the copy saves.  Measured with rocprofv3, in place against
+// staged copy + kernel: 145 x 145 x 200 at rank 36 10.4 against 15.5 us,
+// 256^3 at rank 15 11.9 against 14.8 us; 512 x 512 x 224 at rank 33 (4096
+// tiles) 37.5 against 38.6 us; at rank 65 (three K steps) 66.6 against
+// 41.3 us; the 16^6 train (16384 tiles, rows of its left interface read as
+// eight scalar values each) 39.4 against 32 us; and in the resident timing
+// grid 512 x 217 x 204 and 610 x 340 x 103 (3472 and 3400 tiles) lost 6 us.
+static size_t wave16d_lds(const TTPlan& p) {
+    return (size_t)p.set[0].Kp3 * (round_up(p.n_last, 32) + 16) * sizeof(half_t);
+}
+static bool wave16d_ok(const TTPlan& p) {
+    return p.prec == P16 && p.nsets == 1 && p.d == 3 && p.wave_nkb && p.wave_nkb <= 2 && p.set[0].Kp2 <= 96 &&
+           p.wave_tiles <= 2048 && wave16d_lds(p) <= 65536;
+}
+static void launch_wave16d(const TTPlan& p, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
+    const size_t lds = wave16d_lds(p);
+    const bool wide = p.set[0].Kp2 > 32 * p.wave_nkb;
+#define LRC_TD(K, P, W)                                                                                            \
+    do {                                                                                                           \
+        if (a.vec4) hipLaunchKernelGGL((k_tt_wave16d<K, P, W, false>), grid, dim3(64 * kW16), lds, st, a, ntiles); \
+        else hipLaunchKernelGGL((k_tt_wave16d<K, P, W, true>), grid, dim3(64 * kW16), lds, st, a, ntiles);         \
+    } while (0)
+#define LRC_TDW(K, P)             \
+    do {                          \
+        if (wide) LRC_TD(K, P, true); \
+        else LRC_TD(K, P, false); \
+    } while (0)
+#define LRC_TDK(K)                          \
+    do {                                    \
+        if (p.wave_npb == 1) LRC_TDW(K, 1); \
+        else if (p.wave_npb == 2) LRC_TDW(K, 2); \
+        else LRC_TDW(K, 4);                 \
+    } while (0)
+    if (p.wave_nkb == 1) LRC_TDK(1);
+    else LRC_TDK(2);
+#undef LRC_TDK
+#undef LRC_TDW
+#undef LRC_TD
+}
+
 // The last core goes to LDS when it fits 64 KB at the padded pitch.
 static void launch_wave16(int nkb, int npb, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
     const size_t lds = (size_t)a.ncp * (a.set[0].Kp3 + 8) * sizeof(half_t);
@@ -2301,6 +2530,7 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
         off += (int)round_up((int64_t)p.P * ps.ldf * (int64_t)sizeof(T), 32);
         S.st_mid = S.st_last = S.st_left = nullptr;
         if (p.wave_nkb && sizeof(T) >= 4) continue;   // the wave tiles read the cores in place
+        if (sizeof(T) == 2 && wave16d_ok(p)) continue;  // so do these FP16 wave tiles
         {
             T* smid = static_cast<T*>(ws.take((size_t)p.n_mid * ps.Rt * ps.Kp2 * sizeof(T)));
             T* slast = static_cast<T*>(ws.take((size_t)a.ncp * ps.Kp3 * sizeof(T)));
@@ -2365,6 +2595,7 @@ static hipError_t tt_typed(const TTPlan& p, const void* const* const* cores, voi
         const dim3 gw((unsigned)wave_grid(p));
         if constexpr (sizeof(T) == 8) launch_wave(p.wave_nkb, p.wave_npb, gw, stream, a, p.wave_tiles);
         else if constexpr (sizeof(T) == 4) launch_wave32(p.wave_nkb, p.wave_npb, gw, stream, a, p.wave_tiles);
+        else if (wave16d_ok(p)) launch_wave16d(p, gw, stream, a, p.wave_tiles);
         else launch_wave16(p.wave_nkb, p.wave_npb, gw, stream, a, p.wave_tiles);
         return hipGetLastError();
     }
