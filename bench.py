@@ -16,7 +16,8 @@ Prints one JSON line.  `value` is the step's algorithmic GFLOP divided by
 its wall time; the `roofline` object describes the apply or TT kernel with
 the largest share of the step, timed by the library's HIP-event kernel
 timers over the timed steps; `hbm_ceilings_measured_gbps` holds plain
-read / write / copy stream rates measured in the same run;
+read / write / copy stream rates and `mfma_ceilings_measured_tflops` the
+register-only matrix-core rates (`lrc_mfma_ceiling`) measured in the same run;
 `cpu_baseline` is the CPU oracle on a bounded sample of the same apply and
 TT work (all host threads, with the CPU model and one-thread times of the
 small configurations).
@@ -689,7 +690,7 @@ def capped_ranks(dims, nominal):
     return ranks + [1]
 
 
-def _grid_task(lrc, calls, rounds=3, blocks=5, samples=4, warmup=30, seed=0):
+def _grid_task(lrc, calls, rounds=3, blocks=5, samples=20, warmup=30, seed=0):
     """Times of every method of one task: calls[i]() launches method i.
     Each sample is one event pair around `reps` back-to-back calls, reps
     calibrated per method so that a sample lasts about 2 ms (at most 256).
@@ -764,8 +765,8 @@ def grid(path, dev, lrc):
     out = ["# The paper's resident timing grid on one MI355X (synthetic stand-ins)", "",
            "Command: `python -u bench.py --grid FILE`. Inputs resident in HBM and reused across calls (the",
            "paper's resident protocol, so small tasks run from the Infinity Cache); per task 30 warmups, then",
-           "3 rounds x 5 blocks x 4 samples per method in a seeded shuffled order (the paper takes 20 samples",
-           "per block; 4 keep the run near a minute), each sample one HIP event pair around back-to-back calls",
+           "3 rounds x 5 blocks x 20 samples per method in a seeded shuffled order (the paper's protocol),",
+           "each sample one HIP event pair around back-to-back calls",
            "calibrated to about 2 ms (at most 256 calls); time = geometric mean over tasks of the per-task",
            "medians per call; speedup = geometric mean over tasks",
            "of the median paired (FP64 / method) block-median ratio, with a 10,000-resample bootstrap interval",
@@ -1088,9 +1089,14 @@ def main():
 
     ceil = hbm_ceilings(dev)
     log(f"measured HBM ceilings (GB/s): {ceil}")
+    mceil = {p: round(lrc.mfma_ceiling({"f64": "fp64", "f32": "fp32", "f16": "fp16"}[p]), 1) for p in PEAK_TFLOPS}
+    log(f"measured matrix-core ceilings (TFLOP/s): {mceil}")
     for c in cells:
         if c.get("bound") == "hbm":
             c["frac_of_measured"] = round(c["gbs"] / ceil["copy"], 4)
+        elif c.get("bound") == "mfma":
+            f_, _, p_ = kc[c["kernel"]]
+            c["frac_of_measured"] = round(c["gflops"] / 1e3 / mceil[p_], 4)
 
     roofline = None
     if dom is not None:
@@ -1100,7 +1106,7 @@ def main():
         if dom["bound"] == "mfma":
             ach = f / avg_ms / 1e9
             roofline = {"bound": "mfma", "achieved": round(ach, 3), "peak": PEAK_TFLOPS[p], "unit": "TFLOP/s",
-                        "frac": round(ach / PEAK_TFLOPS[p], 4)}
+                        "frac": round(ach / PEAK_TFLOPS[p], 4), "frac_of_measured_peak": round(ach / mceil[p], 4)}
         else:
             ach = by / avg_ms / 1e6
             roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -1135,7 +1141,7 @@ def main():
         "dtype": "f64/f32/f16(f32-accumulate)", "data": "synthetic",
         "config": {"workload": wl.describe(), "parallelism": "single GPU"},
         "hbm_gbps": round(byts / (ms * 1e-3) / 1e9, 2),
-        "hbm_ceilings_measured_gbps": ceil,
+        "hbm_ceilings_measured_gbps": ceil, "mfma_ceilings_measured_tflops": mceil,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "step_parts": {k: {"gflop": round(f / 1e9, 4), "mb": round(b / 1e6, 2)} for k, (f, b) in counts.items()},

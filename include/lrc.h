@@ -440,6 +440,16 @@ int64_t lrc_profile_labels(char* buf, int64_t len);
 /* LRC_VERSION of the built library. */
 int lrc_version(void);
 
+/* Measurement aid: the matrix-core ceiling of this device, in TFLOP/s, for
+ * the MFMA instruction the kernels use in `prec` (FP64 and FP32 16x16x4,
+ * FP16 16x16x32 with FP32 accumulation), measured by a register-only loop of
+ * independent products on every compute unit (about 10 ms, best of two
+ * timed runs after a warm-up run), so that roofline fractions can be given
+ * against measured as well as published peaks.  Synchronizes the calling
+ * thread's stream.  Errors: LRC_EINVAL (NULL, unknown prec), LRC_ENODEV,
+ * LRC_ENOMEM, LRC_EHIP. */
+int lrc_mfma_ceiling(int prec, double* tflops);
+
 #ifdef __cplusplus
 }
 #endif

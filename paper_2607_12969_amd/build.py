@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "liblrc.so")
-SOURCES = ["apply.hip", "tt.hip", "reduce.hip", "quant.hip", "gauge.hip", "quality.hip", "factor.hip", "lrc_api.cpp"]
+SOURCES = ["apply.hip", "tt.hip", "reduce.hip", "quant.hip", "gauge.hip", "quality.hip", "factor.hip", "ceiling.hip",
+           "lrc_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 

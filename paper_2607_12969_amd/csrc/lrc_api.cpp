@@ -283,6 +283,25 @@ extern "C" {
 
 int lrc_version(void) { return LRC_VERSION; }
 
+int lrc_mfma_ceiling(int prec, double* tflops) {
+    if (!tflops) return fail(LRC_EINVAL, "NULL argument");
+    if (!valid_prec(prec)) return fail(LRC_EINVAL, "unknown precision code %d", prec);
+    int dev;
+    int rc = current_device(&dev, nullptr);
+    if (rc) return rc;
+    int cus = 0;
+    hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess || cus <= 0) return fail_hip(e != hipSuccess ? e : hipErrorInvalidValue, "compute unit count");
+    hipStream_t st = g_stream;
+    Workspace& ws = workspace_for(dev, st);
+    ws.reset();
+    e = ws.reserve(mfma_ceiling_workspace_bytes(cus), st);
+    if (e != hipSuccess) return fail_hip(e, "workspace");
+    e = launch_mfma_ceiling(prec, cus, tflops, ws, st);
+    if (e != hipSuccess) return fail_hip(e, "matrix-core ceiling");
+    return LRC_OK;
+}
+
 int lrc_set_stream(void* hip_stream) {
     g_stream = static_cast<hipStream_t>(hip_stream);
     return LRC_OK;

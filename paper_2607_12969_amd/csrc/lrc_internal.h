@@ -225,6 +225,12 @@ hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Works
 // five partial sums of workgroup w (order at k_tt_cert).
 int64_t tt_cert_parts(const TTPlan& p);
 
+// Matrix-core ceiling (TFLOP/s) of the kernels' MFMA instruction for `prec`
+// on `cus` compute units: a register-only loop, timed with HIP events
+// (synchronizes the stream).
+size_t mfma_ceiling_workspace_bytes(int cus);
+hipError_t launch_mfma_ceiling(int prec, int cus, double* tflops, Workspace& ws, hipStream_t st);
+
 // Quality measures of an FP64 reconstruction (one set, wave tiles) fused
 // into the reconstruction: tt_quality_blocks(p, B) is the number of
 // workgroup partials the fused kernel writes (0: the plan does not take it,

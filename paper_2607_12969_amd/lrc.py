@@ -86,6 +86,8 @@ def lib():
     L.lrc_matrix_apply.restype = ctypes.c_int
     L.lrc_matrix_apply_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _i64, ctypes.c_int]
     L.lrc_matrix_apply_noalloc.restype = ctypes.c_int
+    L.lrc_mfma_ceiling.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    L.lrc_mfma_ceiling.restype = ctypes.c_int
     L.lrc_matrix_apply_path.argtypes = [_i64, _i64, _i64, _i64, ctypes.c_int]
     L.lrc_matrix_apply_path.restype = ctypes.c_int
     L.lrc_set_apply_path.argtypes = [ctypes.c_int]
@@ -540,6 +542,17 @@ def profile_filter(label=None):
 
 def profile_reset():
     lib().lrc_profile_reset()
+
+
+def mfma_ceiling(prec: str) -> float:
+    """Measured matrix-core ceiling (TFLOP/s) of the kernels' MFMA
+    instruction for prec ('fp64', 'fp32' or 'fp16') on the current device."""
+    codes = {"fp64": 0, "fp32": 1, "fp16": 2}
+    if prec not in codes:
+        raise ValueError(f"prec must be one of {sorted(codes)}")
+    out = ctypes.c_double()
+    _check(lib().lrc_mfma_ceiling(codes[prec], ctypes.byref(out)))
+    return float(out.value)
 
 
 def profile_read() -> dict:

@@ -88,3 +88,8 @@ def test_certify_tt_checks_trains():
         lrc.certify_tt(T, [c.float() for c in base], aug, aug_h)
     with pytest.raises(ValueError, match="on the GPU"):
         lrc.certify_tt(T, base, aug, aug_h)                          # consistent, but host tensors
+
+
+def test_mfma_ceiling_rejects_unknown_precision():
+    with pytest.raises(ValueError, match="prec"):
+        lrc.mfma_ceiling("bf16")
