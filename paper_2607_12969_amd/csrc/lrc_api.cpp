@@ -885,7 +885,7 @@ int lrc_tt_quality(const void* const* cores, const int64_t* dims, const int64_t*
     int64_t G = 0;
     if (d >= 3) {
         const int64_t* rs[1] = {ranks};
-        if (plan_tt(plan, dims, rs, 1, d, LRC_FP64, max_lds) == 0) G = tt_quality_blocks(plan, max_lds);
+        if (plan_tt(plan, dims, rs, 1, d, LRC_FP64, max_lds, false) == 0) G = tt_quality_blocks(plan, max_lds);
     }
     size_t need = (size_t)cnt * 8 + (size_t)(d + 4) * 256 + 256;
     if (G > 0)

@@ -199,6 +199,13 @@ struct TTPlan {
     int64_t NL;          // rows of the left interface Z_{d-2} (1 when d <= 2)
     int64_t n_mid;       // n_{d-1}
     int64_t n_last;      // n_d
+    // Wave tiles take a three-core train (first, middle, last).  mid is the
+    // 0-based index of its middle core: d - 2, or d - 3 when the two last
+    // cores are merged into one right core G_{d-1} G_d of r_{d-2} x
+    // (n_{d-1} n_d) (trains with short last modes); the first core is G_1 or
+    // the left interface of cores 1 .. mid.  NL, n_mid, n_last, rL and rM
+    // then describe that train.
+    int mid;
     int BL, BI, P;       // left rows and middle indices per block, P = BL * BI rounded to 16
     int64_t num_i_blocks, num_L_blocks;
     int grid_L;          // workgroups along the left index (each loops over L blocks)
@@ -213,8 +220,10 @@ struct TTPlan {
 // rank_sets[q] is the rank vector (d+1 entries) of core set q.  Returns 0,
 // or -1 when the ranks do not fit the fused kernel's on-chip buffers
 // (max_lds = the device's per-workgroup LDS limit).
+// merge_right = false keeps mid = d - 2 (plans whose kernels index the last
+// mode on its own, such as the fused quality measures).
 int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int nsets, int d, int prec,
-            size_t max_lds);
+            size_t max_lds, bool merge_right = true);
 
 // `label` names the launch for the kernel timers (nullptr: "tt_fused_<type>").
 hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Workspace& ws,

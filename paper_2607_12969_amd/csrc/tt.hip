@@ -207,40 +207,95 @@ __global__ __launch_bounds__(256) void k_stage16(const half_t* __restrict__ gmid
     *reinterpret_cast<half8_t*>(srows + L * Kp2 + s0) = w;
 }
 
-// Left interface of a train with d >= 4 for the wave tiles:
-// Z(p n + i, t) = sum_s z_p(s) G_{d-2}(s, i, t) for every prefix p = (i_1 .. i_{d-3})
-// and n = n_{d-2}, where z_p = G_1(i_1, :) G_2(:, i_2, :) ... is the prefix's
-// row vector.  One workgroup per prefix forms z_p level by level in LDS (sums
-// over s in order in the accumulation precision, as the LDS tiles' chain) and
-// then the n r_{d-2} entries of its rows, rounded once to the storage type.
-// Its rows are the left indices (i_1 .. i_{d-2}) in C order, so it takes the
-// place of G_1 of a three-core train.
+// Side interfaces of a train run by wave tiles as an equivalent three-core
+// train (first, middle, last), formed in one launch before the tiles run.
+//
+// Left interface (mid >= 2):
+// Z(p n + i, t) = sum_s z_p(s) G_mid(s, i, t) for every prefix p = (i_1 .. i_{mid-1})
+// and n = n_mid, where z_p = G_1(i_1, :) G_2(:, i_2, :) ... is the prefix's
+// row vector (sums over s in order in the accumulation precision, as the LDS
+// tiles' chain; every entry rounded once to the storage type).  Its rows are
+// the left indices (i_1 .. i_mid) in C order, so it takes the place of G_1.
+// Left workgroup (q, sp) takes the prefix q = (i_1 .. i_P) of the first P
+// digits: it chains the row vector of cores 1 .. P once (a handful of lanes
+// per step), then expands cores P+1 .. mid - 1 over all their indices at once
+// in LDS (level c holds n_{P+1} ... n_c rows), and writes the rows of the
+// last level (core mid) that fall in its share sp of the prefix's rows.
+// Taking the serial chain only as deep as the LDS levels require keeps most
+// of the work in the wide expansions; the shares keep the grid several
+// workgroups per CU.  Every entry is the same sum in the same order whatever
+// P is.  The cores are read through the caches (copying the levels' cores
+// into LDS first measured slower: 16^6 at ranks 9-25, FP16 9.5 -> 13.1 us).
+//
+// Right core (two last cores merged, mid = d - 3):
+// W(s, i n_d + j) = sum_u G_{d-1}(s, i, u) G_d(u, j), for s < r_{d-2},
+// i < n_{d-1}, j < n_d (sum over u in order in the accumulation precision,
+// rounded once to the storage type), laid out as a last core of
+// r_{d-2} x (n_{d-1} n_d): one thread per entry, in the workgroups after the
+// left ones.
 struct LeftChain {
     const void* core[kMaxD];
     int64_t dims[kMaxD];
     int64_t ranks[kMaxD + 1];
-    int d;
-    int rmax;   // largest rank among r_1 .. r_{d-3} (LDS vectors)
+    int d;                 // cores of the left chain's train: the chain covers cores 1 .. d - 2
+    int P;                 // prefix digits per workgroup, 1 <= P <= d - 3
+    int shares;            // workgroups per prefix
+    int64_t nleft;         // left workgroups (prefixes x shares; 0: no left interface)
+    int64_t buf;           // entries of each of the two LDS level buffers
+    // right core (rtotal > 0)
+    const void* ra;
+    const void* rb;
+    int64_t rna, rnb, rru, rtotal;
 };
+
 template <typename T>
-__global__ __launch_bounds__(256) void k_tt_left(LeftChain lc, T* __restrict__ zo) {
+__global__ __launch_bounds__(256) void k_tt_sides(LeftChain lc, T* __restrict__ zo, T* __restrict__ w) {
     using Acc = typename PrecTraits<T>::acc;
+    const int tid = threadIdx.x;
+    if ((int64_t)blockIdx.x >= lc.nleft) {
+        const int64_t e = ((int64_t)blockIdx.x - lc.nleft) * 256 + tid;
+        if (e >= lc.rtotal) return;
+        const T* ga = static_cast<const T*>(lc.ra);
+        const T* gb = static_cast<const T*>(lc.rb);
+        const int64_t cols = lc.rna * lc.rnb;
+        const int64_t s = e / cols, col = e - s * cols;
+        const int64_t i = col / lc.rnb, j = col - i * lc.rnb;
+        const T* a = ga + (s * lc.rna + i) * lc.rru;
+        Acc sum = 0;
+        // 32 loads in flight (from clamped, in-bounds addresses, widened to
+        // the accumulation type so no load waits on another), then the
+        // products in order
+        for (int64_t u0 = 0; u0 < lc.rru; u0 += 16) {
+            Acc av[16], bv[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int64_t uc = u0 + u < lc.rru ? u0 + u : lc.rru - 1;
+                av[u] = static_cast<Acc>(a[uc]);
+                bv[u] = static_cast<Acc>(gb[uc * lc.rnb + j]);
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (u0 + u < lc.rru) sum += av[u] * bv[u];
+        }
+        w[e] = static_cast<T>(sum);
+        return;
+    }
     extern __shared__ double4_t lsm[];
     Acc* va = reinterpret_cast<Acc*>(lsm);
-    Acc* vb = va + lc.rmax;
-    const int tid = threadIdx.x;
-    const int64_t pfx = blockIdx.x;
-    // the prefix digits i_1 .. i_{d-3}, last digit fastest
+    Acc* vb = va + lc.buf;
+    const int64_t pfx = (int64_t)blockIdx.x / lc.shares;
+    const int sp = (int)((int64_t)blockIdx.x - pfx * lc.shares);
+    // the prefix digits i_1 .. i_P, last digit fastest
     int64_t rest = pfx;
     int64_t dig[kMaxD];
-    for (int c = lc.d - 4; c >= 0; --c) {
+    for (int c = lc.P - 1; c >= 0; --c) {
         dig[c] = rest % lc.dims[c];
         rest /= lc.dims[c];
     }
     const T* g0 = static_cast<const T*>(lc.core[0]);
     for (int t = tid; t < lc.ranks[1]; t += 256) va[t] = static_cast<Acc>(g0[dig[0] * lc.ranks[1] + t]);
     __syncthreads();
-    for (int c = 1; c <= lc.d - 4; ++c) {
+    for (int c = 1; c < lc.P; ++c) {
         const T* g = static_cast<const T*>(lc.core[c]);
         const int rin = (int)lc.ranks[c], rout = (int)lc.ranks[c + 1];
         const int64_t n = lc.dims[c];
@@ -255,18 +310,81 @@ __global__ __launch_bounds__(256) void k_tt_left(LeftChain lc, T* __restrict__ z
         va = vb;
         vb = tmp;
     }
+    // expansions: level c holds rows (i_{P+1} .. i_{c+1}) x r_{c+1}
+    int64_t rows = 1;
+    for (int c = lc.P; c < lc.d - 3; ++c) {
+        const int rin = (int)lc.ranks[c], rout = (int)lc.ranks[c + 1];
+        const int n = (int)lc.dims[c];
+        const int total = (int)(rows * n * rout);   // entries of the level: fits LDS
+        const T* g = static_cast<const T*>(lc.core[c]);
+        for (int e = tid; e < total; e += 256) {
+            const int ri = e / rout, t = e - ri * rout;
+            const int row = ri / n, i = ri - row * n;
+            const Acc* z = va + row * rin;
+            Acc sum = 0;
+#pragma unroll 8
+            for (int s2 = 0; s2 < rin; ++s2) sum += z[s2] * static_cast<Acc>(g[((int64_t)s2 * n + i) * rout + t]);
+            vb[e] = sum;
+        }
+        __syncthreads();
+        Acc* tmp = va;
+        va = vb;
+        vb = tmp;
+        rows *= n;
+    }
+    // last level (core mid): this workgroup's share of the prefix's rows
     const int c = lc.d - 3;
-    const T* g = static_cast<const T*>(lc.core[c]);
     const int rin = (int)lc.ranks[c], rout = (int)lc.ranks[c + 1];
     const int64_t n = lc.dims[c];
-    T* dst = zo + pfx * n * rout;
-    for (int64_t e = tid; e < n * rout; e += 256) {
-        const int64_t i = e / rout;
-        const int t = (int)(e % rout);
+    const int64_t fin = rows * n;                               // rows of the prefix
+    const int64_t per = (fin + lc.shares - 1) / lc.shares;
+    const int64_t r0 = (int64_t)sp * per;
+    const int64_t r1 = (r0 + per < fin) ? r0 + per : fin;
+    T* dst = zo + pfx * fin * rout;
+    const T* g = static_cast<const T*>(lc.core[c]);
+    for (int64_t e = r0 * rout + tid; e < r1 * rout; e += 256) {
+        const int64_t ri = e / rout;
+        const int t = (int)(e - ri * rout);
+        const int64_t row = ri / n, i = ri - row * n;
+        const Acc* z = va + row * rin;
         Acc sum = 0;
 #pragma unroll 8
-        for (int s2 = 0; s2 < rin; ++s2) sum += va[s2] * static_cast<Acc>(g[((int64_t)s2 * n + i) * rout + t]);
+        for (int s2 = 0; s2 < rin; ++s2) sum += z[s2] * static_cast<Acc>(g[((int64_t)s2 * n + i) * rout + t]);
         dst[e] = static_cast<T>(sum);
+    }
+}
+
+// Prefix depth and shares of the left interface: the smallest P whose
+// expansion levels fit both LDS buffers (32 KB) and cost a workgroup no more
+// multiply-adds than its share of the last level (each share repeats them);
+// P = d - 3 (no expansion level) is always possible.  The shares bring the
+// grid to about 1024 workgroups, with at least 16 rows each.
+static void left_split(LeftChain& lc, size_t acc_bytes) {
+    constexpr size_t kLdsBudget = (size_t)32 << 10;
+    constexpr int64_t kTargetWgs = 1024, kMinShareRows = 16;
+    const int d = lc.d;
+    const int64_t* dims = lc.dims;
+    const int64_t* ranks = lc.ranks;
+    for (int P = 1; P <= d - 3; ++P) {
+        int64_t npfx = 1, buf = 1, rows = 1, inter = 0;
+        for (int c = 0; c < P; ++c) npfx *= dims[c];
+        for (int c = 1; c <= P; ++c) buf = std::max(buf, ranks[c]);
+        for (int c = P; c < d - 3; ++c) {
+            rows *= dims[c];
+            buf = std::max(buf, rows * ranks[c + 1]);
+            inter += rows * ranks[c + 1] * ranks[c];
+        }
+        const int64_t fin = rows * dims[d - 3];
+        int64_t shares = (kTargetWgs + npfx - 1) / npfx;
+        shares = std::min(shares, std::max<int64_t>(1, fin / kMinShareRows));
+        shares = std::min<int64_t>(shares, 65535);
+        const int64_t last = (fin + shares - 1) / shares * ranks[d - 2] * ranks[d - 3];
+        if (P < d - 3 && (2 * (size_t)buf * acc_bytes > kLdsBudget || inter > last)) continue;
+        lc.P = P;
+        lc.shares = (int)shares;
+        lc.nleft = npfx * shares;
+        lc.buf = buf;
+        break;
     }
 }
 
@@ -2260,7 +2378,7 @@ static int tune_env(const char* name, int dflt) {
     return v > 0 ? v : dflt;
 }
 int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int nsets, int d, int prec,
-            size_t max_lds) {
+            size_t max_lds, bool merge_right) {
     p = TTPlan{};
     p.d = d;
     p.prec = prec;
@@ -2269,36 +2387,52 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     const int KB = mfma_kb(prec);
     const int e = elem_bytes(prec);
     const int acc_b = (prec == P64) ? 8 : 4;
-    p.n_last = dims[d - 1];
-    p.n_mid = dims[d - 2];
-    p.NL = 1;
-    for (int c = 0; c <= d - 3; ++c) p.NL *= dims[c];
     p.chain_rmax = 1;
     for (int q = 0; q < nsets; ++q) {
-        TTPlanSet& s = p.set[q];
-        for (int c = 0; c <= d; ++c) s.ranks[c] = rank_sets[q][c];
-        s.rM = (int)rank_sets[q][d - 1];
-        s.rL = (int)rank_sets[q][d - 2];
-        s.Kp2 = (int)round_up(s.rL, KB);
-        s.Kp3 = (int)round_up(s.rM, KB);
-        // LDS pitches: consecutive rows of a fragment read land on
-        // different banks (one element of pad; 16 bytes for FP16 rows,
-        // which are read 16 bytes at a time)
-        const int pad = (prec == P16) ? 8 : 1;
-        s.ldl = s.Kp2 + pad;
-        s.ldf = s.Kp3 + pad;
-        s.Rt = (int)round_up(s.rM, 16);
+        for (int c = 0; c <= d; ++c) p.set[q].ranks[c] = rank_sets[q][c];
         if (d >= 4)
             for (int c = 1; c <= d - 2; ++c) p.chain_rmax = (int)std::max<int64_t>(p.chain_rmax, rank_sets[q][c]);
     }
-    // the sets of one kernel share the K extent of the last product (their
-    // chains run in step); the staged cores are zero beyond each rank
     int kp3 = 0;
-    for (int q = 0; q < nsets; ++q) kp3 = std::max(kp3, p.set[q].Kp3);
-    for (int q = 0; q < nsets; ++q) {
-        p.set[q].ldf += kp3 - p.set[q].Kp3;
-        p.set[q].Kp3 = kp3;
-    }
+    // the three-core train with middle core `mid` (see TTPlan)
+    auto set_train = [&](int mid) {
+        p.mid = mid;
+        p.n_mid = dims[mid];
+        p.n_last = 1;
+        for (int c = mid + 1; c < d; ++c) p.n_last *= dims[c];
+        p.NL = 1;
+        for (int c = 0; c < mid; ++c) p.NL *= dims[c];
+        for (int q = 0; q < nsets; ++q) {
+            TTPlanSet& s = p.set[q];
+            s.rM = (int)rank_sets[q][mid + 1];
+            s.rL = (int)rank_sets[q][mid];
+            s.Kp2 = (int)round_up(s.rL, KB);
+            s.Kp3 = (int)round_up(s.rM, KB);
+            // LDS pitches: consecutive rows of a fragment read land on
+            // different banks (one element of pad; 16 bytes for FP16 rows,
+            // which are read 16 bytes at a time)
+            const int pad = (prec == P16) ? 8 : 1;
+            s.ldl = s.Kp2 + pad;
+            s.ldf = s.Kp3 + pad;
+            s.Rt = (int)round_up(s.rM, 16);
+        }
+        // the sets of one kernel share the K extent of the last product (their
+        // chains run in step); the staged cores are zero beyond each rank
+        kp3 = 0;
+        for (int q = 0; q < nsets; ++q) kp3 = std::max(kp3, p.set[q].Kp3);
+        for (int q = 0; q < nsets; ++q) {
+            p.set[q].ldf += kp3 - p.set[q].Kp3;
+            p.set[q].Kp3 = kp3;
+        }
+    };
+    // Trains with a short last mode (rows of n_d e <= 128 bytes) take the two
+    // last cores as one right core for the wave tiles, when its n_{d-1} n_d
+    // columns stay within 4096: the output rows become n_{d-1} times longer
+    // and the left interface n_{d-2} times shorter (16^6 at ranks up to 25:
+    // rows of 16 -> 256 entries, left interface 65536 -> 4096 rows).
+    const bool merge = merge_right && nsets == 1 && d >= 4 && dims[d - 1] * e <= 128 &&
+                       dims[d - 2] * dims[d - 1] <= 4096;
+    set_train(merge ? d - 3 : d - 2);
     // staged cores (layouts at TTSet); ncp covers whole pairs of column blocks
     auto stage_bytes = [&]() {
         size_t b = 0;
@@ -2317,17 +2451,23 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     // selects the LDS tiles; LRC_TT_WAVE_NPB (1, 2 or 4) sets the row blocks
     // per reconstruction tile.
     const char* wv = std::getenv("LRC_TT_WAVE");
-    bool wave_ok = d >= 3 && !(wv && wv[0] == '0') &&
-                   ((prec == P64 && (nsets == 1 || nsets == 3)) || (prec != P64 && nsets == 1));
+    const bool wave_kind = d >= 3 && !(wv && wv[0] == '0') &&
+                           ((prec == P64 && (nsets == 1 || nsets == 3)) || (prec != P64 && nsets == 1));
+    for (int attempt = 0; attempt < 2 && wave_kind; ++attempt) {
+    if (attempt == 1) {
+        if (p.mid == d - 2) break;
+        set_train(d - 2);   // the merged train did not fit the wave tiles
+    }
+    bool wave_ok = true;
     // FP64 / FP32 wave tiles read G_2 and G_3 in place with 32-bit byte offsets
     for (int q = 0; q < nsets && wave_ok; ++q) {
         const TTPlanSet& ps = p.set[q];
         wave_ok = (double)ps.rL * p.n_mid * ps.rM * e < 4294967296.0 && (double)ps.rM * p.n_last * e < 4294967296.0;
-        // d >= 4: one workgroup per prefix (i_1 .. i_{d-3}) forms the left interface, its
-        // row vectors (ranks r_1 .. r_{d-3}) in 2 x 32 KB of LDS
+        // mid >= 2: one workgroup per prefix forms the left interface, its
+        // row vectors (ranks r_1 .. r_{mid-1}) in 2 x 32 KB of LDS
         int64_t npfx = 1;
-        for (int c = 0; c <= d - 4; ++c) npfx *= dims[c];
-        for (int c = 1; c <= d - 3 && wave_ok; ++c) wave_ok = rank_sets[q][c] * acc_b <= 32768;
+        for (int c = 0; c <= p.mid - 2; ++c) npfx *= dims[c];
+        for (int c = 1; c <= p.mid - 1 && wave_ok; ++c) wave_ok = rank_sets[q][c] * acc_b <= 32768;
         wave_ok = wave_ok && npfx < 2147483647;
     }
     if (wave_ok) {
@@ -2382,13 +2522,18 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
             p.wave_tiles = p.num_i_blocks * p.num_L_blocks;
             // FP16 stages its cores (K-contiguous fragments); FP64 / FP32 read them in place
             p.stage_bytes = prec == P16 ? stage_bytes() + (size_t)round_up(p.NL * p.set[0].Kp2 * e, 256) : 0;
-            // d >= 4: the left interface of every set (storage type) and two
-            // chain buffers (accumulation type) for its levels
-            if (d >= 4)
-                for (int q = 0; q < nsets; ++q) p.stage_bytes += (size_t)round_up(p.NL * p.set[q].rL * e, 256);
+            // the left interface of every set (mid >= 2) and the merged right
+            // core (mid = d - 3), in the storage type
+            for (int q = 0; q < nsets; ++q) {
+                if (p.mid >= 2) p.stage_bytes += (size_t)round_up(p.NL * p.set[q].rL * e, 256);
+                if (p.mid == d - 3) p.stage_bytes += (size_t)round_up(p.set[q].rM * p.n_last * e, 256);
+            }
             return 0;
         }
     }
+    }
+    // the LDS tiles take the train as it is
+    if (p.mid != d - 2) set_train(d - 2);
     // at most 64 KB of LDS per workgroup (80 KB for the three-set
     // certificate kernel), so that at least two workgroups share a compute
     // unit; a reconstruction whose buffers do not fit that takes the whole
@@ -2480,30 +2625,48 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
     // the staging copy is timed under the kernel's label with a "_stage" suffix
     char stage_label[64];
     std::snprintf(stage_label, sizeof(stage_label), "%s_stage", label);
-    // wave tiles of a train with d >= 4: its left interface takes the place of
-    // G_1 (formed here, timed with the staging)
+    // wave tiles of a train whose middle core is G_{mid+1}, mid >= 2: the left
+    // interface of cores 1 .. mid takes the place of G_1; with mid = d - 3 the
+    // merged right core takes the place of G_d (both formed here, timed with
+    // the staging)
     const void* left[kTTMaxSets] = {};
-    if (p.wave_nkb && p.d >= 4) {
+    const void* right[kTTMaxSets] = {};
+    if (p.wave_nkb && (p.mid >= 2 || p.mid == p.d - 3)) {
         KernelTimer ts(stage_label, stream);
         for (int q = 0; q < p.nsets; ++q) {
-            T* fin = static_cast<T*>(ws.take((size_t)p.NL * p.set[q].rL * sizeof(T)));
-            if (ws.overrun || !fin) return hipErrorOutOfMemory;
             LeftChain lc{};
-            lc.d = p.d;
-            lc.rmax = 1;
-            for (int c = 0; c < p.d; ++c) {
-                lc.core[c] = cores[q][c];
-                lc.dims[c] = p.dims[c];
+            T* fin = nullptr;
+            T* w = nullptr;
+            size_t lds = 0;
+            if (p.mid >= 2) {
+                fin = static_cast<T*>(ws.take((size_t)p.NL * p.set[q].rL * sizeof(T)));
+                if (ws.overrun || !fin) return hipErrorOutOfMemory;
+                // the chain of cores 1 .. mid is the left chain of a train of mid + 2 cores
+                lc.d = p.mid + 2;
+                for (int c = 0; c < lc.d; ++c) {
+                    lc.core[c] = cores[q][c];
+                    lc.dims[c] = p.dims[c];
+                }
+                for (int c = 0; c <= lc.d; ++c) lc.ranks[c] = p.set[q].ranks[c];
+                left_split(lc, sizeof(typename PrecTraits<T>::acc));
+                lds = 2 * (size_t)lc.buf * sizeof(typename PrecTraits<T>::acc);
+                left[q] = fin;
             }
-            for (int c = 0; c <= p.d; ++c) lc.ranks[c] = p.set[q].ranks[c];
-            for (int c = 1; c <= p.d - 3; ++c) lc.rmax = (int)std::max<int64_t>(lc.rmax, p.set[q].ranks[c]);
-            int64_t npfx = 1;
-            for (int c = 0; c <= p.d - 4; ++c) npfx *= p.dims[c];
-            const size_t lds = 2 * (size_t)lc.rmax * sizeof(typename PrecTraits<T>::acc);
-            hipLaunchKernelGGL(k_tt_left<T>, dim3((unsigned)npfx), dim3(256), lds, stream, lc, fin);
+            if (p.mid == p.d - 3) {
+                lc.rtotal = p.set[q].rM * p.n_last;
+                w = static_cast<T*>(ws.take((size_t)lc.rtotal * sizeof(T)));
+                if (ws.overrun || !w) return hipErrorOutOfMemory;
+                lc.ra = cores[q][p.d - 2];
+                lc.rb = cores[q][p.d - 1];
+                lc.rna = p.dims[p.d - 2];
+                lc.rnb = p.dims[p.d - 1];
+                lc.rru = p.set[q].ranks[p.d - 1];
+                right[q] = w;
+            }
+            const int64_t blocks = lc.nleft + (lc.rtotal + 255) / 256;
+            hipLaunchKernelGGL(k_tt_sides<T>, dim3((unsigned)blocks), dim3(256), lds, stream, lc, fin, w);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
-            left[q] = fin;
         }
     }
     // LDS: the shared Z_{d-2} buffer first, then one Z_{d-1} per set
@@ -2513,8 +2676,8 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
     for (int q = 0; q < p.nsets; ++q) {
         TTSet& S = a.set[q];
         const TTPlanSet& ps = p.set[q];
-        S.core[0] = cores[q][p.d - 2];
-        S.core[1] = cores[q][p.d - 1];
+        S.core[0] = cores[q][p.mid];
+        S.core[1] = right[q] ? right[q] : cores[q][p.d - 1];
         for (int c = 0; c <= p.d - 3; ++c) S.core[2 + c] = cores[q][c];
         if (left[q]) S.core[2] = left[q];   // wave tiles: G_1 of the equivalent three-core train
         for (int c = 0; c <= p.d; ++c) S.ranks[c] = ps.ranks[c];
@@ -2554,7 +2717,7 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
                     const int64_t wg_mid = p.n_mid * (ps.Kp2 / 32), wg_last = a.ncp / 32;
                     const int64_t wg_rows = (p.NL * (ps.Kp2 / 8) + 255) / 256;
                     hipLaunchKernelGGL(k_stage16, dim3((unsigned)(wg_mid + wg_last + wg_rows)), dim3(256), 0, stream,
-                                       (const half_t*)cores[q][p.d - 2], (const half_t*)cores[q][p.d - 1],
+                                       (const half_t*)S.core[0], (const half_t*)S.core[1],
                                        (const half_t*)S.core[2], (half_t*)smid, (half_t*)slast, (half_t*)sl, p.n_mid,
                                        p.n_last, p.NL, ps.rL, ps.rM, ps.Kp2, ps.Kp3, ps.Rt, a.ncp, wg_mid, wg_last);
                     hipError_t e = hipGetLastError();
@@ -2566,8 +2729,8 @@ static hipError_t prepare_tt(const TTPlan& p, const void* const* const* cores, v
                 }
             }
 #define LRC_STAGE(IDX)                                                                                       \
-    hipLaunchKernelGGL((k_stage<T, IDX>), dim3((unsigned)gs), dim3(256), 0, stream, (const T*)cores[q][p.d - 2], \
-                       (const T*)cores[q][p.d - 1], rows ? (const T*)S.core[2] : (const T*)nullptr, smid, slast, sl, \
+    hipLaunchKernelGGL((k_stage<T, IDX>), dim3((unsigned)gs), dim3(256), 0, stream, (const T*)S.core[0], \
+                       (const T*)S.core[1], rows ? (const T*)S.core[2] : (const T*)nullptr, smid, slast, sl, \
                        p.n_mid, p.n_last, p.NL, ps.rL, ps.rM, ps.rL, ps.Kp2, ps.Kp3, ps.Rt, a.ncp)
             if (narrow) LRC_STAGE(uint32_t);
             else LRC_STAGE(int64_t);
@@ -2694,7 +2857,8 @@ hipError_t launch_tt(const TTPlan& p, const void* const* cores, void* out, Works
 static size_t quality_lds(int64_t B) { return (size_t)4 * QS_N * B * sizeof(double); }
 
 int64_t tt_quality_blocks(const TTPlan& p, size_t max_lds) {
-    if (p.prec != P64 || p.nsets != 1 || !p.wave_nkb) return 0;
+    // the measures index the last mode's bands: the train as it is
+    if (p.prec != P64 || p.nsets != 1 || !p.wave_nkb || p.mid != p.d - 2) return 0;
     const size_t lds = quality_lds(p.n_last);
     if (lds > max_lds || lds > 131072) return 0;
     const int64_t per_cu = std::max<int64_t>(1, (int64_t)(163840 / lds));
