@@ -391,7 +391,8 @@ def _time_cell(lrc, fn, reps, labels):
     return wall, {lab: kt[lab][1] / kt[lab][0] for lab in kt}
 
 
-ENV_KNOBS = ("LRC_APPLY_TILE", "LRC_TT_WAVE", "LRC_TT_WAVE_NPB", "LRC_TT_P", "LRC_TT_WGS", "LRC_TT_CERT_SPLIT")
+ENV_KNOBS = ("LRC_APPLY_TILE", "LRC_TT_WAVE", "LRC_TT_WAVE_NPB", "LRC_TT_P", "LRC_TT_WGS", "LRC_TT_CERT_SPLIT",
+             "LRC_TT_MERGE")
 
 
 def env_knobs():

@@ -2098,8 +2098,10 @@ __global__ __launch_bounds__(64 * kW16) void k_tt_wave16d(TTArgs a, int64_t ntil
     }
 }
 
-// The in-place kernel serves three-core FP16 trains whose middle product has
-// at most three K steps, whose last product at most two (three hold 259
+// The in-place kernel serves three-core FP16 trains (and trains of more
+// cores whose two last cores are merged: 16^6 at ranks 9-25, 2048 tiles,
+// 20.5 against 23.8 us with sides, staging and kernel) whose middle product
+// has at most three K steps, whose last product at most two (three hold 259
 // VGPRs, one wave per SIMD) and whose last core fits 64 KB of LDS at its
 // pitch, when they have at most 2048 tiles: there the staging launch weighs
 // most, while with more tiles the gathered middle-core operands of each tile
@@ -2110,11 +2112,12 @@ __global__ __launch_bounds__(64 * kW16) void k_tt_wave16d(TTArgs a, int64_t ntil
 // 41.3 us; the 16^6 train (16384 tiles, rows of its left interface read as
 // eight scalar values each) 39.4 against 32 us; and in the resident timing
 // grid 512 x 217 x 204 and 610 x 340 x 103 (3472 and 3400 tiles) lost 6 us.
+// Unmerged trains of four and more cores keep the staged kernel.
 static size_t wave16d_lds(const TTPlan& p) {
     return (size_t)p.set[0].Kp3 * (round_up(p.n_last, 32) + 16) * sizeof(half_t);
 }
 static bool wave16d_ok(const TTPlan& p) {
-    return p.prec == P16 && p.nsets == 1 && p.d == 3 && p.wave_nkb && p.wave_nkb <= 2 && p.set[0].Kp2 <= 96 &&
+    return p.prec == P16 && p.nsets == 1 && (p.d == 3 || p.mid == p.d - 3) && p.wave_nkb && p.wave_nkb <= 2 && p.set[0].Kp2 <= 96 &&
            p.wave_tiles <= 2048 && wave16d_lds(p) <= 65536;
 }
 static void launch_wave16d(const TTPlan& p, dim3 grid, hipStream_t st, const TTArgs& a, int64_t ntiles) {
@@ -2427,11 +2430,19 @@ int plan_tt(TTPlan& p, const int64_t* dims, const int64_t* const* rank_sets, int
     };
     // Trains with a short last mode (rows of n_d e <= 128 bytes) take the two
     // last cores as one right core for the wave tiles, when its n_{d-1} n_d
-    // columns stay within 4096: the output rows become n_{d-1} times longer
-    // and the left interface n_{d-2} times shorter (16^6 at ranks up to 25:
-    // rows of 16 -> 256 entries, left interface 65536 -> 4096 rows).
-    const bool merge = merge_right && nsets == 1 && d >= 4 && dims[d - 1] * e <= 128 &&
-                       dims[d - 2] * dims[d - 1] <= 4096;
+    // columns stay within 4096 and the merged train still has 2048 tiles of
+    // 16 rows (two waves per SIMD): the output rows become n_{d-1} times
+    // longer and the left interface n_{d-2} times shorter (16^6 at ranks up
+    // to 25: rows of 16 -> 256 entries, left interface 65536 -> 4096 rows).
+    // LRC_TT_MERGE=0 never merges, =1 merges whenever the shapes allow.
+    bool merge = merge_right && nsets == 1 && d >= 4 && dims[d - 2] * dims[d - 1] <= 4096;
+    {
+        int64_t nl = 1;
+        for (int c = 0; c < d - 3; ++c) nl *= dims[c];
+        const char* mv = std::getenv("LRC_TT_MERGE");
+        if (mv && mv[0] == '0') merge = false;
+        else if (!(mv && mv[0] == '1')) merge = merge && dims[d - 1] * e <= 128 && dims[d - 3] * ((nl + 15) / 16) >= 2048;
+    }
     set_train(merge ? d - 3 : d - 2);
     // staged cores (layouts at TTSet); ncp covers whole pairs of column blocks
     auto stage_bytes = [&]() {

@@ -198,7 +198,7 @@ def test_three_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
 
 
 @pytest.mark.parametrize("prec", PRECS)
-@pytest.mark.parametrize("layout", ["wave", "lds"])
+@pytest.mark.parametrize("layout", ["wave", "merged", "lds"])
 @pytest.mark.parametrize("dims,ranks", [
     ((3, 4, 5, 6), (1, 3, 7, 5, 1)),
     ((6, 5, 4, 3, 2), (1, 4, 9, 8, 2, 1)),
@@ -206,8 +206,11 @@ def test_three_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
 ])
 def test_many_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
     """Trains of four and more cores: by wave tiles (the left interface
-    Z_{d-2} formed first, then the three-core kernels) and by LDS tiles (the
-    left chain per tile)."""
+    Z_{d-2} formed first, then the three-core kernels), by wave tiles with the
+    two last cores merged into one right core (the left interface of the
+    cores before the middle one; four cores: G_1 itself), and by LDS tiles
+    (the left chain per tile)."""
+    monkeypatch.setenv("LRC_TT_MERGE", "1" if layout == "merged" else "0")
     if layout == "lds":
         monkeypatch.setenv("LRC_TT_WAVE", "0")
     cores = synth.random_tt_cores(dims, ranks, tag=7 * len(dims) + sum(ranks))
