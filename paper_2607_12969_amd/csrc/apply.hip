@@ -22,6 +22,7 @@
 //              K steps of loads in flight; workgroups are renumbered so
 //              that tiles sharing an operand run on the same XCD.
 #include <cstdlib>
+#include <type_traits>
 
 #include "lrc_device.h"
 #include "lrc_internal.h"
@@ -314,12 +315,6 @@ __device__ __forceinline__ void mma_rows_g(const T* As, const T* Bs, typename C:
                 if (!GUARD || (fn < nfn && fm < nfm)) acc[fn][fm] = mfma(a[fn], b[fm], acc[fn][fm]);
     }
 }
-template <class C, typename T>
-__device__ __forceinline__ void mma_rows(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM],
-                                         int wm, int wn, int lane, int nfm, int nfn) {
-    if (nfm == C::FM && nfn == C::FN) mma_rows_g<C, false>(As, Bs, acc, wm, wn, lane, nfm, nfn);
-    else if (nfm > 0 && nfn > 0) mma_rows_g<C, true>(As, Bs, acc, wm, wn, lane, nfm, nfn);
-}
 
 // Same for K-contiguous tiles As[BM][LDK], Bs[BN][LDK] (phase 2, error norm).
 template <class C, bool GUARD, typename T>
@@ -341,12 +336,6 @@ __device__ __forceinline__ void mma_k_g(const T* As, const T* Bs, typename C::Ac
             for (int fm = 0; fm < C::FM; ++fm)
                 if (!GUARD || (fn < nfn && fm < nfm)) acc[fn][fm] = mfma(a[fn], b[fm], acc[fn][fm]);
     }
-}
-template <class C, typename T>
-__device__ __forceinline__ void mma_k(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM], int wm,
-                                      int wn, int lane, int nfm, int nfn) {
-    if (nfm == C::FM && nfn == C::FN) mma_k_g<C, false>(As, Bs, acc, wm, wn, lane, nfm, nfn);
-    else if (nfm > 0 && nfn > 0) mma_k_g<C, true>(As, Bs, acc, wm, wn, lane, nfm, nfn);
 }
 
 
@@ -379,6 +368,10 @@ __device__ __forceinline__ int live_frags(int64_t start, int64_t lim) {
 // two steps of matrix-core work to arrive.  Steps past the end are fetched
 // from clamped addresses (never stashed), so every path issues the same
 // loads and the compiler's waits cover exactly one stage.
+// The pairs of steps run in a loop whose matrix-core work is unconditional
+// (a conditional product inside it made the compiler keep two copies of the
+// accumulators and move one into the other, behind a drain of the matrix
+// pipeline, every step); an odd last step follows the loop.
 template <class Fetch, class Stash, class Mma>
 __device__ __forceinline__ void pipeline2(int nsteps, Fetch&& fetch, Stash&& stash, Mma&& mma) {
     fetch(0, 0);
@@ -386,19 +379,32 @@ __device__ __forceinline__ void pipeline2(int nsteps, Fetch&& fetch, Stash&& sta
     stash(0, 0, 0);
     fetch(0, 2);
     __syncthreads();
-    for (int j = 0; j < nsteps; j += 2) {
+    int j = 0;
+    for (; j + 1 < nsteps; j += 2) {
         // even step j: buffer 0; odd step j + 1: buffer 1
         mma(0);
-        if (j + 1 < nsteps) stash(1, 1, j + 1);
+        stash(1, 1, j + 1);
         fetch(1, j + 3);
         __syncthreads();
-        if (j + 1 < nsteps) {
-            mma(1);
-            if (j + 2 < nsteps) stash(0, 0, j + 2);
-            fetch(0, j + 4);
-            __syncthreads();
-        }
+        mma(1);
+        if (j + 2 < nsteps) stash(0, 0, j + 2);
+        fetch(0, j + 4);
+        __syncthreads();
     }
+    if (j < nsteps) {
+        mma(0);
+        fetch(1, j + 3);
+        __syncthreads();
+    }
+}
+
+// Calls f(std::false_type) for a tile whose fragments are all live (the
+// branch-free products) and f(std::true_type) otherwise, so that the K loop
+// itself carries no such branch.
+template <class F>
+__device__ __forceinline__ void by_edge(bool full, F&& f) {
+    if (full) f(std::false_type{});
+    else f(std::true_type{});
 }
 
 enum { ATB_APPLY = 0, ATB_GRAM = 1 };
@@ -485,19 +491,21 @@ __global__ __launch_bounds__(C::NT) void k_atb(
     TA ta[2];
     TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
-    pipeline2(
-        nsteps,
-        [&](int st, int j) {
-            const int64_t k0 = kbeg + (int64_t)j * C::BK;
-            ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
-            tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
-        },
-        [&](int st, int buf, int j) {
-            const int64_t k0 = kbeg + (int64_t)j * C::BK;
-            ta[st].stash(As[buf], ga, k0, k0 + C::BK > kend, kend);
-            tb[st].stash(Bs[buf], gb, k0, k0 + C::BK > kend, kend);
-        },
-        [&](int buf) { mma_rows<C>(As[buf], Bs[buf], acc, wm, wn, lane, nfm, nfn); });
+    by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
+        pipeline2(
+            nsteps,
+            [&](int st, int j) {
+                const int64_t k0 = kbeg + (int64_t)j * C::BK;
+                ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
+                tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
+            },
+            [&](int st, int buf, int j) {
+                const int64_t k0 = kbeg + (int64_t)j * C::BK;
+                ta[st].stash(As[buf], ga, k0, k0 + C::BK > kend, kend);
+                tb[st].stash(Bs[buf], gb, k0, k0 + C::BK > kend, kend);
+            },
+            [&](int buf) { mma_rows_g<C, decltype(edge)::value>(As[buf], Bs[buf], acc, wm, wn, lane, nfm, nfn); });
+    });
 
     if (splits > 1) {
         // partial tile: one accumulator vector per fragment, consecutive
@@ -672,19 +680,24 @@ __global__ __launch_bounds__(C::NT) void k_abt(
     TA ta[2];
     TB tb[2];
     const int nsteps = (int)((K + C::BK - 1) / C::BK);
-    pipeline2(
-        nsteps,
-        [&](int st, int j) {
-            const int64_t k0 = (int64_t)j * C::BK;
-            ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
-            tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
-        },
-        [&](int st, int buf, int j) {
-            const int64_t k0 = (int64_t)j * C::BK;
-            ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > Ka, Ka);
-            tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > Kb, Kb);
-        },
-        [&](int buf) { mma_k<C>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane, nfm, nfn); });
+    by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
+        pipeline2(
+            nsteps,
+            [&](int st, int j) {
+                const int64_t k0 = (int64_t)j * C::BK;
+                ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
+                tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
+            },
+            [&](int st, int buf, int j) {
+                const int64_t k0 = (int64_t)j * C::BK;
+                ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > Ka, Ka);
+                tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > Kb, Kb);
+            },
+            [&](int buf) {
+                mma_k_g<C, decltype(edge)::value>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane,
+                                                   nfm, nfn);
+            });
+    });
 
     const int r = lane & 15, g = lane >> 4;
     if (MODE == ABT_STORE) {
@@ -1384,19 +1397,24 @@ __global__ __launch_bounds__(C::NT) void k_abt_part(const double* __restrict__ A
     TA ta[2];
     TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
-    pipeline2(
-        nsteps,
-        [&](int st, int j) {
-            const int64_t k0 = kbeg + (int64_t)j * C::BK;
-            ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
-            tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
-        },
-        [&](int st, int buf, int j) {
-            const int64_t k0 = kbeg + (int64_t)j * C::BK;
-            ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > kend, kend);
-            tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > kend, kend);
-        },
-        [&](int buf) { mma_k<C>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane, nfm, nfn); });
+    by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
+        pipeline2(
+            nsteps,
+            [&](int st, int j) {
+                const int64_t k0 = kbeg + (int64_t)j * C::BK;
+                ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
+                tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
+            },
+            [&](int st, int buf, int j) {
+                const int64_t k0 = kbeg + (int64_t)j * C::BK;
+                ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > kend, kend);
+                tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > kend, kend);
+            },
+            [&](int buf) {
+                mma_k_g<C, decltype(edge)::value>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane,
+                                                   nfm, nfn);
+            });
+    });
     constexpr int NF = C::FN * C::FM;
     AccV* mine = reinterpret_cast<AccV*>(part) + ((tile * splits + sp) * NF) * C::NT + tid;
 #pragma unroll
