@@ -55,9 +55,11 @@ struct Cfg {
 
 // large tiles for large problems, small tiles when a dimension is small
 template <typename T> struct BigCfg;
-// FP64 stays at 64 x 64: a 128 x 128 FP64 accumulator tile does not fit the
-// 256 VGPRs of a wave next to its operands
-template <> struct BigCfg<double> { using C = Cfg<double, 64, 64, 16, 2, 2>; };
+// FP64 takes K steps of 8 with 128 x 128 tiles: its 128 accumulator
+// registers per wave then fit beside the operands (240 VGPRs, two waves per
+// SIMD for phase 2; K steps of 16 spill).  65536 x 4096, k = 512: phase 2
+// 4.87 -> 4.78 ms, phase 1 344 -> 310 us; 8192^2, k = 256: 784 -> 735 us.
+template <> struct BigCfg<double> { using C = Cfg<double, 128, 128, 8, 2, 2>; };
 template <> struct BigCfg<float> { using C = Cfg<float, 128, 128, 16, 2, 2>; };
 template <> struct BigCfg<half_t> { using C = Cfg<half_t, 128, 128, 32, 2, 2>; };
 template <typename T> struct SmallCfg;
@@ -579,17 +581,25 @@ enum { ABT_STORE = 0, ABT_ERR = 1 };
 // (BN * sizeof(T) bytes each), marked nontemporal since nothing here reads
 // Y again.  The tile goes through in bands of rows
 // (all BM rows at once when they fit the operand buffers that `stg` spans,
-// else one wave row of WTM rows per band).  Rows >= M and columns >= N are not
-// written.  vec16: Y and its pitch allow 16-byte stores.
+// else a wave row of WTM rows, or the largest half or quarter of one that
+// fits, per band).  Rows >= M and columns >= N are not written.  vec16: Y
+// and its pitch allow 16-byte stores.
 template <typename T, class C>
 __device__ __forceinline__ void abt_store_staged(const typename C::AccV (&acc)[C::FN][C::FM], T* stg, int tid,
                                                  int wm, int wn, int64_t m0, int64_t n0, int64_t M, int64_t N,
                                                  T* __restrict__ Y, int64_t ldy, int vec16) {
     constexpr int VEC = C::VEC;
     constexpr int LDS_ = C::BN + VEC;   // staged row pitch, 16-byte aligned
-    constexpr bool kWhole = C::BM * LDS_ <= 2 * (C::BM + C::BN) * C::LDK;
-    constexpr int RB = kWhole ? C::BM : C::WTM;   // rows per band
-    static_assert(RB * LDS_ <= 2 * (C::BM + C::BN) * C::LDK, "staging band exceeds the operand buffers");
+    constexpr int CAP = 2 * (C::BM + C::BN) * C::LDK;   // elements the operand buffers hold
+    // rows per band: the whole tile, else the largest of a wave row, half
+    // of one, a quarter of one, ... (down to one fragment) that fits
+    constexpr int RB = C::BM * LDS_ <= CAP          ? C::BM
+                       : C::WTM * LDS_ <= CAP       ? C::WTM
+                       : (C::WTM / 2) * LDS_ <= CAP ? C::WTM / 2
+                       : (C::WTM / 4) * LDS_ <= CAP ? C::WTM / 4
+                                                    : 16;
+    static_assert(RB >= 16 && RB * LDS_ <= CAP, "staging band exceeds the operand buffers");
+    static_assert(RB == C::BM || C::WTM % RB == 0, "bands split wave rows evenly");
     static_assert(C::NT % (C::BN / VEC) == 0 && RB % (C::NT / (C::BN / VEC)) == 0, "band must split evenly");
     constexpr int CPR = C::BN / VEC;       // 16-byte chunks per row
     constexpr int RPP = C::NT / CPR;       // rows per pass
@@ -598,13 +608,17 @@ __device__ __forceinline__ void abt_store_staged(const typename C::AccV (&acc)[C
 #pragma unroll
     for (int band = 0; band < C::BM / RB; ++band) {
         if (band > 0) __syncthreads();   // the previous band has been read
-        if (kWhole || wm == band) {
-            const int rbase = kWhole ? wm * C::WTM : 0;
+        // tile rows [band RB, band RB + RB): staged by the waves of that wave
+        // row, each writing its fragments that fall in the band
+        const int lo = band * RB - wm * C::WTM;   // band start within this wave's rows
+        if (RB == C::BM || (lo >= 0 && lo < C::WTM)) {
 #pragma unroll
             for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
                 for (int fm = 0; fm < C::FM; ++fm) {
-                    T* d = stg + (rbase + fm * 16 + r) * LDS_ + wn * C::WTN + fn * 16;
+                    const int srow = (RB == C::BM) ? wm * C::WTM + fm * 16 : fm * 16 - lo;
+                    if (RB != C::BM && (srow < 0 || srow >= RB)) continue;
+                    T* d = stg + (srow + r) * LDS_ + wn * C::WTN + fn * 16;
                     if (AccRowsContiguous<T>::value) {
                         typedef T v4_t __attribute__((ext_vector_type(4)));
                         v4_t w;
@@ -1086,7 +1100,6 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
             p.big1 = (k >= 128 && b >= 128 && pad_b <= pad_s) ? 1 : 0;
         }
         if (forced_tile()) p.big1 = forced_tile() == 128;
-        if (prec == P64) p.big1 = 0;
         const TileDims d1 = cfg_dims(prec, p.big1);
         const int BK = d1.bk;
         p.tiles_m = (int)((k + d1.bm - 1) / d1.bm);
@@ -1112,7 +1125,6 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
         const int64_t big_tiles = ((m + 127) / 128) * ((b + 127) / 128);
         p.big2 = (m >= 128 && b >= 128 && big_tiles >= 256) ? 1 : 0;
         if (forced_tile()) p.big2 = forced_tile() == 128;
-        if (prec == P64) p.big2 = 0;
     }
     p.mid_bytes = (size_t)b * p.Kp * elem_bytes(prec);
     if (path == 2) {
