@@ -668,7 +668,9 @@ static int certify_matrix(const lrc_cert_args* a, lrc_cert_result* res) {
 }
 
 // FP64 reconstruction into a caller-provided buffer on the calling thread's
-// stream (the FP64 kernel takes no workspace); used by the TT certificate.
+// stream; its side interfaces (trains of four or more cores) take workspace
+// that the caller reserved with tt_stage_need.  Used by the TT certificate
+// and the dense quality path.
 static int tt_into(const void* const* cores, const int64_t* dims, const int64_t* ranks, int d, double* out,
                    Workspace& ws, const char* label = "cert_tt_fused_f64") {
     hipStream_t st = g_stream;
