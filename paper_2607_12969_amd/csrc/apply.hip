@@ -36,8 +36,10 @@ struct Cfg {
     static constexpr int NT = WM * WN * 64;
     static constexpr int KPL = PrecTraits<T>::KPL, KB = PrecTraits<T>::KB;
     static constexpr int VEC = 16 / (int)sizeof(T);       // elements per 16-byte access
-    // tiles with K contiguous: [rows][BK + PADK]; f16 rows stay 16-byte aligned
-    static constexpr int PADK = (KPL == 8) ? 8 : 1;
+    // tiles with K contiguous: [rows][BK + PADK]; rows stay 16-byte aligned
+    // (fragments are read 16 bytes at a time) and start an odd number of
+    // 16-byte chunks apart
+    static constexpr int PADK = 16 / (int)sizeof(T);
     static constexpr int LDK = BK + PADK;
     // tiles with rows contiguous: [BK][rows + PADR]; the pad shifts successive
     // K rows across the LDS banks read by one fragment load
@@ -319,10 +321,40 @@ __device__ __forceinline__ void mma_rows_g(const T* As, const T* Bs, typename C:
 }
 
 // Same for K-contiguous tiles As[BM][LDK], Bs[BN][LDK] (phase 2, error norm).
+// FP64 and FP32 take one K value per lane and MFMA; a lane reads the RV =
+// 16 / sizeof(T) consecutive values of its row at K offset RV g with one
+// 16-byte LDS read and feeds value j to the j-th of RV MFMAs, so that MFMA j
+// of a K block of 4 RV sums over k = RV g + j (the K values are taken in
+// another order; every product is still added once).
 template <class C, bool GUARD, typename T>
 __device__ __forceinline__ void mma_k_g(const T* As, const T* Bs, typename C::AccV (&acc)[C::FN][C::FM], int wm,
                                         int wn, int lane, int nfm, int nfn) {
     const int r = lane & 15, g = lane >> 4;
+    if constexpr (C::KPL == 1) {
+        constexpr int RV = 16 / (int)sizeof(T);
+        static_assert(C::BK % (C::KB * RV) == 0 && (C::LDK * sizeof(T)) % 16 == 0, "16-byte fragment reads");
+        typedef T rv_t __attribute__((ext_vector_type(RV)));
+#pragma unroll
+        for (int kk = 0; kk < C::BK; kk += C::KB * RV) {
+            rv_t a[C::FN], b[C::FM];
+#pragma unroll
+            for (int fn = 0; fn < C::FN; ++fn)
+                if (!GUARD || fn < nfn)
+                    a[fn] = *reinterpret_cast<const rv_t*>(Bs + (wn * C::WTN + fn * 16 + r) * C::LDK + kk + g * RV);
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm)
+                if (!GUARD || fm < nfm)
+                    b[fm] = *reinterpret_cast<const rv_t*>(As + (wm * C::WTM + fm * 16 + r) * C::LDK + kk + g * RV);
+#pragma unroll
+            for (int j = 0; j < RV; ++j)
+#pragma unroll
+                for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+                    for (int fm = 0; fm < C::FM; ++fm)
+                        if (!GUARD || (fn < nfn && fm < nfm)) acc[fn][fm] = mfma(a[fn][j], b[fm][j], acc[fn][fm]);
+        }
+        return;
+    }
 #pragma unroll
     for (int kk = 0; kk < C::BK; kk += C::KB) {
         typename C::Frag a[C::FN], b[C::FM];
