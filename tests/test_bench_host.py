@@ -49,3 +49,19 @@ def test_records_round_trip_and_render(tmp_path, monkeypatch):
     assert "| apply 64x32 k=5 b=3 | f32 |" in md
     assert "| tt 8x8x8 | FP16 compensated | f16 | 4.0 [" in md
     assert '"LRC_TT_P": "32"' in md
+
+
+def test_measured_traffic_follows_the_source_hash(tmp_path, monkeypatch):
+    # the committed counter summary is used only while the kernel sources
+    # hash to the value recorded with it
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    h = bench.kernel_source_hash()
+    row = "| apply_p2_mfma_f64 | k_abt<...> | 1 | 2 | 3.0 | 1.00 | 12345.0 |\n"
+    (prof / "traffic_counters.md").write_text(f"source_hash: {h}\n\n" + row)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: h)
+    assert bench.measured_traffic("apply_p2_mfma_f64") == 12345.0
+    assert bench.measured_traffic("tt_fused_f16") is None
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0" * 16)
+    assert bench.measured_traffic("apply_p2_mfma_f64") is None
