@@ -218,6 +218,23 @@ def test_many_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
 
 
 @pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("merge", ["0", "1"])
+@pytest.mark.parametrize("dims,ranks", [
+    ((8,) * 6, (1, 4, 6, 8, 6, 4, 1)),
+    ((16,) * 6, (1, 8, 16, 24, 16, 8, 1)),
+])
+def test_side_interface_splits(lrc, monkeypatch, prec, merge, dims, ranks):
+    """Trains of six cores whose left interface is split over workgroups in
+    every way the planner uses: prefixes of two digits chained once with four
+    shares of the last level each (8^6 and 16^6 as they are), prefixes of one
+    digit with several shares (the same trains with the two last cores
+    merged into one right core)."""
+    monkeypatch.setenv("LRC_TT_MERGE", merge)
+    cores = synth.random_tt_cores(dims, ranks, tag=900 + sum(ranks) + int(merge))
+    _check(lrc, cores, prec, f"sides{dims} merge={merge}")
+
+
+@pytest.mark.parametrize("prec", PRECS)
 @pytest.mark.parametrize("dims,nominal", [
     ((83, 86, 204), 32), ((83, 86, 204), 36), ((145, 145, 200), 36), ((610, 340, 103), 36),
     ((128, 24, 64, 64), 20), ((192, 24, 64, 16), 16), ((16,) * 6, 12),
