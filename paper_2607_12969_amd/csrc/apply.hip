@@ -406,31 +406,52 @@ __device__ __forceinline__ int live_frags(int64_t start, int64_t lim) {
 // (a conditional product inside it made the compiler keep two copies of the
 // accumulators and move one into the other, behind a drain of the matrix
 // pipeline, every step); an odd last step follows the loop.
-template <class Fetch, class Stash, class Mma>
-__device__ __forceinline__ void pipeline2(int nsteps, Fetch&& fetch, Stash&& stash, Mma&& mma) {
-    fetch(0, 0);
-    fetch(1, 1);
-    stash(0, 0, 0);
-    fetch(0, 2);
+template <bool PEEL, class Fetch, class Stash, class Mma>
+__device__ __forceinline__ void pipeline2(int nsteps, int nfull, Fetch&& fetch, Stash&& stash, Mma&& mma) {
+    if constexpr (!PEEL) nfull = 0;
+    // fetch / stash take std::true_type for steps known to lie inside K
+    // (nfull of them): no edge tests, so the loop body stays one block
+    const std::false_type edge{};
+    const std::true_type inside{};
+    fetch(0, 0, edge);
+    fetch(1, 1, edge);
+    stash(0, 0, 0, edge);
+    fetch(0, 2, edge);
     __syncthreads();
     int j = 0;
+    for (; j + 4 < nfull; j += 2) {
+        mma(0);
+        stash(1, 1, j + 1, inside);
+        fetch(1, j + 3, inside);
+        __syncthreads();
+        mma(1);
+        stash(0, 0, j + 2, inside);
+        fetch(0, j + 4, inside);
+        __syncthreads();
+    }
     for (; j + 1 < nsteps; j += 2) {
         // even step j: buffer 0; odd step j + 1: buffer 1
         mma(0);
-        stash(1, 1, j + 1);
-        fetch(1, j + 3);
+        stash(1, 1, j + 1, edge);
+        fetch(1, j + 3, edge);
         __syncthreads();
         mma(1);
-        if (j + 2 < nsteps) stash(0, 0, j + 2);
-        fetch(0, j + 4);
+        if (j + 2 < nsteps) stash(0, 0, j + 2, edge);
+        fetch(0, j + 4, edge);
         __syncthreads();
     }
     if (j < nsteps) {
         mma(0);
-        fetch(1, j + 3);
+        fetch(1, j + 3, edge);
         __syncthreads();
     }
 }
+
+// Whether the K-contiguous GEMM (phase 2) runs its inner steps edge-free:
+// FP32 phase 2 2.57 -> 2.35 ms at 65536 x 4096, while the FP64 one lost 9 %
+// (its compiler schedule of the single-block loop is slower).
+template <typename T>
+constexpr bool kPeelAbt = sizeof(T) != 8;
 
 // Calls f(std::false_type) for a tile whose fragments are all live (the
 // branch-free products) and f(std::true_type) otherwise, so that the K loop
@@ -526,17 +547,19 @@ __global__ __launch_bounds__(C::NT) void k_atb(
     TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
     by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
-        pipeline2(
-            nsteps,
-            [&](int st, int j) {
+        pipeline2<true>(
+            nsteps, (int)((kend - kbeg) / C::BK),
+            [&](int st, int j, auto in) {
                 const int64_t k0 = kbeg + (int64_t)j * C::BK;
-                ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
-                tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
+                const bool pk = !decltype(in)::value && k0 + C::BK > kend;
+                ta[st].fetch(ga, k0, pk, kend);
+                tb[st].fetch(gb, k0, pk, kend);
             },
-            [&](int st, int buf, int j) {
+            [&](int st, int buf, int j, auto in) {
                 const int64_t k0 = kbeg + (int64_t)j * C::BK;
-                ta[st].stash(As[buf], ga, k0, k0 + C::BK > kend, kend);
-                tb[st].stash(Bs[buf], gb, k0, k0 + C::BK > kend, kend);
+                const bool pk = !decltype(in)::value && k0 + C::BK > kend;
+                ta[st].stash(As[buf], ga, k0, pk, kend);
+                tb[st].stash(Bs[buf], gb, k0, pk, kend);
             },
             [&](int buf) { mma_rows_g<C, decltype(edge)::value>(As[buf], Bs[buf], acc, wm, wn, lane, nfm, nfn); });
     });
@@ -727,17 +750,17 @@ __global__ __launch_bounds__(C::NT) void k_abt(
     TB tb[2];
     const int nsteps = (int)((K + C::BK - 1) / C::BK);
     by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
-        pipeline2(
-            nsteps,
-            [&](int st, int j) {
+        pipeline2<kPeelAbt<T>>(
+            nsteps, (int)(std::min(std::min(Ka, Kb), K) / C::BK),
+            [&](int st, int j, auto in) {
                 const int64_t k0 = (int64_t)j * C::BK;
-                ta[st].fetch(ga, k0, k0 + C::BK > Ka, Ka);
-                tb[st].fetch(gb, k0, k0 + C::BK > Kb, Kb);
+                ta[st].fetch(ga, k0, !decltype(in)::value && k0 + C::BK > Ka, Ka);
+                tb[st].fetch(gb, k0, !decltype(in)::value && k0 + C::BK > Kb, Kb);
             },
-            [&](int st, int buf, int j) {
+            [&](int st, int buf, int j, auto in) {
                 const int64_t k0 = (int64_t)j * C::BK;
-                ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > Ka, Ka);
-                tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > Kb, Kb);
+                ta[st].stash(smem + buf * kAs, ga, k0, !decltype(in)::value && k0 + C::BK > Ka, Ka);
+                tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, !decltype(in)::value && k0 + C::BK > Kb, Kb);
             },
             [&](int buf) {
                 mma_k_g<C, decltype(edge)::value>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane,
@@ -1442,17 +1465,19 @@ __global__ __launch_bounds__(C::NT) void k_abt_part(const double* __restrict__ A
     TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
     by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
-        pipeline2(
-            nsteps,
-            [&](int st, int j) {
+        pipeline2<kPeelAbt<double>>(
+            nsteps, (int)((kend - kbeg) / C::BK),
+            [&](int st, int j, auto in) {
                 const int64_t k0 = kbeg + (int64_t)j * C::BK;
-                ta[st].fetch(ga, k0, k0 + C::BK > kend, kend);
-                tb[st].fetch(gb, k0, k0 + C::BK > kend, kend);
+                const bool pk = !decltype(in)::value && k0 + C::BK > kend;
+                ta[st].fetch(ga, k0, pk, kend);
+                tb[st].fetch(gb, k0, pk, kend);
             },
-            [&](int st, int buf, int j) {
+            [&](int st, int buf, int j, auto in) {
                 const int64_t k0 = kbeg + (int64_t)j * C::BK;
-                ta[st].stash(smem + buf * kAs, ga, k0, k0 + C::BK > kend, kend);
-                tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, k0 + C::BK > kend, kend);
+                const bool pk = !decltype(in)::value && k0 + C::BK > kend;
+                ta[st].stash(smem + buf * kAs, ga, k0, pk, kend);
+                tb[st].stash(smem + 2 * kAs + buf * kBs, gb, k0, pk, kend);
             },
             [&](int buf) {
                 mma_k_g<C, decltype(edge)::value>(smem + buf * kAs, smem + 2 * kAs + buf * kBs, acc, wm, wn, lane,
