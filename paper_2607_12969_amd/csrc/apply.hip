@@ -448,10 +448,15 @@ __device__ __forceinline__ void pipeline2(int nsteps, int nfull, Fetch&& fetch, 
 }
 
 // Whether the K-contiguous GEMM (phase 2) runs its inner steps edge-free:
-// FP32 phase 2 2.57 -> 2.35 ms at 65536 x 4096, while the FP64 one lost 9 %
-// (its compiler schedule of the single-block loop is slower).
-template <typename T>
-constexpr bool kPeelAbt = sizeof(T) != 8;
+// FP32 phase 2 2.57 -> 2.35 ms at 65536 x 4096; FP64 4.73 -> 4.33 ms, once
+// the kernel is held to two waves per SIMD (the edge-free loop took 258
+// registers, one wave per SIMD, and was 9 % slower than the single loop).
+// The FP64 tile that reads a misaligned operand in place keeps the single
+// loop and its own register budget: held to two waves it spills.
+template <typename T, bool MIS = false>
+constexpr bool kPeelAbt = sizeof(T) != 8 || !MIS;
+template <typename T, bool MIS = false>
+constexpr int kAbtMinWaves = kPeelAbt<T, MIS> ? 2 : 1;
 
 // Calls f(std::false_type) for a tile whose fragments are all live (the
 // branch-free products) and f(std::true_type) otherwise, so that the K loop
@@ -712,7 +717,7 @@ __device__ __forceinline__ void abt_store_staged(const typename C::AccV (&acc)[C
 //   ABT_STORE: Y[m][ldy] = C rounded to T.
 //   ABT_ERR  : (T = double) partial sum of (Aref[m][n] - C)^2 per workgroup.
 template <typename T, class C, int MODE, bool MIS = false>
-__global__ __launch_bounds__(C::NT) void k_abt(
+__global__ __launch_bounds__(C::NT, (kAbtMinWaves<T, MIS>)) void k_abt(
     const T* __restrict__ Asrc, int64_t lda, int64_t M, int64_t Ka,
     const T* __restrict__ Bsrc, int64_t ldb, int64_t N, int64_t Kb, int64_t K, int tiles_m, int tiles_n,
     T* __restrict__ Y, int64_t ldy, int vec16,
@@ -750,7 +755,7 @@ __global__ __launch_bounds__(C::NT) void k_abt(
     TB tb[2];
     const int nsteps = (int)((K + C::BK - 1) / C::BK);
     by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
-        pipeline2<kPeelAbt<T>>(
+        pipeline2<kPeelAbt<T, MIS>>(
             nsteps, (int)(std::min(std::min(Ka, Kb), K) / C::BK),
             [&](int st, int j, auto in) {
                 const int64_t k0 = (int64_t)j * C::BK;
@@ -1465,7 +1470,8 @@ __global__ __launch_bounds__(C::NT) void k_abt_part(const double* __restrict__ A
     TB tb[2];
     const int nsteps = (int)((kend - kbeg + C::BK - 1) / C::BK);
     by_edge(nfm == C::FM && nfn == C::FN, [&](auto edge) {
-        pipeline2<kPeelAbt<double>>(
+        // The edge-free inner loop measured no faster for these split-K tiles.
+        pipeline2<false>(
             nsteps, (int)((kend - kbeg) / C::BK),
             [&](int st, int j, auto in) {
                 const int64_t k0 = kbeg + (int64_t)j * C::BK;
