@@ -1137,7 +1137,11 @@ ApplyPlan plan_apply(int64_t m, int64_t n, int64_t k, int64_t b, int prec, int p
     }
 
     p.path = path;
-    p.Kp = round_up(k, 8);
+    // Rows of T'^T and of staged factor copies: on the matrix-core path a
+    // whole number of 64-byte K steps (32 halves, 16 floats, 8 doubles), so
+    // that each step's slice of a row is one aligned 64-byte segment rather
+    // than one that straddles two cache lines; the K steps are as many.
+    p.Kp = round_up(k, path == 2 ? 64 / (int64_t)elem_bytes(prec) : 8);
     const size_t acc_b = (prec == P64) ? 8 : 4;
     if (path == 1) {
         p.tiles_m = (int)((k + 63) / 64);

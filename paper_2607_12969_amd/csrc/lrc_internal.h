@@ -46,7 +46,7 @@ struct KernelTimer {
 // ---------------------------------------------------------------- apply ---
 struct ApplyPlan {
     int path;            // LRC_PATH_STREAM or LRC_PATH_MFMA
-    int64_t Kp;          // k rounded up to the MFMA K step (rows of T'^T)
+    int64_t Kp;          // pitch of the rows of T'^T and of staged copies of U, V (k rounded up)
     // phase 1 (split over n)
     int splits;
     int64_t chunk;       // rows of V / X per split
