@@ -73,6 +73,23 @@ def test_ragged_shapes_both_paths(lrc, prec, m, n, k, b):
         _assert_parity(Y, u, s, v, x, prec)
 
 
+@pytest.mark.parametrize("tile", ["64", "128"])
+def test_forced_tile_edges(tile):
+    """The matrix-core tiles pinned to 64 or 128 rows (LRC_APPLY_TILE, read
+    once per process, so the cases run in a child process): shapes whose
+    tiles are mostly edges, every precision, against the oracle."""
+    import os
+    import subprocess
+    import sys
+    script = os.path.join(os.path.dirname(os.path.abspath(__file__)), "forced_tile_case.py")
+    print(f"apply forced tile {tile}", flush=True)
+    r = subprocess.run([sys.executable, "-u", script], env=dict(os.environ, LRC_APPLY_TILE=tile),
+                       capture_output=True, text=True, timeout=110)
+    print(r.stdout[-4000:], r.stderr[-2000:], flush=True)
+    assert r.returncode == 0
+    assert r.stdout.count(" ok") == 18
+
+
 def test_stream_and_mfma_paths_agree(lrc):
     d = synth.random_factors(800, 600, 41, 8, tag=3)
     for prec in PRECS:
