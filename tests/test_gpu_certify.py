@@ -251,6 +251,22 @@ def test_tt_fused_certificate_shapes(lrc, dims, rb, ra):
         _compare(got, want, eta_rtol=1e-6, err_rtol=1e-6, e_atol=1e-12 * want["norm_ref"])
 
 
+def test_tt_certificate_split_kernels():
+    """LRC_TT_CERT_SPLIT=1 (read once per process, so the cases run in a
+    child process): the base train and the augmented pair as two wave-tile
+    kernels; verdicts and sums as with the one-pass kernel."""
+    import os
+    import subprocess
+    import sys
+    script = os.path.join(os.path.dirname(os.path.abspath(__file__)), "cert_split_case.py")
+    print("certify tt split kernels", flush=True)
+    r = subprocess.run([sys.executable, "-u", script], env=dict(os.environ, LRC_TT_CERT_SPLIT="1"),
+                       capture_output=True, text=True, timeout=110)
+    print(r.stdout[-4000:], r.stderr[-2000:], flush=True)
+    assert r.returncode == 0
+    assert r.stdout.count(" ok") == 6
+
+
 def test_tt_certificate_unfused_fallback(lrc):
     """Ranks whose three on-chip interface sets exceed the fused kernel's LDS
     budget take the dense path: three FP64 reconstructions and one pass of

@@ -198,6 +198,20 @@ def test_three_core_layouts(lrc, monkeypatch, prec, layout, dims, ranks):
 
 
 @pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("rows,wgs", [("16", "64"), ("32", "4096"), ("64", "100000")])
+@pytest.mark.parametrize("dims,ranks", [((37, 29, 45), (1, 13, 21, 1)), ((130, 9, 70), (1, 40, 33, 1))])
+def test_lds_tile_tuning(lrc, monkeypatch, prec, rows, wgs, dims, ranks):
+    """The LDS tiles with every row count per tile (LRC_TT_P = 16, 32, 64)
+    and workgroup targets from far below to far above one per tile
+    (LRC_TT_WGS), on ragged three-core trains."""
+    monkeypatch.setenv("LRC_TT_WAVE", "0")
+    monkeypatch.setenv("LRC_TT_P", rows)
+    monkeypatch.setenv("LRC_TT_WGS", wgs)
+    cores = synth.random_tt_cores(dims, ranks, tag=sum(dims) + 3 * sum(ranks))
+    _check(lrc, cores, prec, f"lds P={rows} wgs={wgs} {dims}")
+
+
+@pytest.mark.parametrize("prec", PRECS)
 @pytest.mark.parametrize("layout", ["wave", "merged", "lds"])
 @pytest.mark.parametrize("dims,ranks", [
     ((3, 4, 5, 6), (1, 3, 7, 5, 1)),
